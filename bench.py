@@ -1,0 +1,350 @@
+#!/usr/bin/env python3
+"""Benchmark of the MI355X tensor-lifecycle data path.
+
+Headline workload (the `value` of the JSON line): publish + hydrate of paged
+KV blocks in a Llama-3-8B-shaped cache -- 32 layers x K/V regions of 32768
+blocks (16 tokens x 8 KV heads x 128 dims x bf16 = 32 KiB), 64 GiB per pool.
+One step gathers 4096 Zipf(1.1) prefix-reuse block ids from pool A into a
+contiguous 8 GiB transfer buffer (tc_gather_blocks) and scatters that buffer
+into pool B at the same ids (tc_scatter_blocks).  `value` is the achieved
+HBM rate over the step: algorithmic bytes (every payload byte read once and
+written once) / step time, in GB/s (1e9 B/s).
+
+The same run also measures the other workloads of the path (reported under
+"workloads"): TP=8 shard materialization of an 8B-shaped bf16 stream, the
+block-scaled fp8 cast of a 70B-shaped TP=8 shard, a 1M-fragment storm and a
+256-expert MoE permutation; and times the CPU oracle on a bounded sample of
+the headline workload (cpu_baseline).
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workloads kv,reshard,...]
+"""
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def _log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+class Timer:
+    """HIP events on the stream the kernels run on."""
+
+    def __init__(self, torch, stream):
+        self.torch = torch
+        self.stream = stream
+
+    def pair(self):
+        e0 = self.torch.cuda.Event(enable_timing=True)
+        e1 = self.torch.cuda.Event(enable_timing=True)
+        return e0, e1
+
+
+def _time_calls(torch, stream, fn, warmup, steps):
+    """Run fn warmup times, then steps times bracketed by events on `stream`;
+    returns per-call milliseconds."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    evs = []
+    for _ in range(steps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        evs.append((e0, e1))
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in evs]
+
+
+def _stats(ms, nbytes):
+    med = statistics.median(ms)
+    return {"ms_median": round(med, 4), "ms_min": round(min(ms), 4), "ms_max": round(max(ms), 4),
+            "algorithmic_bytes": int(nbytes), "GBps": round(nbytes / (med * 1e-3) / 1e9, 1),
+            "frac_of_peak": round(nbytes / (med * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+
+
+def _kernel_source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_06007_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(name.encode() + f.read())
+    return h.hexdigest()
+
+
+def _traffic(kernel, src_hash):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_hash") != src_hash:
+        return None
+    entry = t.get("kernels", {}).get(kernel)
+    return None if entry is None else entry.get("hbm_bytes_per_launch")
+
+
+# ---------------------------------------------------------------------------
+
+def run_kv(torch, tc, synth, args, stream):
+    s = synth.KV_LLAMA3_8B
+    B, nb, R = s.block_bytes, s.num_blocks, s.num_regions
+    _log(f"[kv] allocating 2 x {R * s.region_bytes / 2**30:.0f} GiB pools + {s.transfer_bytes / 2**30:.0f} GiB buffer")
+    pool_a = synth.bf16_normal(R * s.region_bytes // 2, 1.0, synth.SEED_KV_8B, device="cuda").view(torch.uint8)
+    pool_b = torch.full((R * s.region_bytes,), 0xA5, dtype=torch.uint8, device="cuda")
+    buf = torch.empty(s.transfer_bytes, dtype=torch.uint8, device="cuda")
+    ra = [pool_a[r * s.region_bytes:(r + 1) * s.region_bytes] for r in range(R)]
+    rb = [pool_b[r * s.region_bytes:(r + 1) * s.region_bytes] for r in range(R)]
+    ids_np = synth.ids_zipf_prefix_reuse(nb, s.n_ids, 1.1, synth.SEED_KV_8B)
+    ids = torch.from_numpy(ids_np).cuda()
+    torch.cuda.synchronize()
+
+    def gather():
+        tc.tc_gather_blocks(ra, nb, B, B, ids, buf, stream=stream)
+
+    def scatter():
+        tc.tc_scatter_blocks(rb, nb, B, B, ids, buf, stream=stream)
+
+    for _ in range(args.warmup):
+        gather()
+        scatter()
+    torch.cuda.synchronize()
+    # timed region: exactly `steps` steps; events around each call on the
+    # launch stream give the per-kernel durations
+    ev = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record(stream)
+        gather()
+        e[1].record(stream)
+        scatter()
+        e[2].record(stream)
+        ev.append(e)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    g_ms = [a.elapsed_time(b) for a, b, _ in ev]
+    s_ms = [b.elapsed_time(c) for _, b, c in ev]
+    step_ms = wall * 1e3 / args.steps
+    per_call = 2 * s.transfer_bytes           # read + write of every payload byte
+    out = {
+        "step_bytes": 2 * per_call, "step_ms": step_ms,
+        "gather": _stats(g_ms, per_call), "scatter": _stats(s_ms, per_call),
+        "ids_sha256": synth.sha256(ids_np),
+        "ids_distinct": int(len(np.unique(ids_np))),
+    }
+    # CPU oracle on a bounded sample of the same workload
+    if not args.skip_cpu:
+        out["cpu"] = cpu_baseline_kv(torch, synth, s, ra, ids_np)
+    del pool_a, pool_b, buf, ra, rb
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_baseline_kv(torch, synth, s, regions_dev, ids_np, n_sample=512, min_seconds=10.0):
+    """The oracle's gather + scatter on host copies of the first n_sample ids'
+    blocks (all 64 regions), placed at random positions of a 1024-block host
+    pool per region; repeated until min_seconds of CPU work."""
+    import oracle
+    B, R = s.block_bytes, s.num_regions
+    nbh = 1024
+    sample = ids_np[:n_sample]
+    rng = np.random.default_rng(7)
+    pos = rng.choice(nbh, size=n_sample, replace=False).astype(np.int32)
+    host_a = []
+    for r in range(R):
+        blocks = regions_dev[r].view(s.num_blocks, B)[torch.from_numpy(sample.astype(np.int64)).cuda()]
+        h = np.zeros((nbh, B), dtype=np.uint8)
+        h[pos] = blocks.cpu().numpy()
+        host_a.append(h.reshape(-1))
+    host_b = [np.full(nbh * B, 0xA5, dtype=np.uint8) for _ in range(R)]
+    per_rep = 2 * 2 * n_sample * R * B
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        buf = oracle.gather_blocks(host_a, B, B, pos)
+        oracle.scatter_blocks(host_b, B, B, pos, buf)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds:
+            break
+    gbs = per_rep * reps / el / 1e9
+    return {"value": round(gbs, 2), "unit": "GB/s", "cores": oracle.threads(), "kind": "oracle",
+            "sample": (f"gather+scatter of the first {n_sample} of the 4096 ids x {R} regions x "
+                       f"{B} B ({per_rep / 1e9:.2f} GB algorithmic per repetition) between host pools of "
+                       f"{nbh} blocks per region; {reps} repetitions in {el:.1f} s"),
+            "cpu_model": _cpu_model()}
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def run_reshard(torch, tc, synth, args, stream):
+    from paper_2608_06007_amd import views as tcv
+    tp, rank = 8, 3
+    spec = synth.spec_8b(32)
+    n = synth.spec_elems(spec)
+    _log(f"[reshard] 8B-shaped bf16 stream {n * 2 / 1e9:.2f} GB -> TP={tp} rank {rank}")
+    stream_t = synth.bf16_normal(n, 1.0, synth.SEED_RESHARD_8B, device="cuda")
+    frags_np = tc.tc_tp_fragments(tcv.stream_views(spec, tp), tp, rank)
+    frags = torch.from_numpy(frags_np.view(np.int64)).cuda()
+    ws = torch.empty(tc.tc_copy_fragments_workspace(len(frags_np)), dtype=torch.uint8, device="cuda")
+    shard = torch.empty(tcv.shard_elems(spec, tp), dtype=torch.bfloat16, device="cuda")
+    nbytes = 2 * int(frags_np[:, 2].sum())
+    tc.tc_plan_fragments(frags, ws, stream=stream)
+    planned = _time_calls(torch, stream, lambda: tc.tc_copy_planned(stream_t, shard, frags, ws, stream=stream),
+                          args.warmup, args.cast_steps)
+    full = _time_calls(torch, stream, lambda: tc.tc_copy_fragments(stream_t, shard, frags, ws, stream=stream),
+                       args.warmup, args.cast_steps)
+    out = {"fragments": int(len(frags_np)), "copy_planned": _stats(planned, nbytes),
+           "plan_and_copy": _stats(full, nbytes)}
+    del stream_t, shard, frags, ws
+    torch.cuda.empty_cache()
+    return out
+
+
+def run_cast(torch, tc, synth, args, stream):
+    from paper_2608_06007_amd import views as tcv
+    tp, rank = 8, 3
+    spec = synth.spec_70b(80)
+    n = synth.spec_elems(spec)
+    _log(f"[cast] 70B-shaped bf16 weights {n * 2 / 1e9:.1f} GB -> TP={tp} rank {rank} e4m3 + scales")
+    src = synth.bf16_normal(n, 0.02, synth.SEED_CAST_70B, device="cuda")
+    items = tcv.cast_items(spec, tp, rank)
+    shard_n = tcv.shard_elems(spec, tp)
+    n_scales = tcv.scale_elems(spec, tp)
+    q = torch.empty(shard_n, dtype=torch.uint8, device="cuda")
+    sc = torch.empty(n_scales, dtype=torch.float32, device="cuda")
+    ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device="cuda")
+    it = torch.from_numpy(items.view(np.uint8)).cuda()
+    nbytes = 2 * shard_n + shard_n + 4 * n_scales
+    ms = _time_calls(torch, stream, lambda: tc.tc_cast_fp8_blockscaled(src, q, sc, it, ws, stream=stream),
+                     args.warmup, args.cast_steps)
+    out = {"items": int(len(items)), "tiles": int(n_scales), "cast": _stats(ms, nbytes)}
+    del src, q, sc, ws, it
+    torch.cuda.empty_cache()
+    return out
+
+
+def run_storm(torch, tc, synth, args, stream):
+    pool = 16 << 30
+    frags_np = synth.fragment_storm(1_000_000, pool, seed=synth.SEED_STORM)
+    _log(f"[storm] 1,000,000 fragments, {frags_np[:, 2].sum() / 1e9:.2f} GB payload, 16 GiB pools")
+    src = synth.random_bytes(pool, synth.SEED_STORM, device="cuda")
+    dst = torch.empty(pool, dtype=torch.uint8, device="cuda")
+    frags = torch.from_numpy(frags_np.view(np.int64)).cuda()
+    ws = torch.empty(tc.tc_copy_fragments_workspace(len(frags_np)), dtype=torch.uint8, device="cuda")
+    nbytes = 2 * int(frags_np[:, 2].sum())
+    ms = _time_calls(torch, stream, lambda: tc.tc_copy_fragments(src, dst, frags, ws, stream=stream),
+                     args.warmup, args.cast_steps)
+    out = {"fragments": 1_000_000, "payload_bytes": int(frags_np[:, 2].sum()),
+           "plan_and_copy": _stats(ms, nbytes), "descriptors_sha256": synth.sha256(frags_np)}
+    del src, dst, frags, ws
+    torch.cuda.empty_cache()
+    return out
+
+
+def run_moe(torch, tc, synth, args, stream):
+    n_exp, e_bytes = 256, 7168 * 2048
+    frags_np, _ = synth.moe_permutation(n_exp, e_bytes, seed=synth.SEED_STORM)
+    _log(f"[moe] {n_exp} experts x {e_bytes} B permutation")
+    src = synth.random_bytes(n_exp * e_bytes, 40, device="cuda")
+    dst = torch.empty_like(src)
+    frags = torch.from_numpy(frags_np.view(np.int64)).cuda()
+    ws = torch.empty(tc.tc_copy_fragments_workspace(n_exp), dtype=torch.uint8, device="cuda")
+    nbytes = 2 * n_exp * e_bytes
+    ms = _time_calls(torch, stream, lambda: tc.tc_copy_fragments(src, dst, frags, ws, stream=stream),
+                     args.warmup, args.cast_steps)
+    out = {"plan_and_copy": _stats(ms, nbytes)}
+    del src, dst, frags, ws
+    torch.cuda.empty_cache()
+    return out
+
+
+RUNNERS = {"reshard": run_reshard, "cast": run_cast, "storm": run_storm, "moe": run_moe}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cast-steps", type=int, default=20, help="timed launches per extra workload")
+    ap.add_argument("--workloads", default="kv,reshard,cast,storm,moe")
+    ap.add_argument("--skip-cpu", action="store_true", help="skip the CPU oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    import paper_2608_06007_amd as tc
+    tc.load()  # fails loudly if the HIP library is missing
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    wl = [w for w in args.workloads.split(",") if w]
+    src_hash = _kernel_source_hash()
+
+    kv = run_kv(torch, tc, synth, args, stream) if "kv" in wl else None
+    extra = {}
+    for name in wl:
+        if name in RUNNERS:
+            extra[name] = RUNNERS[name](torch, tc, synth, args, stream)
+
+    result = {"metric": "achieved HBM GB/s (and % of peak) for KV block gather/scatter and weight reshard",
+              "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+              "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u8",
+              "data": "synthetic (seeded bf16 N(0,1) KV pools, Zipf(1.1) prefix-reuse ids)"}
+    if kv is not None:
+        value = kv["step_bytes"] / (kv["step_ms"] * 1e-3) / 1e9
+        dom = "gather" if kv["gather"]["ms_median"] >= kv["scatter"]["ms_median"] else "scatter"
+        mean_ms = kv[dom]["ms_median"]
+        ach = kv[dom]["algorithmic_bytes"] / (mean_ms * 1e-3) / 1e9
+        result.update({
+            "value": round(value, 1), "ms_per_step": round(kv["step_ms"], 4),
+            "config": {"workload": "Llama-3-8B-shaped paged KV publish+hydrate: 32 layers x K/V, "
+                                   "8 KV heads, head_dim 128, 16-token bf16 blocks (32 KiB), "
+                                   "32768 blocks/region (64 GiB pool), 4096 Zipf(1.1) ids -> 8 GiB buffer -> pool B",
+                       "bytes_per_step": kv["step_bytes"], "ids_sha256": kv["ids_sha256"]},
+            "roofline": {"bound": "hbm", "kernel": f"k_blocks_vec ({dom})", "achieved": round(ach, 1),
+                         "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+                         "traffic": _traffic(dom, src_hash)},
+            "kernels": {"gather": kv["gather"], "scatter": kv["scatter"]},
+        })
+        if "cpu" in kv:
+            result["cpu_baseline"] = kv["cpu"]
+    result["workloads"] = extra
+    result["kernel_source_sha256"] = src_hash
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

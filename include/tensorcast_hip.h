@@ -1,0 +1,226 @@
+/*
+ * tensorcast_hip.h -- C ABI of the MI355X (gfx950) data path beneath the
+ * tensor lifecycle primitives of TensorCast (arXiv 2608.06007).
+ *
+ * The paper's runtime moves tensor states between engine-resident layouts and
+ * transfer locations: a request's paged KV blocks are exported with publish()
+ * and loaded back with hydrate(); a tensor-parallel rank materializes only
+ * its slice of each weight through view(slice) + tensor_dict(); replicas move
+ * in batches through prefetch_many(); transform_into() transforms a tensor by
+ * a `spec` rule while filling an instance-owned buffer (Sec. 3.2, Table 2).
+ * This library is the device-side hot path of those operations: descriptor
+ * driven gathers and scatters between device layouts and contiguous buffers,
+ * plus a bf16 -> fp8 E4M3 cast with one fp32 scale per 128x128 tile as one
+ * concrete transform_into rule.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers are DEVICE pointers unless a comment says "host".  All device
+ *   buffers belong to the caller (the paper's caller-leased ownership,
+ *   Sec. 3.2 "Artifact") and must stay valid until the work enqueued on
+ *   `stream` has completed.  The library keeps no pointer after returning.
+ * - Calls are asynchronous and stream-ordered: they validate arguments on the
+ *   host, enqueue kernels on `stream` and return.  n == 0 enqueues nothing.
+ * - Calls are pure functions of their inputs, so re-running one after a
+ *   failure is safe (the paper's idempotent retry, Sec. 3.2 "Plan").
+ * - Errors: TC_ERR_INVALID_ARGUMENT for null pointers, negative sizes and
+ *   geometry that cannot be valid; TC_ERR_WORKSPACE for a workspace that is
+ *   too small; TC_ERR_HIP when the HIP runtime rejects a launch (the HIP
+ *   error code is then available from tc_last_hip_error()).  With validation
+ *   on (tc_set_validate(1) or TC_VALIDATE=1 in the environment) the calls
+ *   also copy the descriptors to the host, synchronize the stream, and
+ *   report ids out of range (TC_ERR_OUT_OF_RANGE) and aliasing writes
+ *   (TC_ERR_ALIAS) before launching; without it those are preconditions.
+ */
+#ifndef TENSORCAST_HIP_H
+#define TENSORCAST_HIP_H
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TC_OK = 0,
+  TC_ERR_INVALID_ARGUMENT = 1,
+  TC_ERR_OUT_OF_RANGE = 2,
+  TC_ERR_ALIAS = 3,
+  TC_ERR_HIP = 4,
+  TC_ERR_WORKSPACE = 5
+} tc_status;
+
+/* Largest number of regions a block pool may have. */
+#define TC_MAX_REGIONS 256
+
+/* ------------------------------------------------------------------------
+ * Paged KV blocks: publish / hydrate (Sec. 3.2 "Operation", Table 2;
+ * KV pages as high-cardinality Artifacts, Sec. 4.2 and Sec. 6.3)
+ *
+ * An engine keeps its KV cache in `num_regions` regions (one per layer and
+ * K|V; region r = 2*layer + kv).  Inside a region, block b starts at byte
+ * b * block_stride and holds block_bytes bytes.  Regions may be separate
+ * allocations, or views into one allocation (for [2][blocks][...] or
+ * [blocks][2][...] engine layouts, choose base and stride accordingly).
+ * The transfer buffer is id-major, then region-major: the block of id i in
+ * region r sits at byte (i * num_regions + r) * block_bytes, so one block's
+ * KV for all layers is contiguous.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  const uint64_t* region_base; /* host array [num_regions]: device address of each region */
+  int32_t num_regions;         /* 1 .. TC_MAX_REGIONS */
+  int64_t num_blocks;          /* blocks per region; ids must lie in [0, num_blocks) */
+  int64_t block_bytes;         /* bytes per block and region, > 0 */
+  int64_t block_stride;        /* bytes between consecutive blocks, >= block_bytes */
+} tc_block_pool;
+
+/* publish: out[i][r][0:B] = region_r[ids[i]*stride : +B] for i < n, r < R.
+ * ids: device int32[n]; repeated ids are allowed.  out: device buffer of
+ * n * num_regions * block_bytes bytes that must not overlap the pool. */
+tc_status tc_gather_blocks(const tc_block_pool* pool, const int32_t* ids, int64_t n,
+                           void* out, hipStream_t stream);
+
+/* hydrate: region_r[ids[i]*stride : +B] = in[i][r][0:B] for i < n, r < R.
+ * ids must be distinct (else the result depends on write order; checked as
+ * TC_ERR_ALIAS in validation mode).  in must not overlap the pool. */
+tc_status tc_scatter_blocks(const tc_block_pool* pool, const int32_t* ids, int64_t n,
+                            const void* in, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Fragment lists: batched replica moves (prefetch_many, Table 2) and the
+ * transfer stage of the materialization pipeline (Sec. 5).
+ *
+ * Each descriptor copies len bytes from src_base + src_off to
+ * dst_base + dst_off.  Destination ranges must be pairwise disjoint and must
+ * not overlap any source range (this is a copy, not a memmove).  There is no
+ * alignment requirement; 16-byte-aligned fragments take the fast path.
+ * len == 0 is allowed.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  uint64_t src_off; /* bytes from src_base */
+  uint64_t dst_off; /* bytes from dst_base */
+  uint64_t len;     /* bytes */
+} tc_fragment;
+
+/* Bytes of device workspace tc_copy_fragments / tc_plan_fragments need for
+ * n descriptors (the per-fragment work plan). */
+size_t tc_copy_fragments_workspace(int64_t n);
+
+/* Copy every fragment.  frags: device tc_fragment[n].  workspace: device
+ * buffer of at least tc_copy_fragments_workspace(n) bytes, used for the work
+ * plan (fragments cut into pieces of at most 16 KiB, balanced over the whole
+ * GPU).  The call plans and copies; its workspace may be reused as soon as
+ * the stream has passed the call. */
+tc_status tc_copy_fragments(const void* src_base, void* dst_base, const tc_fragment* frags,
+                            int64_t n, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream);
+
+/* Split planning from copying for descriptor lists that are reused (a
+ * rank's weight-slice list is fixed for a model): tc_plan_fragments writes
+ * the plan for frags into workspace; tc_copy_planned then copies using that
+ * plan, as often as wanted, while frags and workspace stay unchanged. */
+tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream);
+tc_status tc_copy_planned(const void* src_base, void* dst_base, const tc_fragment* frags,
+                          int64_t n, const void* workspace, size_t workspace_bytes,
+                          hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Tensor-parallel views: view(slice) + tensor_dict() (Table 2; each rank
+ * retrieves only its slice of every weight, Sec. 6.1 and 6.2).
+ *
+ * A weight is a row-major matrix [rows][cols] of elem_bytes-byte elements
+ * in a source buffer.  `split` says which of its dimensions the
+ * tensor-parallel group divides: TC_SPLIT_ROWS gives rank r the rows
+ * [r*rows/tp, (r+1)*rows/tp) (column-parallel layers), TC_SPLIT_COLS the
+ * columns [r*cols/tp, (r+1)*cols/tp) (row-parallel layers), TC_SPLIT_NONE the
+ * whole matrix.  The rank's slice is written densely row-major at dst_off
+ * with row stride dst_ld elements.
+ * These two builders run on the host and only describe the moves.
+ * ------------------------------------------------------------------------ */
+typedef enum { TC_SPLIT_NONE = 0, TC_SPLIT_ROWS = 1, TC_SPLIT_COLS = 2 } tc_split;
+
+typedef struct {
+  uint64_t src_off;   /* byte offset of element [0][0] of the full matrix */
+  int64_t rows, cols; /* full matrix shape in elements */
+  int64_t src_ld;     /* elements between source rows (>= cols) */
+  uint64_t dst_off;   /* byte offset of the rank's slice in the destination */
+  int64_t dst_ld;     /* elements between destination rows (>= slice cols) */
+  int32_t elem_bytes; /* 1, 2, 4 or 8 */
+  int32_t split;      /* tc_split */
+} tc_tp_view;
+
+/* Host: number of fragments tc_tp_fragments produces for these views
+ * (-1 on invalid arguments: tp < 1, rank outside [0, tp), a split dimension
+ * not divisible by tp, ld too small, bad elem_bytes). */
+int64_t tc_tp_fragment_count(const tc_tp_view* views /* host */, int64_t n_views, int32_t tp,
+                             int32_t rank);
+
+/* Host: write the fragments that materialize rank `rank`'s slices into
+ * out (host array with room for `capacity` entries); *written receives the
+ * count.  Rows that are contiguous in both source and destination are merged
+ * into one fragment. */
+tc_status tc_tp_fragments(const tc_tp_view* views /* host */, int64_t n_views, int32_t tp,
+                          int32_t rank, tc_fragment* out /* host */, int64_t capacity,
+                          int64_t* written /* host */);
+
+/* ------------------------------------------------------------------------
+ * transform_into with an fp8 spec (Table 2, Sec. 3.2): bf16 -> OCP FP8 E4M3
+ * with one fp32 scale per 128x128 tile, for weight synchronization
+ * (Sec. 6.2).  The paper fixes no numeric format; this rule is:
+ *   per tile (edge tiles partial), amax = max |x| over its elements;
+ *   finite tile, amax > 0: s = RN_f32(amax / 448), q = E4M3(RN_f32(x / s));
+ *   finite tile, amax = 0: s = 0, q = sign bit of x (0x00 or 0x80);
+ *   tile holding Inf/NaN:  s = NaN (0x7FC00000), every q = 0x7F.
+ * E4M3(v): nearest finite E4M3 value with ties to even mantissa, |v| >= 448
+ * saturating to +-448 (0x7E/0xFE), NaN -> 0x7F.  x / s is a correctly
+ * rounded binary32 division; subnormal scales are kept.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  uint64_t src_off;   /* bf16 elements from src_base to element [0][0] */
+  int64_t rows, cols; /* matrix shape (elements) */
+  int64_t src_ld;     /* bf16 elements between source rows (>= cols) */
+  uint64_t dst_off;   /* bytes from dst_base to code [0][0] */
+  int64_t dst_ld;     /* bytes between destination rows (>= cols) */
+  uint64_t scale_off; /* floats from scale_base to scale [0][0] */
+  int64_t scale_ld;   /* floats between rows of the scale grid (>= ceil(cols/128)) */
+} tc_cast_item;
+
+/* Host: the cast item for rank `rank`'s slice of a bf16 weight described by
+ * a view (elem_bytes must be 2; view.dst_off is taken as the code offset in
+ * bytes), with its scale grid at scale_off (row stride = its tile columns).
+ * Returns TC_ERR_INVALID_ARGUMENT for the same reasons as
+ * tc_tp_fragment_count. */
+tc_status tc_tp_cast_item(const tc_tp_view* view /* host */, int32_t tp, int32_t rank,
+                          uint64_t scale_off, tc_cast_item* out /* host */);
+
+/* Bytes of device workspace tc_cast_fp8_blockscaled needs for n items. */
+size_t tc_cast_fp8_workspace(int64_t n_items);
+
+/* Cast every item.  items: device tc_cast_item[n_items].  Destination codes
+ * and scale grids of different items must not overlap.  tile must be 128.
+ * Source rows are read through src_ld, so a strided slice of a full weight
+ * is cast in place without a gather. */
+tc_status tc_cast_fp8_blockscaled(const void* src_base, void* dst_base, float* scale_base,
+                                  const tc_cast_item* items, int64_t n_items, int32_t tile,
+                                  void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* q[i] = E4M3(RN_f32(bf16(src[i]) / scale)) for i < n, one given scale (no
+ * amax).  Quotients that overflow saturate; NaN gives 0x7F. */
+tc_status tc_cast_fp8_scaled(const void* src_bf16, int64_t n, float scale, void* dst_e4m3,
+                             hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+const char* tc_status_string(tc_status status);
+/* hipError_t of the most recent TC_ERR_HIP on the calling thread. */
+int tc_last_hip_error(void);
+/* 1: validate descriptors (synchronous, for debugging); 0: off. */
+void tc_set_validate(int on);
+int tc_get_validate(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TENSORCAST_HIP_H */

@@ -1,0 +1,299 @@
+"""MI355X (gfx950) data path beneath TensorCast's tensor lifecycle primitives.
+
+A thin ctypes binding over ``libtchip.so`` (built from ``csrc/`` by
+``build.py``).  The functions keep the C ABI's names and only marshal
+arguments: torch tensors supply device memory and streams, and every byte
+the path moves is moved by the library's HIP kernels.  There is no CPU
+fallback: if the library is missing, every call raises.
+
+Entry points (see include/tensorcast_hip.h for the contracts):
+
+* ``tc_gather_blocks`` / ``tc_scatter_blocks`` -- publish / hydrate of a
+  request's paged KV blocks (paper Sec. 3.2 "Operation", Table 2).
+* ``tc_copy_fragments`` (+ ``tc_plan_fragments`` / ``tc_copy_planned``) --
+  batched byte fragments, as in prefetch_many and the materialization
+  transfer stage (Table 2, Sec. 5).
+* ``tc_tp_fragments`` / ``tc_tp_cast_item`` -- host builders that describe a
+  tensor-parallel rank's view(slice) of each weight (Table 2, Sec. 6.1-6.2).
+* ``tc_cast_fp8_blockscaled`` / ``tc_cast_fp8_scaled`` -- a transform_into
+  rule: bf16 -> fp8 E4M3 with an fp32 scale per 128x128 tile.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+__all__ = [
+    "TcError", "lib_path", "load",
+    "tc_gather_blocks", "tc_scatter_blocks",
+    "tc_copy_fragments_workspace", "tc_copy_fragments", "tc_plan_fragments", "tc_copy_planned",
+    "tc_tp_fragment_count", "tc_tp_fragments", "tc_tp_cast_item",
+    "tc_cast_fp8_workspace", "tc_cast_fp8_blockscaled", "tc_cast_fp8_scaled",
+    "tc_status_string", "tc_last_hip_error", "tc_set_validate", "tc_get_validate",
+    "FRAGMENT_DTYPE", "TP_VIEW_DTYPE", "CAST_ITEM_DTYPE",
+    "SPLIT_NONE", "SPLIT_ROWS", "SPLIT_COLS", "MAX_REGIONS",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+lib_path = os.path.join(_HERE, "libtchip.so")
+
+MAX_REGIONS = 256
+SPLIT_NONE, SPLIT_ROWS, SPLIT_COLS = 0, 1, 2
+TC_OK = 0
+_STATUS = {0: "TC_OK", 1: "TC_ERR_INVALID_ARGUMENT", 2: "TC_ERR_OUT_OF_RANGE", 3: "TC_ERR_ALIAS",
+           4: "TC_ERR_HIP", 5: "TC_ERR_WORKSPACE"}
+
+# Host layouts of the C structs.
+FRAGMENT_DTYPE = np.dtype([("src_off", "<u8"), ("dst_off", "<u8"), ("len", "<u8")])
+TP_VIEW_DTYPE = np.dtype([("src_off", "<u8"), ("rows", "<i8"), ("cols", "<i8"), ("src_ld", "<i8"),
+                          ("dst_off", "<u8"), ("dst_ld", "<i8"), ("elem_bytes", "<i4"),
+                          ("split", "<i4")])
+CAST_ITEM_DTYPE = np.dtype([("src_off", "<u8"), ("rows", "<i8"), ("cols", "<i8"), ("src_ld", "<i8"),
+                            ("dst_off", "<u8"), ("dst_ld", "<i8"), ("scale_off", "<u8"),
+                            ("scale_ld", "<i8")])
+
+
+class TcError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        name = _STATUS.get(status, str(status))
+        extra = ""
+        if status == 4:
+            extra = f" (hipError {load().tc_last_hip_error()})"
+        super().__init__(f"{what}: {name}{extra}")
+
+
+class _BlockPool(ctypes.Structure):
+    _fields_ = [("region_base", ctypes.POINTER(ctypes.c_uint64)), ("num_regions", ctypes.c_int32),
+                ("num_blocks", ctypes.c_int64), ("block_bytes", ctypes.c_int64),
+                ("block_stride", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def load():
+    """Load libtchip.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(lib_path):
+        raise RuntimeError(f"{lib_path} is missing: build it with paper_2608_06007_amd/build.py")
+    L = ctypes.CDLL(lib_path)
+    c = ctypes
+    P = c.c_void_p
+    L.tc_gather_blocks.argtypes = [c.POINTER(_BlockPool), P, c.c_int64, P, P]
+    L.tc_scatter_blocks.argtypes = [c.POINTER(_BlockPool), P, c.c_int64, P, P]
+    L.tc_copy_fragments_workspace.argtypes = [c.c_int64]
+    L.tc_copy_fragments_workspace.restype = c.c_size_t
+    L.tc_copy_fragments.argtypes = [P, P, P, c.c_int64, P, c.c_size_t, P]
+    L.tc_plan_fragments.argtypes = [P, c.c_int64, P, c.c_size_t, P]
+    L.tc_copy_planned.argtypes = [P, P, P, c.c_int64, P, c.c_size_t, P]
+    L.tc_tp_fragment_count.argtypes = [P, c.c_int64, c.c_int32, c.c_int32]
+    L.tc_tp_fragment_count.restype = c.c_int64
+    L.tc_tp_fragments.argtypes = [P, c.c_int64, c.c_int32, c.c_int32, P, c.c_int64,
+                                  c.POINTER(c.c_int64)]
+    L.tc_tp_cast_item.argtypes = [P, c.c_int32, c.c_int32, c.c_uint64, P]
+    L.tc_cast_fp8_workspace.argtypes = [c.c_int64]
+    L.tc_cast_fp8_workspace.restype = c.c_size_t
+    L.tc_cast_fp8_blockscaled.argtypes = [P, P, P, P, c.c_int64, c.c_int32, P, c.c_size_t, P]
+    L.tc_cast_fp8_scaled.argtypes = [P, c.c_int64, c.c_float, P, P]
+    L.tc_status_string.argtypes = [c.c_int]
+    L.tc_status_string.restype = c.c_char_p
+    L.tc_last_hip_error.restype = c.c_int
+    L.tc_set_validate.argtypes = [c.c_int]
+    L.tc_get_validate.restype = c.c_int
+    for name in ("tc_gather_blocks", "tc_scatter_blocks", "tc_copy_fragments", "tc_plan_fragments",
+                 "tc_copy_planned", "tc_tp_fragments", "tc_tp_cast_item", "tc_cast_fp8_blockscaled",
+                 "tc_cast_fp8_scaled"):
+        getattr(L, name).restype = c.c_int
+    _lib = L
+    return L
+
+
+def _ok(status: int, what: str) -> None:
+    if status != TC_OK:
+        raise TcError(status, what)
+
+
+def _dev_ptr(x) -> int:
+    """Device address of a torch tensor (must live on a GPU) or a raw int."""
+    if isinstance(x, int):
+        return x
+    if not x.is_cuda:
+        raise ValueError("expected a device tensor")
+    return x.data_ptr()
+
+
+def _stream(stream) -> int:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
+# ---------------------------------------------------------------------------
+# publish / hydrate
+# ---------------------------------------------------------------------------
+
+def _pool(regions, num_blocks: int, block_bytes: int, block_stride: int):
+    bases = [_dev_ptr(r) for r in regions]
+    arr = (ctypes.c_uint64 * len(bases))(*bases)
+    pool = _BlockPool(ctypes.cast(arr, ctypes.POINTER(ctypes.c_uint64)), len(bases), num_blocks,
+                      block_bytes, block_stride)
+    return pool, arr
+
+
+def tc_gather_blocks(regions, num_blocks: int, block_bytes: int, block_stride: int, ids, out,
+                     stream=None) -> None:
+    """out[i, r, :block_bytes] = regions[r][ids[i]*stride : +block_bytes] on the device.
+
+    ``regions``: list of device tensors or device addresses (one per layer and
+    K|V); ``ids``: device int32 tensor; ``out``: device tensor of
+    len(ids) * len(regions) * block_bytes bytes."""
+    pool, keep = _pool(regions, num_blocks, block_bytes, block_stride)
+    n = ids.numel()
+    if n and _nbytes(out) < n * len(keep) * block_bytes:
+        raise ValueError("output buffer too small")
+    _ok(load().tc_gather_blocks(ctypes.byref(pool), _dev_ptr(ids) if n else None, n,
+                                _dev_ptr(out) if n else None, _stream(stream)), "tc_gather_blocks")
+
+
+def tc_scatter_blocks(regions, num_blocks: int, block_bytes: int, block_stride: int, ids, inp,
+                      stream=None) -> None:
+    """regions[r][ids[i]*stride : +block_bytes] = inp[i, r, :] on the device (ids distinct)."""
+    pool, keep = _pool(regions, num_blocks, block_bytes, block_stride)
+    n = ids.numel()
+    if n and _nbytes(inp) < n * len(keep) * block_bytes:
+        raise ValueError("input buffer too small")
+    _ok(load().tc_scatter_blocks(ctypes.byref(pool), _dev_ptr(ids) if n else None, n,
+                                 _dev_ptr(inp) if n else None, _stream(stream)), "tc_scatter_blocks")
+
+
+# ---------------------------------------------------------------------------
+# fragments
+# ---------------------------------------------------------------------------
+
+def tc_copy_fragments_workspace(n: int) -> int:
+    return int(load().tc_copy_fragments_workspace(int(n)))
+
+
+def _frag_count(frags) -> int:
+    nb = _nbytes(frags)
+    if nb % 24:
+        raise ValueError("fragment tensor is not a whole number of (src_off, dst_off, len) rows")
+    return nb // 24
+
+
+def tc_copy_fragments(src, dst, frags, workspace, stream=None) -> None:
+    """Copy every (src_off, dst_off, len) row of the device tensor ``frags``
+    (uint64/int64, shape [n, 3]) from ``src`` to ``dst``."""
+    n = _frag_count(frags)
+    _ok(load().tc_copy_fragments(_dev_ptr(src), _dev_ptr(dst), _dev_ptr(frags) if n else None, n,
+                                 _dev_ptr(workspace), _nbytes(workspace), _stream(stream)),
+        "tc_copy_fragments")
+
+
+def tc_plan_fragments(frags, workspace, stream=None) -> None:
+    n = _frag_count(frags)
+    _ok(load().tc_plan_fragments(_dev_ptr(frags) if n else None, n, _dev_ptr(workspace),
+                                 _nbytes(workspace), _stream(stream)), "tc_plan_fragments")
+
+
+def tc_copy_planned(src, dst, frags, workspace, stream=None) -> None:
+    n = _frag_count(frags)
+    _ok(load().tc_copy_planned(_dev_ptr(src), _dev_ptr(dst), _dev_ptr(frags) if n else None, n,
+                               _dev_ptr(workspace), _nbytes(workspace), _stream(stream)),
+        "tc_copy_planned")
+
+
+# ---------------------------------------------------------------------------
+# tensor-parallel views (host builders)
+# ---------------------------------------------------------------------------
+
+def _views(views) -> np.ndarray:
+    v = np.ascontiguousarray(views, dtype=TP_VIEW_DTYPE).reshape(-1)
+    return v
+
+
+def tc_tp_fragment_count(views, tp: int, rank: int) -> int:
+    v = _views(views)
+    n = int(load().tc_tp_fragment_count(v.ctypes.data if v.size else None, v.size, tp, rank))
+    if n < 0:
+        raise TcError(1, "tc_tp_fragment_count")
+    return n
+
+
+def tc_tp_fragments(views, tp: int, rank: int) -> np.ndarray:
+    """Fragments (uint64 [m, 3]) that copy rank ``rank``'s slices."""
+    v = _views(views)
+    m = tc_tp_fragment_count(v, tp, rank)
+    out = np.zeros((m, 3), dtype=np.uint64)
+    written = ctypes.c_int64(0)
+    _ok(load().tc_tp_fragments(v.ctypes.data if v.size else None, v.size, tp, rank,
+                               out.ctypes.data if m else None, m, ctypes.byref(written)),
+        "tc_tp_fragments")
+    return out[:written.value]
+
+
+def tc_tp_cast_item(view, tp: int, rank: int, scale_off: int) -> np.ndarray:
+    """The cast item (CAST_ITEM_DTYPE record) for a rank's slice of a bf16 weight."""
+    v = _views([view] if np.ndim(view) == 0 else view)
+    assert v.size == 1
+    out = np.zeros(1, dtype=CAST_ITEM_DTYPE)
+    _ok(load().tc_tp_cast_item(v.ctypes.data, tp, rank, scale_off, out.ctypes.data),
+        "tc_tp_cast_item")
+    return out[0]
+
+
+# ---------------------------------------------------------------------------
+# transform_into: fp8 cast
+# ---------------------------------------------------------------------------
+
+def tc_cast_fp8_workspace(n_items: int) -> int:
+    return int(load().tc_cast_fp8_workspace(int(n_items)))
+
+
+def tc_cast_fp8_blockscaled(src, dst, scales, items, workspace, stream=None, tile: int = 128) -> None:
+    """Cast every item; ``items`` is a device tensor holding CAST_ITEM_DTYPE
+    records (64 bytes each)."""
+    nb = _nbytes(items)
+    if nb % CAST_ITEM_DTYPE.itemsize:
+        raise ValueError("items tensor is not a whole number of records")
+    n = nb // CAST_ITEM_DTYPE.itemsize
+    _ok(load().tc_cast_fp8_blockscaled(_dev_ptr(src), _dev_ptr(dst), _dev_ptr(scales),
+                                       _dev_ptr(items) if n else None, n, tile, _dev_ptr(workspace),
+                                       _nbytes(workspace), _stream(stream)),
+        "tc_cast_fp8_blockscaled")
+
+
+def tc_cast_fp8_scaled(src, scale: float, dst, stream=None) -> None:
+    """dst[i] = E4M3(RN_f32(src[i] / scale)) for a bf16 device tensor ``src``."""
+    n = src.numel()
+    _ok(load().tc_cast_fp8_scaled(_dev_ptr(src) if n else None, n, float(scale),
+                                  _dev_ptr(dst) if n else None, _stream(stream)),
+        "tc_cast_fp8_scaled")
+
+
+# ---------------------------------------------------------------------------
+
+def tc_status_string(status: int) -> str:
+    return load().tc_status_string(int(status)).decode()
+
+
+def tc_last_hip_error() -> int:
+    return int(load().tc_last_hip_error())
+
+
+def tc_set_validate(on: bool) -> None:
+    load().tc_set_validate(1 if on else 0)
+
+
+def tc_get_validate() -> bool:
+    return bool(load().tc_get_validate())

@@ -1,0 +1,414 @@
+// C ABI of the data path: argument checks, optional validation, launches.
+// Host-only code; the kernels live in tc_moves.hip and tc_cast.hip.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <vector>
+
+#include "tc_internal.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+int g_validate = -1;  // -1: not yet read from the environment
+
+bool validating() {
+  if (g_validate < 0) {
+    const char* e = std::getenv("TC_VALIDATE");
+    g_validate = (e && e[0] && e[0] != '0') ? 1 : 0;
+  }
+  return g_validate == 1;
+}
+
+tc_status hip_fail(hipError_t e) {
+  g_last_hip_error = (int)e;
+  return TC_ERR_HIP;
+}
+
+tc_status check(hipError_t e) { return e == hipSuccess ? TC_OK : hip_fail(e); }
+
+// Copy a device array to the host after the stream has produced it.
+template <typename T>
+tc_status fetch(const T* dev, int64_t n, std::vector<T>* out, hipStream_t s) {
+  out->resize((size_t)n);
+  if (n == 0) return TC_OK;
+  hipError_t e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e);
+  e = hipMemcpy(out->data(), dev, sizeof(T) * (size_t)n, hipMemcpyDeviceToHost);
+  return check(e);
+}
+
+struct Range {
+  uint64_t lo, hi;  // [lo, hi)
+};
+
+// True if any two non-empty ranges overlap.
+bool any_overlap(std::vector<Range> r) {
+  r.erase(std::remove_if(r.begin(), r.end(), [](const Range& x) { return x.hi == x.lo; }), r.end());
+  std::sort(r.begin(), r.end(), [](const Range& a, const Range& b) { return a.lo < b.lo; });
+  for (size_t i = 1; i < r.size(); ++i)
+    if (r[i].lo < r[i - 1].hi) return true;
+  return false;
+}
+
+// True if a range of a overlaps a range of b.
+bool cross_overlap(std::vector<Range> a, std::vector<Range> b) {
+  auto by_lo = [](const Range& x, const Range& y) { return x.lo < y.lo; };
+  auto empty = [](const Range& x) { return x.hi == x.lo; };
+  a.erase(std::remove_if(a.begin(), a.end(), empty), a.end());
+  b.erase(std::remove_if(b.begin(), b.end(), empty), b.end());
+  std::sort(a.begin(), a.end(), by_lo);
+  std::sort(b.begin(), b.end(), by_lo);
+  // sweep: keep the furthest end seen in each list
+  size_t i = 0, j = 0;
+  uint64_t end_a = 0, end_b = 0;
+  while (i < a.size() || j < b.size()) {
+    if (j == b.size() || (i < a.size() && a[i].lo <= b[j].lo)) {
+      if (a[i].lo < end_b) return true;
+      end_a = std::max(end_a, a[i].hi);
+      ++i;
+    } else {
+      if (b[j].lo < end_a) return true;
+      end_b = std::max(end_b, b[j].hi);
+      ++j;
+    }
+  }
+  return false;
+}
+
+bool pool_ok(const tc_block_pool* p) {
+  if (!p || !p->region_base) return false;
+  if (p->num_regions < 1 || p->num_regions > TC_MAX_REGIONS) return false;
+  if (p->num_blocks < 1 || p->block_bytes < 1 || p->block_stride < p->block_bytes) return false;
+  for (int r = 0; r < p->num_regions; ++r)
+    if (p->region_base[r] == 0) return false;
+  return true;
+}
+
+tc_status blocks_common(const tc_block_pool* pool, const int32_t* ids, int64_t n, void* buf,
+                        bool gather, hipStream_t s) {
+  if (n < 0 || !pool_ok(pool)) return TC_ERR_INVALID_ARGUMENT;
+  if (n == 0) return TC_OK;
+  if (!ids || !buf) return TC_ERR_INVALID_ARGUMENT;
+  const int32_t R = pool->num_regions;
+  const int64_t B = pool->block_bytes, stride = pool->block_stride;
+  if (validating()) {
+    std::vector<int32_t> h;
+    tc_status st = fetch(ids, n, &h, s);
+    if (st != TC_OK) return st;
+    std::vector<uint8_t> seen((size_t)pool->num_blocks, 0);
+    for (int32_t id : h) {
+      if (id < 0 || id >= pool->num_blocks) return TC_ERR_OUT_OF_RANGE;
+      if (!gather && seen[(size_t)id]) return TC_ERR_ALIAS;
+      seen[(size_t)id] = 1;
+    }
+    // transfer buffer against the blocks it is exchanged with
+    std::vector<Range> pool_r, buf_r;
+    buf_r.push_back({(uint64_t)(uintptr_t)buf, (uint64_t)(uintptr_t)buf + uint64_t(n * R * B)});
+    for (int r = 0; r < R; ++r) {
+      const uint64_t base = pool->region_base[r];
+      const uint64_t span = uint64_t(pool->num_blocks - 1) * uint64_t(stride) + uint64_t(B);
+      pool_r.push_back({base, base + span});
+    }
+    if (cross_overlap(pool_r, buf_r)) return TC_ERR_ALIAS;
+    if (!gather) {
+      // the blocks written must not overlap one another (regions may share memory)
+      std::vector<Range> w;
+      w.reserve(h.size() * (size_t)R);
+      for (int32_t id : h)
+        for (int r = 0; r < R; ++r) {
+          const uint64_t a = pool->region_base[r] + uint64_t(id) * uint64_t(stride);
+          w.push_back({a, a + uint64_t(B)});
+        }
+      if (any_overlap(w)) return TC_ERR_ALIAS;
+    }
+  }
+  tc::RegionTable tab;
+  bool aligned = (B % 16) == 0 && (stride % 16) == 0 && ((uintptr_t)buf % 16) == 0;
+  for (int r = 0; r < R; ++r) {
+    tab.base[r] = pool->region_base[r];
+    aligned = aligned && (tab.base[r] % 16) == 0;
+  }
+  for (int r = R; r < TC_MAX_REGIONS; ++r) tab.base[r] = 0;
+  return check(tc::launch_blocks(tab, R, B, stride, ids, n, static_cast<uint8_t*>(buf), gather,
+                                 aligned, s));
+}
+
+bool view_ok(const tc_tp_view& v, int32_t tp, int32_t rank) {
+  if (tp < 1 || rank < 0 || rank >= tp) return false;
+  if (v.rows < 0 || v.cols < 0 || v.src_ld < v.cols || v.dst_ld < 0) return false;
+  if (!(v.elem_bytes == 1 || v.elem_bytes == 2 || v.elem_bytes == 4 || v.elem_bytes == 8))
+    return false;
+  if (v.split == TC_SPLIT_ROWS) {
+    if (v.rows % tp) return false;
+    if (v.dst_ld < v.cols) return false;
+  } else if (v.split == TC_SPLIT_COLS) {
+    if (v.cols % tp) return false;
+    if (v.dst_ld < v.cols / tp) return false;
+  } else if (v.split == TC_SPLIT_NONE) {
+    if (v.dst_ld < v.cols) return false;
+  } else {
+    return false;
+  }
+  return true;
+}
+
+// The rank's sub-matrix of a view: first source element, shape.
+struct Slice {
+  uint64_t src_elem;  // element offset from the matrix origin
+  int64_t rows, cols;
+};
+
+Slice slice_of(const tc_tp_view& v, int32_t tp, int32_t rank) {
+  if (v.split == TC_SPLIT_ROWS) {
+    const int64_t k = v.rows / tp;
+    return {uint64_t(rank) * uint64_t(k) * uint64_t(v.src_ld), k, v.cols};
+  }
+  if (v.split == TC_SPLIT_COLS) {
+    const int64_t k = v.cols / tp;
+    return {uint64_t(rank) * uint64_t(k), v.rows, k};
+  }
+  return {0, v.rows, v.cols};
+}
+
+// Fragments of one view: one per row, or one for the whole slice when the
+// rows are contiguous in both source and destination.
+template <typename Emit>
+void view_fragments(const tc_tp_view& v, int32_t tp, int32_t rank, Emit emit) {
+  const Slice sl = slice_of(v, tp, rank);
+  if (sl.rows == 0 || sl.cols == 0) return;
+  const uint64_t eb = uint64_t(v.elem_bytes);
+  const uint64_t row_bytes = uint64_t(sl.cols) * eb;
+  const uint64_t src0 = v.src_off + sl.src_elem * eb;
+  const bool contiguous = (sl.rows == 1) || (v.src_ld == sl.cols && v.dst_ld == sl.cols);
+  if (contiguous) {
+    emit(tc_fragment{src0, v.dst_off, row_bytes * uint64_t(sl.rows)});
+    return;
+  }
+  for (int64_t r = 0; r < sl.rows; ++r)
+    emit(tc_fragment{src0 + uint64_t(r) * uint64_t(v.src_ld) * eb,
+                     v.dst_off + uint64_t(r) * uint64_t(v.dst_ld) * eb, row_bytes});
+}
+
+}  // namespace
+
+namespace tc {
+hipError_t device_info(DeviceInfo* out) {
+  static int cus[64] = {0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  if (cus[dev] == 0) {
+    int c = 0;
+    e = hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    cus[dev] = c > 0 ? c : 1;
+  }
+  out->device = dev;
+  out->cus = cus[dev];
+  return hipSuccess;
+}
+}  // namespace tc
+
+extern "C" {
+
+tc_status tc_gather_blocks(const tc_block_pool* pool, const int32_t* ids, int64_t n, void* out,
+                           hipStream_t stream) {
+  return blocks_common(pool, ids, n, out, true, stream);
+}
+
+tc_status tc_scatter_blocks(const tc_block_pool* pool, const int32_t* ids, int64_t n,
+                            const void* in, hipStream_t stream) {
+  return blocks_common(pool, ids, n, const_cast<void*>(in), false, stream);
+}
+
+size_t tc_copy_fragments_workspace(int64_t n) {
+  if (n < 0) return 0;
+  return tc::frag_workspace_bytes(n);
+}
+
+static tc_status validate_fragments(const void* src_base, const void* dst_base,
+                                    const tc_fragment* frags, int64_t n, hipStream_t s) {
+  std::vector<tc_fragment> h;
+  tc_status st = fetch(frags, n, &h, s);
+  if (st != TC_OK) return st;
+  std::vector<Range> d, sr;
+  d.reserve(h.size());
+  sr.reserve(h.size());
+  const uint64_t sb = (uint64_t)(uintptr_t)src_base, db = (uint64_t)(uintptr_t)dst_base;
+  for (const tc_fragment& f : h) {
+    if (f.src_off + f.len < f.src_off || f.dst_off + f.len < f.dst_off) return TC_ERR_OUT_OF_RANGE;
+    d.push_back({db + f.dst_off, db + f.dst_off + f.len});
+    sr.push_back({sb + f.src_off, sb + f.src_off + f.len});
+  }
+  if (any_overlap(d)) return TC_ERR_ALIAS;
+  if (cross_overlap(d, sr)) return TC_ERR_ALIAS;
+  return TC_OK;
+}
+
+tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+  if (n < 0) return TC_ERR_INVALID_ARGUMENT;
+  if (n == 0) return TC_OK;
+  if (!frags || !workspace) return TC_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < tc::frag_workspace_bytes(n)) return TC_ERR_WORKSPACE;
+  if ((uintptr_t)workspace % 8) return TC_ERR_INVALID_ARGUMENT;
+  return check(tc::launch_plan_fragments(frags, n, workspace, stream));
+}
+
+tc_status tc_copy_planned(const void* src_base, void* dst_base, const tc_fragment* frags,
+                          int64_t n, const void* workspace, size_t workspace_bytes,
+                          hipStream_t stream) {
+  if (n < 0) return TC_ERR_INVALID_ARGUMENT;
+  if (n == 0) return TC_OK;
+  if (!src_base || !dst_base || !frags || !workspace) return TC_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < tc::frag_workspace_bytes(n)) return TC_ERR_WORKSPACE;
+  if ((uintptr_t)workspace % 8) return TC_ERR_INVALID_ARGUMENT;
+  if (validating()) {
+    tc_status st = validate_fragments(src_base, dst_base, frags, n, stream);
+    if (st != TC_OK) return st;
+  }
+  tc::DeviceInfo di;
+  hipError_t e = tc::device_info(&di);
+  if (e != hipSuccess) return hip_fail(e);
+  return check(tc::launch_copy_planned(static_cast<const uint8_t*>(src_base),
+                                       static_cast<uint8_t*>(dst_base), frags, n, workspace, di,
+                                       stream));
+}
+
+tc_status tc_copy_fragments(const void* src_base, void* dst_base, const tc_fragment* frags,
+                            int64_t n, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream) {
+  if (n < 0) return TC_ERR_INVALID_ARGUMENT;
+  if (n == 0) return TC_OK;
+  if (!src_base || !dst_base || !frags || !workspace) return TC_ERR_INVALID_ARGUMENT;
+  tc_status st = tc_plan_fragments(frags, n, workspace, workspace_bytes, stream);
+  if (st != TC_OK) return st;
+  return tc_copy_planned(src_base, dst_base, frags, n, workspace, workspace_bytes, stream);
+}
+
+int64_t tc_tp_fragment_count(const tc_tp_view* views, int64_t n_views, int32_t tp, int32_t rank) {
+  if (n_views < 0 || (n_views > 0 && !views)) return -1;
+  int64_t count = 0;
+  for (int64_t i = 0; i < n_views; ++i) {
+    if (!view_ok(views[i], tp, rank)) return -1;
+    view_fragments(views[i], tp, rank, [&](const tc_fragment&) { ++count; });
+  }
+  return count;
+}
+
+tc_status tc_tp_fragments(const tc_tp_view* views, int64_t n_views, int32_t tp, int32_t rank,
+                          tc_fragment* out, int64_t capacity, int64_t* written) {
+  if (!written || n_views < 0 || (n_views > 0 && !views) || capacity < 0) return TC_ERR_INVALID_ARGUMENT;
+  const int64_t need = tc_tp_fragment_count(views, n_views, tp, rank);
+  if (need < 0) return TC_ERR_INVALID_ARGUMENT;
+  if (need > capacity || (need > 0 && !out)) return TC_ERR_WORKSPACE;
+  int64_t k = 0;
+  for (int64_t i = 0; i < n_views; ++i)
+    view_fragments(views[i], tp, rank, [&](const tc_fragment& f) { out[k++] = f; });
+  *written = k;
+  return TC_OK;
+}
+
+tc_status tc_tp_cast_item(const tc_tp_view* view, int32_t tp, int32_t rank, uint64_t scale_off,
+                          tc_cast_item* out) {
+  if (!view || !out) return TC_ERR_INVALID_ARGUMENT;
+  if (view->elem_bytes != 2 || !view_ok(*view, tp, rank)) return TC_ERR_INVALID_ARGUMENT;
+  if (view->src_off % 2) return TC_ERR_INVALID_ARGUMENT;
+  const Slice sl = slice_of(*view, tp, rank);
+  tc_cast_item it;
+  it.src_off = view->src_off / 2 + sl.src_elem;
+  it.rows = sl.rows;
+  it.cols = sl.cols;
+  it.src_ld = view->src_ld;
+  it.dst_off = view->dst_off;
+  it.dst_ld = view->dst_ld;
+  it.scale_off = scale_off;
+  it.scale_ld = (sl.cols + 127) / 128;
+  *out = it;
+  return TC_OK;
+}
+
+size_t tc_cast_fp8_workspace(int64_t n_items) {
+  if (n_items < 0) return 0;
+  return tc::cast_workspace_bytes(n_items);
+}
+
+tc_status tc_cast_fp8_blockscaled(const void* src_base, void* dst_base, float* scale_base,
+                                  const tc_cast_item* items, int64_t n_items, int32_t tile,
+                                  void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (n_items < 0 || tile != 128) return TC_ERR_INVALID_ARGUMENT;
+  if (n_items == 0) return TC_OK;
+  if (!src_base || !dst_base || !scale_base || !items || !workspace) return TC_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < tc::cast_workspace_bytes(n_items)) return TC_ERR_WORKSPACE;
+  if ((uintptr_t)workspace % 8 || (uintptr_t)src_base % 2 || (uintptr_t)scale_base % 4)
+    return TC_ERR_INVALID_ARGUMENT;
+  if (validating()) {
+    std::vector<tc_cast_item> h;
+    tc_status st = fetch(items, n_items, &h, stream);
+    if (st != TC_OK) return st;
+    std::vector<Range> q, sc, src;
+    const uint64_t db = (uint64_t)(uintptr_t)dst_base, sb = (uint64_t)(uintptr_t)scale_base;
+    const uint64_t xb = (uint64_t)(uintptr_t)src_base;
+    for (const tc_cast_item& it : h) {
+      if (it.rows < 0 || it.cols < 0 || it.src_ld < it.cols || it.dst_ld < it.cols)
+        return TC_ERR_INVALID_ARGUMENT;
+      const int64_t tc_cols = (it.cols + 127) / 128, tr = (it.rows + 127) / 128;
+      if (it.scale_ld < tc_cols) return TC_ERR_INVALID_ARGUMENT;
+      if (it.rows == 0 || it.cols == 0) continue;
+      // destination rows
+      for (int64_t r = 0; r < it.rows; ++r) {
+        const uint64_t a = db + it.dst_off + uint64_t(r) * uint64_t(it.dst_ld);
+        q.push_back({a, a + uint64_t(it.cols)});
+        const uint64_t x = xb + 2 * (it.src_off + uint64_t(r) * uint64_t(it.src_ld));
+        src.push_back({x, x + 2 * uint64_t(it.cols)});
+      }
+      for (int64_t r = 0; r < tr; ++r) {
+        const uint64_t a = sb + 4 * (it.scale_off + uint64_t(r) * uint64_t(it.scale_ld));
+        sc.push_back({a, a + 4 * uint64_t(tc_cols)});
+      }
+    }
+    std::vector<Range> outs = q;
+    outs.insert(outs.end(), sc.begin(), sc.end());
+    if (any_overlap(outs)) return TC_ERR_ALIAS;
+    if (cross_overlap(outs, src)) return TC_ERR_ALIAS;
+  }
+  tc::DeviceInfo di;
+  hipError_t e = tc::device_info(&di);
+  if (e != hipSuccess) return hip_fail(e);
+  return check(tc::launch_cast_blockscaled(static_cast<const uint16_t*>(src_base),
+                                           static_cast<uint8_t*>(dst_base), scale_base, items,
+                                           n_items, workspace, di, stream));
+}
+
+tc_status tc_cast_fp8_scaled(const void* src_bf16, int64_t n, float scale, void* dst_e4m3,
+                             hipStream_t stream) {
+  if (n < 0) return TC_ERR_INVALID_ARGUMENT;
+  if (n == 0) return TC_OK;
+  if (!src_bf16 || !dst_e4m3 || (uintptr_t)src_bf16 % 2) return TC_ERR_INVALID_ARGUMENT;
+  return check(tc::launch_cast_scaled(static_cast<const uint16_t*>(src_bf16), n, scale,
+                                      static_cast<uint8_t*>(dst_e4m3), stream));
+}
+
+const char* tc_status_string(tc_status s) {
+  switch (s) {
+    case TC_OK: return "ok";
+    case TC_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case TC_ERR_OUT_OF_RANGE: return "descriptor out of range";
+    case TC_ERR_ALIAS: return "aliasing writes";
+    case TC_ERR_HIP: return "HIP runtime error";
+    case TC_ERR_WORKSPACE: return "workspace too small";
+  }
+  return "unknown status";
+}
+
+int tc_last_hip_error(void) { return g_last_hip_error; }
+
+void tc_set_validate(int on) { g_validate = on ? 1 : 0; }
+
+int tc_get_validate(void) { return validating() ? 1 : 0; }
+
+}  // extern "C"

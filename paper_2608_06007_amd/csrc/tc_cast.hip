@@ -1,0 +1,330 @@
+// bf16 -> fp8 E4M3 cast with one fp32 scale per 128x128 tile (a
+// transform_into rule for weight synchronization), for gfx950.
+//
+// Per tile: amax from the bf16 bit patterns (|x| as a 15-bit integer, so
+// Inf/NaN are caught by the same max), s = amax / 448 (correctly rounded),
+// then q = E4M3(RN(x / s)).
+//
+// Quotient without a division per element: with r = RN(1/s) (normal s),
+// q0 = RN(x * r) differs from RN(x / s) by at most ~1.5 * 2^-23 relative.
+// lo = RN(q0 * (1 - 2^-20)) and hi = RN(q0 * (1 + 2^-20)) bracket RN(x / s),
+// and the E4M3 rounding is monotonic, so when lo and hi convert to the same
+// code that code is E4M3(RN(x / s)).  Otherwise (within ~2^-20 of a rounding
+// midpoint, about one element in 65536) the element is redone with a true
+// division.  Subnormal scales (tiny amax) use the division throughout.
+//
+// Conversion: v_cvt_pk_fp8_f32 rounds to nearest even into the OCP E4M3
+// format.  For |v| < 464 it equals the saturating E4M3 rounding; the
+// quotients of a finite tile stay below 449 (|x| <= amax and s is amax/448
+// rounded to nearest, worst case a subnormal s with 8 significant bits), and
+// lo/hi stay below 450, so no clamp is needed on this path.
+#include "tc_internal.h"
+
+namespace tc {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kThreads = 256;
+constexpr int kWaveLanes = 64;
+constexpr int kTile = 128;
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Two E4M3 codes packed into bits [15:0] (word 0) or [31:16] (word 1) of old.
+template <bool kHiWord>
+__device__ __forceinline__ uint32_t cvt2(float a, float b, uint32_t old) {
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)old, kHiWord);
+}
+
+// Max of |bf16| over the two halves of w, as 15-bit integers (packed u16 max).
+__device__ __forceinline__ uint32_t absmax2(uint32_t acc, uint32_t w) {
+  const u16x2 a = __builtin_bit_cast(u16x2, acc);
+  const u16x2 b = __builtin_bit_cast(u16x2, w & 0x7FFF7FFFu);
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(a, b));
+}
+
+// Four codes of RN(x/s) for the bf16 pairs in words w0 (elements 0,1) and
+// w1 (elements 2,3), division-free unless near a rounding midpoint.
+__device__ __forceinline__ uint32_t codes4_fast(uint32_t w0, uint32_t w1, float r, float s) {
+  const float x0 = bf16_lo(w0), x1 = bf16_hi(w0), x2 = bf16_lo(w1), x3 = bf16_hi(w1);
+  const float q0 = x0 * r, q1 = x1 * r, q2 = x2 * r, q3 = x3 * r;
+  constexpr float kDown = 1.0f - 0x1.0p-20f;
+  constexpr float kUp = 1.0f + 0x1.0p-20f;
+  uint32_t lo = cvt2<false>(q0 * kDown, q1 * kDown, 0);
+  lo = cvt2<true>(q2 * kDown, q3 * kDown, lo);
+  uint32_t hi = cvt2<false>(q0 * kUp, q1 * kUp, 0);
+  hi = cvt2<true>(q2 * kUp, q3 * kUp, hi);
+  if (lo != hi) {
+    // Near a rounding midpoint: use the correctly rounded quotient.
+    lo = cvt2<false>(x0 / s, x1 / s, 0);
+    lo = cvt2<true>(x2 / s, x3 / s, lo);
+  }
+  return lo;
+}
+
+// Four codes of RN(x/s) with a true division per element.
+__device__ __forceinline__ uint32_t codes4_div(uint32_t w0, uint32_t w1, float s) {
+  uint32_t c = cvt2<false>(bf16_lo(w0) / s, bf16_hi(w0) / s, 0);
+  return cvt2<true>(bf16_lo(w1) / s, bf16_hi(w1) / s, c);
+}
+
+// Codes when the tile's amax is 0: only the sign bits survive.
+__device__ __forceinline__ uint32_t codes4_zero(uint32_t w0, uint32_t w1) {
+  return ((w0 >> 8) & 0x80u) | ((w0 >> 16) & 0x8000u) | ((w1 << 8) & 0x800000u) |
+         (w1 & 0x80000000u);
+}
+
+// Single-element code for the generic path (same rules as the tile path).
+__device__ __forceinline__ uint8_t code1(uint16_t bits, int mode, float s) {
+  // mode 0: finite tile, 1: zero tile, 2: non-finite tile
+  if (mode == 2) return 0x7F;
+  if (mode == 1) return (bits & 0x8000u) ? 0x80 : 0x00;
+  const float q = __uint_as_float(uint32_t(bits) << 16) / s;
+  return (uint8_t)(cvt2<false>(q, q, 0) & 0xFFu);
+}
+
+// Reduce a per-thread 15-bit amax over the workgroup.  red is a 2 x 4 array
+// used alternately by consecutive tiles, so one barrier per tile suffices.
+__device__ __forceinline__ uint32_t block_amax(uint32_t m, uint32_t* red) {
+#pragma unroll
+  for (int d = kWaveLanes / 2; d >= 1; d >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, d, kWaveLanes));
+  if ((threadIdx.x & (kWaveLanes - 1)) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  return max(max(red[0], red[1]), max(red[2], red[3]));
+}
+
+// Item whose tile range contains tile t: last i in [0, n) with
+// prefix[i] <= t, given prefix[0] <= t < prefix[n].
+__device__ int64_t find_item(const uint64_t* __restrict__ prefix, int64_t n, uint64_t t, int lane) {
+  int64_t lo = 0, hi = n;
+  while (hi - lo > 1) {
+    const int64_t step = (hi - lo + kWaveLanes - 1) / kWaveLanes;
+    const int64_t p = lo + (int64_t(lane) + 1) * step;
+    const bool pred = lane < kWaveLanes - 1 && p < hi && prefix[p] <= t;
+    lo += int64_t(__popcll(__ballot(pred))) * step;
+    hi = min(hi, lo + step);
+  }
+  return lo;
+}
+
+// One workgroup: prefix[i] = number of tiles of items [0, i), prefix[n] = total.
+__global__ __launch_bounds__(kThreads) void k_cast_plan(const tc_cast_item* __restrict__ items,
+                                                       const int64_t n,
+                                                       uint64_t* __restrict__ prefix) {
+  __shared__ uint64_t wave_tot[kThreads / kWaveLanes];
+  const int lane = threadIdx.x & (kWaveLanes - 1);
+  const int w = threadIdx.x >> 6;
+  uint64_t carry = 0;
+  for (int64_t base = 0; base < n; base += kThreads) {
+    const int64_t i = base + threadIdx.x;
+    uint64_t v = 0;
+    if (i < n) {
+      const int64_t rows = items[i].rows, cols = items[i].cols;
+      v = uint64_t((rows + kTile - 1) / kTile) * uint64_t((cols + kTile - 1) / kTile);
+    }
+    uint64_t incl = v;
+#pragma unroll
+    for (int d = 1; d < kWaveLanes; d <<= 1) {
+      const uint32_t lo = __shfl_up((uint32_t)incl, d, kWaveLanes);
+      const uint32_t hi = __shfl_up((uint32_t)(incl >> 32), d, kWaveLanes);
+      if (lane >= d) incl += (uint64_t(hi) << 32) | lo;
+    }
+    if (lane == kWaveLanes - 1) wave_tot[w] = incl;
+    __syncthreads();
+    uint64_t before = 0, total = 0;
+#pragma unroll
+    for (int k = 0; k < kThreads / kWaveLanes; ++k) {
+      if (k < w) before += wave_tot[k];
+      total += wave_tot[k];
+    }
+    __syncthreads();
+    if (i < n) prefix[i] = carry + before + incl - v;
+    carry += total;
+  }
+  if (threadIdx.x == 0) prefix[n] = carry;
+}
+
+// Persistent grid: workgroup b takes tiles b, b + grid, ...
+__global__ __launch_bounds__(kThreads) void k_cast_tiles(const uint16_t* __restrict__ src,
+                                                        uint8_t* __restrict__ dst,
+                                                        float* __restrict__ scales,
+                                                        const tc_cast_item* __restrict__ items,
+                                                        const int64_t n_items,
+                                                        const uint64_t* __restrict__ prefix) {
+  __shared__ uint32_t red[2][kThreads / kWaveLanes];
+  const int lane = threadIdx.x & (kWaveLanes - 1);
+  const uint64_t total = prefix[n_items];
+  // Fast-path thread layout: 16 lanes per row (8 bf16 = 16 B each), 16 rows
+  // per pass, 8 passes.
+  const int seg = threadIdx.x & 15;
+  const int prow = threadIdx.x >> 4;
+  int parity = 0;
+  for (uint64_t t = blockIdx.x; t < total; t += gridDim.x, parity ^= 1) {
+    uint32_t* rbuf = red[parity];
+    const int64_t it = find_item(prefix, n_items, t, lane);
+    const tc_cast_item item = items[it];
+    const int64_t tiles_c = (item.cols + kTile - 1) / kTile;
+    const int64_t local = int64_t(t - prefix[it]);
+    const int64_t ti = local / tiles_c, tj = local - ti * tiles_c;
+    const int64_t r0 = ti * kTile, c0 = tj * kTile;
+    const int64_t h = min<int64_t>(kTile, item.rows - r0);
+    const int64_t wd = min<int64_t>(kTile, item.cols - c0);
+    const uint16_t* xs = src + item.src_off + r0 * item.src_ld + c0;
+    uint8_t* qs = dst + item.dst_off + r0 * item.dst_ld + c0;
+    float* sp = scales + item.scale_off + ti * item.scale_ld + tj;
+    const bool fast = h == kTile && wd == kTile &&
+                      ((reinterpret_cast<uintptr_t>(xs) | uint64_t(item.src_ld) * 2) & 15) == 0 &&
+                      ((reinterpret_cast<uintptr_t>(qs) | uint64_t(item.dst_ld)) & 7) == 0;
+    if (fast) {
+      u32x4 v[8];
+#pragma unroll
+      for (int p = 0; p < 8; ++p)
+        v[p] = *reinterpret_cast<const u32x4*>(xs + int64_t(p * 16 + prow) * item.src_ld + seg * 8);
+      uint32_t m2 = 0;
+#pragma unroll
+      for (int p = 0; p < 8; ++p) {
+        m2 = absmax2(m2, v[p].x);
+        m2 = absmax2(m2, v[p].y);
+        m2 = absmax2(m2, v[p].z);
+        m2 = absmax2(m2, v[p].w);
+      }
+      const uint32_t amax_bits = block_amax(max(m2 & 0xFFFFu, m2 >> 16), rbuf);
+      float s;
+      u32x2 out[8];
+      if (amax_bits >= 0x7F80u) {  // Inf or NaN in the tile
+        s = __uint_as_float(0x7FC00000u);
+#pragma unroll
+        for (int p = 0; p < 8; ++p) out[p] = u32x2{0x7F7F7F7Fu, 0x7F7F7F7Fu};
+      } else if (amax_bits == 0) {
+        s = 0.0f;
+#pragma unroll
+        for (int p = 0; p < 8; ++p)
+          out[p] = u32x2{codes4_zero(v[p].x, v[p].y), codes4_zero(v[p].z, v[p].w)};
+      } else {
+        s = __uint_as_float(amax_bits << 16) / 448.0f;
+        if (s >= 0x1.0p-126f) {
+          const float r = 1.0f / s;
+#pragma unroll
+          for (int p = 0; p < 8; ++p)
+            out[p] = u32x2{codes4_fast(v[p].x, v[p].y, r, s), codes4_fast(v[p].z, v[p].w, r, s)};
+        } else {
+#pragma unroll
+          for (int p = 0; p < 8; ++p)
+            out[p] = u32x2{codes4_div(v[p].x, v[p].y, s), codes4_div(v[p].z, v[p].w, s)};
+        }
+      }
+#pragma unroll
+      for (int p = 0; p < 8; ++p)
+        *reinterpret_cast<u32x2*>(qs + int64_t(p * 16 + prow) * item.dst_ld + seg * 8) = out[p];
+      if (threadIdx.x == 0) *sp = s;
+    } else {
+      // Edge or unaligned tile: element by element.
+      const int64_t cnt = h * wd;
+      uint32_t m = 0;
+      for (int64_t e = threadIdx.x; e < cnt; e += kThreads) {
+        const int64_t rr = e / wd, cc = e - rr * wd;
+        m = max(m, uint32_t(xs[rr * item.src_ld + cc]) & 0x7FFFu);
+      }
+      const uint32_t amax_bits = block_amax(m, rbuf);
+      int mode;
+      float s;
+      if (amax_bits >= 0x7F80u) {
+        mode = 2;
+        s = __uint_as_float(0x7FC00000u);
+      } else if (amax_bits == 0) {
+        mode = 1;
+        s = 0.0f;
+      } else {
+        mode = 0;
+        s = __uint_as_float(amax_bits << 16) / 448.0f;
+      }
+      for (int64_t e = threadIdx.x; e < cnt; e += kThreads) {
+        const int64_t rr = e / wd, cc = e - rr * wd;
+        qs[rr * item.dst_ld + cc] = code1(xs[rr * item.src_ld + cc], mode, s);
+      }
+      if (threadIdx.x == 0) *sp = s;
+    }
+  }
+}
+
+// Elementwise cast with one given scale: 8 elements per thread.
+__global__ __launch_bounds__(kThreads) void k_cast_scaled(const uint16_t* __restrict__ src,
+                                                         const int64_t n, const float s,
+                                                         uint8_t* __restrict__ dst,
+                                                         const int vec_ok) {
+  const int64_t stride = int64_t(gridDim.x) * kThreads;
+  for (int64_t g = int64_t(blockIdx.x) * kThreads + threadIdx.x; g * 8 < n; g += stride) {
+    const int64_t i0 = g * 8;
+    uint16_t x[8];
+    if (vec_ok && i0 + 8 <= n) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(src + i0);
+      x[0] = v.x & 0xFFFF; x[1] = v.x >> 16; x[2] = v.y & 0xFFFF; x[3] = v.y >> 16;
+      x[4] = v.z & 0xFFFF; x[5] = v.z >> 16; x[6] = v.w & 0xFFFF; x[7] = v.w >> 16;
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) x[k] = i0 + k < n ? src[i0 + k] : 0;
+    }
+    uint8_t c[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const float q = __uint_as_float(uint32_t(x[k]) << 16) / s;
+      const uint32_t a = __float_as_uint(q) & 0x7FFFFFFFu;
+      if (a > 0x7F800000u)
+        c[k] = 0x7F;  // NaN, whatever its sign
+      else if (a >= 0x43E00000u)  // |q| >= 448 (and Inf): saturate
+        c[k] = (uint8_t)(((__float_as_uint(q) >> 24) & 0x80u) | 0x7Eu);
+      else
+        c[k] = (uint8_t)(cvt2<false>(q, q, 0) & 0xFFu);
+    }
+    if (vec_ok && i0 + 8 <= n) {
+      const u32x2 o = {uint32_t(c[0]) | uint32_t(c[1]) << 8 | uint32_t(c[2]) << 16 | uint32_t(c[3]) << 24,
+                       uint32_t(c[4]) | uint32_t(c[5]) << 8 | uint32_t(c[6]) << 16 | uint32_t(c[7]) << 24};
+      *reinterpret_cast<u32x2*>(dst + i0) = o;
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (i0 + k < n) dst[i0 + k] = c[k];
+    }
+  }
+}
+
+int g_cast_blocks_per_cu = 0;
+
+}  // namespace
+
+size_t cast_workspace_bytes(int64_t n_items) { return size_t(8) * size_t(n_items + 1) + 256; }
+
+hipError_t launch_cast_blockscaled(const uint16_t* src, uint8_t* dst, float* scales,
+                                   const tc_cast_item* items, int64_t n_items, void* ws,
+                                   const DeviceInfo& di, hipStream_t s) {
+  if (g_cast_blocks_per_cu == 0) {
+    int per_cu = 0;
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_cast_tiles, kThreads, 0);
+    if (e != hipSuccess) return e;
+    g_cast_blocks_per_cu = per_cu > 0 ? per_cu : 1;
+  }
+  uint64_t* prefix = reinterpret_cast<uint64_t*>(ws);
+  hipLaunchKernelGGL(k_cast_plan, dim3(1), dim3(kThreads), 0, s, items, n_items, prefix);
+  const unsigned grid = (unsigned)(di.cus * g_cast_blocks_per_cu);
+  hipLaunchKernelGGL(k_cast_tiles, dim3(grid), dim3(kThreads), 0, s, src, dst, scales, items,
+                     n_items, (const uint64_t*)prefix);
+  return hipGetLastError();
+}
+
+hipError_t launch_cast_scaled(const uint16_t* src, int64_t n, float scale, uint8_t* dst,
+                              hipStream_t s) {
+  const int vec_ok = ((reinterpret_cast<uintptr_t>(src) & 15) == 0 &&
+                      (reinterpret_cast<uintptr_t>(dst) & 7) == 0);
+  const int64_t groups = (n + 7) / 8;
+  int64_t blocks = (groups + kThreads - 1) / kThreads;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(k_cast_scaled, dim3((unsigned)blocks), dim3(kThreads), 0, s, src, n, scale,
+                     dst, vec_ok);
+  return hipGetLastError();
+}
+
+}  // namespace tc

@@ -1,0 +1,69 @@
+"""Describe a model's weights as tensor-parallel views.
+
+The source is one contiguous stream of row-major matrices in spec order
+(each (name, rows, cols, split) entry directly follows the previous one);
+the destination is the rank's shard: its slices in the same order, each
+packed densely row-major.  These helpers only compute the offsets of that
+layout; the moves themselves are described by the library's builders
+(``tc_tp_fragments``, ``tc_tp_cast_item``) and done by its kernels.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import (CAST_ITEM_DTYPE, SPLIT_COLS, SPLIT_NONE, SPLIT_ROWS, TP_VIEW_DTYPE,
+               tc_tp_cast_item)
+
+_SPLIT = {"rows": SPLIT_ROWS, "cols": SPLIT_COLS, "none": SPLIT_NONE}
+
+
+def slice_shape(rows: int, cols: int, split: str, tp: int):
+    if split == "rows":
+        return rows // tp, cols
+    if split == "cols":
+        return rows, cols // tp
+    return rows, cols
+
+
+def stream_views(spec, tp: int, elem_bytes: int = 2, dst_elem_bytes: int | None = None) -> np.ndarray:
+    """One TP_VIEW_DTYPE record per matrix.  ``dst_elem_bytes`` sets the size
+    of a destination element used for dst offsets (defaults to elem_bytes;
+    1 for an fp8 destination)."""
+    deb = elem_bytes if dst_elem_bytes is None else dst_elem_bytes
+    v = np.zeros(len(spec), dtype=TP_VIEW_DTYPE)
+    src = dst = 0
+    for k, (_name, rows, cols, split) in enumerate(spec):
+        sr, sc = slice_shape(rows, cols, split, tp)
+        v[k] = (src, rows, cols, cols, dst, sc, elem_bytes, _SPLIT[split])
+        src += rows * cols * elem_bytes
+        dst += sr * sc * deb
+    return v
+
+
+def shard_elems(spec, tp: int) -> int:
+    total = 0
+    for (_name, rows, cols, split) in spec:
+        sr, sc = slice_shape(rows, cols, split, tp)
+        total += sr * sc
+    return total
+
+
+def scale_elems(spec, tp: int, tile: int = 128) -> int:
+    total = 0
+    for (_name, rows, cols, split) in spec:
+        sr, sc = slice_shape(rows, cols, split, tp)
+        total += ((sr + tile - 1) // tile) * ((sc + tile - 1) // tile)
+    return total
+
+
+def cast_items(spec, tp: int, rank: int) -> np.ndarray:
+    """CAST_ITEM_DTYPE records that cast rank ``rank``'s bf16 slices of a
+    contiguous bf16 stream into a packed fp8 shard with packed scale grids."""
+    views = stream_views(spec, tp, elem_bytes=2, dst_elem_bytes=1)
+    items = np.zeros(len(spec), dtype=CAST_ITEM_DTYPE)
+    scale_off = 0
+    for k, (_name, rows, cols, split) in enumerate(spec):
+        items[k] = tc_tp_cast_item(views[k], tp, rank, scale_off)
+        sr, sc = slice_shape(rows, cols, split, tp)
+        scale_off += ((sr + 127) // 128) * ((sc + 127) // 128)
+    return items

@@ -8,3 +8,23 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: runs HIP kernels on an MI355X (gfx950) GPU")
+
+
+import gc
+
+import pytest
+
+
+@pytest.fixture(autouse=True)
+def _release_device_memory():
+    """Free cached device memory between tests: the full-size cases need
+    most of the GPU's 288 GB."""
+    yield
+    gc.collect()
+    try:
+        import torch
+        if torch.cuda.is_available():
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
+    except Exception:
+        pass

@@ -1,0 +1,186 @@
+"""GPU parity: paged-KV block gather (publish) and scatter (hydrate).
+
+The HIP path (through the C ABI) against the CPU oracle, byte for byte, on
+the same seeded inputs; full-size Llama-3-8B-shaped pools are checked on
+sampled blocks against the oracle and, for every block, by properties.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+import paper_2608_06007_amd as tc
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _host(t):
+    return t.detach().to("cpu").numpy()
+
+
+def _regions_random(R, nb, B, stride, seed):
+    g = torch.Generator(device=DEV)
+    g.manual_seed(seed)
+    span = (nb - 1) * stride + B
+    return [torch.randint(0, 256, (span,), dtype=torch.uint8, device=DEV, generator=g) for _ in range(R)]
+
+
+def _run_pair(regions, nb, B, stride, ids_np, sentinel=0xA5):
+    """GPU gather + scatter into a sentinel pool, and the same with the oracle."""
+    R = len(regions)
+    ids = torch.from_numpy(ids_np.astype(np.int32)).to(DEV)
+    out = torch.empty(len(ids_np) * R * B, dtype=torch.uint8, device=DEV)
+    tc.tc_gather_blocks(regions, nb, B, stride, ids, out)
+    dst = [torch.full_like(r, sentinel) for r in regions]
+    tc.tc_scatter_blocks(dst, nb, B, stride, ids, out)
+    torch.cuda.synchronize()
+    host_src = [_host(r) for r in regions]
+    want = oracle.gather_blocks(host_src, B, stride, ids_np)
+    assert np.array_equal(_host(out).reshape(want.shape), want)
+    host_dst = [np.full_like(h, sentinel) for h in host_src]
+    oracle.scatter_blocks(host_dst, B, stride, ids_np, want)
+    for d, h in zip(dst, host_dst):
+        assert np.array_equal(_host(d), h)
+
+
+def test_tiny_config():
+    """2 layers x K/V, 4 heads, dim 64, 16-token blocks, 256 blocks, 32 ids."""
+    s = synth.KV_TINY
+    vals = synth.bf16_normal(s.num_regions * s.region_bytes // 2, 1.0, synth.SEED_KV_TINY, device=DEV)
+    flat = vals.view(torch.uint8)
+    regions = [flat[r * s.region_bytes:(r + 1) * s.region_bytes] for r in range(s.num_regions)]
+    ids = synth.ids_without_replacement(s.num_blocks, s.n_ids, synth.SEED_KV_TINY)
+    _run_pair(regions, s.num_blocks, s.block_bytes, s.block_bytes, ids)
+
+
+@pytest.mark.parametrize("B,stride", [(8192, 8192), (8192 + 16, 8192 + 48), (100, 104), (16, 16),
+                                      (40000, 40960), (3, 7)])
+def test_block_geometries(B, stride):
+    nb = 40
+    regions = _regions_random(3, nb, B, stride, 7)
+    ids = synth.ids_without_replacement(nb, 25, seed=8)
+    _run_pair(regions, nb, B, stride, ids)
+
+
+def test_edge_ids():
+    nb, B = 64, 4096
+    regions = _regions_random(4, nb, B, B, 9)
+    _run_pair(regions, nb, B, B, np.array([nb - 1], dtype=np.int32))        # single, max id
+    _run_pair(regions, nb, B, B, np.arange(nb, dtype=np.int32))             # all ids: plain copy
+    _run_pair(regions, nb, B, B, np.array([0], dtype=np.int32))
+
+
+def test_gather_repeated_ids_and_empty():
+    nb, B = 16, 2048
+    regions = _regions_random(2, nb, B, B, 10)
+    ids_np = np.array([5, 5, 1, 5], dtype=np.int32)
+    ids = torch.from_numpy(ids_np).to(DEV)
+    out = torch.empty(4 * 2 * B, dtype=torch.uint8, device=DEV)
+    tc.tc_gather_blocks(regions, nb, B, B, ids, out)
+    torch.cuda.synchronize()
+    want = oracle.gather_blocks([_host(r) for r in regions], B, B, ids_np)
+    assert np.array_equal(_host(out).reshape(want.shape), want)
+    empty = torch.empty(0, dtype=torch.int32, device=DEV)
+    tc.tc_gather_blocks(regions, nb, B, B, empty, out)        # n = 0: nothing happens
+    tc.tc_scatter_blocks(regions, nb, B, B, empty, out)
+
+
+def test_interleaved_engine_layout():
+    """One allocation laid out [blocks][2][...]: K and V of a layer are two
+    regions with base offset block_bytes apart and stride 2*block_bytes."""
+    nb, B = 32, 1024
+    layers = 3
+    g = torch.Generator(device=DEV)
+    g.manual_seed(11)
+    allocs = [torch.randint(0, 256, (nb * 2 * B,), dtype=torch.uint8, device=DEV, generator=g)
+              for _ in range(layers)]
+    regions = []
+    for a in allocs:
+        regions += [a.data_ptr(), a.data_ptr() + B]
+    ids_np = synth.ids_without_replacement(nb, 12, seed=12)
+    ids = torch.from_numpy(ids_np).to(DEV)
+    out = torch.empty(12 * 2 * layers * B, dtype=torch.uint8, device=DEV)
+    tc.tc_gather_blocks(regions, nb, B, 2 * B, ids, out)
+    dst_allocs = [torch.full_like(a, 0x33) for a in allocs]
+    dst_regions = []
+    for a in dst_allocs:
+        dst_regions += [a.data_ptr(), a.data_ptr() + B]
+    tc.tc_scatter_blocks(dst_regions, nb, B, 2 * B, ids, out)
+    torch.cuda.synchronize()
+    host = []
+    for a in allocs:
+        h = _host(a)
+        host += [h[:(nb - 1) * 2 * B + B], h[B:]]
+    want = oracle.gather_blocks(host, B, 2 * B, ids_np)
+    assert np.array_equal(_host(out).reshape(want.shape), want)
+    for a, d in zip(allocs, dst_allocs):
+        av, dv = _host(a).reshape(nb, 2 * B), _host(d).reshape(nb, 2 * B)
+        mask = np.zeros(nb, dtype=bool)
+        mask[ids_np] = True
+        assert np.array_equal(dv[mask], av[mask]) and np.all(dv[~mask] == 0x33)
+
+
+def test_validation_mode_reports_bad_ids():
+    nb, B = 8, 256
+    regions = _regions_random(2, nb, B, B, 13)
+    out = torch.empty(2 * 2 * B, dtype=torch.uint8, device=DEV)
+    tc.tc_set_validate(True)
+    try:
+        with pytest.raises(tc.TcError) as e:
+            tc.tc_gather_blocks(regions, nb, B, B, torch.tensor([0, 8], dtype=torch.int32, device=DEV), out)
+        assert e.value.status == 2
+        with pytest.raises(tc.TcError) as e:
+            tc.tc_scatter_blocks(regions, nb, B, B, torch.tensor([3, 3], dtype=torch.int32, device=DEV), out)
+        assert e.value.status == 3
+        # a good call still works with validation on
+        tc.tc_gather_blocks(regions, nb, B, B, torch.tensor([1, 2], dtype=torch.int32, device=DEV), out)
+        torch.cuda.synchronize()
+    finally:
+        tc.tc_set_validate(False)
+
+
+def test_llama3_8b_full_size():
+    """32 layers x K/V, 8 heads, dim 128, 16-token blocks, 32768 blocks per
+    region (64 GiB per pool), 4096 Zipf(1.1) ids: the benchmark's workload."""
+    s = synth.KV_LLAMA3_8B
+    B, nb, R = s.block_bytes, s.num_blocks, s.num_regions
+    try:
+        _full_size_body(s, B, nb, R)
+    finally:
+        torch.cuda.synchronize()
+
+
+def _full_size_body(s, B, nb, R):
+    pool_a = synth.bf16_normal(R * s.region_bytes // 2, 1.0, synth.SEED_KV_8B, device=DEV).view(torch.uint8)
+    regions_a = [pool_a[r * s.region_bytes:(r + 1) * s.region_bytes] for r in range(R)]
+    ids_np = synth.ids_zipf_prefix_reuse(nb, s.n_ids, 1.1, synth.SEED_KV_8B)
+    ids = torch.from_numpy(ids_np).to(DEV)
+    buf = torch.empty(s.transfer_bytes, dtype=torch.uint8, device=DEV)
+    tc.tc_gather_blocks(regions_a, nb, B, B, ids, buf)
+    pool_b = torch.full((R * s.region_bytes,), 0xA5, dtype=torch.uint8, device=DEV)
+    regions_b = [pool_b[r * s.region_bytes:(r + 1) * s.region_bytes] for r in range(R)]
+    tc.tc_scatter_blocks(regions_b, nb, B, B, ids, buf)
+    torch.cuda.synchronize()
+    bufv = buf.view(s.n_ids, R, B)
+    # sampled (i, r) chunks against the oracle on host copies of the source blocks
+    rng = np.random.default_rng(99)
+    sample_i = rng.choice(s.n_ids, size=64, replace=False)
+    for r in [0, 1, R // 2, R - 1]:
+        src_blocks = _host(regions_a[r].view(nb, B)[ids[sample_i].long()])
+        mini = [src_blocks.reshape(-1)]
+        want = oracle.gather_blocks(mini, B, B, np.arange(len(sample_i), dtype=np.int32))
+        assert np.array_equal(_host(bufv[sample_i, r]), want[:, 0, :])
+    # every block: equal to torch.index_select on the source, and hydrated pool
+    # B holds the same blocks with every other block still the sentinel
+    idl = ids.long()
+    mask = torch.zeros(nb, dtype=torch.bool, device=DEV)
+    mask[idl] = True
+    for r in range(R):
+        a = regions_a[r].view(nb, B)
+        b = regions_b[r].view(nb, B)
+        assert torch.equal(torch.index_select(a, 0, idl), bufv[:, r])
+        assert torch.equal(b[idl], a[idl])
+        assert bool((b[~mask] == 0xA5).all())

@@ -1,0 +1,256 @@
+"""GPU parity: bf16 -> fp8 E4M3 casts.
+
+HIP path through the C ABI against the CPU oracle, bit for bit (codes and
+scale bits): every bf16 pattern at many scales, block-scaled matrices with
+ragged and strided tiles and special tiles, a TP=8 shard of 70B-shaped
+weights on a few layers in full and at full size on sampled tiles.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+import paper_2608_06007_amd as tc
+from paper_2608_06007_amd import views as tcv
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+ALL_BF16 = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+
+
+def _host(t):
+    return t.detach().to("cpu").numpy()
+
+
+def _to_dev_bits(bits: np.ndarray):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(DEV).view(torch.bfloat16)
+
+
+def _gpu_scaled(bits: np.ndarray, scale: float) -> np.ndarray:
+    x = _to_dev_bits(bits)
+    q = torch.empty(x.numel(), dtype=torch.uint8, device=DEV)
+    tc.tc_cast_fp8_scaled(x, scale, q)
+    torch.cuda.synchronize()
+    return _host(q)
+
+
+def test_every_bf16_pattern_scale_one():
+    got = _gpu_scaled(ALL_BF16, 1.0)
+    want = oracle.cast_fp8_scaled(ALL_BF16, 1.0)
+    assert np.array_equal(got, want)
+
+
+def test_every_bf16_pattern_many_scales():
+    rng = np.random.default_rng(50)
+    bits = np.concatenate([rng.integers(0x00800000, 0x7F000000, size=48, dtype=np.int64),
+                           rng.integers(1, 0x00800000, size=8, dtype=np.int64),
+                           (np.arange(-12, 13) + 127) << 23]).astype(np.uint32)
+    for s in bits.view(np.float32):
+        got = _gpu_scaled(ALL_BF16, float(s))
+        want = oracle.cast_fp8_scaled(ALL_BF16, float(s))
+        bad = np.nonzero(got != want)[0]
+        assert bad.size == 0, (float(s), [(hex(int(ALL_BF16[i])), hex(got[i]), hex(want[i])) for i in bad[:5]])
+
+
+def test_scaled_odd_sizes_and_offsets():
+    rng = np.random.default_rng(51)
+    bits = rng.integers(0, 1 << 16, size=10007, dtype=np.int64).astype(np.uint16)
+    x = _to_dev_bits(bits)
+    for start, stop in [(0, 10007), (1, 10000), (3, 4), (5, 5)]:
+        xs = x[start:stop]
+        q = torch.empty(xs.numel() + 3, dtype=torch.uint8, device=DEV)[1:1 + xs.numel()]
+        tc.tc_cast_fp8_scaled(xs, 0.37, q)
+        torch.cuda.synchronize()
+        assert np.array_equal(_host(q), oracle.cast_fp8_scaled(bits[start:stop], 0.37))
+
+
+# ---------------------------------------------------------------------------
+
+def _bits_from_float(a: np.ndarray) -> np.ndarray:
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16)
+
+
+def _cast_matrices(src_bits_1d: np.ndarray, mats, code_pad=0, scale_pad=0):
+    """mats: list of (src_off, rows, cols, src_ld) in bf16 elements of the
+    1-D source.  Codes packed row-major (row stride cols + code_pad), scale
+    grids packed (row stride tiles_c + scale_pad).  Returns GPU and oracle
+    results per matrix."""
+    items = np.zeros(len(mats), dtype=tc.CAST_ITEM_DTYPE)
+    q_off = s_off = 0
+    for k, (so, rows, cols, ld) in enumerate(mats):
+        tr, tcn = (rows + 127) // 128, (cols + 127) // 128
+        items[k] = (so, rows, cols, ld, q_off, cols + code_pad, s_off, tcn + scale_pad)
+        q_off += rows * (cols + code_pad)
+        s_off += tr * (tcn + scale_pad)
+    src = _to_dev_bits(src_bits_1d)
+    dst = torch.full((max(q_off, 1),), 0xCC, dtype=torch.uint8, device=DEV)
+    scales = torch.full((max(s_off, 1),), -7.0, dtype=torch.float32, device=DEV)
+    dev_items = torch.from_numpy(items.view(np.uint8)).to(DEV)
+    ws = torch.empty(tc.tc_cast_fp8_workspace(len(mats)), dtype=torch.uint8, device=DEV)
+    tc.tc_cast_fp8_blockscaled(src, dst, scales, dev_items, ws)
+    torch.cuda.synchronize()
+    hq, hs = _host(dst), _host(scales)
+    for k, (so, rows, cols, ld) in enumerate(mats):
+        it = items[k]
+        view = np.lib.stride_tricks.as_strided(src_bits_1d[so:], shape=(rows, cols), strides=(2 * ld, 2))
+        q, s = oracle.cast_fp8_blockscaled(view)
+        gq = np.lib.stride_tricks.as_strided(hq[it["dst_off"]:], shape=(rows, cols),
+                                             strides=(int(it["dst_ld"]), 1))
+        tr, tcn = s.shape
+        gs = np.lib.stride_tricks.as_strided(hs[it["scale_off"]:], shape=(tr, tcn),
+                                             strides=(4 * int(it["scale_ld"]), 4))
+        assert np.array_equal(gs.view(np.uint32), s.view(np.uint32)), f"scales of matrix {k}"
+        if not np.array_equal(gq, q):
+            bad = np.argwhere(gq != q)
+            r, c = bad[0]
+            raise AssertionError(f"matrix {k}: {len(bad)} codes differ, first at {(r, c)}: "
+                                 f"x={hex(int(view[r, c]))} gpu={hex(int(gq[r, c]))} oracle={hex(int(q[r, c]))}")
+    return hq, hs
+
+
+def test_blockscaled_ragged_strided_and_offsets():
+    rng = np.random.default_rng(52)
+    a = rng.normal(0, 0.02, size=600 * 700).astype(np.float32)
+    bits = _bits_from_float(a)
+    mats = [(0, 256, 384, 384),            # whole tiles, packed
+            (0, 300, 200, 700),            # ragged rows and cols, strided rows
+            (8, 128, 128, 700),            # aligned strided tile
+            (3, 130, 129, 700),            # unaligned source (odd element offset)
+            (1000, 1, 1, 1),               # single element
+            (2000, 5, 300, 301)]           # odd row stride
+    _cast_matrices(bits, mats)
+    _cast_matrices(bits, mats, code_pad=5, scale_pad=2)     # unaligned code rows
+
+
+def test_blockscaled_special_tiles():
+    rng = np.random.default_rng(53)
+    a = rng.normal(0, 1, size=(256, 640)).astype(np.float32)
+    a[0:128, 0:128] = 0.0
+    a[0:128, 0:128][::3, ::5] = -0.0
+    a[0:128, 128:256][7, 9] = np.inf
+    a[0:128, 256:384][100, 1] = np.nan
+    a[0:128, 384:512][3, 3] = -np.inf
+    a[128:256, 0:128] *= 1e-38                  # subnormal bf16 values, subnormal scale
+    a[128:256, 128:256] = 0.0
+    a[128:256, 128:256][5, 5] = 2.0 ** -133
+    a[128:256, 128:256][6, 6] = -(2.0 ** -133)
+    a[128:256, 256:384] *= 1e30                 # huge values
+    a[128:256, 384:512] = 448.0                 # amax exactly 448 -> scale 1
+    a[128:256, 384:512][::2] = -1.0
+    a[128:256, 512:640] = rng.choice([1.0, -2.0, 0.5, 3.0], size=(128, 128))  # exact quotients, ties
+    bits = _bits_from_float(a).reshape(-1)
+    _cast_matrices(bits, [(0, 256, 640, 640)])
+    _cast_matrices(bits, [(1, 255, 600, 640)])  # the same through the edge path
+
+
+def test_blockscaled_rounding_midpoints():
+    """Tiles whose quotients land on and around E4M3 rounding midpoints."""
+    rng = np.random.default_rng(54)
+    mats = []
+    parts = []
+    off = 0
+    for t in range(24):
+        amax = float(np.float32(rng.uniform(0.5, 4.0)))
+        s = np.float32(amax) / np.float32(448.0)
+        # midpoints of the E4M3 grid, mapped back to x = mid * s, rounded to bf16
+        mids = np.array([(a + b) / 2 for a, b in zip(_E4M3_POS[:-1], _E4M3_POS[1:])], dtype=np.float64)
+        x = rng.choice(mids, size=128 * 128) * float(s) * rng.choice([-1.0, 1.0], size=128 * 128)
+        x *= 1 + rng.integers(-4, 5, size=x.size) * 2.0 ** -9
+        x[0] = amax
+        bits = _bits_from_float(x.astype(np.float32))
+        parts.append(bits)
+        mats.append((off, 128, 128, 128))
+        off += bits.size
+    _cast_matrices(np.concatenate(parts), mats)
+
+
+_E4M3_POS = sorted({abs(oracle.e4m3_decode(c)) for c in range(0x7F)})
+
+
+@pytest.mark.parametrize("layers,ranks", [(2, [0, 3, 7])])
+def test_tp_shard_cast_70b_layers(layers, ranks):
+    """70B-shaped layers (hidden 8192, 64 q / 8 kv heads, MLP 28672), N(0, 0.02),
+    cast into TP=8 shards, compared in full with the oracle."""
+    spec = synth.spec_70b(layers)
+    n = synth.spec_elems(spec)
+    stream = synth.bf16_normal(n, 0.02, synth.SEED_CAST_70B, device=DEV)
+    host = _host(stream.view(torch.int16)).view(np.uint16)
+    tp = 8
+    for rank in ranks:
+        items = tcv.cast_items(spec, tp, rank)
+        q = torch.empty(tcv.shard_elems(spec, tp), dtype=torch.uint8, device=DEV)
+        s = torch.empty(tcv.scale_elems(spec, tp), dtype=torch.float32, device=DEV)
+        ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device=DEV)
+        tc.tc_cast_fp8_blockscaled(stream, q, s, torch.from_numpy(items.view(np.uint8)).to(DEV), ws)
+        torch.cuda.synchronize()
+        hq, hs = _host(q), _host(s)
+        off = 0
+        for it, (_, rows, cols, split) in zip(items, spec):
+            w = host[off:off + rows * cols].reshape(rows, cols)
+            off += rows * cols
+            want_q, want_s = oracle.cast_fp8_blockscaled(oracle.tp_slice(w, split, tp, rank))
+            r, c = want_q.shape
+            assert np.array_equal(hq[it["dst_off"]:it["dst_off"] + r * c].reshape(r, c), want_q)
+            tr, tcn = want_s.shape
+            got_s = hs[it["scale_off"]:it["scale_off"] + tr * tcn].reshape(tr, tcn)
+            assert np.array_equal(got_s.view(np.uint32), want_s.view(np.uint32))
+    del stream
+    torch.cuda.empty_cache()
+
+
+def test_tp_shard_cast_70b_full_size():
+    """All 80 layers (136.9 GB of bf16 in HBM), rank 3 of TP=8: the shard
+    slices hold N(0, 0.02) values and everything outside them is poisoned with
+    a huge value, so a read outside the slice would change the scales.
+    Sampled tiles against the oracle; every scale is checked to be a normal
+    N(0, 0.02) tile scale (no poison), and every tile's largest code is +-448."""
+    tp, rank = 8, 3
+    spec = synth.spec_70b(80)
+    n = synth.spec_elems(spec)
+    stream = torch.full((n,), 3.0e38, dtype=torch.bfloat16, device=DEV)
+    items = tcv.cast_items(spec, tp, rank)
+    fill = synth.bf16_normal(tcv.shard_elems(spec, tp), 0.02, synth.SEED_CAST_70B, device=DEV)
+    # place the values into the rank's slices with torch indexing
+    off = 0
+    foff = 0
+    for (_, rows, cols, split) in spec:
+        w = stream[off:off + rows * cols].view(rows, cols)
+        off += rows * cols
+        sl = w[rank * rows // tp:(rank + 1) * rows // tp] if split == "rows" else \
+            w[:, rank * cols // tp:(rank + 1) * cols // tp]
+        k = sl.numel()
+        sl.copy_(fill[foff:foff + k].view(sl.shape))
+        foff += k
+    del fill
+    q = torch.empty(tcv.shard_elems(spec, tp), dtype=torch.uint8, device=DEV)
+    s = torch.empty(tcv.scale_elems(spec, tp), dtype=torch.float32, device=DEV)
+    ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device=DEV)
+    tc.tc_cast_fp8_blockscaled(stream, q, s, torch.from_numpy(items.view(np.uint8)).to(DEV), ws)
+    torch.cuda.synchronize()
+    # no poisoned tile: every scale is what an N(0, 0.02) tile gives
+    assert bool(((s > 1e-5) & (s < 1e-3)).all())
+    # sampled tiles against the oracle
+    rng = np.random.default_rng(55)
+    for k in rng.choice(len(items), size=40, replace=False):
+        it = items[k]
+        rows, cols = int(it["rows"]), int(it["cols"])
+        tr, tcn = (rows + 127) // 128, (cols + 127) // 128
+        ti, tj = int(rng.integers(0, tr)), int(rng.integers(0, tcn))
+        r0, c0 = ti * 128, tj * 128
+        ld = int(it["src_ld"])
+        base = int(it["src_off"]) + r0 * ld + c0
+        rows_t = stream[base:base + 127 * ld + 128].view(torch.int16)
+        tile = _host(rows_t).view(np.uint16)
+        view = np.lib.stride_tricks.as_strided(tile, shape=(128, 128), strides=(2 * ld, 2))
+        want_q, want_s = oracle.cast_fp8_blockscaled(view)
+        dq = int(it["dst_off"]) + r0 * int(it["dst_ld"]) + c0
+        got_q = _host(q[dq:dq + 127 * int(it["dst_ld"]) + 128])
+        got_q = np.lib.stride_tricks.as_strided(got_q, shape=(128, 128), strides=(int(it["dst_ld"]), 1))
+        assert np.array_equal(got_q, want_q), (k, ti, tj)
+        got_s = _host(s[int(it["scale_off"]) + ti * int(it["scale_ld"]) + tj])
+        assert got_s.view(np.uint32) == want_s.view(np.uint32)[0, 0]
+    del stream, q, s
+    torch.cuda.empty_cache()

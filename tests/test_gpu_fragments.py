@@ -1,0 +1,200 @@
+"""GPU parity: fragment copies and tensor-parallel shard materialization.
+
+HIP path through the C ABI against the CPU oracle, byte for byte, on the
+same seeded inputs: small storms (aligned and byte-granular), edge cases,
+planned reuse, MoE expert permutations, a TP=8 shard of 8B-shaped weights,
+and the full-size fragment storm.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+import paper_2608_06007_amd as tc
+from paper_2608_06007_amd import views as tcv
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _host(t):
+    return t.detach().to("cpu").numpy()
+
+
+def _rand_bytes(n, seed):
+    return synth.random_bytes(n, seed, device=DEV)
+
+
+def _copy_and_check(src, frags_np, dst_size, sentinel=0x5A, planned=False):
+    frags = torch.from_numpy(frags_np.astype(np.uint64).view(np.int64)).to(DEV)
+    dst = torch.full((dst_size,), sentinel, dtype=torch.uint8, device=DEV)
+    n = len(frags_np)
+    ws = torch.empty(max(tc.tc_copy_fragments_workspace(n), 8), dtype=torch.uint8, device=DEV)
+    if planned:
+        tc.tc_plan_fragments(frags, ws)
+        tc.tc_copy_planned(src, dst, frags, ws)
+    else:
+        tc.tc_copy_fragments(src, dst, frags, ws)
+    torch.cuda.synchronize()
+    want = np.full(dst_size, sentinel, dtype=np.uint8)
+    oracle.copy_fragments(_host(src), want, frags_np)
+    got = _host(dst)
+    step = 1 << 28
+    for a in range(0, dst_size, step):
+        g, w = got[a:a + step], want[a:a + step]
+        if not np.array_equal(g, w):
+            bad = np.nonzero(g != w)[0]
+            raise AssertionError(f"{bad.size} bytes differ in chunk at {a}, first at {bad[:5] + a}")
+    return dst, frags, ws
+
+
+@pytest.mark.parametrize("align", [16, 4, 1])
+def test_storm_small(align):
+    pool = 256 << 20
+    frags = synth.fragment_storm(20000, pool, seed=31 + align, align=align)
+    _copy_and_check(_rand_bytes(pool, 32), frags, pool)
+
+
+def test_mixed_misalignment():
+    """src and dst with different residues mod 16 (byte path), and equal
+    residues that are not 0 (vector body with byte head/tail)."""
+    rng = np.random.default_rng(33)
+    rows = []
+    off_s = off_d = 0
+    for k in range(3000):
+        ln = int(rng.integers(0, 40000))
+        ps, pd = int(rng.integers(0, 16)), int(rng.integers(0, 16))
+        if k % 2:
+            pd = ps
+        rows.append((off_s + ps, off_d + pd, ln))
+        off_s += ps + ln + 16
+        off_d += pd + ln + 16
+    frags = np.array(rows, dtype=np.uint64)
+    _copy_and_check(_rand_bytes(off_s, 34), frags, off_d)
+
+
+def test_edge_fragments():
+    src = _rand_bytes(4 << 20, 35)
+    rows = [(0, 0, 0), (5, 9, 0)]                          # empty fragments
+    rows += [(100, 200, 1), (1000, 300, 15), (2000, 400, 16), (3000, 500, 17)]
+    rows += [(16, 1 << 20, (1 << 20) + 3)]                 # larger than a piece, ragged
+    rows += [(3 << 20, 5 << 19, 16384), (7 << 19, 11 << 18, 16385)]
+    rows += [(2048 + k, 8192 + 4 * k, 0) for k in range(50)]  # many zero-length in a row
+    _copy_and_check(src, np.array(rows, dtype=np.uint64), 4 << 20)
+    # single fragment covering the whole buffer = plain copy
+    _copy_and_check(src, np.array([(0, 0, 4 << 20)], dtype=np.uint64), 4 << 20)
+    # nothing to do
+    empty = torch.zeros((0, 3), dtype=torch.int64, device=DEV)
+    tc.tc_copy_fragments(src, src, empty, torch.empty(8, dtype=torch.uint8, device=DEV))
+
+
+def test_plan_reuse_and_order_independence():
+    pool = 64 << 20
+    frags = synth.fragment_storm(5000, pool, seed=36)
+    src = _rand_bytes(pool, 37)
+    dst, fr, ws = _copy_and_check(src, frags, pool, planned=True)
+    # the same plan again
+    dst2 = torch.full_like(dst, 0x5A)
+    tc.tc_copy_planned(src, dst2, fr, ws)
+    # a shuffled list planned afresh gives the same bytes
+    perm = np.random.default_rng(38).permutation(len(frags))
+    dst3, _, _ = _copy_and_check(src, frags[perm], pool)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, dst2) and torch.equal(dst, dst3)
+
+
+def test_validation_mode_reports_overlaps():
+    src = _rand_bytes(1 << 20, 39)
+    dst = torch.zeros(1 << 20, dtype=torch.uint8, device=DEV)
+    ws = torch.empty(tc.tc_copy_fragments_workspace(2), dtype=torch.uint8, device=DEV)
+    bad = torch.tensor([[0, 0, 100], [200, 50, 100]], dtype=torch.int64, device=DEV)
+    tc.tc_set_validate(True)
+    try:
+        with pytest.raises(tc.TcError) as e:
+            tc.tc_copy_fragments(src, dst, bad, ws)
+        assert e.value.status == 3
+        same = torch.tensor([[0, 50, 100]], dtype=torch.int64, device=DEV)
+        with pytest.raises(tc.TcError) as e:       # src and dst ranges overlap in one buffer
+            tc.tc_copy_fragments(src, src, same, ws)
+        assert e.value.status == 3
+    finally:
+        tc.tc_set_validate(False)
+
+
+def test_moe_permutation_small_and_full():
+    for n_exp, e_bytes in [(32, 65536), (256, 7168 * 2048)]:
+        frags, perm = synth.moe_permutation(n_exp, e_bytes, seed=synth.SEED_STORM)
+        src = _rand_bytes(n_exp * e_bytes, 40)
+        fr = torch.from_numpy(frags.view(np.int64)).to(DEV)
+        dst = torch.empty_like(src)
+        ws = torch.empty(tc.tc_copy_fragments_workspace(n_exp), dtype=torch.uint8, device=DEV)
+        tc.tc_copy_fragments(src, dst, fr, ws)
+        torch.cuda.synchronize()
+        # expert slot j holds source expert perm[j] (torch indexing on the device)
+        p = torch.from_numpy(perm).to(DEV)
+        assert torch.equal(dst.view(n_exp, e_bytes), src.view(n_exp, e_bytes)[p])
+        # sampled bytes against the oracle
+        idx = np.random.default_rng(41).choice(n_exp, size=4, replace=False)
+        for j in idx:
+            want = np.zeros(e_bytes, dtype=np.uint8)
+            oracle.copy_fragments(_host(src[int(perm[j]) * e_bytes:(int(perm[j]) + 1) * e_bytes]), want,
+                                  np.array([[0, 0, e_bytes]], dtype=np.uint64))
+            assert np.array_equal(_host(dst[int(j) * e_bytes:(int(j) + 1) * e_bytes]), want)
+        del src, dst
+
+
+@pytest.mark.parametrize("layers,tp,ranks", [(2, 8, range(8)), (32, 8, [3])])
+def test_tp_shard_8b(layers, tp, ranks):
+    """8B-shaped weights (q/o 4096x4096, k/v 1024x4096, gate/up 14336x4096,
+    down 4096x14336) in a contiguous bf16 stream, materialized into TP=8
+    shards through the builder's fragments and the fragment copy."""
+    spec = synth.spec_8b(layers)
+    n = synth.spec_elems(spec)
+    stream = synth.bf16_normal(n, 1.0, synth.SEED_RESHARD_8B, device=DEV)
+    v = tcv.stream_views(spec, tp)
+    shard_n = tcv.shard_elems(spec, tp)
+    for rank in ranks:
+        frags_np = tc.tc_tp_fragments(v, tp, rank)
+        frags = torch.from_numpy(frags_np.view(np.int64)).to(DEV)
+        ws = torch.empty(tc.tc_copy_fragments_workspace(len(frags_np)), dtype=torch.uint8, device=DEV)
+        shard = torch.empty(shard_n, dtype=torch.bfloat16, device=DEV)
+        tc.tc_copy_fragments(stream, shard, frags, ws)
+        torch.cuda.synchronize()
+        got = _host(shard.view(torch.int16)).view(np.uint16)
+        if layers <= 2:
+            want = oracle.tp_shard(_host(stream.view(torch.int16)).view(np.uint16), spec, tp, rank)
+            assert np.array_equal(got, want)
+        else:
+            # full size: per layer, the oracle's slices of that layer's weights
+            per_layer = synth.spec_elems(spec[:7])
+            shard_layer = tcv.shard_elems(spec[:7], tp)
+            for l in [0, 1, 17, layers - 1]:
+                lw = _host(stream[l * per_layer:(l + 1) * per_layer].view(torch.int16)).view(np.uint16)
+                want = oracle.tp_shard(lw, spec[7 * l:7 * l + 7], tp, rank)
+                assert np.array_equal(got[l * shard_layer:(l + 1) * shard_layer], want)
+            # every layer: torch slicing on the device
+            off_s = off_d = 0
+            for (_, rows, cols, split) in spec:
+                w = stream[off_s:off_s + rows * cols].view(rows, cols)
+                off_s += rows * cols
+                sl = w[rank * rows // tp:(rank + 1) * rows // tp] if split == "rows" else \
+                    w[:, rank * cols // tp:(rank + 1) * cols // tp]
+                k = sl.numel()
+                assert torch.equal(shard[off_d:off_d + k].view(sl.shape).view(torch.int16),
+                                   sl.contiguous().view(torch.int16))
+                off_d += k
+    del stream
+    torch.cuda.empty_cache()
+
+
+def test_storm_full_size():
+    """1,000,000 fragments, log-uniform 64 B - 64 KiB, in two 16 GiB pools,
+    compared in full with the oracle run on host copies."""
+    pool = 16 << 30
+    frags = synth.fragment_storm(1_000_000, pool, seed=synth.SEED_STORM)
+    src = _rand_bytes(pool, synth.SEED_STORM)
+    dst, _, _ = _copy_and_check(src, frags, pool)
+    del src, dst
+    torch.cuda.empty_cache()

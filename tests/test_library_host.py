@@ -1,0 +1,144 @@
+"""Host-side checks of the C-ABI library (CPU only, no kernel launches).
+
+* The library loads and exports every function the public header declares.
+* Argument errors are reported before any device work.
+* The tensor-parallel builders describe exactly the oracle's numpy slices:
+  their fragments, applied by the oracle's byte copier to host buffers,
+  reproduce the oracle's shard.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+import paper_2608_06007_amd as tc
+from paper_2608_06007_amd import views as tcv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tensorcast_hip.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(tc.lib_path):
+        from paper_2608_06007_amd import build
+        build.build()
+    return tc.load()
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tc_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_function(lib):
+    names = _declared_functions()
+    assert len(names) >= 15
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    assert tc.tc_status_string(0) == "ok"
+    assert tc.tc_status_string(5) == "workspace too small"
+
+
+def test_argument_errors_need_no_gpu(lib):
+    P = ctypes.c_void_p
+    # gather with a null pool
+    assert lib.tc_gather_blocks(None, P(16), 1, P(16), None) == 1
+    # zero-length calls are no-ops even with null pointers
+    arr = (ctypes.c_uint64 * 1)(4096)
+    pool = tc._BlockPool(ctypes.cast(arr, ctypes.POINTER(ctypes.c_uint64)), 1, 4, 64, 64)
+    assert lib.tc_gather_blocks(ctypes.byref(pool), None, 0, None, None) == 0
+    # stride smaller than the block
+    pool_bad = tc._BlockPool(ctypes.cast(arr, ctypes.POINTER(ctypes.c_uint64)), 1, 4, 64, 32)
+    assert lib.tc_gather_blocks(ctypes.byref(pool_bad), P(16), 1, P(16), None) == 1
+    # too many regions
+    big = (ctypes.c_uint64 * 300)(*([4096] * 300))
+    pool_big = tc._BlockPool(ctypes.cast(big, ctypes.POINTER(ctypes.c_uint64)), 300, 4, 64, 64)
+    assert lib.tc_gather_blocks(ctypes.byref(pool_big), P(16), 1, P(16), None) == 1
+    # fragments: workspace too small, negative count
+    assert lib.tc_copy_fragments(P(16), P(16), P(16), 10, P(16), 8, None) == 5
+    assert lib.tc_copy_fragments(P(16), P(16), P(16), -1, P(16), 1 << 20, None) == 1
+    assert lib.tc_copy_fragments(None, None, None, 0, None, 0, None) == 0
+    # cast: tile other than 128
+    assert lib.tc_cast_fp8_blockscaled(P(16), P(16), P(16), P(16), 1, 64, P(16), 1 << 20, None) == 1
+    assert lib.tc_cast_fp8_scaled(P(16), -5, ctypes.c_float(1.0), P(16), None) == 1
+    assert tc.tc_copy_fragments_workspace(1000) >= 8 * 1001
+    assert tc.tc_cast_fp8_workspace(10) >= 8 * 11
+
+
+def test_validate_flag_roundtrip(lib):
+    tc.tc_set_validate(True)
+    assert tc.tc_get_validate()
+    tc.tc_set_validate(False)
+    assert not tc.tc_get_validate()
+
+
+SPEC = synth.spec_scaled(layers=2, hidden=256, q_heads=4, kv_heads=2, head_dim=64, mlp=384)
+
+
+@pytest.mark.parametrize("tp", [1, 2, 4, 8])
+def test_tp_fragments_reproduce_oracle_shard(lib, tp):
+    n = synth.spec_elems(SPEC)
+    rng = np.random.default_rng(20)
+    stream = rng.integers(0, 1 << 16, size=n, dtype=np.uint64).astype(np.uint16)
+    src = stream.view(np.uint8)
+    v = tcv.stream_views(SPEC, tp)
+    for rank in range(tp):
+        frags = tc.tc_tp_fragments(v, tp, rank)
+        dst = np.full(tcv.shard_elems(SPEC, tp) * 2, 0xEE, dtype=np.uint8)
+        oracle.copy_fragments(src, dst, frags)
+        want = oracle.tp_shard(stream, SPEC, tp, rank)
+        assert np.array_equal(dst.view(np.uint16), want)
+
+
+def test_tp_fragments_merge_contiguous_rows(lib):
+    # row-split slices are contiguous runs: one fragment per matrix;
+    # column-split slices need one fragment per row
+    v = tcv.stream_views(SPEC, 8)
+    frags = tc.tc_tp_fragments(v, 8, 3)
+    per_layer = 5 + 256 + 256          # q k v gate up + o rows + down rows
+    assert len(frags) == 2 * per_layer
+    assert tc.tc_tp_fragment_count(v, 8, 3) == len(frags)
+
+
+def test_tp_builder_rejects_bad_views(lib):
+    v = tcv.stream_views(SPEC, 8)
+    with pytest.raises(tc.TcError):
+        tc.tc_tp_fragments(v, 3, 0)          # 256 rows not divisible by 3
+    with pytest.raises(tc.TcError):
+        tc.tc_tp_fragments(v, 8, 8)          # rank out of range
+    bad = v.copy()
+    bad[0]["src_ld"] = 10                    # ld < cols
+    with pytest.raises(tc.TcError):
+        tc.tc_tp_fragments(bad, 8, 0)
+
+
+def test_cast_items_describe_the_slices(lib):
+    tp, rank = 4, 1
+    items = tcv.cast_items(SPEC, tp, rank)
+    n = synth.spec_elems(SPEC)
+    stream = np.arange(n, dtype=np.int64)
+    off = 0
+    q_off = 0
+    s_off = 0
+    for it, (_, rows, cols, split) in zip(items, SPEC):
+        w = stream[off:off + rows * cols].reshape(rows, cols)
+        off += rows * cols
+        sl = oracle.tp_slice(w, split, tp, rank)
+        assert (it["rows"], it["cols"]) == sl.shape
+        # element [0][0] and the row stride of the slice inside the stream
+        assert it["src_off"] == sl[0, 0]
+        if sl.shape[0] > 1:
+            assert it["src_ld"] == sl[1, 0] - sl[0, 0]
+        assert it["dst_off"] == q_off and it["dst_ld"] == sl.shape[1]
+        assert it["scale_off"] == s_off and it["scale_ld"] == (sl.shape[1] + 127) // 128
+        q_off += sl.size
+        s_off += ((sl.shape[0] + 127) // 128) * ((sl.shape[1] + 127) // 128)
