@@ -217,12 +217,12 @@ def run_reshard(torch, tc, synth, args, stream):
     ws = torch.empty(tc.tc_copy_fragments_workspace(len(frags_np)), dtype=torch.uint8, device="cuda")
     shard = torch.empty(tcv.shard_elems(spec, tp), dtype=torch.bfloat16, device="cuda")
     nbytes = 2 * int(frags_np[:, 2].sum())
-    tc.tc_plan_fragments(frags, ws, stream=stream)
-    planned = _time_calls(torch, stream, lambda: tc.tc_copy_planned(stream_t, shard, frags, ws, stream=stream),
+    total = tc.tc_plan_fragments(frags, ws, stream=stream)
+    planned = _time_calls(torch, stream, lambda: tc.tc_copy_planned(stream_t, shard, ws, total, stream=stream),
                           args.warmup, args.cast_steps)
     full = _time_calls(torch, stream, lambda: tc.tc_copy_fragments(stream_t, shard, frags, ws, stream=stream),
                        args.warmup, args.cast_steps)
-    out = {"fragments": int(len(frags_np)), "copy_planned": _stats(planned, nbytes),
+    out = {"fragments": int(len(frags_np)), "tasks": int(total), "copy_planned": _stats(planned, nbytes),
            "plan_and_copy": _stats(full, nbytes)}
     del stream_t, shard, frags, ws
     torch.cuda.empty_cache()
@@ -242,7 +242,7 @@ def run_cast(torch, tc, synth, args, stream):
     q = torch.empty(shard_n, dtype=torch.uint8, device="cuda")
     sc = torch.empty(n_scales, dtype=torch.float32, device="cuda")
     ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device="cuda")
-    it = torch.from_numpy(items.view(np.uint8)).cuda()
+    it = items
     nbytes = 2 * shard_n + shard_n + 4 * n_scales
     ms = _time_calls(torch, stream, lambda: tc.tc_cast_fp8_blockscaled(src, q, sc, it, ws, stream=stream),
                      args.warmup, args.cast_steps)

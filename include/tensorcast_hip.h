@@ -104,28 +104,36 @@ typedef struct {
   uint64_t len;     /* bytes */
 } tc_fragment;
 
-/* Bytes of device workspace tc_copy_fragments / tc_plan_fragments need for
- * n descriptors (the per-fragment work plan). */
+/* Recommended bytes of device workspace for a plan of n descriptors.  A
+ * plan cuts every fragment into tasks of at most `piece` bytes (4 KiB, or the
+ * next power of two that keeps the task table inside the workspace) and
+ * spreads the tasks over the whole GPU.  Any workspace holding at least
+ * n + 1 tasks works (24 bytes each, plus 16 bytes per descriptor of planning
+ * scratch); this size keeps 4 KiB pieces for payloads up to ~8 KiB per
+ * fragment plus 4 GiB. */
 size_t tc_copy_fragments_workspace(int64_t n);
 
-/* Copy every fragment.  frags: device tc_fragment[n].  workspace: device
- * buffer of at least tc_copy_fragments_workspace(n) bytes, used for the work
- * plan (fragments cut into pieces of at most 16 KiB, balanced over the whole
- * GPU).  The call plans and copies; its workspace may be reused as soon as
- * the stream has passed the call. */
+/* Copy every fragment: tc_plan_fragments + tc_copy_planned.  frags: device
+ * tc_fragment[n].  workspace: device buffer, 256-byte aligned.  The call
+ * BLOCKS the host once, until the plan's task count has been computed on the
+ * stream (the copy's launch size depends on it); the copy itself is
+ * asynchronous.  The workspace may be reused once the stream has passed the
+ * copy. */
 tc_status tc_copy_fragments(const void* src_base, void* dst_base, const tc_fragment* frags,
                             int64_t n, void* workspace, size_t workspace_bytes,
                             hipStream_t stream);
 
-/* Split planning from copying for descriptor lists that are reused (a
- * rank's weight-slice list is fixed for a model): tc_plan_fragments writes
- * the plan for frags into workspace; tc_copy_planned then copies using that
- * plan, as often as wanted, while frags and workspace stay unchanged. */
+/* Plan once, copy many times (a rank's weight-slice list is fixed for a
+ * model).  tc_plan_fragments writes the plan for frags into workspace and
+ * returns its task count in *total_tasks (host); it synchronizes the stream
+ * once.  tc_copy_planned then copies with that plan -- asynchronously, as
+ * often as wanted -- for any src/dst bases, while the workspace is kept
+ * unchanged.  total_tasks == 0 means there is nothing to copy. */
 tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace,
-                            size_t workspace_bytes, hipStream_t stream);
-tc_status tc_copy_planned(const void* src_base, void* dst_base, const tc_fragment* frags,
-                          int64_t n, const void* workspace, size_t workspace_bytes,
-                          hipStream_t stream);
+                            size_t workspace_bytes, uint64_t* total_tasks /* host, out */,
+                            hipStream_t stream);
+tc_status tc_copy_planned(const void* src_base, void* dst_base, const void* workspace,
+                          size_t workspace_bytes, uint64_t total_tasks, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Tensor-parallel views: view(slice) + tensor_dict() (Table 2; each rank
@@ -199,10 +207,14 @@ tc_status tc_tp_cast_item(const tc_tp_view* view /* host */, int32_t tp, int32_t
 /* Bytes of device workspace tc_cast_fp8_blockscaled needs for n items. */
 size_t tc_cast_fp8_workspace(int64_t n_items);
 
-/* Cast every item.  items: device tc_cast_item[n_items].  Destination codes
- * and scale grids of different items must not overlap.  tile must be 128.
- * Source rows are read through src_ld, so a strided slice of a full weight
- * is cast in place without a gather. */
+/* Cast every item.  items: HOST array tc_cast_item[n_items] (a model has a
+ * few hundred); the library copies it, with its tile offsets, into the
+ * device workspace (256-byte aligned) through pinned staging memory, so the
+ * host array may be reused as soon as the call returns.  Destination codes
+ * and scale grids of different items must not overlap one another or the
+ * source.  tile must be 128.  Source rows are read through src_ld, so a
+ * strided slice of a full weight is cast in place without a gather.  The
+ * workspace may be reused once the stream has passed the call. */
 tc_status tc_cast_fp8_blockscaled(const void* src_base, void* dst_base, float* scale_base,
                                   const tc_cast_item* items, int64_t n_items, int32_t tile,
                                   void* workspace, size_t workspace_bytes, hipStream_t stream);

@@ -89,8 +89,8 @@ def load():
     L.tc_copy_fragments_workspace.argtypes = [c.c_int64]
     L.tc_copy_fragments_workspace.restype = c.c_size_t
     L.tc_copy_fragments.argtypes = [P, P, P, c.c_int64, P, c.c_size_t, P]
-    L.tc_plan_fragments.argtypes = [P, c.c_int64, P, c.c_size_t, P]
-    L.tc_copy_planned.argtypes = [P, P, P, c.c_int64, P, c.c_size_t, P]
+    L.tc_plan_fragments.argtypes = [P, c.c_int64, P, c.c_size_t, c.POINTER(c.c_uint64), P]
+    L.tc_copy_planned.argtypes = [P, P, P, c.c_size_t, c.c_uint64, P]
     L.tc_tp_fragment_count.argtypes = [P, c.c_int64, c.c_int32, c.c_int32]
     L.tc_tp_fragment_count.restype = c.c_int64
     L.tc_tp_fragments.argtypes = [P, c.c_int64, c.c_int32, c.c_int32, P, c.c_int64,
@@ -193,23 +193,28 @@ def _frag_count(frags) -> int:
 
 def tc_copy_fragments(src, dst, frags, workspace, stream=None) -> None:
     """Copy every (src_off, dst_off, len) row of the device tensor ``frags``
-    (uint64/int64, shape [n, 3]) from ``src`` to ``dst``."""
+    (uint64/int64, shape [n, 3]) from ``src`` to ``dst``.  Blocks once until
+    the plan's task count is known."""
     n = _frag_count(frags)
     _ok(load().tc_copy_fragments(_dev_ptr(src), _dev_ptr(dst), _dev_ptr(frags) if n else None, n,
                                  _dev_ptr(workspace), _nbytes(workspace), _stream(stream)),
         "tc_copy_fragments")
 
 
-def tc_plan_fragments(frags, workspace, stream=None) -> None:
+def tc_plan_fragments(frags, workspace, stream=None) -> int:
+    """Plan the copy of ``frags`` into ``workspace``; returns the task count."""
     n = _frag_count(frags)
+    total = ctypes.c_uint64(0)
     _ok(load().tc_plan_fragments(_dev_ptr(frags) if n else None, n, _dev_ptr(workspace),
-                                 _nbytes(workspace), _stream(stream)), "tc_plan_fragments")
+                                 _nbytes(workspace), ctypes.byref(total), _stream(stream)),
+        "tc_plan_fragments")
+    return int(total.value)
 
 
-def tc_copy_planned(src, dst, frags, workspace, stream=None) -> None:
-    n = _frag_count(frags)
-    _ok(load().tc_copy_planned(_dev_ptr(src), _dev_ptr(dst), _dev_ptr(frags) if n else None, n,
-                               _dev_ptr(workspace), _nbytes(workspace), _stream(stream)),
+def tc_copy_planned(src, dst, workspace, total_tasks: int, stream=None) -> None:
+    """Copy with a plan made by tc_plan_fragments (same workspace, unchanged)."""
+    _ok(load().tc_copy_planned(_dev_ptr(src), _dev_ptr(dst), _dev_ptr(workspace),
+                               _nbytes(workspace), int(total_tasks), _stream(stream)),
         "tc_copy_planned")
 
 
@@ -261,14 +266,12 @@ def tc_cast_fp8_workspace(n_items: int) -> int:
 
 
 def tc_cast_fp8_blockscaled(src, dst, scales, items, workspace, stream=None, tile: int = 128) -> None:
-    """Cast every item; ``items`` is a device tensor holding CAST_ITEM_DTYPE
-    records (64 bytes each)."""
-    nb = _nbytes(items)
-    if nb % CAST_ITEM_DTYPE.itemsize:
-        raise ValueError("items tensor is not a whole number of records")
-    n = nb // CAST_ITEM_DTYPE.itemsize
+    """Cast every item; ``items`` is a host numpy array of CAST_ITEM_DTYPE
+    records (the library stages it into ``workspace``)."""
+    it = np.ascontiguousarray(items, dtype=CAST_ITEM_DTYPE).reshape(-1)
+    n = it.size
     _ok(load().tc_cast_fp8_blockscaled(_dev_ptr(src), _dev_ptr(dst), _dev_ptr(scales),
-                                       _dev_ptr(items) if n else None, n, tile, _dev_ptr(workspace),
+                                       it.ctypes.data if n else None, n, tile, _dev_ptr(workspace),
                                        _nbytes(workspace), _stream(stream)),
         "tc_cast_fp8_blockscaled")
 

@@ -5,6 +5,8 @@
 #include <algorithm>
 #include <cstdlib>
 #include <cstring>
+#include <initializer_list>
+#include <mutex>
 #include <vector>
 
 #include "tc_internal.h"
@@ -192,6 +194,56 @@ void view_fragments(const tc_tp_view& v, int32_t tp, int32_t rank, Emit emit) {
                      v.dst_off + uint64_t(r) * uint64_t(v.dst_ld) * eb, row_bytes});
 }
 
+
+// Pinned host staging for small host-side tables copied to a device
+// workspace: one buffer per device, reused once the previous copy out of it
+// has completed.
+struct Piece {
+  const void* data;
+  size_t bytes;
+  size_t offset;  // in the device destination
+};
+
+struct Staging {
+  void* host = nullptr;
+  size_t cap = 0;
+  hipEvent_t done = nullptr;
+};
+
+std::mutex g_staging_mu;
+Staging g_staging[64];
+
+tc_status stage_to_device(void* dev_dst, hipStream_t s, std::initializer_list<Piece> pieces) {
+  size_t need = 0;
+  for (const Piece& p : pieces) need = std::max(need, p.offset + p.bytes);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e);
+  if (dev < 0 || dev >= 64) return hip_fail(hipErrorInvalidDevice);
+  std::lock_guard<std::mutex> lock(g_staging_mu);
+  Staging& st = g_staging[dev];
+  if (st.done) {
+    e = hipEventSynchronize(st.done);  // the previous copy has left the buffer
+    if (e != hipSuccess) return hip_fail(e);
+  } else {
+    e = hipEventCreateWithFlags(&st.done, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  if (st.cap < need) {
+    if (st.host) (void)hipHostFree(st.host);
+    st.host = nullptr;
+    st.cap = 0;
+    size_t cap = std::max<size_t>(need, 1 << 16);
+    e = hipHostMalloc(&st.host, cap, hipHostMallocDefault);
+    if (e != hipSuccess) return hip_fail(e);
+    st.cap = cap;
+  }
+  for (const Piece& p : pieces) std::memcpy(static_cast<uint8_t*>(st.host) + p.offset, p.data, p.bytes);
+  e = hipMemcpyAsync(dev_dst, st.host, need, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipEventRecord(st.done, s);
+  return check(e);
+}
+
 }  // namespace
 
 namespace tc {
@@ -230,53 +282,95 @@ size_t tc_copy_fragments_workspace(int64_t n) {
   return tc::frag_workspace_bytes(n);
 }
 
-static tc_status validate_fragments(const void* src_base, const void* dst_base,
-                                    const tc_fragment* frags, int64_t n, hipStream_t s) {
-  std::vector<tc_fragment> h;
-  tc_status st = fetch(frags, n, &h, s);
-  if (st != TC_OK) return st;
+// Debug checks of a descriptor list: no overflow, destination ranges pairwise
+// disjoint and, when both bases are known, no destination range overlapping
+// a source range.
+static tc_status check_ranges(const void* src_base, const void* dst_base,
+                              const std::vector<tc_fragment>& h) {
   std::vector<Range> d, sr;
   d.reserve(h.size());
   sr.reserve(h.size());
   const uint64_t sb = (uint64_t)(uintptr_t)src_base, db = (uint64_t)(uintptr_t)dst_base;
   for (const tc_fragment& f : h) {
     if (f.src_off + f.len < f.src_off || f.dst_off + f.len < f.dst_off) return TC_ERR_OUT_OF_RANGE;
+    if (sb + f.src_off + f.len < sb || db + f.dst_off + f.len < db) return TC_ERR_OUT_OF_RANGE;
     d.push_back({db + f.dst_off, db + f.dst_off + f.len});
     sr.push_back({sb + f.src_off, sb + f.src_off + f.len});
   }
   if (any_overlap(d)) return TC_ERR_ALIAS;
-  if (cross_overlap(d, sr)) return TC_ERR_ALIAS;
+  if (src_base && dst_base && cross_overlap(d, sr)) return TC_ERR_ALIAS;
   return TC_OK;
 }
 
-tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace,
-                            size_t workspace_bytes, hipStream_t stream) {
-  if (n < 0) return TC_ERR_INVALID_ARGUMENT;
-  if (n == 0) return TC_OK;
-  if (!frags || !workspace) return TC_ERR_INVALID_ARGUMENT;
-  if (workspace_bytes < tc::frag_workspace_bytes(n)) return TC_ERR_WORKSPACE;
-  if ((uintptr_t)workspace % 8) return TC_ERR_INVALID_ARGUMENT;
-  return check(tc::launch_plan_fragments(frags, n, workspace, stream));
+static uint64_t pow2_at_least(uint64_t x) {
+  uint64_t p = 1;
+  while (p < x) p <<= 1;
+  return p;
 }
 
-tc_status tc_copy_planned(const void* src_base, void* dst_base, const tc_fragment* frags,
-                          int64_t n, const void* workspace, size_t workspace_bytes,
-                          hipStream_t stream) {
+tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace,
+                            size_t workspace_bytes, uint64_t* total_tasks, hipStream_t stream) {
   if (n < 0) return TC_ERR_INVALID_ARGUMENT;
+  if (total_tasks) *total_tasks = 0;
   if (n == 0) return TC_OK;
-  if (!src_base || !dst_base || !frags || !workspace) return TC_ERR_INVALID_ARGUMENT;
-  if (workspace_bytes < tc::frag_workspace_bytes(n)) return TC_ERR_WORKSPACE;
-  if ((uintptr_t)workspace % 8) return TC_ERR_INVALID_ARGUMENT;
+  if (!frags || !workspace || (uintptr_t)workspace % 256) return TC_ERR_INVALID_ARGUMENT;
+  const tc::PlanLayout L = tc::plan_layout(n, workspace_bytes);
+  if (L.capacity < uint64_t(n) + 1) return TC_ERR_WORKSPACE;
   if (validating()) {
-    tc_status st = validate_fragments(src_base, dst_base, frags, n, stream);
+    std::vector<tc_fragment> h;
+    tc_status st = fetch(frags, n, &h, stream);
+    if (st != TC_OK) return st;
+    st = check_ranges(nullptr, nullptr, h);
     if (st != TC_OK) return st;
   }
-  tc::DeviceInfo di;
-  hipError_t e = tc::device_info(&di);
+  uint64_t piece = tc::kMinPiece;
+  tc::PlanHeader hdr;
+  for (int attempt = 0; attempt < 2; ++attempt) {
+    hipError_t e = tc::launch_plan_count(frags, n, piece, workspace, L, stream);
+    if (e != hipSuccess) return hip_fail(e);
+    // The launch size of the copy depends on the task count: read it back.
+    e = hipMemcpyAsync(&hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(e);
+    if (hdr.total_tasks <= L.capacity) break;
+    // Too many 4 KiB pieces for the workspace: larger pieces bound the count
+    // by n + payload / piece <= capacity.
+    const uint64_t room = L.capacity - uint64_t(n);
+    piece = pow2_at_least(std::max<uint64_t>(tc::kMinPiece, (hdr.payload + room - 1) / room));
+  }
+  if (hdr.total_tasks > L.capacity) return TC_ERR_WORKSPACE;
+  hipError_t e = tc::launch_plan_expand(frags, n, hdr.total_tasks, piece, workspace, L, stream);
   if (e != hipSuccess) return hip_fail(e);
-  return check(tc::launch_copy_planned(static_cast<const uint8_t*>(src_base),
-                                       static_cast<uint8_t*>(dst_base), frags, n, workspace, di,
-                                       stream));
+  if (total_tasks) *total_tasks = hdr.total_tasks;
+  return TC_OK;
+}
+
+tc_status tc_copy_planned(const void* src_base, void* dst_base, const void* workspace,
+                          size_t workspace_bytes, uint64_t total_tasks, hipStream_t stream) {
+  if (total_tasks == 0) return TC_OK;
+  if (!src_base || !dst_base || !workspace || (uintptr_t)workspace % 256)
+    return TC_ERR_INVALID_ARGUMENT;
+  // The plan's own fragment count sizes its layout.
+  tc::PlanHeader hdr;
+  hipError_t e = hipSuccess;
+  if (validating()) {
+    e = hipMemcpyAsync(&hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(e);
+    if (hdr.total_tasks != total_tasks) return TC_ERR_INVALID_ARGUMENT;
+    const tc::PlanLayout L = tc::plan_layout((int64_t)hdr.n, workspace_bytes);
+    if (total_tasks > L.capacity) return TC_ERR_WORKSPACE;
+    std::vector<tc_fragment> tasks;
+    tc_status st = fetch(reinterpret_cast<const tc_fragment*>(static_cast<const uint8_t*>(workspace) +
+                                                              tc::kTasksOffset),
+                         (int64_t)total_tasks, &tasks, stream);
+    if (st != TC_OK) return st;
+    st = check_ranges(src_base, dst_base, tasks);
+    if (st != TC_OK) return st;
+  }
+  return check(tc::launch_copy_tasks(static_cast<const uint8_t*>(src_base),
+                                     static_cast<uint8_t*>(dst_base), workspace, total_tasks,
+                                     stream));
 }
 
 tc_status tc_copy_fragments(const void* src_base, void* dst_base, const tc_fragment* frags,
@@ -285,9 +379,17 @@ tc_status tc_copy_fragments(const void* src_base, void* dst_base, const tc_fragm
   if (n < 0) return TC_ERR_INVALID_ARGUMENT;
   if (n == 0) return TC_OK;
   if (!src_base || !dst_base || !frags || !workspace) return TC_ERR_INVALID_ARGUMENT;
-  tc_status st = tc_plan_fragments(frags, n, workspace, workspace_bytes, stream);
+  if (validating()) {
+    std::vector<tc_fragment> h;
+    tc_status st = fetch(frags, n, &h, stream);
+    if (st != TC_OK) return st;
+    st = check_ranges(src_base, dst_base, h);
+    if (st != TC_OK) return st;
+  }
+  uint64_t total = 0;
+  tc_status st = tc_plan_fragments(frags, n, workspace, workspace_bytes, &total, stream);
   if (st != TC_OK) return st;
-  return tc_copy_planned(src_base, dst_base, frags, n, workspace, workspace_bytes, stream);
+  return tc_copy_planned(src_base, dst_base, workspace, workspace_bytes, total, stream);
 }
 
 int64_t tc_tp_fragment_count(const tc_tp_view* views, int64_t n_views, int32_t tp, int32_t rank) {
@@ -344,44 +446,56 @@ tc_status tc_cast_fp8_blockscaled(const void* src_base, void* dst_base, float* s
   if (n_items == 0) return TC_OK;
   if (!src_base || !dst_base || !scale_base || !items || !workspace) return TC_ERR_INVALID_ARGUMENT;
   if (workspace_bytes < tc::cast_workspace_bytes(n_items)) return TC_ERR_WORKSPACE;
-  if ((uintptr_t)workspace % 8 || (uintptr_t)src_base % 2 || (uintptr_t)scale_base % 4)
+  if ((uintptr_t)workspace % 256 || (uintptr_t)src_base % 2 || (uintptr_t)scale_base % 4)
     return TC_ERR_INVALID_ARGUMENT;
+  // Geometry and the tile prefix, on the host.
+  std::vector<uint64_t> prefix((size_t)n_items + 1);
+  uint64_t total = 0;
+  for (int64_t i = 0; i < n_items; ++i) {
+    const tc_cast_item& it = items[i];
+    if (it.rows < 0 || it.cols < 0 || it.src_ld < it.cols || it.dst_ld < it.cols)
+      return TC_ERR_INVALID_ARGUMENT;
+    const uint64_t tr = uint64_t((it.rows + 127) / 128), tcn = uint64_t((it.cols + 127) / 128);
+    if (it.rows > 0 && it.cols > 0 && it.scale_ld < int64_t(tcn)) return TC_ERR_INVALID_ARGUMENT;
+    prefix[(size_t)i] = total;
+    total += (it.rows > 0 && it.cols > 0) ? tr * tcn : 0;
+  }
+  prefix[(size_t)n_items] = total;
+  if (total == 0) return TC_OK;
   if (validating()) {
-    std::vector<tc_cast_item> h;
-    tc_status st = fetch(items, n_items, &h, stream);
-    if (st != TC_OK) return st;
-    std::vector<Range> q, sc, src;
+    std::vector<Range> q, sc, srcr;
     const uint64_t db = (uint64_t)(uintptr_t)dst_base, sb = (uint64_t)(uintptr_t)scale_base;
     const uint64_t xb = (uint64_t)(uintptr_t)src_base;
-    for (const tc_cast_item& it : h) {
-      if (it.rows < 0 || it.cols < 0 || it.src_ld < it.cols || it.dst_ld < it.cols)
-        return TC_ERR_INVALID_ARGUMENT;
-      const int64_t tc_cols = (it.cols + 127) / 128, tr = (it.rows + 127) / 128;
-      if (it.scale_ld < tc_cols) return TC_ERR_INVALID_ARGUMENT;
+    for (int64_t i = 0; i < n_items; ++i) {
+      const tc_cast_item& it = items[i];
       if (it.rows == 0 || it.cols == 0) continue;
-      // destination rows
+      const int64_t tcn = (it.cols + 127) / 128, tr = (it.rows + 127) / 128;
       for (int64_t r = 0; r < it.rows; ++r) {
         const uint64_t a = db + it.dst_off + uint64_t(r) * uint64_t(it.dst_ld);
         q.push_back({a, a + uint64_t(it.cols)});
         const uint64_t x = xb + 2 * (it.src_off + uint64_t(r) * uint64_t(it.src_ld));
-        src.push_back({x, x + 2 * uint64_t(it.cols)});
+        srcr.push_back({x, x + 2 * uint64_t(it.cols)});
       }
       for (int64_t r = 0; r < tr; ++r) {
         const uint64_t a = sb + 4 * (it.scale_off + uint64_t(r) * uint64_t(it.scale_ld));
-        sc.push_back({a, a + 4 * uint64_t(tc_cols)});
+        sc.push_back({a, a + 4 * uint64_t(tcn)});
       }
     }
     std::vector<Range> outs = q;
     outs.insert(outs.end(), sc.begin(), sc.end());
     if (any_overlap(outs)) return TC_ERR_ALIAS;
-    if (cross_overlap(outs, src)) return TC_ERR_ALIAS;
+    if (cross_overlap(outs, srcr)) return TC_ERR_ALIAS;
   }
-  tc::DeviceInfo di;
-  hipError_t e = tc::device_info(&di);
-  if (e != hipSuccess) return hip_fail(e);
+  // Items and prefix go to the workspace through pinned staging memory, so
+  // the caller's host array is free as soon as this call returns.
+  const size_t items_bytes = sizeof(tc_cast_item) * (size_t)n_items;
+  const size_t prefix_at = (items_bytes + 255) & ~size_t(255);
+  tc_status st = stage_to_device(workspace, stream, {{items, items_bytes, 0},
+                                                     {prefix.data(), 8 * prefix.size(), prefix_at}});
+  if (st != TC_OK) return st;
   return check(tc::launch_cast_blockscaled(static_cast<const uint16_t*>(src_base),
-                                           static_cast<uint8_t*>(dst_base), scale_base, items,
-                                           n_items, workspace, di, stream));
+                                           static_cast<uint8_t*>(dst_base), scale_base, workspace,
+                                           n_items, total, stream));
 }
 
 tc_status tc_cast_fp8_scaled(const void* src_bf16, int64_t n, float scale, void* dst_e4m3,

@@ -87,18 +87,40 @@ __device__ __forceinline__ uint8_t code1(uint16_t bits, int mode, float s) {
   return (uint8_t)(cvt2<false>(q, q, 0) & 0xFFu);
 }
 
-// Reduce a per-thread 15-bit amax over the workgroup.  red is a 2 x 4 array
-// used alternately by consecutive tiles, so one barrier per tile suffices.
+constexpr int kCastThreads = 1024;  // one 128x128 tile per workgroup, 16 elements per thread
+constexpr int kCastWaves = kCastThreads / kWaveLanes;
+constexpr int kXcds = 8;
+constexpr uint64_t kCastXcdGroup = 16;  // consecutive tiles per XCD run
+
+// Work item of block b when the 8 XCDs each take runs of G consecutive tiles
+// (a bijection on [0, N); the last partial round keeps the identity order).
+__device__ __forceinline__ uint64_t xcd_grouped(uint64_t b, uint64_t N, uint64_t G) {
+  const uint64_t round = uint64_t(kXcds) * G;
+  const uint64_t full = (N / round) * round;
+  if (b >= full) return b;
+  const uint64_t x = b % kXcds, l = b / kXcds;
+  return (l / G) * round + x * G + (l % G);
+}
+
+__device__ __forceinline__ u32x4 ld_nt(const u32x4* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ void st_nt(u32x2* p, u32x2 v) { __builtin_nontemporal_store(v, p); }
+
+// Reduce a per-thread 15-bit amax over the workgroup.  red has one slot per
+// wave and is used alternately by consecutive tiles (two buffers), so one
+// barrier per tile suffices.
 __device__ __forceinline__ uint32_t block_amax(uint32_t m, uint32_t* red) {
 #pragma unroll
   for (int d = kWaveLanes / 2; d >= 1; d >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, d, kWaveLanes));
   if ((threadIdx.x & (kWaveLanes - 1)) == 0) red[threadIdx.x >> 6] = m;
   __syncthreads();
-  return max(max(red[0], red[1]), max(red[2], red[3]));
+  uint32_t r = 0;
+#pragma unroll
+  for (int k = 0; k < kCastWaves; ++k) r = max(r, red[k]);
+  return r;
 }
 
 // Item whose tile range contains tile t: last i in [0, n) with
-// prefix[i] <= t, given prefix[0] <= t < prefix[n].
+// prefix[i] <= t, given prefix[0] <= t < prefix[n].  64-way search per wave.
 __device__ int64_t find_item(const uint64_t* __restrict__ prefix, int64_t n, uint64_t t, int lane) {
   int64_t lo = 0, hi = n;
   while (hi - lo > 1) {
@@ -111,60 +133,25 @@ __device__ int64_t find_item(const uint64_t* __restrict__ prefix, int64_t n, uin
   return lo;
 }
 
-// One workgroup: prefix[i] = number of tiles of items [0, i), prefix[n] = total.
-__global__ __launch_bounds__(kThreads) void k_cast_plan(const tc_cast_item* __restrict__ items,
-                                                       const int64_t n,
-                                                       uint64_t* __restrict__ prefix) {
-  __shared__ uint64_t wave_tot[kThreads / kWaveLanes];
+// One workgroup per tile (grid-stride only when the grid is capped).  The
+// items and their tile prefix are staged by the host into the workspace.
+__global__ __launch_bounds__(kCastThreads) void k_cast_tiles(const uint16_t* __restrict__ src,
+                                                            uint8_t* __restrict__ dst,
+                                                            float* __restrict__ scales,
+                                                            const tc_cast_item* __restrict__ items,
+                                                            const uint64_t* __restrict__ prefix,
+                                                            const int64_t n_items,
+                                                            const uint64_t total) {
+  __shared__ uint32_t red[2][kCastWaves];
   const int lane = threadIdx.x & (kWaveLanes - 1);
-  const int w = threadIdx.x >> 6;
-  uint64_t carry = 0;
-  for (int64_t base = 0; base < n; base += kThreads) {
-    const int64_t i = base + threadIdx.x;
-    uint64_t v = 0;
-    if (i < n) {
-      const int64_t rows = items[i].rows, cols = items[i].cols;
-      v = uint64_t((rows + kTile - 1) / kTile) * uint64_t((cols + kTile - 1) / kTile);
-    }
-    uint64_t incl = v;
-#pragma unroll
-    for (int d = 1; d < kWaveLanes; d <<= 1) {
-      const uint32_t lo = __shfl_up((uint32_t)incl, d, kWaveLanes);
-      const uint32_t hi = __shfl_up((uint32_t)(incl >> 32), d, kWaveLanes);
-      if (lane >= d) incl += (uint64_t(hi) << 32) | lo;
-    }
-    if (lane == kWaveLanes - 1) wave_tot[w] = incl;
-    __syncthreads();
-    uint64_t before = 0, total = 0;
-#pragma unroll
-    for (int k = 0; k < kThreads / kWaveLanes; ++k) {
-      if (k < w) before += wave_tot[k];
-      total += wave_tot[k];
-    }
-    __syncthreads();
-    if (i < n) prefix[i] = carry + before + incl - v;
-    carry += total;
-  }
-  if (threadIdx.x == 0) prefix[n] = carry;
-}
-
-// Persistent grid: workgroup b takes tiles b, b + grid, ...
-__global__ __launch_bounds__(kThreads) void k_cast_tiles(const uint16_t* __restrict__ src,
-                                                        uint8_t* __restrict__ dst,
-                                                        float* __restrict__ scales,
-                                                        const tc_cast_item* __restrict__ items,
-                                                        const int64_t n_items,
-                                                        const uint64_t* __restrict__ prefix) {
-  __shared__ uint32_t red[2][kThreads / kWaveLanes];
-  const int lane = threadIdx.x & (kWaveLanes - 1);
-  const uint64_t total = prefix[n_items];
-  // Fast-path thread layout: 16 lanes per row (8 bf16 = 16 B each), 16 rows
-  // per pass, 8 passes.
+  // Fast-path layout: 16 lanes per row (8 bf16 = 16 B each), 64 rows per
+  // pass; each thread takes rows prow and prow + 64.
   const int seg = threadIdx.x & 15;
   const int prow = threadIdx.x >> 4;
   int parity = 0;
-  for (uint64_t t = blockIdx.x; t < total; t += gridDim.x, parity ^= 1) {
+  for (uint64_t b = blockIdx.x; b < total; b += gridDim.x, parity ^= 1) {
     uint32_t* rbuf = red[parity];
+    const uint64_t t = xcd_grouped(b, total, kCastXcdGroup);
     const int64_t it = find_item(prefix, n_items, t, lane);
     const tc_cast_item item = items[it];
     const int64_t tiles_c = (item.cols + kTile - 1) / kTile;
@@ -180,52 +167,47 @@ __global__ __launch_bounds__(kThreads) void k_cast_tiles(const uint16_t* __restr
                       ((reinterpret_cast<uintptr_t>(xs) | uint64_t(item.src_ld) * 2) & 15) == 0 &&
                       ((reinterpret_cast<uintptr_t>(qs) | uint64_t(item.dst_ld)) & 7) == 0;
     if (fast) {
-      u32x4 v[8];
-#pragma unroll
-      for (int p = 0; p < 8; ++p)
-        v[p] = *reinterpret_cast<const u32x4*>(xs + int64_t(p * 16 + prow) * item.src_ld + seg * 8);
+      const u32x4 v0 = ld_nt(reinterpret_cast<const u32x4*>(xs + int64_t(prow) * item.src_ld + seg * 8));
+      const u32x4 v1 =
+          ld_nt(reinterpret_cast<const u32x4*>(xs + int64_t(prow + 64) * item.src_ld + seg * 8));
       uint32_t m2 = 0;
-#pragma unroll
-      for (int p = 0; p < 8; ++p) {
-        m2 = absmax2(m2, v[p].x);
-        m2 = absmax2(m2, v[p].y);
-        m2 = absmax2(m2, v[p].z);
-        m2 = absmax2(m2, v[p].w);
-      }
+      m2 = absmax2(m2, v0.x);
+      m2 = absmax2(m2, v0.y);
+      m2 = absmax2(m2, v0.z);
+      m2 = absmax2(m2, v0.w);
+      m2 = absmax2(m2, v1.x);
+      m2 = absmax2(m2, v1.y);
+      m2 = absmax2(m2, v1.z);
+      m2 = absmax2(m2, v1.w);
       const uint32_t amax_bits = block_amax(max(m2 & 0xFFFFu, m2 >> 16), rbuf);
       float s;
-      u32x2 out[8];
+      u32x2 o0, o1;
       if (amax_bits >= 0x7F80u) {  // Inf or NaN in the tile
         s = __uint_as_float(0x7FC00000u);
-#pragma unroll
-        for (int p = 0; p < 8; ++p) out[p] = u32x2{0x7F7F7F7Fu, 0x7F7F7F7Fu};
+        o0 = o1 = u32x2{0x7F7F7F7Fu, 0x7F7F7F7Fu};
       } else if (amax_bits == 0) {
         s = 0.0f;
-#pragma unroll
-        for (int p = 0; p < 8; ++p)
-          out[p] = u32x2{codes4_zero(v[p].x, v[p].y), codes4_zero(v[p].z, v[p].w)};
+        o0 = u32x2{codes4_zero(v0.x, v0.y), codes4_zero(v0.z, v0.w)};
+        o1 = u32x2{codes4_zero(v1.x, v1.y), codes4_zero(v1.z, v1.w)};
       } else {
         s = __uint_as_float(amax_bits << 16) / 448.0f;
         if (s >= 0x1.0p-126f) {
           const float r = 1.0f / s;
-#pragma unroll
-          for (int p = 0; p < 8; ++p)
-            out[p] = u32x2{codes4_fast(v[p].x, v[p].y, r, s), codes4_fast(v[p].z, v[p].w, r, s)};
+          o0 = u32x2{codes4_fast(v0.x, v0.y, r, s), codes4_fast(v0.z, v0.w, r, s)};
+          o1 = u32x2{codes4_fast(v1.x, v1.y, r, s), codes4_fast(v1.z, v1.w, r, s)};
         } else {
-#pragma unroll
-          for (int p = 0; p < 8; ++p)
-            out[p] = u32x2{codes4_div(v[p].x, v[p].y, s), codes4_div(v[p].z, v[p].w, s)};
+          o0 = u32x2{codes4_div(v0.x, v0.y, s), codes4_div(v0.z, v0.w, s)};
+          o1 = u32x2{codes4_div(v1.x, v1.y, s), codes4_div(v1.z, v1.w, s)};
         }
       }
-#pragma unroll
-      for (int p = 0; p < 8; ++p)
-        *reinterpret_cast<u32x2*>(qs + int64_t(p * 16 + prow) * item.dst_ld + seg * 8) = out[p];
+      st_nt(reinterpret_cast<u32x2*>(qs + int64_t(prow) * item.dst_ld + seg * 8), o0);
+      st_nt(reinterpret_cast<u32x2*>(qs + int64_t(prow + 64) * item.dst_ld + seg * 8), o1);
       if (threadIdx.x == 0) *sp = s;
     } else {
       // Edge or unaligned tile: element by element.
       const int64_t cnt = h * wd;
       uint32_t m = 0;
-      for (int64_t e = threadIdx.x; e < cnt; e += kThreads) {
+      for (int64_t e = threadIdx.x; e < cnt; e += kCastThreads) {
         const int64_t rr = e / wd, cc = e - rr * wd;
         m = max(m, uint32_t(xs[rr * item.src_ld + cc]) & 0x7FFFu);
       }
@@ -242,7 +224,7 @@ __global__ __launch_bounds__(kThreads) void k_cast_tiles(const uint16_t* __restr
         mode = 0;
         s = __uint_as_float(amax_bits << 16) / 448.0f;
       }
-      for (int64_t e = threadIdx.x; e < cnt; e += kThreads) {
+      for (int64_t e = threadIdx.x; e < cnt; e += kCastThreads) {
         const int64_t rr = e / wd, cc = e - rr * wd;
         qs[rr * item.dst_ld + cc] = code1(xs[rr * item.src_ld + cc], mode, s);
       }
@@ -292,26 +274,27 @@ __global__ __launch_bounds__(kThreads) void k_cast_scaled(const uint16_t* __rest
   }
 }
 
-int g_cast_blocks_per_cu = 0;
+constexpr uint64_t kMaxGrid = uint64_t(1) << 22;
 
 }  // namespace
 
-size_t cast_workspace_bytes(int64_t n_items) { return size_t(8) * size_t(n_items + 1) + 256; }
+static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+size_t cast_workspace_bytes(int64_t n_items) {
+  return align256(sizeof(tc_cast_item) * size_t(n_items)) + 8 * size_t(n_items + 1);
+}
 
 hipError_t launch_cast_blockscaled(const uint16_t* src, uint8_t* dst, float* scales,
-                                   const tc_cast_item* items, int64_t n_items, void* ws,
-                                   const DeviceInfo& di, hipStream_t s) {
-  if (g_cast_blocks_per_cu == 0) {
-    int per_cu = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_cast_tiles, kThreads, 0);
-    if (e != hipSuccess) return e;
-    g_cast_blocks_per_cu = per_cu > 0 ? per_cu : 1;
-  }
-  uint64_t* prefix = reinterpret_cast<uint64_t*>(ws);
-  hipLaunchKernelGGL(k_cast_plan, dim3(1), dim3(kThreads), 0, s, items, n_items, prefix);
-  const unsigned grid = (unsigned)(di.cus * g_cast_blocks_per_cu);
-  hipLaunchKernelGGL(k_cast_tiles, dim3(grid), dim3(kThreads), 0, s, src, dst, scales, items,
-                     n_items, (const uint64_t*)prefix);
+                                   const void* ws, int64_t n_items, uint64_t total_tiles,
+                                   hipStream_t s) {
+  if (total_tiles == 0) return hipSuccess;
+  const uint8_t* base = static_cast<const uint8_t*>(ws);
+  const tc_cast_item* items = reinterpret_cast<const tc_cast_item*>(base);
+  const uint64_t* prefix =
+      reinterpret_cast<const uint64_t*>(base + align256(sizeof(tc_cast_item) * size_t(n_items)));
+  const unsigned grid = (unsigned)(total_tiles < kMaxGrid ? total_tiles : kMaxGrid);
+  hipLaunchKernelGGL(k_cast_tiles, dim3(grid), dim3(kCastThreads), 0, s, src, dst, scales, items,
+                     prefix, n_items, total_tiles);
   return hipGetLastError();
 }
 

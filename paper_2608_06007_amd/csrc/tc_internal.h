@@ -8,17 +8,42 @@
 
 namespace tc {
 
-// Fragments are cut into pieces of at most this many bytes; a wave copies
-// one piece at a time.
-constexpr uint64_t kPieceBytes = 16 * 1024;
-// Tasks (pieces) a wave takes per visit of the plan.
-constexpr int kTasksPerChunk = 8;
-// Descriptors summed by one workgroup of the planning kernels.
+// Fragment plans cut fragments into tasks of at most `piece` bytes; the piece
+// is the smallest power of two >= kMinPiece that keeps the task table within
+// the workspace.
+constexpr uint64_t kMinPiece = 4096;
+// Descriptors handled by one workgroup of the planning kernels.
 constexpr int kPlanPerBlock = 1024;
 
 struct RegionTable {
   uint64_t base[TC_MAX_REGIONS];
 };
+
+// One task of a fragment plan: a byte run of at most `piece` bytes.
+struct Task {
+  uint64_t src_off, dst_off, len;
+};
+
+// Header at the start of a fragment-plan workspace.
+struct PlanHeader {
+  uint64_t total_tasks;  // written by the planning kernels
+  uint64_t piece;        // task size chosen for this plan
+  uint64_t payload;      // sum of the fragment lengths
+  uint64_t n;            // number of fragments planned
+  uint64_t capacity;     // task-table entries that fit the workspace
+  uint64_t pad[3];
+};
+
+// Workspace layout: header | tasks[capacity] | ... | tstart[n + 1] | block sums.
+// The task table sits at a fixed offset so a copy needs only the workspace
+// base; the planning scratch lives at the end.
+constexpr size_t kTasksOffset = 256;
+struct PlanLayout {
+  size_t tstart, blocks, capacity;
+};
+PlanLayout plan_layout(int64_t n, size_t ws_bytes);
+size_t frag_workspace_bytes(int64_t n);
+size_t frag_workspace_min_bytes(int64_t n);
 
 // Launch geometry of the current device.
 struct DeviceInfo {
@@ -33,18 +58,22 @@ hipError_t launch_blocks(const RegionTable& tab, int32_t num_regions, int64_t bl
                          bool gather, bool aligned, hipStream_t s);
 
 // --- fragments ---------------------------------------------------------
-// Workspace layout (bytes): [0, 8*(n+1))       tstart: first task of each fragment, tstart[n] = total
-//                            [.., + 8*nblocks)  per-block task sums, then their exclusive prefix
-size_t frag_workspace_bytes(int64_t n);
-hipError_t launch_plan_fragments(const tc_fragment* frags, int64_t n, void* ws, hipStream_t s);
-hipError_t launch_copy_planned(const uint8_t* src, uint8_t* dst, const tc_fragment* frags,
-                               int64_t n, const void* ws, const DeviceInfo& di, hipStream_t s);
+// Count pieces of `piece` bytes per fragment and write tstart; the header
+// receives the totals.  Enqueued only (no synchronization).
+hipError_t launch_plan_count(const tc_fragment* frags, int64_t n, uint64_t piece, void* ws,
+                             const PlanLayout& L, hipStream_t s);
+// Expand the counted plan into its task table (total_tasks known on the host).
+hipError_t launch_plan_expand(const tc_fragment* frags, int64_t n, uint64_t total_tasks,
+                              uint64_t piece, void* ws, const PlanLayout& L, hipStream_t s);
+hipError_t launch_copy_tasks(const uint8_t* src, uint8_t* dst, const void* ws,
+                             uint64_t total_tasks, hipStream_t s);
 
 // --- fp8 cast ----------------------------------------------------------
+// ws holds the items followed by their tile prefix (n + 1 entries).
 size_t cast_workspace_bytes(int64_t n_items);
 hipError_t launch_cast_blockscaled(const uint16_t* src, uint8_t* dst, float* scales,
-                                   const tc_cast_item* items, int64_t n_items, void* ws,
-                                   const DeviceInfo& di, hipStream_t s);
+                                   const void* ws, int64_t n_items, uint64_t total_tiles,
+                                   hipStream_t s);
 hipError_t launch_cast_scaled(const uint16_t* src, int64_t n, float scale, uint8_t* dst,
                               hipStream_t s);
 

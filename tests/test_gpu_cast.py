@@ -88,9 +88,8 @@ def _cast_matrices(src_bits_1d: np.ndarray, mats, code_pad=0, scale_pad=0):
     src = _to_dev_bits(src_bits_1d)
     dst = torch.full((max(q_off, 1),), 0xCC, dtype=torch.uint8, device=DEV)
     scales = torch.full((max(s_off, 1),), -7.0, dtype=torch.float32, device=DEV)
-    dev_items = torch.from_numpy(items.view(np.uint8)).to(DEV)
     ws = torch.empty(tc.tc_cast_fp8_workspace(len(mats)), dtype=torch.uint8, device=DEV)
-    tc.tc_cast_fp8_blockscaled(src, dst, scales, dev_items, ws)
+    tc.tc_cast_fp8_blockscaled(src, dst, scales, items, ws)
     torch.cuda.synchronize()
     hq, hs = _host(dst), _host(scales)
     for k, (so, rows, cols, ld) in enumerate(mats):
@@ -184,7 +183,7 @@ def test_tp_shard_cast_70b_layers(layers, ranks):
         q = torch.empty(tcv.shard_elems(spec, tp), dtype=torch.uint8, device=DEV)
         s = torch.empty(tcv.scale_elems(spec, tp), dtype=torch.float32, device=DEV)
         ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device=DEV)
-        tc.tc_cast_fp8_blockscaled(stream, q, s, torch.from_numpy(items.view(np.uint8)).to(DEV), ws)
+        tc.tc_cast_fp8_blockscaled(stream, q, s, items, ws)
         torch.cuda.synchronize()
         hq, hs = _host(q), _host(s)
         off = 0
@@ -228,7 +227,7 @@ def test_tp_shard_cast_70b_full_size():
     q = torch.empty(tcv.shard_elems(spec, tp), dtype=torch.uint8, device=DEV)
     s = torch.empty(tcv.scale_elems(spec, tp), dtype=torch.float32, device=DEV)
     ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device=DEV)
-    tc.tc_cast_fp8_blockscaled(stream, q, s, torch.from_numpy(items.view(np.uint8)).to(DEV), ws)
+    tc.tc_cast_fp8_blockscaled(stream, q, s, items, ws)
     torch.cuda.synchronize()
     # no poisoned tile: every scale is what an N(0, 0.02) tile gives
     assert bool(((s > 1e-5) & (s < 1e-3)).all())

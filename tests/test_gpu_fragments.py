@@ -33,8 +33,9 @@ def _copy_and_check(src, frags_np, dst_size, sentinel=0x5A, planned=False):
     n = len(frags_np)
     ws = torch.empty(max(tc.tc_copy_fragments_workspace(n), 8), dtype=torch.uint8, device=DEV)
     if planned:
-        tc.tc_plan_fragments(frags, ws)
-        tc.tc_copy_planned(src, dst, frags, ws)
+        total = tc.tc_plan_fragments(frags, ws)
+        tc.tc_copy_planned(src, dst, ws, total)
+        ws.total = total
     else:
         tc.tc_copy_fragments(src, dst, frags, ws)
     torch.cuda.synchronize()
@@ -97,7 +98,7 @@ def test_plan_reuse_and_order_independence():
     dst, fr, ws = _copy_and_check(src, frags, pool, planned=True)
     # the same plan again
     dst2 = torch.full_like(dst, 0x5A)
-    tc.tc_copy_planned(src, dst2, fr, ws)
+    tc.tc_copy_planned(src, dst2, ws, ws.total)
     # a shuffled list planned afresh gives the same bytes
     perm = np.random.default_rng(38).permutation(len(frags))
     dst3, _, _ = _copy_and_check(src, frags[perm], pool)

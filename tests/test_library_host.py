@@ -64,13 +64,22 @@ def test_argument_errors_need_no_gpu(lib):
     pool_big = tc._BlockPool(ctypes.cast(big, ctypes.POINTER(ctypes.c_uint64)), 300, 4, 64, 64)
     assert lib.tc_gather_blocks(ctypes.byref(pool_big), P(16), 1, P(16), None) == 1
     # fragments: workspace too small, negative count
-    assert lib.tc_copy_fragments(P(16), P(16), P(16), 10, P(16), 8, None) == 5
+    assert lib.tc_copy_fragments(P(16), P(16), P(16), 10, P(4096), 8, None) == 5
+    assert lib.tc_copy_fragments(P(16), P(16), P(16), 10, P(4100), 1 << 20, None) == 1  # misaligned
     assert lib.tc_copy_fragments(P(16), P(16), P(16), -1, P(16), 1 << 20, None) == 1
     assert lib.tc_copy_fragments(None, None, None, 0, None, 0, None) == 0
     # cast: tile other than 128
     assert lib.tc_cast_fp8_blockscaled(P(16), P(16), P(16), P(16), 1, 64, P(16), 1 << 20, None) == 1
     assert lib.tc_cast_fp8_scaled(P(16), -5, ctypes.c_float(1.0), P(16), None) == 1
-    assert tc.tc_copy_fragments_workspace(1000) >= 8 * 1001
+    assert tc.tc_copy_fragments_workspace(1000) >= 24 * 1001
+    # cast items are checked on the host before anything is staged
+    items = np.zeros(1, dtype=tc.CAST_ITEM_DTYPE)
+    items[0] = (0, 128, 256, 100, 0, 256, 0, 2)          # src_ld < cols
+    assert lib.tc_cast_fp8_blockscaled(P(16), P(16), P(16), items.ctypes.data, 1, 128, P(4096),
+                                       1 << 20, None) == 1
+    items[0] = (0, 128, 256, 256, 0, 256, 0, 1)          # scale_ld < tile columns
+    assert lib.tc_cast_fp8_blockscaled(P(16), P(16), P(16), items.ctypes.data, 1, 128, P(4096),
+                                       1 << 20, None) == 1
     assert tc.tc_cast_fp8_workspace(10) >= 8 * 11
 
 
