@@ -448,20 +448,32 @@ tc_status tc_cast_fp8_blockscaled(const void* src_base, void* dst_base, float* s
   if (workspace_bytes < tc::cast_workspace_bytes(n_items)) return TC_ERR_WORKSPACE;
   if ((uintptr_t)workspace % 256 || (uintptr_t)src_base % 2 || (uintptr_t)scale_base % 4)
     return TC_ERR_INVALID_ARGUMENT;
-  // Geometry and the tile prefix, on the host.
-  std::vector<uint64_t> prefix((size_t)n_items + 1);
-  uint64_t total = 0;
-  for (int64_t i = 0; i < n_items; ++i) {
+  // Geometry and the tile ranges, on the host: full tiles of vector-aligned
+  // items go to the streaming kernel, every other tile to the edge kernel.
+  const size_t N = (size_t)n_items;
+  std::vector<uint64_t> fprefix(N + 1), eprefix(N + 1);
+  std::vector<uint8_t> aligned(N);
+  uint64_t full = 0, edge = 0;
+  for (size_t i = 0; i < N; ++i) {
     const tc_cast_item& it = items[i];
     if (it.rows < 0 || it.cols < 0 || it.src_ld < it.cols || it.dst_ld < it.cols)
       return TC_ERR_INVALID_ARGUMENT;
     const uint64_t tr = uint64_t((it.rows + 127) / 128), tcn = uint64_t((it.cols + 127) / 128);
     if (it.rows > 0 && it.cols > 0 && it.scale_ld < int64_t(tcn)) return TC_ERR_INVALID_ARGUMENT;
-    prefix[(size_t)i] = total;
-    total += (it.rows > 0 && it.cols > 0) ? tr * tcn : 0;
+    const uint64_t x = (uint64_t)(uintptr_t)src_base + 2 * it.src_off;
+    const uint64_t q = (uint64_t)(uintptr_t)dst_base + it.dst_off;
+    aligned[i] = (x % 16 == 0 && (2 * uint64_t(it.src_ld)) % 16 == 0 && q % 8 == 0 &&
+                  uint64_t(it.dst_ld) % 8 == 0) ? 1 : 0;
+    const uint64_t all = (it.rows > 0 && it.cols > 0) ? tr * tcn : 0;
+    const uint64_t f = aligned[i] ? uint64_t(it.rows / 128) * uint64_t(it.cols / 128) : 0;
+    fprefix[i] = full;
+    eprefix[i] = edge;
+    full += f;
+    edge += all - f;
   }
-  prefix[(size_t)n_items] = total;
-  if (total == 0) return TC_OK;
+  fprefix[N] = full;
+  eprefix[N] = edge;
+  if (full + edge == 0) return TC_OK;
   if (validating()) {
     std::vector<Range> q, sc, srcr;
     const uint64_t db = (uint64_t)(uintptr_t)dst_base, sb = (uint64_t)(uintptr_t)scale_base;
@@ -486,16 +498,18 @@ tc_status tc_cast_fp8_blockscaled(const void* src_base, void* dst_base, float* s
     if (any_overlap(outs)) return TC_ERR_ALIAS;
     if (cross_overlap(outs, srcr)) return TC_ERR_ALIAS;
   }
-  // Items and prefix go to the workspace through pinned staging memory, so
-  // the caller's host array is free as soon as this call returns.
-  const size_t items_bytes = sizeof(tc_cast_item) * (size_t)n_items;
-  const size_t prefix_at = (items_bytes + 255) & ~size_t(255);
-  tc_status st = stage_to_device(workspace, stream, {{items, items_bytes, 0},
-                                                     {prefix.data(), 8 * prefix.size(), prefix_at}});
+  // Items and tile tables go to the workspace through pinned staging memory,
+  // so the caller's host array is free as soon as this call returns.
+  const tc::CastLayout L = tc::cast_layout(n_items);
+  tc_status st = stage_to_device(workspace, stream,
+                                 {{items, sizeof(tc_cast_item) * N, L.items},
+                                  {fprefix.data(), 8 * (N + 1), L.full_prefix},
+                                  {eprefix.data(), 8 * (N + 1), L.edge_prefix},
+                                  {aligned.data(), N, L.aligned}});
   if (st != TC_OK) return st;
   return check(tc::launch_cast_blockscaled(static_cast<const uint16_t*>(src_base),
                                            static_cast<uint8_t*>(dst_base), scale_base, workspace,
-                                           n_items, total, stream));
+                                           n_items, full, edge, stream));
 }
 
 tc_status tc_cast_fp8_scaled(const void* src_bf16, int64_t n, float scale, void* dst_e4m3,

@@ -87,10 +87,14 @@ __device__ __forceinline__ uint8_t code1(uint16_t bits, int mode, float s) {
   return (uint8_t)(cvt2<false>(q, q, 0) & 0xFFu);
 }
 
-constexpr int kCastThreads = 1024;  // one 128x128 tile per workgroup, 16 elements per thread
+// One 128x128 tile per workgroup of 512 threads: 32 elements (4 x 16 B) per
+// thread, 16 threads per 256-byte row, 32 rows per pass, 4 passes.
+constexpr int kCastThreads = 512;
 constexpr int kCastWaves = kCastThreads / kWaveLanes;
+constexpr int kRowsPerPass = kCastThreads / 16;
+constexpr int kPasses = kTile / kRowsPerPass;
 constexpr int kXcds = 8;
-constexpr uint64_t kCastXcdGroup = 16;  // consecutive tiles per XCD run
+constexpr uint64_t kCastXcdGroup = 4;  // consecutive tiles per XCD run
 
 // Work item of block b when the 8 XCDs each take runs of G consecutive tiles
 // (a bijection on [0, N); the last partial round keeps the identity order).
@@ -105,9 +109,8 @@ __device__ __forceinline__ uint64_t xcd_grouped(uint64_t b, uint64_t N, uint64_t
 __device__ __forceinline__ u32x4 ld_nt(const u32x4* p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ void st_nt(u32x2* p, u32x2 v) { __builtin_nontemporal_store(v, p); }
 
-// Reduce a per-thread 15-bit amax over the workgroup.  red has one slot per
-// wave and is used alternately by consecutive tiles (two buffers), so one
-// barrier per tile suffices.
+// Reduce a per-thread 15-bit amax over the workgroup (one tile per
+// workgroup, so red is written once).
 __device__ __forceinline__ uint32_t block_amax(uint32_t m, uint32_t* red) {
 #pragma unroll
   for (int d = kWaveLanes / 2; d >= 1; d >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, d, kWaveLanes));
@@ -133,104 +136,132 @@ __device__ int64_t find_item(const uint64_t* __restrict__ prefix, int64_t n, uin
   return lo;
 }
 
-// One workgroup per tile (grid-stride only when the grid is capped).  The
-// items and their tile prefix are staged by the host into the workspace.
-__global__ __launch_bounds__(kCastThreads) void k_cast_tiles(const uint16_t* __restrict__ src,
-                                                            uint8_t* __restrict__ dst,
-                                                            float* __restrict__ scales,
-                                                            const tc_cast_item* __restrict__ items,
-                                                            const uint64_t* __restrict__ prefix,
-                                                            const int64_t n_items,
-                                                            const uint64_t total) {
-  __shared__ uint32_t red[2][kCastWaves];
+// Full tiles of items whose rows are 16-byte aligned (source) and 8-byte
+// aligned (codes): one workgroup per tile, tile t0 + (XCD-grouped block).
+// prefix counts each item's full tiles (rows/128 x cols/128, or 0).
+__global__ __launch_bounds__(kCastThreads) void k_cast_full(const uint16_t* __restrict__ src,
+                                                           uint8_t* __restrict__ dst,
+                                                           float* __restrict__ scales,
+                                                           const tc_cast_item* __restrict__ items,
+                                                           const uint64_t* __restrict__ prefix,
+                                                           const int64_t n_items,
+                                                           const uint64_t t0, const uint64_t count) {
+  __shared__ uint32_t red[kCastWaves];
   const int lane = threadIdx.x & (kWaveLanes - 1);
-  // Fast-path layout: 16 lanes per row (8 bf16 = 16 B each), 64 rows per
-  // pass; each thread takes rows prow and prow + 64.
-  const int seg = threadIdx.x & 15;
+  const int seg = threadIdx.x & 15;  // 16 lanes per 256-byte row (8 bf16 = 16 B each)
   const int prow = threadIdx.x >> 4;
-  int parity = 0;
-  for (uint64_t b = blockIdx.x; b < total; b += gridDim.x, parity ^= 1) {
-    uint32_t* rbuf = red[parity];
-    const uint64_t t = xcd_grouped(b, total, kCastXcdGroup);
-    const int64_t it = find_item(prefix, n_items, t, lane);
-    const tc_cast_item item = items[it];
-    const int64_t tiles_c = (item.cols + kTile - 1) / kTile;
-    const int64_t local = int64_t(t - prefix[it]);
-    const int64_t ti = local / tiles_c, tj = local - ti * tiles_c;
-    const int64_t r0 = ti * kTile, c0 = tj * kTile;
-    const int64_t h = min<int64_t>(kTile, item.rows - r0);
-    const int64_t wd = min<int64_t>(kTile, item.cols - c0);
-    const uint16_t* xs = src + item.src_off + r0 * item.src_ld + c0;
-    uint8_t* qs = dst + item.dst_off + r0 * item.dst_ld + c0;
-    float* sp = scales + item.scale_off + ti * item.scale_ld + tj;
-    const bool fast = h == kTile && wd == kTile &&
-                      ((reinterpret_cast<uintptr_t>(xs) | uint64_t(item.src_ld) * 2) & 15) == 0 &&
-                      ((reinterpret_cast<uintptr_t>(qs) | uint64_t(item.dst_ld)) & 7) == 0;
-    if (fast) {
-      const u32x4 v0 = ld_nt(reinterpret_cast<const u32x4*>(xs + int64_t(prow) * item.src_ld + seg * 8));
-      const u32x4 v1 =
-          ld_nt(reinterpret_cast<const u32x4*>(xs + int64_t(prow + 64) * item.src_ld + seg * 8));
-      uint32_t m2 = 0;
-      m2 = absmax2(m2, v0.x);
-      m2 = absmax2(m2, v0.y);
-      m2 = absmax2(m2, v0.z);
-      m2 = absmax2(m2, v0.w);
-      m2 = absmax2(m2, v1.x);
-      m2 = absmax2(m2, v1.y);
-      m2 = absmax2(m2, v1.z);
-      m2 = absmax2(m2, v1.w);
-      const uint32_t amax_bits = block_amax(max(m2 & 0xFFFFu, m2 >> 16), rbuf);
-      float s;
-      u32x2 o0, o1;
-      if (amax_bits >= 0x7F80u) {  // Inf or NaN in the tile
-        s = __uint_as_float(0x7FC00000u);
-        o0 = o1 = u32x2{0x7F7F7F7Fu, 0x7F7F7F7Fu};
-      } else if (amax_bits == 0) {
-        s = 0.0f;
-        o0 = u32x2{codes4_zero(v0.x, v0.y), codes4_zero(v0.z, v0.w)};
-        o1 = u32x2{codes4_zero(v1.x, v1.y), codes4_zero(v1.z, v1.w)};
-      } else {
-        s = __uint_as_float(amax_bits << 16) / 448.0f;
-        if (s >= 0x1.0p-126f) {
-          const float r = 1.0f / s;
-          o0 = u32x2{codes4_fast(v0.x, v0.y, r, s), codes4_fast(v0.z, v0.w, r, s)};
-          o1 = u32x2{codes4_fast(v1.x, v1.y, r, s), codes4_fast(v1.z, v1.w, r, s)};
-        } else {
-          o0 = u32x2{codes4_div(v0.x, v0.y, s), codes4_div(v0.z, v0.w, s)};
-          o1 = u32x2{codes4_div(v1.x, v1.y, s), codes4_div(v1.z, v1.w, s)};
-        }
-      }
-      st_nt(reinterpret_cast<u32x2*>(qs + int64_t(prow) * item.dst_ld + seg * 8), o0);
-      st_nt(reinterpret_cast<u32x2*>(qs + int64_t(prow + 64) * item.dst_ld + seg * 8), o1);
-      if (threadIdx.x == 0) *sp = s;
+  const uint64_t t = t0 + xcd_grouped(blockIdx.x, count, kCastXcdGroup);
+  const int64_t it = find_item(prefix, n_items, t, lane);
+  const tc_cast_item item = items[it];
+  const int64_t full_c = item.cols / kTile;
+  const int64_t local = int64_t(t - prefix[it]);
+  const int64_t ti = local / full_c, tj = local - ti * full_c;
+  const uint16_t* xs = src + item.src_off + ti * kTile * item.src_ld + tj * kTile;
+  uint8_t* qs = dst + item.dst_off + ti * kTile * item.dst_ld + tj * kTile;
+
+  u32x4 v[kPasses];
+#pragma unroll
+  for (int p = 0; p < kPasses; ++p)
+    v[p] = ld_nt(reinterpret_cast<const u32x4*>(xs + int64_t(p * kRowsPerPass + prow) * item.src_ld + seg * 8));
+  uint32_t m2 = 0;
+#pragma unroll
+  for (int p = 0; p < kPasses; ++p) {
+    m2 = absmax2(m2, v[p].x);
+    m2 = absmax2(m2, v[p].y);
+    m2 = absmax2(m2, v[p].z);
+    m2 = absmax2(m2, v[p].w);
+  }
+  const uint32_t amax_bits = block_amax(max(m2 & 0xFFFFu, m2 >> 16), red);
+  float s;
+  u32x2 o[kPasses];
+  if (amax_bits >= 0x7F80u) {  // Inf or NaN in the tile
+    s = __uint_as_float(0x7FC00000u);
+#pragma unroll
+    for (int p = 0; p < kPasses; ++p) o[p] = u32x2{0x7F7F7F7Fu, 0x7F7F7F7Fu};
+  } else if (amax_bits == 0) {
+    s = 0.0f;
+#pragma unroll
+    for (int p = 0; p < kPasses; ++p) o[p] = u32x2{codes4_zero(v[p].x, v[p].y), codes4_zero(v[p].z, v[p].w)};
+  } else {
+    s = __uint_as_float(amax_bits << 16) / 448.0f;
+    if (s >= 0x1.0p-126f) {
+      const float r = 1.0f / s;
+#pragma unroll
+      for (int p = 0; p < kPasses; ++p)
+        o[p] = u32x2{codes4_fast(v[p].x, v[p].y, r, s), codes4_fast(v[p].z, v[p].w, r, s)};
     } else {
-      // Edge or unaligned tile: element by element.
-      const int64_t cnt = h * wd;
-      uint32_t m = 0;
-      for (int64_t e = threadIdx.x; e < cnt; e += kCastThreads) {
-        const int64_t rr = e / wd, cc = e - rr * wd;
-        m = max(m, uint32_t(xs[rr * item.src_ld + cc]) & 0x7FFFu);
-      }
-      const uint32_t amax_bits = block_amax(m, rbuf);
-      int mode;
-      float s;
-      if (amax_bits >= 0x7F80u) {
-        mode = 2;
-        s = __uint_as_float(0x7FC00000u);
-      } else if (amax_bits == 0) {
-        mode = 1;
-        s = 0.0f;
-      } else {
-        mode = 0;
-        s = __uint_as_float(amax_bits << 16) / 448.0f;
-      }
-      for (int64_t e = threadIdx.x; e < cnt; e += kCastThreads) {
-        const int64_t rr = e / wd, cc = e - rr * wd;
-        qs[rr * item.dst_ld + cc] = code1(xs[rr * item.src_ld + cc], mode, s);
-      }
-      if (threadIdx.x == 0) *sp = s;
+#pragma unroll
+      for (int p = 0; p < kPasses; ++p)
+        o[p] = u32x2{codes4_div(v[p].x, v[p].y, s), codes4_div(v[p].z, v[p].w, s)};
     }
   }
+#pragma unroll
+  for (int p = 0; p < kPasses; ++p)
+    st_nt(reinterpret_cast<u32x2*>(qs + int64_t(p * kRowsPerPass + prow) * item.dst_ld + seg * 8), o[p]);
+  if (threadIdx.x == 0) scales[item.scale_off + ti * item.scale_ld + tj] = s;
+}
+
+// The remaining tiles: partial tiles at the bottom and right edges, and every
+// tile of items that are not aligned for the vector path.  Element by
+// element; prefix counts each item's remaining tiles.  Within an item they
+// are numbered row of tiles by row of tiles: first the tile rows from fr
+// (all tile columns), then the tile columns from fc of the first fr rows,
+// where fr x fc is the item's full-tile grid (0 x 0 for unaligned items).
+__global__ __launch_bounds__(kCastThreads) void k_cast_edge(const uint16_t* __restrict__ src,
+                                                           uint8_t* __restrict__ dst,
+                                                           float* __restrict__ scales,
+                                                           const tc_cast_item* __restrict__ items,
+                                                           const uint64_t* __restrict__ prefix,
+                                                           const uint8_t* __restrict__ aligned,
+                                                           const int64_t n_items,
+                                                           const uint64_t t0, const uint64_t count) {
+  __shared__ uint32_t red[kCastWaves];
+  const int lane = threadIdx.x & (kWaveLanes - 1);
+  const uint64_t t = t0 + blockIdx.x;
+  const int64_t it = find_item(prefix, n_items, t, lane);
+  const tc_cast_item item = items[it];
+  const int64_t tr = (item.rows + kTile - 1) / kTile, tcn = (item.cols + kTile - 1) / kTile;
+  const int64_t fr = aligned[it] ? item.rows / kTile : 0;
+  const int64_t fc = aligned[it] ? item.cols / kTile : 0;
+  const int64_t e = int64_t(t - prefix[it]);
+  int64_t ti, tj;
+  if (e < (tr - fr) * tcn) {
+    ti = fr + e / tcn;
+    tj = e % tcn;
+  } else {
+    const int64_t e2 = e - (tr - fr) * tcn;
+    ti = e2 / (tcn - fc);
+    tj = fc + e2 % (tcn - fc);
+  }
+  const int64_t r0 = ti * kTile, c0 = tj * kTile;
+  const int64_t h = min<int64_t>(kTile, item.rows - r0);
+  const int64_t wd = min<int64_t>(kTile, item.cols - c0);
+  const uint16_t* xs = src + item.src_off + r0 * item.src_ld + c0;
+  uint8_t* qs = dst + item.dst_off + r0 * item.dst_ld + c0;
+  const int64_t cnt = h * wd;
+  uint32_t m = 0;
+  for (int64_t k = threadIdx.x; k < cnt; k += kCastThreads) {
+    const int64_t rr = k / wd, cc = k - rr * wd;
+    m = max(m, uint32_t(xs[rr * item.src_ld + cc]) & 0x7FFFu);
+  }
+  const uint32_t amax_bits = block_amax(m, red);
+  int mode;
+  float s;
+  if (amax_bits >= 0x7F80u) {
+    mode = 2;
+    s = __uint_as_float(0x7FC00000u);
+  } else if (amax_bits == 0) {
+    mode = 1;
+    s = 0.0f;
+  } else {
+    mode = 0;
+    s = __uint_as_float(amax_bits << 16) / 448.0f;
+  }
+  for (int64_t k = threadIdx.x; k < cnt; k += kCastThreads) {
+    const int64_t rr = k / wd, cc = k - rr * wd;
+    qs[rr * item.dst_ld + cc] = code1(xs[rr * item.src_ld + cc], mode, s);
+  }
+  if (threadIdx.x == 0) scales[item.scale_off + ti * item.scale_ld + tj] = s;
 }
 
 // Elementwise cast with one given scale: 8 elements per thread.
@@ -274,27 +305,44 @@ __global__ __launch_bounds__(kThreads) void k_cast_scaled(const uint16_t* __rest
   }
 }
 
+// Largest grid of one launch (gridDim.x * blockDim.x stays below 2^32).
 constexpr uint64_t kMaxGrid = uint64_t(1) << 22;
 
 }  // namespace
 
 static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-size_t cast_workspace_bytes(int64_t n_items) {
-  return align256(sizeof(tc_cast_item) * size_t(n_items)) + 8 * size_t(n_items + 1);
+CastLayout cast_layout(int64_t n_items) {
+  CastLayout L;
+  L.items = 0;
+  L.full_prefix = align256(sizeof(tc_cast_item) * size_t(n_items));
+  L.edge_prefix = L.full_prefix + align256(8 * size_t(n_items + 1));
+  L.aligned = L.edge_prefix + align256(8 * size_t(n_items + 1));
+  L.bytes = L.aligned + align256(size_t(n_items));
+  return L;
 }
 
+size_t cast_workspace_bytes(int64_t n_items) { return cast_layout(n_items).bytes; }
+
 hipError_t launch_cast_blockscaled(const uint16_t* src, uint8_t* dst, float* scales,
-                                   const void* ws, int64_t n_items, uint64_t total_tiles,
-                                   hipStream_t s) {
-  if (total_tiles == 0) return hipSuccess;
+                                   const void* ws, int64_t n_items, uint64_t full_tiles,
+                                   uint64_t edge_tiles, hipStream_t s) {
+  const CastLayout L = cast_layout(n_items);
   const uint8_t* base = static_cast<const uint8_t*>(ws);
-  const tc_cast_item* items = reinterpret_cast<const tc_cast_item*>(base);
-  const uint64_t* prefix =
-      reinterpret_cast<const uint64_t*>(base + align256(sizeof(tc_cast_item) * size_t(n_items)));
-  const unsigned grid = (unsigned)(total_tiles < kMaxGrid ? total_tiles : kMaxGrid);
-  hipLaunchKernelGGL(k_cast_tiles, dim3(grid), dim3(kCastThreads), 0, s, src, dst, scales, items,
-                     prefix, n_items, total_tiles);
+  const tc_cast_item* items = reinterpret_cast<const tc_cast_item*>(base + L.items);
+  const uint64_t* fp = reinterpret_cast<const uint64_t*>(base + L.full_prefix);
+  const uint64_t* ep = reinterpret_cast<const uint64_t*>(base + L.edge_prefix);
+  const uint8_t* al = base + L.aligned;
+  for (uint64_t t0 = 0; t0 < full_tiles; t0 += kMaxGrid) {
+    const uint64_t cnt = full_tiles - t0 < kMaxGrid ? full_tiles - t0 : kMaxGrid;
+    hipLaunchKernelGGL(k_cast_full, dim3((unsigned)cnt), dim3(kCastThreads), 0, s, src, dst, scales,
+                       items, fp, n_items, t0, cnt);
+  }
+  for (uint64_t t0 = 0; t0 < edge_tiles; t0 += kMaxGrid) {
+    const uint64_t cnt = edge_tiles - t0 < kMaxGrid ? edge_tiles - t0 : kMaxGrid;
+    hipLaunchKernelGGL(k_cast_edge, dim3((unsigned)cnt), dim3(kCastThreads), 0, s, src, dst, scales,
+                       items, ep, al, n_items, t0, cnt);
+  }
   return hipGetLastError();
 }
 

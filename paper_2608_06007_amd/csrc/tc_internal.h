@@ -69,11 +69,16 @@ hipError_t launch_copy_tasks(const uint8_t* src, uint8_t* dst, const void* ws,
                              uint64_t total_tasks, hipStream_t s);
 
 // --- fp8 cast ----------------------------------------------------------
-// ws holds the items followed by their tile prefix (n + 1 entries).
+// Workspace: items | prefix of full (vector-path) tiles | prefix of the other
+// tiles | per-item vector-path flag.  Byte offsets:
+struct CastLayout {
+  size_t items, full_prefix, edge_prefix, aligned, bytes;
+};
+CastLayout cast_layout(int64_t n_items);
 size_t cast_workspace_bytes(int64_t n_items);
 hipError_t launch_cast_blockscaled(const uint16_t* src, uint8_t* dst, float* scales,
-                                   const void* ws, int64_t n_items, uint64_t total_tiles,
-                                   hipStream_t s);
+                                   const void* ws, int64_t n_items, uint64_t full_tiles,
+                                   uint64_t edge_tiles, hipStream_t s);
 hipError_t launch_cast_scaled(const uint16_t* src, int64_t n, float scale, uint8_t* dst,
                               hipStream_t s);
 
