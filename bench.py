@@ -287,7 +287,23 @@ def run_moe(torch, tc, synth, args, stream):
     return out
 
 
-RUNNERS = {"reshard": run_reshard, "cast": run_cast, "storm": run_storm, "moe": run_moe}
+def run_calib(torch, tc, synth, args, stream):
+    """A plain device copy of known size (torch's copy_, 4 GiB): the
+    reference for scaling hardware byte counters, and the measured copy
+    rate of the runtime's own copy path."""
+    n = 4 << 30
+    _log("[calib] torch copy_ of 4 GiB")
+    src = synth.random_bytes(n, 41, device="cuda")
+    dst = torch.empty_like(src)
+    ms = _time_calls(torch, stream, lambda: dst.copy_(src), args.warmup, args.cast_steps)
+    out = {"bytes_each_way": n, "torch_copy": _stats(ms, 2 * n)}
+    del src, dst
+    torch.cuda.empty_cache()
+    return out
+
+
+RUNNERS = {"reshard": run_reshard, "cast": run_cast, "storm": run_storm, "moe": run_moe,
+           "calib": run_calib}
 
 
 def main():
@@ -296,7 +312,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cast-steps", type=int, default=20, help="timed launches per extra workload")
-    ap.add_argument("--workloads", default="kv,reshard,cast,storm,moe")
+    ap.add_argument("--workloads", default="kv,reshard,cast,storm,moe,calib")
     ap.add_argument("--skip-cpu", action="store_true", help="skip the CPU oracle baseline")
     args = ap.parse_args()
     if args.gpus != 1:
