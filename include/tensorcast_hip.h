@@ -105,12 +105,13 @@ typedef struct {
 } tc_fragment;
 
 /* Recommended bytes of device workspace for a plan of n descriptors.  A
- * plan cuts every fragment into tasks of at most `piece` bytes (4 KiB, or the
+ * plan cuts every fragment into tasks of at most `piece` bytes (1 KiB, or the
  * next power of two that keeps the task table inside the workspace) and
- * spreads the tasks over the whole GPU.  Any workspace holding at least
- * n + 1 tasks works (24 bytes each, plus 16 bytes per descriptor of planning
- * scratch); this size keeps 4 KiB pieces for payloads up to ~8 KiB per
- * fragment plus 4 GiB. */
+ * spreads the tasks over the whole GPU, one task per wave.  Any workspace
+ * holding at least n + 1 tasks works (16 bytes each, plus 16 bytes per
+ * descriptor of planning scratch); this size keeps 1 KiB pieces for payloads
+ * up to ~3 KiB per fragment plus 8 GiB.  Offsets plus lengths must stay
+ * below 2^48. */
 size_t tc_copy_fragments_workspace(int64_t n);
 
 /* Copy every fragment: tc_plan_fragments + tc_copy_planned.  frags: device

@@ -293,6 +293,8 @@ static tc_status check_ranges(const void* src_base, const void* dst_base,
   const uint64_t sb = (uint64_t)(uintptr_t)src_base, db = (uint64_t)(uintptr_t)dst_base;
   for (const tc_fragment& f : h) {
     if (f.src_off + f.len < f.src_off || f.dst_off + f.len < f.dst_off) return TC_ERR_OUT_OF_RANGE;
+    if (f.src_off + f.len > tc::kOffsetLimit || f.dst_off + f.len > tc::kOffsetLimit)
+      return TC_ERR_OUT_OF_RANGE;
     if (sb + f.src_off + f.len < sb || db + f.dst_off + f.len < db) return TC_ERR_OUT_OF_RANGE;
     d.push_back({db + f.dst_off, db + f.dst_off + f.len});
     sr.push_back({sb + f.src_off, sb + f.src_off + f.len});
@@ -360,11 +362,17 @@ tc_status tc_copy_planned(const void* src_base, void* dst_base, const void* work
     if (hdr.total_tasks != total_tasks) return TC_ERR_INVALID_ARGUMENT;
     const tc::PlanLayout L = tc::plan_layout((int64_t)hdr.n, workspace_bytes);
     if (total_tasks > L.capacity) return TC_ERR_WORKSPACE;
-    std::vector<tc_fragment> tasks;
-    tc_status st = fetch(reinterpret_cast<const tc_fragment*>(static_cast<const uint8_t*>(workspace) +
-                                                              tc::kTasksOffset),
-                         (int64_t)total_tasks, &tasks, stream);
+    std::vector<tc::Task> packed;
+    tc_status st = fetch(reinterpret_cast<const tc::Task*>(static_cast<const uint8_t*>(workspace) +
+                                                           tc::kTasksOffset),
+                         (int64_t)total_tasks, &packed, stream);
     if (st != TC_OK) return st;
+    std::vector<tc_fragment> tasks(packed.size());
+    for (size_t i = 0; i < packed.size(); ++i) {
+      const tc::Task& t = packed[i];
+      tasks[i] = tc_fragment{t.lo & (tc::kOffsetLimit - 1),
+                             (t.lo >> 48) | ((t.hi & 0xFFFFFFFFu) << 16), t.hi >> 32};
+    }
     st = check_ranges(src_base, dst_base, tasks);
     if (st != TC_OK) return st;
   }

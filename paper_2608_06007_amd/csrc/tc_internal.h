@@ -8,10 +8,10 @@
 
 namespace tc {
 
-// Fragment plans cut fragments into tasks of at most `piece` bytes; the piece
-// is the smallest power of two >= kMinPiece that keeps the task table within
-// the workspace.
-constexpr uint64_t kMinPiece = 4096;
+// Fragment plans cut fragments into tasks of at most `piece` bytes, one task
+// per wave (64 lanes x 16 B = 1 KiB per pass); the piece is the smallest
+// power of two >= kMinPiece that keeps the task table within the workspace.
+constexpr uint64_t kMinPiece = 1024;
 // Descriptors handled by one workgroup of the planning kernels.
 constexpr int kPlanPerBlock = 1024;
 
@@ -19,10 +19,14 @@ struct RegionTable {
   uint64_t base[TC_MAX_REGIONS];
 };
 
-// One task of a fragment plan: a byte run of at most `piece` bytes.
+// One task of a fragment plan, a byte run of at most `piece` bytes, packed in
+// 16 bytes: src_off (48 bits) | dst_off (48 bits) | len (32 bits).  Offsets
+// must stay below 2^48 (256 TiB).
 struct Task {
-  uint64_t src_off, dst_off, len;
+  uint64_t lo;  // src_off | dst_off << 48
+  uint64_t hi;  // dst_off >> 16 | len << 32
 };
+constexpr uint64_t kOffsetLimit = uint64_t(1) << 48;
 
 // Header at the start of a fragment-plan workspace.
 struct PlanHeader {

@@ -19,7 +19,8 @@ constexpr int kThreads = 256;  // 4 waves of 64 lanes
 constexpr int kWaveLanes = 64;
 constexpr int64_t kTileBytes = int64_t(kThreads) * 16;  // 4 KiB per workgroup
 constexpr int kXcds = 8;
-constexpr uint64_t kXcdGroup = 64;  // consecutive tiles per XCD run
+constexpr uint64_t kXcdGroup = 64;           // consecutive tiles per XCD run
+constexpr uint64_t kXcdGroupScatter = 512;   // hydrate: longer runs stream its reads better
 
 // Work item of block b when the 8 XCDs each take runs of G consecutive items
 // (a bijection on [0, N); the last partial round keeps the identity order).
@@ -47,7 +48,7 @@ __global__ __launch_bounds__(kThreads) void k_blocks_vec(const RegionTable tab, 
                                                         const uint64_t tiles_per_chunk,
                                                         uint8_t* __restrict__ buf) {
   for (uint64_t b = blockIdx.x; b < total_tiles; b += gridDim.x) {
-    const uint64_t w = xcd_grouped(b, total_tiles, kXcdGroup);
+    const uint64_t w = xcd_grouped(b, total_tiles, kGather ? kXcdGroup : kXcdGroupScatter);
     const uint64_t c = w / tiles_per_chunk;
     const uint64_t k = w - c * tiles_per_chunk;
     const uint64_t i = c / uint64_t(R);
@@ -198,58 +199,126 @@ __global__ __launch_bounds__(kThreads) void k_plan_tstart(const tc_fragment* __r
   }
 }
 
-// Task t -> last fragment f with tstart[f] <= t (binary search; tstart[0] = 0
-// <= t < tstart[n]).
+// Last f in [lo, hi) with tstart[f] <= t, given tstart[lo] <= t < tstart[hi]
+// (64-way search by one wave).
+__device__ int64_t wave_find(const uint64_t* __restrict__ tstart, int64_t lo, int64_t hi,
+                             uint64_t t, int lane) {
+  while (hi - lo > 1) {
+    const int64_t step = (hi - lo + kWaveLanes - 1) / kWaveLanes;
+    const int64_t p = lo + (int64_t(lane) + 1) * step;
+    const bool pred = lane < kWaveLanes - 1 && p < hi && tstart[p] <= t;
+    lo += int64_t(__popcll(__ballot(pred))) * step;
+    hi = min(hi, lo + step);
+  }
+  return lo;
+}
+
+__device__ __forceinline__ Task pack_task(uint64_t src, uint64_t dst, uint64_t len) {
+  return Task{src | (dst << 48), (dst >> 16) | (len << 32)};
+}
+
+constexpr int kExpandPerBlock = 1024;  // tasks written by one workgroup
+
+// Block j writes tasks [j * 1024, (j + 1) * 1024).  Wave 0 finds the first
+// and last task's fragments; if they span at most 1024 fragments their
+// tstart entries go to LDS and every task finds its fragment there,
+// otherwise (long runs of empty fragments) each task searches globally.
 __global__ __launch_bounds__(kThreads) void k_plan_expand(const tc_fragment* __restrict__ frags,
                                                          const int64_t n,
                                                          const uint64_t* __restrict__ tstart,
                                                          const uint64_t total, const uint64_t piece,
                                                          Task* __restrict__ tasks) {
-  const uint64_t t = uint64_t(blockIdx.x) * kThreads + threadIdx.x;
-  if (t >= total) return;
-  int64_t lo = 0, hi = n;  // tstart[lo] <= t < tstart[hi]
-  while (hi - lo > 1) {
-    const int64_t mid = lo + (hi - lo) / 2;
-    if (tstart[mid] <= t)
-      lo = mid;
-    else
-      hi = mid;
+  __shared__ uint64_t win[kExpandPerBlock + 1];
+  __shared__ int64_t range[2];
+  const int lane = threadIdx.x & (kWaveLanes - 1);
+  const uint64_t t0 = uint64_t(blockIdx.x) * kExpandPerBlock;
+  const uint64_t t1 = min(total, t0 + kExpandPerBlock);
+  if (threadIdx.x < kWaveLanes) {
+    const int64_t f0 = wave_find(tstart, 0, n, t0, lane);
+    const int64_t f1 = wave_find(tstart, f0, n, t1 - 1, lane);
+    if (lane == 0) {
+      range[0] = f0;
+      range[1] = f1;
+    }
   }
-  const tc_fragment f = frags[lo];
-  const uint64_t off = (t - tstart[lo]) * piece;
-  const uint64_t rem = f.len - off;
-  tasks[t] = Task{f.src_off + off, f.dst_off + off, rem < piece ? rem : piece};
+  __syncthreads();
+  const int64_t f0 = range[0], f1 = range[1];
+  const int64_t span = f1 - f0 + 1;
+  const bool local = span <= kExpandPerBlock;
+  if (local)
+    for (int64_t k = threadIdx.x; k <= span; k += kThreads) win[k] = tstart[f0 + k];
+  __syncthreads();
+  for (uint64_t t = t0 + threadIdx.x; t < t1; t += kThreads) {
+    int64_t lo, hi;
+    uint64_t start;
+    if (local) {  // win[lo] <= t < win[hi], indices relative to f0
+      lo = 0;
+      hi = span;
+      while (hi - lo > 1) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (win[mid] <= t)
+          lo = mid;
+        else
+          hi = mid;
+      }
+      start = win[lo];
+      lo += f0;
+    } else {
+      lo = f0;
+      hi = f1 + 1;
+      while (hi - lo > 1) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (tstart[mid] <= t)
+          lo = mid;
+        else
+          hi = mid;
+      }
+      start = tstart[lo];
+    }
+    const tc_fragment f = frags[lo];
+    const uint64_t off = (t - start) * piece;
+    const uint64_t rem = f.len - off;
+    tasks[t] = pack_task(f.src_off + off, f.dst_off + off, rem < piece ? rem : piece);
+  }
 }
 
 // ------------------------------------------------------------------------
-// Planned copy: one workgroup per task (tasks of one XCD run consecutive).
+// Planned copy: one task per wave, four consecutive tasks per workgroup
+// (workgroups of one XCD run consecutive).
 // ------------------------------------------------------------------------
+constexpr int kTasksPerBlock = kThreads / kWaveLanes;
+
 __global__ __launch_bounds__(kThreads) void k_copy_tasks(const uint8_t* __restrict__ src,
                                                         uint8_t* __restrict__ dst,
                                                         const Task* __restrict__ tasks,
-                                                        const uint64_t total) {
-  for (uint64_t b = blockIdx.x; b < total; b += gridDim.x) {
-    const Task tk = tasks[xcd_grouped(b, total, kXcdGroup)];
-    const uint8_t* s = src + tk.src_off;
-    uint8_t* d = dst + tk.dst_off;
-    uint64_t len = tk.len;
+                                                        const uint64_t total,
+                                                        const uint64_t nblocks) {
+  const int lane = threadIdx.x & (kWaveLanes - 1);
+  const uint64_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  for (uint64_t b = blockIdx.x; b < nblocks; b += gridDim.x) {
+    const uint64_t t = xcd_grouped(b, nblocks, kXcdGroup) * kTasksPerBlock + w;
+    if (t >= total) continue;
+    const Task tk = tasks[t];
+    const uint8_t* s = src + (tk.lo & (kOffsetLimit - 1));
+    uint8_t* d = dst + ((tk.lo >> 48) | ((tk.hi & 0xFFFFFFFFu) << 16));
+    uint64_t len = tk.hi >> 32;
     const uintptr_t sa = reinterpret_cast<uintptr_t>(s), da = reinterpret_cast<uintptr_t>(d);
     if (((sa ^ da) & 15) == 0) {
       // byte head up to 16-byte alignment, 16-byte body, byte tail
       uint64_t head = (16 - (sa & 15)) & 15;
       if (head > len) head = len;
-      if (threadIdx.x < head) d[threadIdx.x] = s[threadIdx.x];
+      if (uint64_t(lane) < head) d[lane] = s[lane];
       s += head;
       d += head;
       len -= head;
       const uint64_t n16 = len >> 4;
       const u32x4* sv = reinterpret_cast<const u32x4*>(s);
       u32x4* dv = reinterpret_cast<u32x4*>(d);
-      for (uint64_t i = threadIdx.x; i < n16; i += kThreads) st_nt(dv + i, ld_nt(sv + i));
+      for (uint64_t i = lane; i < n16; i += kWaveLanes) st_nt(dv + i, ld_nt(sv + i));
       const uint64_t tail = len & 15;
-      if (threadIdx.x < tail) d[(n16 << 4) + threadIdx.x] = s[(n16 << 4) + threadIdx.x];
+      if (uint64_t(lane) < tail) d[(n16 << 4) + lane] = s[(n16 << 4) + lane];
     } else {
-      for (uint64_t i = threadIdx.x; i < len; i += kThreads) d[i] = s[i];
+      for (uint64_t i = lane; i < len; i += kWaveLanes) d[i] = s[i];
     }
   }
 }
@@ -304,11 +373,11 @@ PlanLayout plan_layout(int64_t n, size_t ws_bytes) {
   return L;
 }
 
-// Room for n + 2 * (n + 2^20) tasks: pieces stay at 4 KiB unless the payload
-// averages more than ~8 KiB per fragment beyond the first 4 GiB.
+// Room for 4n + 2^23 tasks: pieces stay at 1 KiB while the payload is below
+// ~3 KiB per fragment plus 8 GiB.
 size_t frag_workspace_bytes(int64_t n) {
-  return kTasksOffset + sizeof(Task) * (size_t(n) + 2 * (size_t(n) + (size_t(1) << 20))) +
-         plan_tail_bytes(n) + 256;
+  return kTasksOffset + sizeof(Task) * (4 * size_t(n) + (size_t(1) << 23)) + plan_tail_bytes(n) +
+         256;
 }
 
 size_t frag_workspace_min_bytes(int64_t n) {
@@ -338,7 +407,7 @@ hipError_t launch_plan_expand(const tc_fragment* frags, int64_t n, uint64_t tota
   uint8_t* base = static_cast<uint8_t*>(ws);
   const uint64_t* tstart = reinterpret_cast<const uint64_t*>(base + L.tstart);
   Task* tasks = reinterpret_cast<Task*>(base + kTasksOffset);
-  const uint64_t grid = (total + kThreads - 1) / kThreads;
+  const uint64_t grid = (total + kExpandPerBlock - 1) / kExpandPerBlock;
   hipLaunchKernelGGL(k_plan_expand, dim3((unsigned)grid), dim3(kThreads), 0, s, frags, n, tstart,
                      total, piece, tasks);
   return hipGetLastError();
@@ -348,8 +417,9 @@ hipError_t launch_copy_tasks(const uint8_t* src, uint8_t* dst, const void* ws, u
                              hipStream_t s) {
   if (total == 0) return hipSuccess;
   const Task* tasks = reinterpret_cast<const Task*>(static_cast<const uint8_t*>(ws) + kTasksOffset);
-  hipLaunchKernelGGL(k_copy_tasks, dim3(grid_for(total)), dim3(kThreads), 0, s, src, dst, tasks,
-                     total);
+  const uint64_t nblocks = (total + kTasksPerBlock - 1) / kTasksPerBlock;
+  hipLaunchKernelGGL(k_copy_tasks, dim3(grid_for(nblocks)), dim3(kThreads), 0, s, src, dst, tasks,
+                     total, nblocks);
   return hipGetLastError();
 }
 
