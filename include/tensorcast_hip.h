@@ -113,6 +113,9 @@ typedef struct {
  * up to ~3 KiB per fragment plus 8 GiB.  Offsets plus lengths must stay
  * below 2^48. */
 size_t tc_copy_fragments_workspace(int64_t n);
+/* Smallest workspace a plan of n descriptors accepts (room for n + 1 tasks;
+ * the task size then grows to fit). */
+size_t tc_copy_fragments_workspace_min(int64_t n);
 
 /* Copy every fragment: tc_plan_fragments + tc_copy_planned.  frags: device
  * tc_fragment[n].  workspace: device buffer, 256-byte aligned.  The call

@@ -28,7 +28,7 @@ import numpy as np
 __all__ = [
     "TcError", "lib_path", "load",
     "tc_gather_blocks", "tc_scatter_blocks",
-    "tc_copy_fragments_workspace", "tc_copy_fragments", "tc_plan_fragments", "tc_copy_planned",
+    "tc_copy_fragments_workspace", "tc_copy_fragments_workspace_min", "tc_copy_fragments", "tc_plan_fragments", "tc_copy_planned",
     "tc_tp_fragment_count", "tc_tp_fragments", "tc_tp_cast_item",
     "tc_cast_fp8_workspace", "tc_cast_fp8_blockscaled", "tc_cast_fp8_scaled",
     "tc_status_string", "tc_last_hip_error", "tc_set_validate", "tc_get_validate",
@@ -88,6 +88,8 @@ def load():
     L.tc_scatter_blocks.argtypes = [c.POINTER(_BlockPool), P, c.c_int64, P, P]
     L.tc_copy_fragments_workspace.argtypes = [c.c_int64]
     L.tc_copy_fragments_workspace.restype = c.c_size_t
+    L.tc_copy_fragments_workspace_min.argtypes = [c.c_int64]
+    L.tc_copy_fragments_workspace_min.restype = c.c_size_t
     L.tc_copy_fragments.argtypes = [P, P, P, c.c_int64, P, c.c_size_t, P]
     L.tc_plan_fragments.argtypes = [P, c.c_int64, P, c.c_size_t, c.POINTER(c.c_uint64), P]
     L.tc_copy_planned.argtypes = [P, P, P, c.c_size_t, c.c_uint64, P]
@@ -182,6 +184,10 @@ def tc_scatter_blocks(regions, num_blocks: int, block_bytes: int, block_stride: 
 
 def tc_copy_fragments_workspace(n: int) -> int:
     return int(load().tc_copy_fragments_workspace(int(n)))
+
+
+def tc_copy_fragments_workspace_min(n: int) -> int:
+    return int(load().tc_copy_fragments_workspace_min(int(n)))
 
 
 def _frag_count(frags) -> int:

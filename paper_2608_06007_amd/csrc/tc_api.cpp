@@ -282,6 +282,11 @@ size_t tc_copy_fragments_workspace(int64_t n) {
   return tc::frag_workspace_bytes(n);
 }
 
+size_t tc_copy_fragments_workspace_min(int64_t n) {
+  if (n < 0) return 0;
+  return tc::frag_workspace_min_bytes(n);
+}
+
 // Debug checks of a descriptor list: no overflow, destination ranges pairwise
 // disjoint and, when both bases are known, no destination range overlapping
 // a source range.
@@ -339,6 +344,8 @@ tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace
     // by n + payload / piece <= capacity.
     const uint64_t room = L.capacity - uint64_t(n);
     piece = pow2_at_least(std::max<uint64_t>(tc::kMinPiece, (hdr.payload + room - 1) / room));
+    // a task's length is stored in 32 bits
+    piece = std::min<uint64_t>(piece, uint64_t(1) << 31);
   }
   if (hdr.total_tasks > L.capacity) return TC_ERR_WORKSPACE;
   hipError_t e = tc::launch_plan_expand(frags, n, hdr.total_tasks, piece, workspace, L, stream);

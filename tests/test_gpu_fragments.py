@@ -27,11 +27,13 @@ def _rand_bytes(n, seed):
     return synth.random_bytes(n, seed, device=DEV)
 
 
-def _copy_and_check(src, frags_np, dst_size, sentinel=0x5A, planned=False):
+def _copy_and_check(src, frags_np, dst_size, sentinel=0x5A, planned=False, ws_bytes=None):
     frags = torch.from_numpy(frags_np.astype(np.uint64).view(np.int64)).to(DEV)
     dst = torch.full((dst_size,), sentinel, dtype=torch.uint8, device=DEV)
     n = len(frags_np)
-    ws = torch.empty(max(tc.tc_copy_fragments_workspace(n), 8), dtype=torch.uint8, device=DEV)
+    if ws_bytes is None:
+        ws_bytes = tc.tc_copy_fragments_workspace(n)
+    ws = torch.empty(max(ws_bytes, 8), dtype=torch.uint8, device=DEV)
     if planned:
         total = tc.tc_plan_fragments(frags, ws)
         tc.tc_copy_planned(src, dst, ws, total)
@@ -106,6 +108,23 @@ def test_plan_reuse_and_order_independence():
     assert torch.equal(dst, dst2) and torch.equal(dst, dst3)
 
 
+@pytest.mark.parametrize("extra_tasks", [1, 100, 5000])
+def test_small_workspace_grows_the_task_size(extra_tasks):
+    """With room for only n + k tasks the plan picks larger pieces; the copy
+    must not change."""
+    pool = 64 << 20
+    frags = synth.fragment_storm(3000, pool, seed=42)
+    n = len(frags)
+    ws_bytes = tc.tc_copy_fragments_workspace_min(n) + 16 * (extra_tasks - 1)
+    src = _rand_bytes(pool, 43)
+    dst, fr, ws = _copy_and_check(src, frags, pool, planned=True, ws_bytes=ws_bytes)
+    assert ws.total <= n + extra_tasks + 32      # capacity rounds to 256-byte alignment
+    with pytest.raises(tc.TcError) as e:          # below the minimum
+        tc.tc_plan_fragments(fr, torch.empty(tc.tc_copy_fragments_workspace_min(n) - 4096,
+                                             dtype=torch.uint8, device=DEV))
+    assert e.value.status == 5
+
+
 def test_validation_mode_reports_overlaps():
     src = _rand_bytes(1 << 20, 39)
     dst = torch.zeros(1 << 20, dtype=torch.uint8, device=DEV)
@@ -120,6 +139,10 @@ def test_validation_mode_reports_overlaps():
         with pytest.raises(tc.TcError) as e:       # src and dst ranges overlap in one buffer
             tc.tc_copy_fragments(src, src, same, ws)
         assert e.value.status == 3
+        huge = torch.tensor([[0, (1 << 48) - 8, 100]], dtype=torch.int64, device=DEV)
+        with pytest.raises(tc.TcError) as e:       # offsets must stay below 2^48
+            tc.tc_copy_fragments(src, dst, huge, ws)
+        assert e.value.status == 2
     finally:
         tc.tc_set_validate(False)
 
