@@ -77,28 +77,37 @@ def _stats(ms, nbytes):
             "frac_of_peak": round(nbytes / (med * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
 
 
-def _kernel_source_hash():
+KERNEL_SOURCES = {"gather": "tc_moves.hip", "scatter": "tc_moves.hip", "reshard": "tc_moves.hip",
+                  "cast": "tc_cast.hip"}
+
+
+def _source_hash(*names):
+    """sha256 over the named files of the HIP sources plus their shared header."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_06007_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".h", ".cpp")):
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(name.encode() + f.read())
+    for name in sorted(set(names) | {"tc_internal.h"}):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + f.read())
     return h.hexdigest()
 
 
-def _traffic(kernel, src_hash):
+def _kernel_source_hash():
+    csrc = os.path.join(ROOT, "paper_2608_06007_amd", "csrc")
+    return _source_hash(*[n for n in os.listdir(csrc) if n.endswith((".hip", ".h", ".cpp"))])
+
+
+def _traffic(kernel):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they were
-    taken on the current kernel sources."""
+    taken on the current source of that kernel (else None)."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("source_hash") != src_hash:
-        return None
     entry = t.get("kernels", {}).get(kernel)
-    return None if entry is None else entry.get("hbm_bytes_per_launch")
+    if entry is None or entry.get("source_sha256") != _source_hash(KERNEL_SOURCES[kernel]):
+        return None
+    return entry.get("hbm_bytes_per_launch")
 
 
 # ---------------------------------------------------------------------------
@@ -352,7 +361,7 @@ def main():
                        "bytes_per_step": kv["step_bytes"], "ids_sha256": kv["ids_sha256"]},
             "roofline": {"bound": "hbm", "kernel": f"k_blocks_vec ({dom})", "achieved": round(ach, 1),
                          "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
-                         "traffic": _traffic(dom, src_hash)},
+                         "traffic": _traffic(dom)},
             "kernels": {"gather": kv["gather"], "scatter": kv["scatter"]},
         })
         if "cpu" in kv:
