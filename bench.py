@@ -238,6 +238,38 @@ def run_reshard(torch, tc, synth, args, stream):
     return out
 
 
+def run_reshard44(torch, tc, synth, args, stream):
+    """Cross-layout reshard: the 8B-shaped weights stored as their 8 TP=8
+    shards (rank-major) rearranged into rank 1 of a TP=4 split."""
+    from paper_2608_06007_amd import views as tcv
+    spec = synth.spec_8b(32)
+    n = synth.spec_elems(spec)
+    _log("[reshard_tp8_tp4] 8 TP=8 shards -> TP=4 rank 1")
+    stream_t = synth.bf16_normal(n, 1.0, synth.SEED_RESHARD_8B, device="cuda")
+    parts = []
+    for r in range(8):
+        off = 0
+        for (_, rows, cols, split) in spec:
+            w = stream_t[off:off + rows * cols].view(rows, cols)
+            off += rows * cols
+            sl = w[r * rows // 8:(r + 1) * rows // 8] if split == "rows" else w[:, r * cols // 8:(r + 1) * cols // 8]
+            parts.append(sl.reshape(-1))
+    src = torch.cat(parts)
+    del parts, stream_t
+    frags_np = tc.tc_reshard_fragments(tcv.reshard_views(spec, 8, 4), 4, 1)
+    frags = torch.from_numpy(frags_np.view(np.int64)).cuda()
+    ws = torch.empty(tc.tc_copy_fragments_workspace(len(frags_np)), dtype=torch.uint8, device="cuda")
+    dst = torch.empty(tcv.shard_elems(spec, 4), dtype=torch.bfloat16, device="cuda")
+    total = tc.tc_plan_fragments(frags, ws, stream=stream)
+    nbytes = 2 * int(frags_np[:, 2].sum())
+    ms = _time_calls(torch, stream, lambda: tc.tc_copy_planned(src, dst, ws, total, stream=stream),
+                     args.warmup, args.cast_steps)
+    out = {"fragments": int(len(frags_np)), "tasks": int(total), "copy_planned": _stats(ms, nbytes)}
+    del src, dst, frags, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def run_cast(torch, tc, synth, args, stream):
     from paper_2608_06007_amd import views as tcv
     tp, rank = 8, 3
@@ -311,8 +343,8 @@ def run_calib(torch, tc, synth, args, stream):
     return out
 
 
-RUNNERS = {"reshard": run_reshard, "cast": run_cast, "storm": run_storm, "moe": run_moe,
-           "calib": run_calib}
+RUNNERS = {"reshard": run_reshard, "reshard_tp8_tp4": run_reshard44, "cast": run_cast,
+           "storm": run_storm, "moe": run_moe, "calib": run_calib}
 
 
 def main():
@@ -321,7 +353,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cast-steps", type=int, default=20, help="timed launches per extra workload")
-    ap.add_argument("--workloads", default="kv,reshard,cast,storm,moe,calib")
+    ap.add_argument("--workloads", default="kv,reshard,reshard_tp8_tp4,cast,storm,moe,calib")
     ap.add_argument("--skip-cpu", action="store_true", help="skip the CPU oracle baseline")
     args = ap.parse_args()
     if args.gpus != 1:

@@ -179,6 +179,46 @@ tc_status tc_tp_fragments(const tc_tp_view* views /* host */, int64_t n_views, i
                           int64_t* written /* host */);
 
 /* ------------------------------------------------------------------------
+ * Cross-layout reshard: a weight stored as the slices of a src_tp-way
+ * tensor-parallel split is rearranged into one rank's slice of a dst_tp-way
+ * split along the same dimension (resharding checkpoint tensors into the
+ * layouts other parallel configurations need, Sec. 2.1; rank-specific
+ * resharding with view() and transform_into(), Sec. 7).
+ *
+ * Source rank s holds its slice densely row-major at byte src_off[s] of the
+ * source buffer: rows [s*rows/src_tp, (s+1)*rows/src_tp) for TC_SPLIT_ROWS,
+ * columns [s*cols/src_tp, ...) for TC_SPLIT_COLS, the whole matrix for
+ * TC_SPLIT_NONE (then only src_off[0] is read).  The destination rank's slice
+ * is written densely row-major at byte dst_off of the destination buffer.
+ * Slices of consecutive views placed back to back give fused layouts (for
+ * example q, k, v of one rank stacked by rows).  Host builder only; the moves
+ * run through tc_plan_fragments / tc_copy_planned.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  const uint64_t* src_off; /* host array [src_tp]: byte offset of each source rank's slice */
+  int64_t rows, cols;      /* full matrix shape in elements */
+  int32_t elem_bytes;      /* 1, 2, 4 or 8 */
+  int32_t split;           /* tc_split, the same dimension on both sides */
+  int32_t src_tp;          /* ranks of the source split (>= 1) */
+  int32_t reserved;        /* 0 */
+  uint64_t dst_off;        /* byte offset of the destination rank's slice */
+} tc_reshard_view;
+
+/* Host: number of fragments tc_reshard_fragments produces (-1 on invalid
+ * arguments: a null src_off, tp < 1, rank out of range, a split dimension
+ * not divisible by src_tp or dst_tp, bad elem_bytes). */
+int64_t tc_reshard_fragment_count(const tc_reshard_view* views /* host */, int64_t n_views,
+                                  int32_t dst_tp, int32_t dst_rank);
+
+/* Host: write the fragments that build rank dst_rank's slices of a
+ * dst_tp-way split into out (room for `capacity`); *written gets the count.
+ * Contiguous runs are merged: a row split needs one fragment per overlapping
+ * source rank, a column split one per row and overlapping source rank. */
+tc_status tc_reshard_fragments(const tc_reshard_view* views /* host */, int64_t n_views,
+                               int32_t dst_tp, int32_t dst_rank, tc_fragment* out /* host */,
+                               int64_t capacity, int64_t* written /* host */);
+
+/* ------------------------------------------------------------------------
  * transform_into with an fp8 spec (Table 2, Sec. 3.2): bf16 -> OCP FP8 E4M3
  * with one fp32 scale per 128x128 tile, for weight synchronization
  * (Sec. 6.2).  The paper fixes no numeric format; this rule is:

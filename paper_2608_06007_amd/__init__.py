@@ -30,6 +30,7 @@ __all__ = [
     "tc_gather_blocks", "tc_scatter_blocks",
     "tc_copy_fragments_workspace", "tc_copy_fragments_workspace_min", "tc_copy_fragments", "tc_plan_fragments", "tc_copy_planned",
     "tc_tp_fragment_count", "tc_tp_fragments", "tc_tp_cast_item",
+    "tc_reshard_fragment_count", "tc_reshard_fragments",
     "tc_cast_fp8_workspace", "tc_cast_fp8_blockscaled", "tc_cast_fp8_scaled",
     "tc_status_string", "tc_last_hip_error", "tc_set_validate", "tc_get_validate",
     "FRAGMENT_DTYPE", "TP_VIEW_DTYPE", "CAST_ITEM_DTYPE",
@@ -65,6 +66,12 @@ class TcError(RuntimeError):
         super().__init__(f"{what}: {name}{extra}")
 
 
+class _ReshardView(ctypes.Structure):
+    _fields_ = [("src_off", ctypes.POINTER(ctypes.c_uint64)), ("rows", ctypes.c_int64),
+                ("cols", ctypes.c_int64), ("elem_bytes", ctypes.c_int32), ("split", ctypes.c_int32),
+                ("src_tp", ctypes.c_int32), ("reserved", ctypes.c_int32), ("dst_off", ctypes.c_uint64)]
+
+
 class _BlockPool(ctypes.Structure):
     _fields_ = [("region_base", ctypes.POINTER(ctypes.c_uint64)), ("num_regions", ctypes.c_int32),
                 ("num_blocks", ctypes.c_int64), ("block_bytes", ctypes.c_int64),
@@ -98,6 +105,10 @@ def load():
     L.tc_tp_fragments.argtypes = [P, c.c_int64, c.c_int32, c.c_int32, P, c.c_int64,
                                   c.POINTER(c.c_int64)]
     L.tc_tp_cast_item.argtypes = [P, c.c_int32, c.c_int32, c.c_uint64, P]
+    L.tc_reshard_fragment_count.argtypes = [P, c.c_int64, c.c_int32, c.c_int32]
+    L.tc_reshard_fragment_count.restype = c.c_int64
+    L.tc_reshard_fragments.argtypes = [P, c.c_int64, c.c_int32, c.c_int32, P, c.c_int64,
+                                       c.POINTER(c.c_int64)]
     L.tc_cast_fp8_workspace.argtypes = [c.c_int64]
     L.tc_cast_fp8_workspace.restype = c.c_size_t
     L.tc_cast_fp8_blockscaled.argtypes = [P, P, P, P, c.c_int64, c.c_int32, P, c.c_size_t, P]
@@ -108,7 +119,8 @@ def load():
     L.tc_set_validate.argtypes = [c.c_int]
     L.tc_get_validate.restype = c.c_int
     for name in ("tc_gather_blocks", "tc_scatter_blocks", "tc_copy_fragments", "tc_plan_fragments",
-                 "tc_copy_planned", "tc_tp_fragments", "tc_tp_cast_item", "tc_cast_fp8_blockscaled",
+                 "tc_copy_planned", "tc_tp_fragments", "tc_tp_cast_item", "tc_reshard_fragments",
+                 "tc_cast_fp8_blockscaled",
                  "tc_cast_fp8_scaled"):
         getattr(L, name).restype = c.c_int
     _lib = L
@@ -261,6 +273,39 @@ def tc_tp_cast_item(view, tp: int, rank: int, scale_off: int) -> np.ndarray:
     _ok(load().tc_tp_cast_item(v.ctypes.data, tp, rank, scale_off, out.ctypes.data),
         "tc_tp_cast_item")
     return out[0]
+
+
+def _reshard_array(views):
+    """views: sequence of (src_offsets, rows, cols, elem_bytes, split, dst_off)."""
+    keep = []
+    arr = (_ReshardView * len(views))()
+    for k, (offs, rows, cols, eb, split, dst_off) in enumerate(views):
+        o = (ctypes.c_uint64 * len(offs))(*[int(x) for x in offs])
+        keep.append(o)
+        arr[k] = _ReshardView(ctypes.cast(o, ctypes.POINTER(ctypes.c_uint64)), rows, cols, eb, split,
+                              len(offs), 0, dst_off)
+    return arr, keep
+
+
+def tc_reshard_fragment_count(views, dst_tp: int, dst_rank: int) -> int:
+    arr, _keep = _reshard_array(views)
+    n = int(load().tc_reshard_fragment_count(arr if len(views) else None, len(views), dst_tp, dst_rank))
+    if n < 0:
+        raise TcError(1, "tc_reshard_fragment_count")
+    return n
+
+
+def tc_reshard_fragments(views, dst_tp: int, dst_rank: int) -> np.ndarray:
+    """Fragments (uint64 [m, 3]) that build rank ``dst_rank`` of a ``dst_tp``-way
+    split from the source slices described by ``views``."""
+    arr, _keep = _reshard_array(views)
+    m = tc_reshard_fragment_count(views, dst_tp, dst_rank)
+    out = np.zeros((m, 3), dtype=np.uint64)
+    written = ctypes.c_int64(0)
+    _ok(load().tc_reshard_fragments(arr if len(views) else None, len(views), dst_tp, dst_rank,
+                                    out.ctypes.data if m else None, m, ctypes.byref(written)),
+        "tc_reshard_fragments")
+    return out[:written.value]
 
 
 # ---------------------------------------------------------------------------

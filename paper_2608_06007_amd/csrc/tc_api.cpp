@@ -244,6 +244,48 @@ tc_status stage_to_device(void* dev_dst, hipStream_t s, std::initializer_list<Pi
   return check(e);
 }
 
+bool elem_ok(int32_t eb) { return eb == 1 || eb == 2 || eb == 4 || eb == 8; }
+
+bool reshard_ok(const tc_reshard_view& v, int32_t dst_tp, int32_t dst_rank) {
+  if (!v.src_off || v.src_tp < 1 || dst_tp < 1 || dst_rank < 0 || dst_rank >= dst_tp) return false;
+  if (v.rows < 0 || v.cols < 0 || !elem_ok(v.elem_bytes)) return false;
+  if (v.split == TC_SPLIT_ROWS) return v.rows % v.src_tp == 0 && v.rows % dst_tp == 0;
+  if (v.split == TC_SPLIT_COLS) return v.cols % v.src_tp == 0 && v.cols % dst_tp == 0;
+  return v.split == TC_SPLIT_NONE;
+}
+
+// Fragments that fill the destination rank's slice from the overlapping
+// source slices.
+template <typename Emit>
+void reshard_fragments(const tc_reshard_view& v, int32_t dst_tp, int32_t d, Emit emit) {
+  if (v.rows == 0 || v.cols == 0) return;
+  const uint64_t eb = uint64_t(v.elem_bytes);
+  if (v.split == TC_SPLIT_NONE) {
+    emit(tc_fragment{v.src_off[0], v.dst_off, uint64_t(v.rows) * uint64_t(v.cols) * eb});
+    return;
+  }
+  const bool by_rows = v.split == TC_SPLIT_ROWS;
+  const int64_t extent = by_rows ? v.rows : v.cols;
+  const int64_t ns = extent / v.src_tp, nd = extent / dst_tp;  // slice widths
+  const int64_t d0 = int64_t(d) * nd, d1 = d0 + nd;
+  for (int64_t s = d0 / ns; s <= (d1 - 1) / ns; ++s) {
+    const int64_t a = std::max(d0, s * ns), b = std::min(d1, (s + 1) * ns);
+    if (by_rows) {
+      const uint64_t row = uint64_t(v.cols) * eb;
+      emit(tc_fragment{v.src_off[s] + uint64_t(a - s * ns) * row, v.dst_off + uint64_t(a - d0) * row,
+                       uint64_t(b - a) * row});
+    } else if (ns == nd && a == s * ns && b - a == ns) {
+      // identical column blocks: the whole slice is one contiguous run
+      emit(tc_fragment{v.src_off[s], v.dst_off, uint64_t(v.rows) * uint64_t(ns) * eb});
+    } else {
+      for (int64_t r = 0; r < v.rows; ++r)
+        emit(tc_fragment{v.src_off[s] + (uint64_t(r) * uint64_t(ns) + uint64_t(a - s * ns)) * eb,
+                         v.dst_off + (uint64_t(r) * uint64_t(nd) + uint64_t(a - d0)) * eb,
+                         uint64_t(b - a) * eb});
+    }
+  }
+}
+
 }  // namespace
 
 namespace tc {
@@ -426,6 +468,32 @@ tc_status tc_tp_fragments(const tc_tp_view* views, int64_t n_views, int32_t tp, 
   int64_t k = 0;
   for (int64_t i = 0; i < n_views; ++i)
     view_fragments(views[i], tp, rank, [&](const tc_fragment& f) { out[k++] = f; });
+  *written = k;
+  return TC_OK;
+}
+
+int64_t tc_reshard_fragment_count(const tc_reshard_view* views, int64_t n_views, int32_t dst_tp,
+                                  int32_t dst_rank) {
+  if (n_views < 0 || (n_views > 0 && !views)) return -1;
+  int64_t count = 0;
+  for (int64_t i = 0; i < n_views; ++i) {
+    if (!reshard_ok(views[i], dst_tp, dst_rank)) return -1;
+    reshard_fragments(views[i], dst_tp, dst_rank, [&](const tc_fragment&) { ++count; });
+  }
+  return count;
+}
+
+tc_status tc_reshard_fragments(const tc_reshard_view* views, int64_t n_views, int32_t dst_tp,
+                               int32_t dst_rank, tc_fragment* out, int64_t capacity,
+                               int64_t* written) {
+  if (!written || n_views < 0 || (n_views > 0 && !views) || capacity < 0)
+    return TC_ERR_INVALID_ARGUMENT;
+  const int64_t need = tc_reshard_fragment_count(views, n_views, dst_tp, dst_rank);
+  if (need < 0) return TC_ERR_INVALID_ARGUMENT;
+  if (need > capacity || (need > 0 && !out)) return TC_ERR_WORKSPACE;
+  int64_t k = 0;
+  for (int64_t i = 0; i < n_views; ++i)
+    reshard_fragments(views[i], dst_tp, dst_rank, [&](const tc_fragment& f) { out[k++] = f; });
   *written = k;
   return TC_OK;
 }

@@ -67,3 +67,28 @@ def cast_items(spec, tp: int, rank: int) -> np.ndarray:
         sr, sc = slice_shape(rows, cols, split, tp)
         scale_off += ((sr + 127) // 128) * ((sc + 127) // 128)
     return items
+
+
+def shard_slice_offsets(spec, tp: int, elem_bytes: int = 2):
+    """Byte offset of every matrix's slice inside one rank's packed shard (spec
+    order), and the shard's size in bytes."""
+    offs = []
+    off = 0
+    for (_name, rows, cols, split) in spec:
+        sr, sc = slice_shape(rows, cols, split, tp)
+        offs.append(off)
+        off += sr * sc * elem_bytes
+    return offs, off
+
+
+def reshard_views(spec, src_tp: int, dst_tp: int, elem_bytes: int = 2):
+    """Views for tc_reshard_fragments: the source buffer holds the src_tp
+    shards one after another (rank-major, each packed in spec order); the
+    destination is one rank's packed shard of the dst_tp split."""
+    soffs, sbytes = shard_slice_offsets(spec, src_tp, elem_bytes)
+    doffs, _ = shard_slice_offsets(spec, dst_tp, elem_bytes)
+    out = []
+    for k, (_name, rows, cols, split) in enumerate(spec):
+        src = [r * sbytes + soffs[k] for r in range(src_tp)]
+        out.append((src, rows, cols, elem_bytes, _SPLIT[split], doffs[k]))
+    return out

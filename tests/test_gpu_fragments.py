@@ -222,3 +222,67 @@ def test_storm_full_size():
     dst, _, _ = _copy_and_check(src, frags, pool)
     del src, dst
     torch.cuda.empty_cache()
+
+
+def _torch_shards(stream, spec, tp):
+    """All tp shards of a contiguous stream, rank-major, built with torch
+    slicing on the device (independent of the library)."""
+    parts = []
+    for r in range(tp):
+        off = 0
+        for (_, rows, cols, split) in spec:
+            w = stream[off:off + rows * cols].view(rows, cols)
+            off += rows * cols
+            sl = w[r * rows // tp:(r + 1) * rows // tp] if split == "rows" else \
+                w[:, r * cols // tp:(r + 1) * cols // tp]
+            parts.append(sl.reshape(-1))
+    return torch.cat(parts)
+
+
+@pytest.mark.parametrize("src_tp,dst_tp,ranks", [(8, 4, range(4)), (4, 8, [0, 3, 7]), (8, 1, [0]),
+                                                 (2, 8, [5])])
+def test_cross_layout_reshard_8b(src_tp, dst_tp, ranks):
+    """2 layers of the 8B shapes stored as src_tp shards, rearranged into
+    dst_tp shards by the builder's fragments and the planned copy."""
+    spec = synth.spec_8b(2)
+    n = synth.spec_elems(spec)
+    stream = synth.bf16_normal(n, 1.0, synth.SEED_RESHARD_8B, device=DEV)
+    src = _torch_shards(stream, spec, src_tp)
+    host = _host(stream.view(torch.int16)).view(np.uint16)
+    views = tcv.reshard_views(spec, src_tp, dst_tp)
+    for rank in ranks:
+        frags_np = tc.tc_reshard_fragments(views, dst_tp, rank)
+        frags = torch.from_numpy(frags_np.view(np.int64)).to(DEV)
+        ws = torch.empty(tc.tc_copy_fragments_workspace(len(frags_np)), dtype=torch.uint8, device=DEV)
+        total = tc.tc_plan_fragments(frags, ws)
+        dst = torch.empty(tcv.shard_elems(spec, dst_tp), dtype=torch.bfloat16, device=DEV)
+        tc.tc_copy_planned(src, dst, ws, total)
+        torch.cuda.synchronize()
+        want = oracle.tp_shard(host, spec, dst_tp, rank)
+        assert np.array_equal(_host(dst.view(torch.int16)).view(np.uint16), want)
+
+
+def test_cross_layout_reshard_8b_full_size():
+    """32 layers of the 8B shapes: the TP=8 shards (13.96 GB) rearranged into
+    TP=4 rank 1; every slice checked against torch slicing of the stream on
+    the device, two layers against the oracle."""
+    spec = synth.spec_8b(32)
+    n = synth.spec_elems(spec)
+    stream = synth.bf16_normal(n, 1.0, synth.SEED_RESHARD_8B, device=DEV)
+    src = _torch_shards(stream, spec, 8)
+    frags_np = tc.tc_reshard_fragments(tcv.reshard_views(spec, 8, 4), 4, 1)
+    frags = torch.from_numpy(frags_np.view(np.int64)).to(DEV)
+    ws = torch.empty(tc.tc_copy_fragments_workspace(len(frags_np)), dtype=torch.uint8, device=DEV)
+    total = tc.tc_plan_fragments(frags, ws)
+    dst = torch.empty(tcv.shard_elems(spec, 4), dtype=torch.bfloat16, device=DEV)
+    tc.tc_copy_planned(src, dst, ws, total)
+    torch.cuda.synchronize()
+    want = _torch_shards(stream, spec, 4)[1 * dst.numel():2 * dst.numel()]
+    assert torch.equal(dst.view(torch.int16), want.view(torch.int16))
+    per_layer = synth.spec_elems(spec[:7])
+    shard_layer = tcv.shard_elems(spec[:7], 4)
+    got = _host(dst.view(torch.int16)).view(np.uint16)
+    for l in [0, 31]:
+        lw = _host(stream[l * per_layer:(l + 1) * per_layer].view(torch.int16)).view(np.uint16)
+        assert np.array_equal(got[l * shard_layer:(l + 1) * shard_layer],
+                              oracle.tp_shard(lw, spec[7 * l:7 * l + 7], 4, 1))

@@ -151,3 +151,43 @@ def test_cast_items_describe_the_slices(lib):
         assert it["scale_off"] == s_off and it["scale_ld"] == (sl.shape[1] + 127) // 128
         q_off += sl.size
         s_off += ((sl.shape[0] + 127) // 128) * ((sl.shape[1] + 127) // 128)
+
+
+@pytest.mark.parametrize("src_tp,dst_tp", [(8, 4), (4, 8), (8, 1), (1, 8), (2, 8), (8, 8), (4, 2)])
+def test_reshard_fragments_reproduce_oracle_shard(lib, src_tp, dst_tp):
+    """Source = the src_tp oracle shards back to back; the builder's fragments,
+    applied with the oracle's byte copier, must give the oracle's dst shard."""
+    n = synth.spec_elems(SPEC)
+    rng = np.random.default_rng(21)
+    stream = rng.integers(0, 1 << 16, size=n, dtype=np.uint64).astype(np.uint16)
+    src = np.concatenate([oracle.tp_shard(stream, SPEC, src_tp, r) for r in range(src_tp)])
+    views = tcv.reshard_views(SPEC, src_tp, dst_tp)
+    for rank in range(dst_tp):
+        frags = tc.tc_reshard_fragments(views, dst_tp, rank)
+        dst = np.full(tcv.shard_elems(SPEC, dst_tp), 0xBEEF, dtype=np.uint16)
+        oracle.copy_fragments(src.view(np.uint8), dst.view(np.uint8), frags)
+        assert np.array_equal(dst, oracle.tp_shard(stream, SPEC, dst_tp, rank))
+
+
+def test_reshard_round_trip_and_fragment_counts(lib):
+    """TP8 -> TP4 -> TP8 gives back every TP8 shard; a row split needs one
+    fragment per overlapping source rank, a column split one per row."""
+    n = synth.spec_elems(SPEC)
+    stream = np.arange(n, dtype=np.uint64).astype(np.uint16) ^ np.uint16(0x5A5A)
+    tp8 = np.concatenate([oracle.tp_shard(stream, SPEC, 8, r) for r in range(8)])
+    tp4 = []
+    for r in range(4):
+        dst = np.zeros(tcv.shard_elems(SPEC, 4), dtype=np.uint16)
+        oracle.copy_fragments(tp8.view(np.uint8), dst.view(np.uint8),
+                              tc.tc_reshard_fragments(tcv.reshard_views(SPEC, 8, 4), 4, r))
+        tp4.append(dst)
+    tp4 = np.concatenate(tp4)
+    for r in range(8):
+        dst = np.zeros(tcv.shard_elems(SPEC, 8), dtype=np.uint16)
+        oracle.copy_fragments(tp4.view(np.uint8), dst.view(np.uint8),
+                              tc.tc_reshard_fragments(tcv.reshard_views(SPEC, 4, 8), 8, r))
+        assert np.array_equal(dst, tp8.reshape(8, -1)[r])
+    # per layer: q k v gate up -> 2 source ranks each; o, down -> 2 x 256 rows
+    assert tc.tc_reshard_fragment_count(tcv.reshard_views(SPEC, 8, 4), 4, 1) == 2 * (5 * 2 + 2 * 256 * 2)
+    with pytest.raises(tc.TcError):
+        tc.tc_reshard_fragments(tcv.reshard_views(SPEC, 8, 3), 3, 0)   # 3 does not divide
