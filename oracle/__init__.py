@@ -18,6 +18,8 @@ What each function follows:
 * ``cast_fp8_blockscaled`` / ``cast_fp8_scaled`` / ``e4m3_encode`` -- one
   concrete transform_into `spec` rule (Table 2): bf16 -> OCP FP8 E4M3 with
   an fp32 scale per 128x128 tile.
+* ``dequant_fp8_blockscaled`` -- its inverse, back to bf16, for resharding
+  stored fp8 checkpoints into other layouts (Sec. 2.1, Sec. 7).
 """
 from __future__ import annotations
 
@@ -61,6 +63,11 @@ def _load():
     lib.orc_cast_fp8_blockscaled.argtypes = [c.c_void_p, c.c_int64, c.c_int64, c.c_int64,
                                              c.c_void_p, c.c_int64, c.c_void_p, c.c_int64]
     lib.orc_cast_fp8_blockscaled.restype = None
+    lib.orc_dequant_fp8_blockscaled.argtypes = [c.c_void_p, c.c_int64, c.c_int64, c.c_int64,
+                                                c.c_void_p, c.c_int64, c.c_void_p, c.c_int64]
+    lib.orc_dequant_fp8_blockscaled.restype = None
+    lib.orc_bf16_round.argtypes = [c.c_float]
+    lib.orc_bf16_round.restype = c.c_uint16
     _lib = lib
     return lib
 
@@ -210,3 +217,24 @@ def cast_fp8_blockscaled(x_bits: np.ndarray):
     if rows and cols:
         _load().orc_cast_fp8_blockscaled(_ptr(x), rows, cols, ld, _ptr(q), cols, _ptr(s), tc)
     return q, s
+
+
+def bf16_round(v: float) -> int:
+    return int(_load().orc_bf16_round(float(v)))
+
+
+def dequant_fp8_blockscaled(q: np.ndarray, scales: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns [rows, cols] of RN_bf16(RN_f32(dec(q) * s)) with s the
+    scale of each element's 128x128 tile."""
+    q = np.asarray(q)
+    assert q.dtype == np.uint8 and q.ndim == 2
+    if q.strides[1] != 1:
+        q = np.ascontiguousarray(q)
+    rows, cols = q.shape
+    s = np.ascontiguousarray(scales, dtype=np.float32)
+    assert s.shape == scale_grid(rows, cols)
+    y = np.empty((rows, cols), dtype=np.uint16)
+    if rows and cols:
+        _load().orc_dequant_fp8_blockscaled(_ptr(q), rows, cols, q.strides[0], _ptr(s), s.shape[1],
+                                            _ptr(y), cols)
+    return y

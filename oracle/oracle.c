@@ -219,3 +219,36 @@ void orc_cast_fp8_blockscaled(const uint16_t* x, int64_t rows, int64_t cols,
     }
   }
 }
+
+/* ------------------------------------------------------------------ */
+/* Inverse cast                                                        */
+/* ------------------------------------------------------------------ */
+
+/* bf16 keeps the top 16 bits of a binary32 value: round the dropped 16 bits
+ * to nearest, ties to the even kept bit. */
+uint16_t orc_bf16_round(float v) {
+  if (isnan(v)) return 0x7FC0;
+  uint32_t u;
+  memcpy(&u, &v, 4);
+  uint32_t kept = u >> 16, dropped = u & 0xFFFFu;
+  if (dropped > 0x8000u || (dropped == 0x8000u && (kept & 1u))) kept += 1; /* carries into the exponent */
+  return (uint16_t)kept;
+}
+
+void orc_dequant_fp8_blockscaled(const uint8_t* q, int64_t rows, int64_t cols, int64_t q_ld,
+                                 const float* scales, int64_t scale_ld, uint16_t* y,
+                                 int64_t y_ld) {
+  ieee_mode();
+#pragma omp parallel
+  {
+    ieee_mode();
+#pragma omp for schedule(static)
+    for (int64_t r = 0; r < rows; r++) {
+      for (int64_t c = 0; c < cols; c++) {
+        float s = scales[(r / 128) * scale_ld + c / 128];
+        float v = orc_e4m3_decode(q[r * q_ld + c]) * s; /* binary32 product, round to nearest even */
+        y[r * y_ld + c] = orc_bf16_round(v);
+      }
+    }
+  }
+}

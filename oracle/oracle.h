@@ -82,6 +82,17 @@ void orc_cast_fp8_blockscaled(const uint16_t* x, int64_t rows, int64_t cols,
                               int64_t ld, uint8_t* q, int64_t q_ld,
                               float* scales, int64_t scale_ld);
 
+/* Inverse of the block-scaled cast: y = RN_bf16(RN_f32(dec(q) * s)) for
+ * every code of a [rows][cols] matrix (row stride q_ld bytes) with the fp32
+ * scale of its 128x128 tile (grid row stride scale_ld).  A NaN result (code
+ * 0x7F/0xFF, NaN scale, or 0 * Inf) is written as 0x7FC0.  y is [rows][y_ld]
+ * raw bf16 patterns. */
+void orc_dequant_fp8_blockscaled(const uint8_t* q, int64_t rows, int64_t cols, int64_t q_ld,
+                                 const float* scales, int64_t scale_ld, uint16_t* y,
+                                 int64_t y_ld);
+/* RN_bf16 of a binary32 value (ties to even; NaN -> 0x7FC0). */
+uint16_t orc_bf16_round(float v);
+
 #ifdef __cplusplus
 }
 #endif

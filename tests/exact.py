@@ -105,3 +105,33 @@ def quotient_code(x: float, s: float) -> int:
     neg = (math.copysign(1.0, x) < 0) != (s < 0)
     q = rn_f32(Fraction(x) / Fraction(s), negative_zero=neg)
     return encode_float(q)
+
+
+def rn_bf16_of_f32(x: float) -> int:
+    """bf16 bit pattern of a binary32 value rounded to 8 significant bits
+    (nearest, ties to even), computed on the exact value; NaN -> 0x7FC0."""
+    if math.isnan(x):
+        return 0x7FC0
+    sign = 0x8000 if math.copysign(1.0, x) < 0 else 0
+    if math.isinf(x):
+        return sign | 0x7F80
+    a = Fraction(abs(x))
+    if a == 0:
+        return sign
+    two = Fraction(2)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    while two ** e > a:
+        e -= 1
+    while two ** (e + 1) <= a:
+        e += 1
+    e = max(e, -126)
+    quantum = two ** (e - 7)                  # 8 significant bits
+    m = a / quantum
+    n = m.numerator // m.denominator
+    rem = m - n
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    val = n * quantum
+    if val >= two ** 128:
+        return sign | 0x7F80
+    return sign | (f32_bits(float(val)) >> 16)

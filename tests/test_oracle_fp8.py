@@ -244,3 +244,65 @@ def test_blockscaled_invariants():
             bound = np.where(normal, (2.0 ** -4 + 2.0 ** -23) * np.abs(xs),
                              2.0 ** -10 * sc + 2.0 ** -23 * np.abs(xs))
             assert np.all(err <= bound * (1 + 1e-12))
+
+
+# ---------------------------------------------------------------------------
+# inverse cast: E4M3 + tile scale -> bf16
+# ---------------------------------------------------------------------------
+
+def _dequant_exact(code: int, s: float) -> int:
+    v = exact.e4m3_value(code)
+    if v is None or math.isnan(s):
+        return 0x7FC0
+    if math.isinf(s):
+        if v == 0:
+            return 0x7FC0                     # 0 * Inf
+        neg = (v < 0) != (s < 0)
+        return (0x8000 if neg else 0) | 0x7F80
+    prod = Fraction(v) * Fraction(s)
+    neg_zero = prod == 0 and ((code & 0x80) != 0) != (math.copysign(1.0, s) < 0)
+    return exact.rn_bf16_of_f32(exact.rn_f32(prod, negative_zero=neg_zero))
+
+
+def test_dequant_every_code_at_many_scales():
+    rng = np.random.default_rng(60)
+    scales = list(_random_scales(rng, 24)) + [0.0, -0.0, 1.0, 2.0 ** -140, 3.4e38, float("inf"),
+                                              float("nan")]
+    codes = np.arange(256, dtype=np.uint8)
+    for s in scales:
+        s32 = float(np.float32(s))
+        q = np.tile(codes, 128).reshape(128, 256)
+        sg = np.full((1, 2), s32, dtype=np.float32)
+        y = oracle.dequant_fp8_blockscaled(q, sg)
+        want = np.array([_dequant_exact(int(c), s32) for c in codes], dtype=np.uint16)
+        assert np.array_equal(y[0], want), s32
+        assert np.array_equal(y[77], want)
+
+
+def test_dequant_matches_torch_for_finite_results():
+    """torch: float8_e4m3fn -> float32, times the scale, -> bfloat16 (RNE)."""
+    rng = np.random.default_rng(61)
+    q = rng.integers(0, 256, size=(256, 384), dtype=np.int64).astype(np.uint8)
+    s = (rng.uniform(0.5, 2.0, size=(2, 3)) * 10.0 ** rng.integers(-30, 30, size=(2, 3))).astype(np.float32)
+    y = oracle.dequant_fp8_blockscaled(q, s)
+    t = torch.from_numpy(q).view(torch.float8_e4m3fn).float()
+    tiles = torch.from_numpy(np.repeat(np.repeat(s, 128, axis=0), 128, axis=1))
+    ref = (t * tiles).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    finite = np.isfinite((t * tiles).numpy())
+    assert np.array_equal(y[finite], ref[finite])
+
+
+def test_dequant_inverts_the_cast_within_the_rounding_bound():
+    rng = np.random.default_rng(62)
+    a = rng.normal(0, 0.02, size=(300, 260)).astype(np.float32)
+    xb = _bits_from_float(a)
+    q, s = oracle.cast_fp8_blockscaled(xb)
+    y = oracle.dequant_fp8_blockscaled(q, s)
+    x = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).float().numpy().astype(np.float64)
+    back = torch.from_numpy(y.view(np.int16)).view(torch.bfloat16).float().numpy().astype(np.float64)
+    scale_el = np.repeat(np.repeat(s.astype(np.float64), 128, axis=0), 128, axis=1)[:300, :260]
+    normal = np.abs(x) / scale_el >= 2.0 ** -6
+    # E4M3 relative error 2^-4, then bf16 rounding 2^-9 of the result
+    bound = np.where(normal, (2.0 ** -4) * np.abs(x), 2.0 ** -10 * scale_el) * (1 + 2.0 ** -8) + \
+        2.0 ** -9 * np.abs(back)
+    assert np.all(np.abs(back - x) <= bound)
