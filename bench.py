@@ -288,7 +288,16 @@ def run_cast(torch, tc, synth, args, stream):
     ms = _time_calls(torch, stream, lambda: tc.tc_cast_fp8_blockscaled(src, q, sc, it, ws, stream=stream),
                      args.warmup, args.cast_steps)
     out = {"items": int(len(items)), "tiles": int(n_scales), "cast": _stats(ms, nbytes)}
-    del src, q, sc, ws, it
+    del src
+    torch.cuda.empty_cache()
+    # the inverse rule on the shard just produced: e4m3 + scales -> bf16
+    ditems = tcv.dequant_items(spec, tp)
+    y = torch.empty(shard_n, dtype=torch.bfloat16, device="cuda")
+    dws = torch.empty(tc.tc_dequant_fp8_workspace(len(ditems)), dtype=torch.uint8, device="cuda")
+    dms = _time_calls(torch, stream, lambda: tc.tc_dequant_fp8_blockscaled(q, sc, y, ditems, dws, stream=stream),
+                      args.warmup, args.cast_steps)
+    out["dequant"] = _stats(dms, shard_n + 4 * n_scales + 2 * shard_n)
+    del q, sc, ws, it, y, dws
     torch.cuda.empty_cache()
     return out
 

@@ -268,6 +268,34 @@ tc_status tc_cast_fp8_blockscaled(const void* src_base, void* dst_base, float* s
 tc_status tc_cast_fp8_scaled(const void* src_bf16, int64_t n, float scale, void* dst_e4m3,
                              hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * The inverse rule: E4M3 codes with their per-tile fp32 scales back to bf16,
+ * so fp8 artifacts can be resharded or consumed by bf16 engines (resharding
+ * into other layouts, Sec. 2.1; rank-specific transform_into, Sec. 7):
+ *   y = RN_bf16(RN_f32(E4M3value(q) * s)), s the scale of q's 128x128 tile;
+ *   a NaN product (code 0x7F/0xFF, NaN scale, 0 * Inf) gives 0x7FC0.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  uint64_t src_off;   /* bytes from the code base to code [0][0] */
+  int64_t rows, cols; /* matrix shape (elements) */
+  int64_t src_ld;     /* bytes between code rows (>= cols) */
+  uint64_t dst_off;   /* bf16 elements from dst_base to element [0][0] */
+  int64_t dst_ld;     /* bf16 elements between destination rows (>= cols) */
+  uint64_t scale_off; /* floats from scale_base to scale [0][0] */
+  int64_t scale_ld;   /* floats between rows of the scale grid (>= ceil(cols/128)) */
+} tc_dequant_item;
+
+/* Bytes of device workspace tc_dequant_fp8_blockscaled needs for n items. */
+size_t tc_dequant_fp8_workspace(int64_t n_items);
+
+/* Dequantize every item.  items: HOST array, staged like the cast's.  The
+ * bf16 destinations must not overlap one another or the sources.  tile must
+ * be 128. */
+tc_status tc_dequant_fp8_blockscaled(const void* codes_base, const float* scale_base,
+                                     void* dst_base, const tc_dequant_item* items /* host */,
+                                     int64_t n_items, int32_t tile, void* workspace,
+                                     size_t workspace_bytes, hipStream_t stream);
+
 /* ------------------------------------------------------------------------ */
 const char* tc_status_string(tc_status status);
 /* hipError_t of the most recent TC_ERR_HIP on the calling thread. */

@@ -32,6 +32,7 @@ __all__ = [
     "tc_tp_fragment_count", "tc_tp_fragments", "tc_tp_cast_item",
     "tc_reshard_fragment_count", "tc_reshard_fragments",
     "tc_cast_fp8_workspace", "tc_cast_fp8_blockscaled", "tc_cast_fp8_scaled",
+    "tc_dequant_fp8_workspace", "tc_dequant_fp8_blockscaled", "DEQUANT_ITEM_DTYPE",
     "tc_status_string", "tc_last_hip_error", "tc_set_validate", "tc_get_validate",
     "FRAGMENT_DTYPE", "TP_VIEW_DTYPE", "CAST_ITEM_DTYPE",
     "SPLIT_NONE", "SPLIT_ROWS", "SPLIT_COLS", "MAX_REGIONS",
@@ -51,6 +52,9 @@ FRAGMENT_DTYPE = np.dtype([("src_off", "<u8"), ("dst_off", "<u8"), ("len", "<u8"
 TP_VIEW_DTYPE = np.dtype([("src_off", "<u8"), ("rows", "<i8"), ("cols", "<i8"), ("src_ld", "<i8"),
                           ("dst_off", "<u8"), ("dst_ld", "<i8"), ("elem_bytes", "<i4"),
                           ("split", "<i4")])
+DEQUANT_ITEM_DTYPE = np.dtype([("src_off", "<u8"), ("rows", "<i8"), ("cols", "<i8"), ("src_ld", "<i8"),
+                               ("dst_off", "<u8"), ("dst_ld", "<i8"), ("scale_off", "<u8"),
+                               ("scale_ld", "<i8")])
 CAST_ITEM_DTYPE = np.dtype([("src_off", "<u8"), ("rows", "<i8"), ("cols", "<i8"), ("src_ld", "<i8"),
                             ("dst_off", "<u8"), ("dst_ld", "<i8"), ("scale_off", "<u8"),
                             ("scale_ld", "<i8")])
@@ -113,6 +117,9 @@ def load():
     L.tc_cast_fp8_workspace.restype = c.c_size_t
     L.tc_cast_fp8_blockscaled.argtypes = [P, P, P, P, c.c_int64, c.c_int32, P, c.c_size_t, P]
     L.tc_cast_fp8_scaled.argtypes = [P, c.c_int64, c.c_float, P, P]
+    L.tc_dequant_fp8_workspace.argtypes = [c.c_int64]
+    L.tc_dequant_fp8_workspace.restype = c.c_size_t
+    L.tc_dequant_fp8_blockscaled.argtypes = [P, P, P, P, c.c_int64, c.c_int32, P, c.c_size_t, P]
     L.tc_status_string.argtypes = [c.c_int]
     L.tc_status_string.restype = c.c_char_p
     L.tc_last_hip_error.restype = c.c_int
@@ -120,7 +127,7 @@ def load():
     L.tc_get_validate.restype = c.c_int
     for name in ("tc_gather_blocks", "tc_scatter_blocks", "tc_copy_fragments", "tc_plan_fragments",
                  "tc_copy_planned", "tc_tp_fragments", "tc_tp_cast_item", "tc_reshard_fragments",
-                 "tc_cast_fp8_blockscaled",
+                 "tc_cast_fp8_blockscaled", "tc_dequant_fp8_blockscaled",
                  "tc_cast_fp8_scaled"):
         getattr(L, name).restype = c.c_int
     _lib = L
@@ -333,6 +340,21 @@ def tc_cast_fp8_scaled(src, scale: float, dst, stream=None) -> None:
     _ok(load().tc_cast_fp8_scaled(_dev_ptr(src) if n else None, n, float(scale),
                                   _dev_ptr(dst) if n else None, _stream(stream)),
         "tc_cast_fp8_scaled")
+
+
+def tc_dequant_fp8_workspace(n_items: int) -> int:
+    return int(load().tc_dequant_fp8_workspace(int(n_items)))
+
+
+def tc_dequant_fp8_blockscaled(codes, scales, dst, items, workspace, stream=None, tile: int = 128) -> None:
+    """bf16 = RN_bf16(RN_f32(E4M3(q) * s)) for every item; ``items`` is a host
+    numpy array of DEQUANT_ITEM_DTYPE records."""
+    it = np.ascontiguousarray(items, dtype=DEQUANT_ITEM_DTYPE).reshape(-1)
+    n = it.size
+    _ok(load().tc_dequant_fp8_blockscaled(_dev_ptr(codes), _dev_ptr(scales), _dev_ptr(dst),
+                                          it.ctypes.data if n else None, n, tile,
+                                          _dev_ptr(workspace), _nbytes(workspace), _stream(stream)),
+        "tc_dequant_fp8_blockscaled")
 
 
 # ---------------------------------------------------------------------------

@@ -595,6 +595,81 @@ tc_status tc_cast_fp8_blockscaled(const void* src_base, void* dst_base, float* s
                                            n_items, full, edge, stream));
 }
 
+size_t tc_dequant_fp8_workspace(int64_t n_items) {
+  if (n_items < 0) return 0;
+  return tc::cast_workspace_bytes(n_items);
+}
+
+static_assert(sizeof(tc_dequant_item) == sizeof(tc_cast_item), "shared workspace layout");
+
+tc_status tc_dequant_fp8_blockscaled(const void* codes_base, const float* scale_base,
+                                     void* dst_base, const tc_dequant_item* items, int64_t n_items,
+                                     int32_t tile, void* workspace, size_t workspace_bytes,
+                                     hipStream_t stream) {
+  if (n_items < 0 || tile != 128) return TC_ERR_INVALID_ARGUMENT;
+  if (n_items == 0) return TC_OK;
+  if (!codes_base || !scale_base || !dst_base || !items || !workspace) return TC_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < tc::cast_workspace_bytes(n_items)) return TC_ERR_WORKSPACE;
+  if ((uintptr_t)workspace % 256 || (uintptr_t)dst_base % 2 || (uintptr_t)scale_base % 4)
+    return TC_ERR_INVALID_ARGUMENT;
+  const size_t N = (size_t)n_items;
+  std::vector<uint64_t> fprefix(N + 1), eprefix(N + 1);
+  std::vector<uint8_t> aligned(N);
+  uint64_t full = 0, edge = 0;
+  for (size_t i = 0; i < N; ++i) {
+    const tc_dequant_item& it = items[i];
+    if (it.rows < 0 || it.cols < 0 || it.src_ld < it.cols || it.dst_ld < it.cols)
+      return TC_ERR_INVALID_ARGUMENT;
+    const uint64_t tr = uint64_t((it.rows + 127) / 128), tcn = uint64_t((it.cols + 127) / 128);
+    if (it.rows > 0 && it.cols > 0 && it.scale_ld < int64_t(tcn)) return TC_ERR_INVALID_ARGUMENT;
+    const uint64_t q = (uint64_t)(uintptr_t)codes_base + it.src_off;
+    const uint64_t y = (uint64_t)(uintptr_t)dst_base + 2 * it.dst_off;
+    aligned[i] = (q % 8 == 0 && uint64_t(it.src_ld) % 8 == 0 && y % 16 == 0 &&
+                  (2 * uint64_t(it.dst_ld)) % 16 == 0) ? 1 : 0;
+    const uint64_t all = (it.rows > 0 && it.cols > 0) ? tr * tcn : 0;
+    const uint64_t f = aligned[i] ? uint64_t(it.rows / 128) * uint64_t(it.cols / 128) : 0;
+    fprefix[i] = full;
+    eprefix[i] = edge;
+    full += f;
+    edge += all - f;
+  }
+  fprefix[N] = full;
+  eprefix[N] = edge;
+  if (full + edge == 0) return TC_OK;
+  if (validating()) {
+    std::vector<Range> outs, srcs;
+    const uint64_t db = (uint64_t)(uintptr_t)dst_base, qb = (uint64_t)(uintptr_t)codes_base;
+    const uint64_t sb = (uint64_t)(uintptr_t)scale_base;
+    for (size_t i = 0; i < N; ++i) {
+      const tc_dequant_item& it = items[i];
+      if (it.rows == 0 || it.cols == 0) continue;
+      const int64_t tcn = (it.cols + 127) / 128, tr = (it.rows + 127) / 128;
+      for (int64_t r = 0; r < it.rows; ++r) {
+        const uint64_t a = db + 2 * (it.dst_off + uint64_t(r) * uint64_t(it.dst_ld));
+        outs.push_back({a, a + 2 * uint64_t(it.cols)});
+        const uint64_t x = qb + it.src_off + uint64_t(r) * uint64_t(it.src_ld);
+        srcs.push_back({x, x + uint64_t(it.cols)});
+      }
+      for (int64_t r = 0; r < tr; ++r) {
+        const uint64_t a = sb + 4 * (it.scale_off + uint64_t(r) * uint64_t(it.scale_ld));
+        srcs.push_back({a, a + 4 * uint64_t(tcn)});
+      }
+    }
+    if (any_overlap(outs)) return TC_ERR_ALIAS;
+    if (cross_overlap(outs, srcs)) return TC_ERR_ALIAS;
+  }
+  const tc::CastLayout L = tc::cast_layout(n_items);
+  tc_status st = stage_to_device(workspace, stream,
+                                 {{items, sizeof(tc_dequant_item) * N, L.items},
+                                  {fprefix.data(), 8 * (N + 1), L.full_prefix},
+                                  {eprefix.data(), 8 * (N + 1), L.edge_prefix},
+                                  {aligned.data(), N, L.aligned}});
+  if (st != TC_OK) return st;
+  return check(tc::launch_dequant_blockscaled(static_cast<const uint8_t*>(codes_base), scale_base,
+                                              static_cast<uint16_t*>(dst_base), workspace, n_items,
+                                              full, edge, stream));
+}
+
 tc_status tc_cast_fp8_scaled(const void* src_bf16, int64_t n, float scale, void* dst_e4m3,
                              hipStream_t stream) {
   if (n < 0) return TC_ERR_INVALID_ARGUMENT;

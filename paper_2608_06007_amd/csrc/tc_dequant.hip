@@ -1,0 +1,161 @@
+// The inverse of the block-scaled cast for gfx950: E4M3 codes with one fp32
+// scale per 128x128 tile back to bf16, y = RN_bf16(RN_f32(value(q) * s)).
+//
+// Layout mirrors the cast: one 512-thread workgroup per full tile of an
+// aligned item (16 lanes x 8 codes per 128-byte code row, 32 rows per pass,
+// 4 passes; 8 bf16 = 16 B stored per lane and pass), non-temporal loads and
+// stores, XCD groups of 4 tiles; partial tiles and unaligned items go to an
+// element-wise kernel.  Decoding uses v_cvt_pk_f32_fp8, which is exact for
+// every finite E4M3 code and gives NaN for S.1111.111; the bf16 rounding is
+// done on the integer bits (nearest, ties to even; NaN -> 0x7FC0).
+#include "tc_internal.h"
+
+namespace tc {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWaveLanes = 64;
+constexpr int kTile = 128;
+constexpr int kThreads = 512;
+constexpr int kRowsPerPass = kThreads / 16;
+constexpr int kPasses = kTile / kRowsPerPass;
+constexpr int kXcds = 8;
+constexpr uint64_t kXcdGroup = 4;
+constexpr uint64_t kMaxGrid = uint64_t(1) << 22;
+
+__device__ __forceinline__ uint64_t xcd_grouped(uint64_t b, uint64_t N, uint64_t G) {
+  const uint64_t round = uint64_t(kXcds) * G;
+  const uint64_t full = (N / round) * round;
+  if (b >= full) return b;
+  const uint64_t x = b % kXcds, l = b / kXcds;
+  return (l / G) * round + x * G + (l % G);
+}
+
+__device__ int64_t find_item(const uint64_t* __restrict__ prefix, int64_t n, uint64_t t, int lane) {
+  int64_t lo = 0, hi = n;
+  while (hi - lo > 1) {
+    const int64_t step = (hi - lo + kWaveLanes - 1) / kWaveLanes;
+    const int64_t p = lo + (int64_t(lane) + 1) * step;
+    const bool pred = lane < kWaveLanes - 1 && p < hi && prefix[p] <= t;
+    lo += int64_t(__popcll(__ballot(pred))) * step;
+    hi = min(hi, lo + step);
+  }
+  return lo;
+}
+
+// bf16 bits of a binary32 value: nearest, ties to even; NaN -> 0x7FC0.
+__device__ __forceinline__ uint32_t bf16_bits(float v) {
+  const uint32_t u = __float_as_uint(v);
+  const uint32_t r = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+  return (u & 0x7FFFFFFFu) > 0x7F800000u ? 0x7FC0u : r;
+}
+
+// Four codes (one 32-bit word) -> four bf16 (two 32-bit words).
+__device__ __forceinline__ u32x2 dequant4(uint32_t w, float s) {
+  const f32x2 a = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, false);
+  const f32x2 b = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, true);
+  return u32x2{bf16_bits(a.x * s) | (bf16_bits(a.y * s) << 16),
+               bf16_bits(b.x * s) | (bf16_bits(b.y * s) << 16)};
+}
+
+__global__ __launch_bounds__(kThreads) void k_dequant_full(const uint8_t* __restrict__ codes,
+                                                          const float* __restrict__ scales,
+                                                          uint16_t* __restrict__ dst,
+                                                          const tc_dequant_item* __restrict__ items,
+                                                          const uint64_t* __restrict__ prefix,
+                                                          const int64_t n_items, const uint64_t t0,
+                                                          const uint64_t count) {
+  const int lane = threadIdx.x & (kWaveLanes - 1);
+  const int seg = threadIdx.x & 15;  // 8 codes per lane, 16 lanes per 128-byte row
+  const int prow = threadIdx.x >> 4;
+  const uint64_t t = t0 + xcd_grouped(blockIdx.x, count, kXcdGroup);
+  const int64_t it = find_item(prefix, n_items, t, lane);
+  const tc_dequant_item item = items[it];
+  const int64_t full_c = item.cols / kTile;
+  const int64_t local = int64_t(t - prefix[it]);
+  const int64_t ti = local / full_c, tj = local - ti * full_c;
+  const uint8_t* qs = codes + item.src_off + ti * kTile * item.src_ld + tj * kTile;
+  uint16_t* ys = dst + item.dst_off + ti * kTile * item.dst_ld + tj * kTile;
+  const float s = scales[item.scale_off + ti * item.scale_ld + tj];
+  u32x2 v[kPasses];
+#pragma unroll
+  for (int p = 0; p < kPasses; ++p)
+    v[p] = __builtin_nontemporal_load(
+        reinterpret_cast<const u32x2*>(qs + int64_t(p * kRowsPerPass + prow) * item.src_ld + seg * 8));
+#pragma unroll
+  for (int p = 0; p < kPasses; ++p) {
+    const u32x2 lo = dequant4(v[p].x, s), hi = dequant4(v[p].y, s);
+    __builtin_nontemporal_store(
+        u32x4{lo.x, lo.y, hi.x, hi.y},
+        reinterpret_cast<u32x4*>(ys + int64_t(p * kRowsPerPass + prow) * item.dst_ld + seg * 8));
+  }
+}
+
+// Partial tiles and unaligned items, element by element; numbered within an
+// item like the cast's edge tiles.
+__global__ __launch_bounds__(kThreads) void k_dequant_edge(const uint8_t* __restrict__ codes,
+                                                          const float* __restrict__ scales,
+                                                          uint16_t* __restrict__ dst,
+                                                          const tc_dequant_item* __restrict__ items,
+                                                          const uint64_t* __restrict__ prefix,
+                                                          const uint8_t* __restrict__ aligned,
+                                                          const int64_t n_items, const uint64_t t0,
+                                                          const uint64_t count) {
+  const int lane = threadIdx.x & (kWaveLanes - 1);
+  const uint64_t t = t0 + blockIdx.x;
+  const int64_t it = find_item(prefix, n_items, t, lane);
+  const tc_dequant_item item = items[it];
+  const int64_t tr = (item.rows + kTile - 1) / kTile, tcn = (item.cols + kTile - 1) / kTile;
+  const int64_t fr = aligned[it] ? item.rows / kTile : 0;
+  const int64_t fc = aligned[it] ? item.cols / kTile : 0;
+  const int64_t e = int64_t(t - prefix[it]);
+  int64_t ti, tj;
+  if (e < (tr - fr) * tcn) {
+    ti = fr + e / tcn;
+    tj = e % tcn;
+  } else {
+    const int64_t e2 = e - (tr - fr) * tcn;
+    ti = e2 / (tcn - fc);
+    tj = fc + e2 % (tcn - fc);
+  }
+  const int64_t r0 = ti * kTile, c0 = tj * kTile;
+  const int64_t h = min<int64_t>(kTile, item.rows - r0);
+  const int64_t wd = min<int64_t>(kTile, item.cols - c0);
+  const uint8_t* qs = codes + item.src_off + r0 * item.src_ld + c0;
+  uint16_t* ys = dst + item.dst_off + r0 * item.dst_ld + c0;
+  const float s = scales[item.scale_off + ti * item.scale_ld + tj];
+  for (int64_t k = threadIdx.x; k < h * wd; k += kThreads) {
+    const int64_t rr = k / wd, cc = k - rr * wd;
+    const f32x2 v = __builtin_amdgcn_cvt_pk_f32_fp8((int)qs[rr * item.src_ld + cc], false);
+    ys[rr * item.dst_ld + cc] = (uint16_t)bf16_bits(v.x * s);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_dequant_blockscaled(const uint8_t* codes, const float* scales, uint16_t* dst,
+                                      const void* ws, int64_t n_items, uint64_t full_tiles,
+                                      uint64_t edge_tiles, hipStream_t s) {
+  const CastLayout L = cast_layout(n_items);
+  const uint8_t* base = static_cast<const uint8_t*>(ws);
+  const tc_dequant_item* items = reinterpret_cast<const tc_dequant_item*>(base + L.items);
+  const uint64_t* fp = reinterpret_cast<const uint64_t*>(base + L.full_prefix);
+  const uint64_t* ep = reinterpret_cast<const uint64_t*>(base + L.edge_prefix);
+  const uint8_t* al = base + L.aligned;
+  for (uint64_t t0 = 0; t0 < full_tiles; t0 += kMaxGrid) {
+    const uint64_t cnt = full_tiles - t0 < kMaxGrid ? full_tiles - t0 : kMaxGrid;
+    hipLaunchKernelGGL(k_dequant_full, dim3((unsigned)cnt), dim3(kThreads), 0, s, codes, scales, dst,
+                       items, fp, n_items, t0, cnt);
+  }
+  for (uint64_t t0 = 0; t0 < edge_tiles; t0 += kMaxGrid) {
+    const uint64_t cnt = edge_tiles - t0 < kMaxGrid ? edge_tiles - t0 : kMaxGrid;
+    hipLaunchKernelGGL(k_dequant_edge, dim3((unsigned)cnt), dim3(kThreads), 0, s, codes, scales, dst,
+                       items, ep, al, n_items, t0, cnt);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace tc

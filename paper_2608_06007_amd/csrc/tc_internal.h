@@ -85,5 +85,10 @@ hipError_t launch_cast_blockscaled(const uint16_t* src, uint8_t* dst, float* sca
                                    uint64_t edge_tiles, hipStream_t s);
 hipError_t launch_cast_scaled(const uint16_t* src, int64_t n, float scale, uint8_t* dst,
                               hipStream_t s);
+// The inverse cast uses the same workspace layout (its items are the same
+// size as cast items).
+hipError_t launch_dequant_blockscaled(const uint8_t* codes, const float* scales, uint16_t* dst,
+                                      const void* ws, int64_t n_items, uint64_t full_tiles,
+                                      uint64_t edge_tiles, hipStream_t s);
 
 }  // namespace tc

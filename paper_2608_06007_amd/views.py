@@ -11,8 +11,8 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import (CAST_ITEM_DTYPE, SPLIT_COLS, SPLIT_NONE, SPLIT_ROWS, TP_VIEW_DTYPE,
-               tc_tp_cast_item)
+from . import (CAST_ITEM_DTYPE, DEQUANT_ITEM_DTYPE, SPLIT_COLS, SPLIT_NONE, SPLIT_ROWS,
+               TP_VIEW_DTYPE, tc_tp_cast_item)
 
 _SPLIT = {"rows": SPLIT_ROWS, "cols": SPLIT_COLS, "none": SPLIT_NONE}
 
@@ -92,3 +92,18 @@ def reshard_views(spec, src_tp: int, dst_tp: int, elem_bytes: int = 2):
         src = [r * sbytes + soffs[k] for r in range(src_tp)]
         out.append((src, rows, cols, elem_bytes, _SPLIT[split], doffs[k]))
     return out
+
+
+def dequant_items(spec, tp: int):
+    """DEQUANT_ITEM_DTYPE records that turn one rank's packed fp8 shard (codes
+    and scale grids laid out as cast_items writes them) back into its packed
+    bf16 shard."""
+    items = np.zeros(len(spec), dtype=DEQUANT_ITEM_DTYPE)
+    q_off = s_off = 0
+    for k, (_name, rows, cols, split) in enumerate(spec):
+        sr, sc = slice_shape(rows, cols, split, tp)
+        tcn = (sc + 127) // 128
+        items[k] = (q_off, sr, sc, sc, q_off, sc, s_off, tcn)
+        q_off += sr * sc
+        s_off += ((sr + 127) // 128) * tcn
+    return items

@@ -253,3 +253,98 @@ def test_tp_shard_cast_70b_full_size():
         assert got_s.view(np.uint32) == want_s.view(np.uint32)[0, 0]
     del stream, q, s
     torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------------------
+# inverse cast
+# ---------------------------------------------------------------------------
+
+def _dequant_matrices(codes_1d: np.ndarray, scales_1d: np.ndarray, mats, dst_pad=0):
+    """mats: (code_off, rows, cols, code_ld, scale_off, scale_ld); bf16 outputs
+    packed with row stride cols + dst_pad.  Compared with the oracle."""
+    items = np.zeros(len(mats), dtype=tc.DEQUANT_ITEM_DTYPE)
+    y_off = 0
+    for k, (qo, rows, cols, ld, so, sld) in enumerate(mats):
+        items[k] = (qo, rows, cols, ld, y_off, cols + dst_pad, so, sld)
+        y_off += rows * (cols + dst_pad)
+    q = torch.from_numpy(codes_1d).to(DEV)
+    s = torch.from_numpy(scales_1d.astype(np.float32)).to(DEV)
+    y = torch.full((max(y_off, 1),), -1, dtype=torch.int16, device=DEV)
+    ws = torch.empty(tc.tc_dequant_fp8_workspace(len(mats)), dtype=torch.uint8, device=DEV)
+    tc.tc_dequant_fp8_blockscaled(q, s, y, items, ws)
+    torch.cuda.synchronize()
+    hy = _host(y).view(np.uint16)
+    for k, (qo, rows, cols, ld, so, sld) in enumerate(mats):
+        it = items[k]
+        qv = np.lib.stride_tricks.as_strided(codes_1d[qo:], shape=(rows, cols), strides=(ld, 1))
+        tr, tcn = (rows + 127) // 128, (cols + 127) // 128
+        sv = np.lib.stride_tricks.as_strided(scales_1d.astype(np.float32)[so:], shape=(tr, tcn),
+                                             strides=(4 * sld, 4))
+        want = oracle.dequant_fp8_blockscaled(qv, np.ascontiguousarray(sv))
+        got = np.lib.stride_tricks.as_strided(hy[int(it["dst_off"]):], shape=(rows, cols),
+                                              strides=(2 * int(it["dst_ld"]), 2))
+        if not np.array_equal(got, want):
+            bad = np.argwhere(got != want)
+            r, c = bad[0]
+            raise AssertionError(f"matrix {k}: {len(bad)} differ, first {(r, c)}: q={hex(int(qv[r, c]))} "
+                                 f"gpu={hex(int(got[r, c]))} oracle={hex(int(want[r, c]))}")
+
+
+def test_dequant_every_code_many_scales():
+    rng = np.random.default_rng(70)
+    sbits = np.concatenate([rng.integers(0x00800000, 0x7F000000, size=40, dtype=np.int64),
+                            rng.integers(1, 0x00800000, size=6, dtype=np.int64),
+                            [0, 0x80000000, 0x3F800000, 0x7F7FFFFF, 0x7F800000, 0x7FC00000]]).astype(np.uint32)
+    scales = sbits.view(np.float32)
+    codes = np.tile(np.arange(256, dtype=np.uint8), 128 * 2).reshape(-1)        # [128][512]
+    mats = [(0, 128, 512, 512, 4 * k, 4) for k in range(len(scales))]          # one scale per tile row
+    sgrid = np.repeat(scales, 4)
+    _dequant_matrices(codes, sgrid, mats)
+
+
+def test_dequant_ragged_strided_unaligned():
+    rng = np.random.default_rng(71)
+    codes = rng.integers(0, 256, size=700 * 600, dtype=np.int64).astype(np.uint8)
+    scales = (rng.uniform(0.5, 2, size=64) * 10.0 ** rng.integers(-20, 20, size=64)).astype(np.float32)
+    scales[5] = 0.0
+    scales[9] = np.nan
+    mats = [(0, 256, 384, 384, 0, 3),        # whole tiles
+            (0, 300, 200, 600, 10, 2),       # ragged, strided
+            (8, 128, 128, 600, 20, 1),       # aligned strided tile
+            (3, 130, 129, 600, 30, 2),       # unaligned codes
+            (1000, 1, 1, 1, 40, 1),
+            (2000, 5, 300, 301, 50, 3)]
+    _dequant_matrices(codes, scales, mats)
+    _dequant_matrices(codes, scales, mats, dst_pad=3)   # unaligned bf16 rows
+
+
+def test_cast_then_dequant_70b_layers():
+    """Two 70B-shaped layers: cast rank 5 of TP=8 to fp8, dequantize the
+    shard back to bf16, and compare both results with the oracle."""
+    spec = synth.spec_70b(2)
+    n = synth.spec_elems(spec)
+    stream = synth.bf16_normal(n, 0.02, synth.SEED_CAST_70B, device=DEV)
+    tp, rank = 8, 5
+    items = tcv.cast_items(spec, tp, rank)
+    q = torch.empty(tcv.shard_elems(spec, tp), dtype=torch.uint8, device=DEV)
+    s = torch.empty(tcv.scale_elems(spec, tp), dtype=torch.float32, device=DEV)
+    ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device=DEV)
+    tc.tc_cast_fp8_blockscaled(stream, q, s, items, ws)
+    y = torch.empty(tcv.shard_elems(spec, tp), dtype=torch.bfloat16, device=DEV)
+    ditems = tcv.dequant_items(spec, tp)
+    dws = torch.empty(tc.tc_dequant_fp8_workspace(len(ditems)), dtype=torch.uint8, device=DEV)
+    tc.tc_dequant_fp8_blockscaled(q, s, y, ditems, dws)
+    torch.cuda.synchronize()
+    hq, hs, hy = _host(q), _host(s), _host(y.view(torch.int16)).view(np.uint16)
+    host = _host(stream.view(torch.int16)).view(np.uint16)
+    off = 0
+    for it, dit, (_, rows, cols, split) in zip(items, ditems, spec):
+        w = host[off:off + rows * cols].reshape(rows, cols)
+        off += rows * cols
+        want_q, want_s = oracle.cast_fp8_blockscaled(oracle.tp_slice(w, split, tp, rank))
+        r, c = want_q.shape
+        assert np.array_equal(hq[it["dst_off"]:it["dst_off"] + r * c].reshape(r, c), want_q)
+        want_y = oracle.dequant_fp8_blockscaled(want_q, want_s)
+        assert np.array_equal(hy[dit["dst_off"]:dit["dst_off"] + r * c].reshape(r, c), want_y)
+    del stream
+    torch.cuda.empty_cache()

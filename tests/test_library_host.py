@@ -81,6 +81,16 @@ def test_argument_errors_need_no_gpu(lib):
     assert lib.tc_cast_fp8_blockscaled(P(16), P(16), P(16), items.ctypes.data, 1, 128, P(4096),
                                        1 << 20, None) == 1
     assert tc.tc_cast_fp8_workspace(10) >= 8 * 11
+    # inverse cast: tile and geometry checks before anything is staged
+    ditems = np.zeros(1, dtype=tc.DEQUANT_ITEM_DTYPE)
+    ditems[0] = (0, 128, 256, 256, 0, 256, 0, 2)
+    assert lib.tc_dequant_fp8_blockscaled(P(16), P(16), P(16), ditems.ctypes.data, 1, 64, P(4096),
+                                          1 << 20, None) == 1
+    ditems[0] = (0, 128, 256, 200, 0, 256, 0, 2)          # code row stride < cols
+    assert lib.tc_dequant_fp8_blockscaled(P(16), P(16), P(16), ditems.ctypes.data, 1, 128, P(4096),
+                                          1 << 20, None) == 1
+    assert lib.tc_dequant_fp8_blockscaled(P(16), P(16), P(16), ditems.ctypes.data, 1, 128, P(4096),
+                                          16, None) == 5
 
 
 def test_validate_flag_roundtrip(lib):
