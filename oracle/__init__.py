@@ -18,6 +18,8 @@ What each function follows:
 * ``cast_fp8_blockscaled`` / ``cast_fp8_scaled`` / ``e4m3_encode`` -- one
   concrete transform_into `spec` rule (Table 2): bf16 -> OCP FP8 E4M3 with
   an fp32 scale per 128x128 tile.
+* ``fragment_digests`` -- a per-fragment integrity digest, for the verify
+  stage of the materialization pipeline (Sec. 5).
 * ``dequant_fp8_blockscaled`` -- its inverse, back to bf16, for resharding
   stored fp8 checkpoints into other layouts (Sec. 2.1, Sec. 7).
 """
@@ -66,6 +68,8 @@ def _load():
     lib.orc_dequant_fp8_blockscaled.argtypes = [c.c_void_p, c.c_int64, c.c_int64, c.c_int64,
                                                 c.c_void_p, c.c_int64, c.c_void_p, c.c_int64]
     lib.orc_dequant_fp8_blockscaled.restype = None
+    lib.orc_fragment_digests.argtypes = [c.c_void_p, c.c_void_p, c.c_int64, c.c_int, c.c_void_p]
+    lib.orc_fragment_digests.restype = None
     lib.orc_bf16_round.argtypes = [c.c_float]
     lib.orc_bf16_round.restype = c.c_uint16
     _lib = lib
@@ -238,3 +242,15 @@ def dequant_fp8_blockscaled(q: np.ndarray, scales: np.ndarray) -> np.ndarray:
         _load().orc_dequant_fp8_blockscaled(_ptr(q), rows, cols, q.strides[0], _ptr(s), s.shape[1],
                                             _ptr(y), cols)
     return y
+
+
+def fragment_digests(buf: np.ndarray, frags: np.ndarray, use_src: bool = True) -> np.ndarray:
+    """[n, 2] uint64: S1 = sum of the fragment's bytes, S2 = sum of (i+1)*b_i,
+    both mod 2^64, over the bytes at src_off (or dst_off) of each fragment."""
+    frags = np.ascontiguousarray(frags, dtype=np.uint64).reshape(-1, 3)
+    col = 0 if use_src else 1
+    if len(frags) and int((frags[:, col] + frags[:, 2]).max()) > buf.size:
+        raise ValueError("oracle digest: fragment out of range")
+    out = np.zeros((len(frags), 2), dtype=np.uint64)
+    _load().orc_fragment_digests(_ptr(buf), _ptr(frags), len(frags), 1 if use_src else 0, _ptr(out))
+    return out

@@ -252,3 +252,22 @@ void orc_dequant_fp8_blockscaled(const uint8_t* q, int64_t rows, int64_t cols, i
     }
   }
 }
+
+/* ------------------------------------------------------------------ */
+/* Fragment digests                                                    */
+/* ------------------------------------------------------------------ */
+
+void orc_fragment_digests(const uint8_t* base, const orc_frag* f, int64_t n, int use_src,
+                          uint64_t* out) {
+#pragma omp parallel for schedule(dynamic, 64)
+  for (int64_t d = 0; d < n; d++) {
+    const uint8_t* p = base + (use_src ? f[d].src_off : f[d].dst_off);
+    uint64_t s1 = 0, s2 = 0;
+    for (uint64_t i = 0; i < f[d].len; i++) {
+      s1 += p[i];
+      s2 += (i + 1) * (uint64_t)p[i];
+    }
+    out[2 * d] = s1;
+    out[2 * d + 1] = s2;
+  }
+}

@@ -90,6 +90,14 @@ void orc_cast_fp8_blockscaled(const uint16_t* x, int64_t rows, int64_t cols,
 void orc_dequant_fp8_blockscaled(const uint8_t* q, int64_t rows, int64_t cols, int64_t q_ld,
                                  const float* scales, int64_t scale_ld, uint16_t* y,
                                  int64_t y_ld);
+/* Integrity digest of each fragment (the materialization pipeline's verify
+ * stage): with b_i the fragment's i-th byte (i from 0),
+ *   S1 = sum_i b_i,   S2 = sum_i (i + 1) * b_i,   both mod 2^64.
+ * Read at src_off (use_src != 0) or dst_off of each descriptor; out[2f],
+ * out[2f + 1] receive S1, S2 of fragment f. */
+void orc_fragment_digests(const uint8_t* base, const orc_frag* f, int64_t n, int use_src,
+                          uint64_t* out);
+
 /* RN_bf16 of a binary32 value (ties to even; NaN -> 0x7FC0). */
 uint16_t orc_bf16_round(float v);
 

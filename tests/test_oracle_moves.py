@@ -158,3 +158,42 @@ def test_zipf_ids_distinct_and_skewed():
     assert ids.min() >= 0 and ids.max() < 32768
     raw = synth.ids_zipf_prefix_reuse(32768, 4096, 1.1, seed=1002, keep_duplicates=True)
     assert len(np.unique(raw)) < 4096                # prefix reuse repeats blocks
+
+
+def _fletcher64_recurrence(data: bytes):
+    """Sequential Fletcher-style sums: A_k = A_(k-1) + b_k, B_k = B_(k-1) + A_k."""
+    a = b = 0
+    for x in data:
+        a = (a + x) % (1 << 64)
+        b = (b + a) % (1 << 64)
+    return a, b
+
+
+def test_digests_hand_values_and_fletcher_relation():
+    buf = np.array([1, 2, 3, 250, 0, 7], dtype=np.uint8)
+    d = oracle.fragment_digests(buf, np.array([[0, 0, 3], [3, 0, 3], [0, 0, 0]], dtype=np.uint64))
+    assert d[0].tolist() == [6, 1 * 1 + 2 * 2 + 3 * 3]
+    assert d[1].tolist() == [257, 250 + 0 + 21]
+    assert d[2].tolist() == [0, 0]
+    # the weighted sum equals (n + 1) * A_n - B_n of the sequential recurrence
+    rng = np.random.default_rng(90)
+    data = rng.integers(0, 256, size=5000, dtype=np.int64).astype(np.uint8)
+    a, b = _fletcher64_recurrence(bytes(data))
+    s = oracle.fragment_digests(data, np.array([[0, 0, data.size]], dtype=np.uint64))[0]
+    assert int(s[0]) == a == int(data.astype(np.uint64).sum())
+    assert int(s[1]) == ((data.size + 1) * a - b) % (1 << 64)
+
+
+def test_digests_detect_swaps_and_use_dst_offsets():
+    rng = np.random.default_rng(91)
+    buf = rng.integers(0, 256, size=4096, dtype=np.int64).astype(np.uint8)
+    f = np.array([[100, 1000, 777]], dtype=np.uint64)
+    d0 = oracle.fragment_digests(buf, f)
+    swapped = buf.copy()
+    i, j = 150, 400
+    assert swapped[i] != swapped[j]
+    swapped[i], swapped[j] = swapped[j], swapped[i]
+    d1 = oracle.fragment_digests(swapped, f)
+    assert d1[0, 0] == d0[0, 0] and d1[0, 1] != d0[0, 1]    # same bytes, different order
+    dd = oracle.fragment_digests(np.roll(buf, 900), f, use_src=False)
+    assert np.array_equal(dd, d0)                             # dst_off 1000 holds src bytes from 100
