@@ -231,9 +231,18 @@ def run_reshard(torch, tc, synth, args, stream):
                           args.warmup, args.cast_steps)
     full = _time_calls(torch, stream, lambda: tc.tc_copy_fragments(stream_t, shard, frags, ws, stream=stream),
                        args.warmup, args.cast_steps)
-    out = {"fragments": int(len(frags_np)), "tasks": int(total), "copy_planned": _stats(planned, nbytes),
-           "plan_and_copy": _stats(full, nbytes)}
-    del stream_t, shard, frags, ws
+    nf = len(frags_np)
+    digests = torch.empty(2 * nf, dtype=torch.int64, device="cuda")
+    with_digest = _time_calls(
+        torch, stream, lambda: tc.tc_copy_planned_digest(stream_t, shard, ws, total, nf, digests, stream=stream),
+        args.warmup, args.cast_steps)
+    digest_only = _time_calls(
+        torch, stream, lambda: tc.tc_digest_planned(stream_t, tc.DIGEST_SRC, ws, total, nf, digests, stream=stream),
+        args.warmup, args.cast_steps)
+    out = {"fragments": int(nf), "tasks": int(total), "copy_planned": _stats(planned, nbytes),
+           "plan_and_copy": _stats(full, nbytes), "copy_planned_digest": _stats(with_digest, nbytes),
+           "digest_only_read": _stats(digest_only, nbytes // 2)}
+    del stream_t, shard, frags, ws, digests
     torch.cuda.empty_cache()
     return out
 

@@ -108,9 +108,9 @@ typedef struct {
  * plan cuts every fragment into tasks of at most `piece` bytes (1 KiB, or the
  * next power of two that keeps the task table inside the workspace) and
  * spreads the tasks over the whole GPU, one task per wave.  Any workspace
- * holding at least n + 1 tasks works (16 bytes each, plus 16 bytes per
- * descriptor of planning scratch); this size keeps 1 KiB pieces for payloads
- * up to ~3 KiB per fragment plus 8 GiB.  Offsets plus lengths must stay
+ * holding at least n + 1 tasks works (32 bytes each: the packed task and its
+ * digest slot, plus 16 bytes per descriptor of planning scratch); this size
+ * keeps 1 KiB pieces for payloads up to ~3 KiB per fragment plus 8 GiB.  Offsets plus lengths must stay
  * below 2^48. */
 size_t tc_copy_fragments_workspace(int64_t n);
 /* Smallest workspace a plan of n descriptors accepts (room for n + 1 tasks;
@@ -138,6 +138,43 @@ tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace
                             hipStream_t stream);
 tc_status tc_copy_planned(const void* src_base, void* dst_base, const void* workspace,
                           size_t workspace_bytes, uint64_t total_tasks, hipStream_t stream);
+
+/* Integrity digests (the "verify integrity" stage of the materialization
+ * pipeline, Sec. 5).  The paper names the stage but no checksum; this
+ * library's digest of a fragment with bytes b_0 .. b_(len-1) is the pair
+ *   S1 = sum_i b_i            (mod 2^64)
+ *   S2 = sum_i (i + 1) * b_i  (mod 2^64)
+ * which changes when any single byte changes and when two differing bytes
+ * swap places (a Fletcher-style position-weighted sum, computable in parallel
+ * over any cut of the fragment).
+ *
+ * tc_copy_planned_digest: tc_copy_planned with the same plan, that also
+ * writes the digest of every planned fragment, taken over the bytes it
+ * copies, into digests[2f], digests[2f + 1] (device uint64_t[2n], 8-byte
+ * aligned; fragments in the order given to tc_plan_fragments).  n must be
+ * the plan's descriptor count.  The copy reads each source byte once and
+ * writes it once; the digests cost 32 bytes of workspace traffic per task
+ * and a short reduction.  The workspace is written (its digest slots), so
+ * two digest calls with one workspace must not overlap in time; the plan
+ * itself is left unchanged.  Asynchronous.
+ *
+ * tc_digest_planned: the digests alone, read from base at the fragments'
+ * source offsets (side TC_DIGEST_SRC: what a publisher records) or at their
+ * destination offsets (TC_DIGEST_DST: what a reader checks after the copy).
+ * Nothing is written outside digests and the workspace's digest slots.
+ *
+ * Errors: TC_ERR_INVALID_ARGUMENT for n < 0, null pointers with work to do, a
+ * misaligned workspace or digest array, and (when validating) a header that
+ * disagrees with n or total_tasks; TC_ERR_WORKSPACE if total_tasks exceeds
+ * the workspace's task capacity for n descriptors. */
+#define TC_DIGEST_SRC 0
+#define TC_DIGEST_DST 1
+tc_status tc_copy_planned_digest(const void* src_base, void* dst_base, void* workspace,
+                                 size_t workspace_bytes, uint64_t total_tasks, int64_t n,
+                                 uint64_t* digests, hipStream_t stream);
+tc_status tc_digest_planned(const void* base, int32_t side, void* workspace,
+                            size_t workspace_bytes, uint64_t total_tasks, int64_t n,
+                            uint64_t* digests, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Tensor-parallel views: view(slice) + tensor_dict() (Table 2; each rank

@@ -13,6 +13,8 @@ Entry points (see include/tensorcast_hip.h for the contracts):
 * ``tc_copy_fragments`` (+ ``tc_plan_fragments`` / ``tc_copy_planned``) --
   batched byte fragments, as in prefetch_many and the materialization
   transfer stage (Table 2, Sec. 5).
+* ``tc_copy_planned_digest`` / ``tc_digest_planned`` -- the same copies with
+  a per-fragment integrity digest (the verify stage of Sec. 5).
 * ``tc_tp_fragments`` / ``tc_tp_cast_item`` -- host builders that describe a
   tensor-parallel rank's view(slice) of each weight (Table 2, Sec. 6.1-6.2).
 * ``tc_cast_fp8_blockscaled`` / ``tc_cast_fp8_scaled`` -- a transform_into
@@ -29,6 +31,7 @@ __all__ = [
     "TcError", "lib_path", "load",
     "tc_gather_blocks", "tc_scatter_blocks",
     "tc_copy_fragments_workspace", "tc_copy_fragments_workspace_min", "tc_copy_fragments", "tc_plan_fragments", "tc_copy_planned",
+    "tc_copy_planned_digest", "tc_digest_planned", "DIGEST_SRC", "DIGEST_DST",
     "tc_tp_fragment_count", "tc_tp_fragments", "tc_tp_cast_item",
     "tc_reshard_fragment_count", "tc_reshard_fragments",
     "tc_cast_fp8_workspace", "tc_cast_fp8_blockscaled", "tc_cast_fp8_scaled",
@@ -43,6 +46,7 @@ lib_path = os.path.join(_HERE, "libtchip.so")
 
 MAX_REGIONS = 256
 SPLIT_NONE, SPLIT_ROWS, SPLIT_COLS = 0, 1, 2
+DIGEST_SRC, DIGEST_DST = 0, 1
 TC_OK = 0
 _STATUS = {0: "TC_OK", 1: "TC_ERR_INVALID_ARGUMENT", 2: "TC_ERR_OUT_OF_RANGE", 3: "TC_ERR_ALIAS",
            4: "TC_ERR_HIP", 5: "TC_ERR_WORKSPACE"}
@@ -104,6 +108,8 @@ def load():
     L.tc_copy_fragments.argtypes = [P, P, P, c.c_int64, P, c.c_size_t, P]
     L.tc_plan_fragments.argtypes = [P, c.c_int64, P, c.c_size_t, c.POINTER(c.c_uint64), P]
     L.tc_copy_planned.argtypes = [P, P, P, c.c_size_t, c.c_uint64, P]
+    L.tc_copy_planned_digest.argtypes = [P, P, P, c.c_size_t, c.c_uint64, c.c_int64, P, P]
+    L.tc_digest_planned.argtypes = [P, c.c_int32, P, c.c_size_t, c.c_uint64, c.c_int64, P, P]
     L.tc_tp_fragment_count.argtypes = [P, c.c_int64, c.c_int32, c.c_int32]
     L.tc_tp_fragment_count.restype = c.c_int64
     L.tc_tp_fragments.argtypes = [P, c.c_int64, c.c_int32, c.c_int32, P, c.c_int64,
@@ -126,7 +132,7 @@ def load():
     L.tc_set_validate.argtypes = [c.c_int]
     L.tc_get_validate.restype = c.c_int
     for name in ("tc_gather_blocks", "tc_scatter_blocks", "tc_copy_fragments", "tc_plan_fragments",
-                 "tc_copy_planned", "tc_tp_fragments", "tc_tp_cast_item", "tc_reshard_fragments",
+                 "tc_copy_planned", "tc_copy_planned_digest", "tc_digest_planned", "tc_tp_fragments", "tc_tp_cast_item", "tc_reshard_fragments",
                  "tc_cast_fp8_blockscaled", "tc_dequant_fp8_blockscaled",
                  "tc_cast_fp8_scaled"):
         getattr(L, name).restype = c.c_int
@@ -241,6 +247,37 @@ def tc_copy_planned(src, dst, workspace, total_tasks: int, stream=None) -> None:
     _ok(load().tc_copy_planned(_dev_ptr(src), _dev_ptr(dst), _dev_ptr(workspace),
                                _nbytes(workspace), int(total_tasks), _stream(stream)),
         "tc_copy_planned")
+
+
+def _digest_out(digests, n: int) -> int:
+    if digests.dtype not in (_torch().uint64, _torch().int64) or digests.numel() < 2 * n:
+        raise ValueError("digests must be a device uint64/int64 tensor of at least 2n words")
+    return _dev_ptr(digests)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def tc_copy_planned_digest(src, dst, workspace, total_tasks: int, n: int, digests,
+                           stream=None) -> None:
+    """tc_copy_planned that also writes digests[f] = (S1, S2) of each of the
+    plan's n fragments (``digests``: device uint64/int64 tensor, 2n words)."""
+    _ok(load().tc_copy_planned_digest(_dev_ptr(src), _dev_ptr(dst), _dev_ptr(workspace),
+                                      _nbytes(workspace), int(total_tasks), int(n),
+                                      _digest_out(digests, n), _stream(stream)),
+        "tc_copy_planned_digest")
+
+
+def tc_digest_planned(base, side: int, workspace, total_tasks: int, n: int, digests,
+                      stream=None) -> None:
+    """Digests of the plan's fragments read from ``base`` at their source
+    (DIGEST_SRC) or destination (DIGEST_DST) offsets."""
+    _ok(load().tc_digest_planned(_dev_ptr(base), int(side), _dev_ptr(workspace),
+                                 _nbytes(workspace), int(total_tasks), int(n),
+                                 _digest_out(digests, n), _stream(stream)),
+        "tc_digest_planned")
 
 
 # ---------------------------------------------------------------------------

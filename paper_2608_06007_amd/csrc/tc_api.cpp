@@ -430,6 +430,70 @@ tc_status tc_copy_planned(const void* src_base, void* dst_base, const void* work
                                      stream));
 }
 
+// Shared by the digest entry points: argument checks, the plan's layout for
+// n fragments, and (when validating) the header's agreement with n and the
+// task count.
+static tc_status digest_common(const void* read_base, void* workspace, size_t workspace_bytes,
+                               uint64_t total_tasks, int64_t n, const uint64_t* digests,
+                               hipStream_t stream, tc::PlanLayout* L) {
+  if (n < 0) return TC_ERR_INVALID_ARGUMENT;
+  if (n == 0) return total_tasks == 0 ? TC_OK : TC_ERR_INVALID_ARGUMENT;
+  if (!digests || !workspace || (uintptr_t)workspace % 256 || (uintptr_t)digests % 8)
+    return TC_ERR_INVALID_ARGUMENT;
+  if (total_tasks && !read_base) return TC_ERR_INVALID_ARGUMENT;
+  *L = tc::plan_layout(n, workspace_bytes);
+  if (total_tasks > L->capacity) return TC_ERR_WORKSPACE;
+  if (validating()) {
+    tc::PlanHeader hdr;
+    hipError_t e = hipMemcpyAsync(&hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(e);
+    if (hdr.total_tasks != total_tasks || hdr.n != uint64_t(n)) return TC_ERR_INVALID_ARGUMENT;
+  }
+  return TC_OK;
+}
+
+tc_status tc_copy_planned_digest(const void* src_base, void* dst_base, void* workspace,
+                                 size_t workspace_bytes, uint64_t total_tasks, int64_t n,
+                                 uint64_t* digests, hipStream_t stream) {
+  if (total_tasks && !dst_base) return TC_ERR_INVALID_ARGUMENT;
+  tc::PlanLayout L;
+  tc_status st =
+      digest_common(src_base, workspace, workspace_bytes, total_tasks, n, digests, stream, &L);
+  if (st != TC_OK || n == 0) return st;
+  if (validating() && total_tasks) {
+    // the planned ranges must not alias, as for tc_copy_planned
+    std::vector<tc::Task> packed;
+    st = fetch(reinterpret_cast<const tc::Task*>(static_cast<const uint8_t*>(workspace) +
+                                                 tc::kTasksOffset),
+               (int64_t)total_tasks, &packed, stream);
+    if (st != TC_OK) return st;
+    std::vector<tc_fragment> tasks(packed.size());
+    for (size_t i = 0; i < packed.size(); ++i) {
+      const tc::Task& t = packed[i];
+      tasks[i] = tc_fragment{t.lo & (tc::kOffsetLimit - 1),
+                             (t.lo >> 48) | ((t.hi & 0xFFFFFFFFu) << 16), t.hi >> 32};
+    }
+    st = check_ranges(src_base, dst_base, tasks);
+    if (st != TC_OK) return st;
+  }
+  return check(tc::launch_copy_digest(static_cast<const uint8_t*>(src_base),
+                                      static_cast<uint8_t*>(dst_base), workspace, L, n,
+                                      total_tasks, 0, digests, stream));
+}
+
+tc_status tc_digest_planned(const void* base, int32_t side, void* workspace,
+                            size_t workspace_bytes, uint64_t total_tasks, int64_t n,
+                            uint64_t* digests, hipStream_t stream) {
+  if (side != TC_DIGEST_SRC && side != TC_DIGEST_DST) return TC_ERR_INVALID_ARGUMENT;
+  tc::PlanLayout L;
+  tc_status st = digest_common(base, workspace, workspace_bytes, total_tasks, n, digests, stream, &L);
+  if (st != TC_OK || n == 0) return st;
+  return check(tc::launch_copy_digest(static_cast<const uint8_t*>(base), nullptr, workspace, L, n,
+                                      total_tasks, side == TC_DIGEST_SRC ? 1 : 2, digests,
+                                      stream));
+}
+
 tc_status tc_copy_fragments(const void* src_base, void* dst_base, const tc_fragment* frags,
                             int64_t n, void* workspace, size_t workspace_bytes,
                             hipStream_t stream) {

@@ -38,12 +38,14 @@ struct PlanHeader {
   uint64_t pad[3];
 };
 
-// Workspace layout: header | tasks[capacity] | ... | tstart[n + 1] | block sums.
-// The task table sits at a fixed offset so a copy needs only the workspace
-// base; the planning scratch lives at the end.
+// Workspace layout: header | tasks[capacity] | digest slots[capacity] | ... |
+// tstart[n + 1] | block sums.  The task table sits at a fixed offset so a copy
+// needs only the workspace base; the planning scratch lives at the end and
+// stays valid with the plan (the digest reduction reads tstart).
 constexpr size_t kTasksOffset = 256;
+constexpr size_t kTaskBytes = 32;  // a task and its 16-byte digest slot
 struct PlanLayout {
-  size_t tstart, blocks, capacity;
+  size_t tstart, blocks, capacity, slots;
 };
 PlanLayout plan_layout(int64_t n, size_t ws_bytes);
 size_t frag_workspace_bytes(int64_t n);
@@ -71,6 +73,13 @@ hipError_t launch_plan_expand(const tc_fragment* frags, int64_t n, uint64_t tota
                               uint64_t piece, void* ws, const PlanLayout& L, hipStream_t s);
 hipError_t launch_copy_tasks(const uint8_t* src, uint8_t* dst, const void* ws,
                              uint64_t total_tasks, hipStream_t s);
+// Copy (mode 0) or only read (1: at the tasks' source offsets, 2: at their
+// destination offsets) with a plan, and write each fragment's digest pair
+// into digests[2n]: zero fill, per-task sums into the digest slots, then a
+// reduction per fragment.  `src` is the buffer read in every mode.
+hipError_t launch_copy_digest(const uint8_t* src, uint8_t* dst, void* ws, const PlanLayout& L,
+                              int64_t n, uint64_t total, int mode, uint64_t* digests,
+                              hipStream_t s);
 
 // --- fp8 cast ----------------------------------------------------------
 // Workspace: items | prefix of full (vector-path) tiles | prefix of the other

@@ -115,7 +115,7 @@ def test_small_workspace_grows_the_task_size(extra_tasks):
     pool = 64 << 20
     frags = synth.fragment_storm(3000, pool, seed=42)
     n = len(frags)
-    ws_bytes = tc.tc_copy_fragments_workspace_min(n) + 16 * (extra_tasks - 1)
+    ws_bytes = tc.tc_copy_fragments_workspace_min(n) + 32 * (extra_tasks - 1)
     src = _rand_bytes(pool, 43)
     dst, fr, ws = _copy_and_check(src, frags, pool, planned=True, ws_bytes=ws_bytes)
     assert ws.total <= n + extra_tasks + 32      # capacity rounds to 256-byte alignment

@@ -72,6 +72,15 @@ def test_argument_errors_need_no_gpu(lib):
     assert lib.tc_cast_fp8_blockscaled(P(16), P(16), P(16), P(16), 1, 64, P(16), 1 << 20, None) == 1
     assert lib.tc_cast_fp8_scaled(P(16), -5, ctypes.c_float(1.0), P(16), None) == 1
     assert tc.tc_copy_fragments_workspace(1000) >= 24 * 1001
+    # digests: negative count, unknown side, misaligned digest array, no
+    # destination with work to do, task count beyond the workspace
+    U64 = ctypes.c_uint64
+    assert lib.tc_copy_planned_digest(P(16), P(16), P(4096), 1 << 20, U64(1), -1, P(16), None) == 1
+    assert lib.tc_digest_planned(P(16), 2, P(4096), 1 << 20, U64(1), 1, P(16), None) == 1
+    assert lib.tc_digest_planned(P(16), 0, P(4096), 1 << 20, U64(1), 1, P(12), None) == 1
+    assert lib.tc_copy_planned_digest(P(16), None, P(4096), 1 << 20, U64(1), 1, P(16), None) == 1
+    assert lib.tc_copy_planned_digest(P(16), P(16), P(4096), 4096, U64(1000), 1, P(16), None) == 5
+    assert lib.tc_copy_planned_digest(None, None, None, 0, U64(0), 0, None, None) == 0
     # cast items are checked on the host before anything is staged
     items = np.zeros(1, dtype=tc.CAST_ITEM_DTYPE)
     items[0] = (0, 128, 256, 100, 0, 256, 0, 2)          # src_ld < cols
