@@ -346,6 +346,69 @@ def run_moe(torch, tc, synth, args, stream):
     return out
 
 
+PEAK_PCIE_GBS = 64.0  # PCIe 5.0 x16, one direction (32 GT/s x 16 lanes, 128b/130b)
+
+
+def run_stage(torch, tc, synth, args, stream):
+    """Host <-> device staging at the KV shape: the 4096 ids' blocks (8 GiB)
+    published from the device pool into host memory and hydrated back, through
+    the stager's pinned ring (pageable host buffer) and directly (pinned host
+    buffer); beside them the runtime's own path (gather + pageable copy, and
+    pageable copy + scatter).  Wall clock around each call plus a device
+    synchronize: these calls involve the host."""
+    s = synth.KV_LLAMA3_8B
+    B, nb, R = s.block_bytes, s.num_blocks, s.num_regions
+    _log(f"[stage] {R * s.region_bytes / 2**30:.0f} GiB pool, {s.transfer_bytes / 2**30:.0f} GiB host buffers")
+    pool = synth.bf16_normal(R * s.region_bytes // 2, 1.0, synth.SEED_KV_8B, device="cuda").view(torch.uint8)
+    regions = [pool[r * s.region_bytes:(r + 1) * s.region_bytes] for r in range(R)]
+    ids = torch.from_numpy(synth.ids_zipf_prefix_reuse(nb, s.n_ids, 1.1, synth.SEED_KV_8B)).cuda()
+    nbytes = s.transfer_bytes
+    host = np.empty(nbytes, np.uint8)
+    host.fill(0)
+    pinned = torch.empty(nbytes, dtype=torch.uint8).pin_memory()
+    stage = torch.empty(128 << 20, dtype=torch.uint8, device="cuda")
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    host_t = torch.from_numpy(host)
+    steps = max(3, min(args.cast_steps, 8))
+
+    def wall(fn):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        ms = []
+        for _ in range(steps):
+            t0 = time.perf_counter()
+            fn()
+            torch.cuda.synchronize()
+            ms.append((time.perf_counter() - t0) * 1e3)
+        st = _stats(ms, nbytes)
+        st["frac_of_pcie"] = round(st["GBps"] / PEAK_PCIE_GBS, 4)
+        del st["frac_of_peak"]
+        return st
+
+    out = {"bytes": nbytes, "pcie_peak_GBps": PEAK_PCIE_GBS}
+    with tc.Stager() as stg:
+        h = stg.handle
+        out["publish_pageable"] = wall(lambda: tc.tc_publish_to_host(h, regions, nb, B, B, ids, host, stage, stream=stream))
+        out["hydrate_pageable"] = wall(lambda: tc.tc_hydrate_from_host(h, regions, nb, B, B, ids, host, stage, stream=stream))
+        out["publish_pinned"] = wall(lambda: tc.tc_publish_to_host(h, regions, nb, B, B, ids, pinned, stage, stream=stream))
+        out["hydrate_pinned"] = wall(lambda: tc.tc_hydrate_from_host(h, regions, nb, B, B, ids, pinned, stage, stream=stream))
+
+    def runtime_publish():
+        tc.tc_gather_blocks(regions, nb, B, B, ids, buf, stream=stream)
+        host_t.copy_(buf)
+
+    def runtime_hydrate():
+        buf.copy_(host_t)
+        tc.tc_scatter_blocks(regions, nb, B, B, ids, buf, stream=stream)
+
+    out["runtime_publish_pageable"] = wall(runtime_publish)
+    out["runtime_hydrate_pageable"] = wall(runtime_hydrate)
+    del pool, regions, pinned, stage, buf, host_t, host
+    torch.cuda.empty_cache()
+    return out
+
+
 def run_calib(torch, tc, synth, args, stream):
     """A plain device copy of known size (torch's copy_, 4 GiB): the
     reference for scaling hardware byte counters, and the measured copy
@@ -362,7 +425,7 @@ def run_calib(torch, tc, synth, args, stream):
 
 
 RUNNERS = {"reshard": run_reshard, "reshard_tp8_tp4": run_reshard44, "cast": run_cast,
-           "storm": run_storm, "moe": run_moe, "calib": run_calib}
+           "storm": run_storm, "moe": run_moe, "stage": run_stage, "calib": run_calib}
 
 
 def main():
@@ -371,7 +434,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cast-steps", type=int, default=20, help="timed launches per extra workload")
-    ap.add_argument("--workloads", default="kv,reshard,reshard_tp8_tp4,cast,storm,moe,calib")
+    ap.add_argument("--workloads", default="kv,reshard,reshard_tp8_tp4,cast,storm,moe,stage,calib")
     ap.add_argument("--skip-cpu", action="store_true", help="skip the CPU oracle baseline")
     args = ap.parse_args()
     if args.gpus != 1:

@@ -333,6 +333,66 @@ tc_status tc_dequant_fp8_blockscaled(const void* codes_base, const float* scale_
                                      int64_t n_items, int32_t tile, void* workspace,
                                      size_t workspace_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Host <-> device staging: the materialization pipeline's pinned streaming
+ * buffers and asynchronous copy streams (Sec. 5; the same mechanism serves
+ * the parallel read streams of weight loading, Sec. 6.2), for bytes that live
+ * in host memory -- a transfer buffer kept in host DRAM, or a host-memory
+ * tier.
+ *
+ * A stager is bound to the device current when it is created.  It owns
+ * `slots` pinned host buffers of `slot_bytes` each (hipHostMalloc), a copy
+ * stream of default priority, and `host_threads` host threads (counting the
+ * caller) that copy between pageable memory and the pinned slots.  Zero
+ * selects the defaults: 32 MiB slots, 4 slots, 4 threads.  Pageable bytes
+ * travel in slot-sized chunks: while the DMA engine moves chunk k over PCIe,
+ * the host threads copy chunk k + 1 and the device scatters or gathers the
+ * chunk before.  With TC_HOST_PINNED the caller's host buffer is itself
+ * pinned (hipHostMalloc) and the DMA reads or writes it directly.
+ *
+ * One call at a time per stager (an internal lock serializes callers).  The
+ * stager allocates no device memory: device staging is the caller's
+ * dev_stage buffer, cut into up to 8 slots of whole ids.
+ *
+ * Ordering: each call starts after the work already enqueued on `stream`;
+ * device results are ordered before later work on `stream`.
+ *   tc_stage_h2d / tc_hydrate_from_host return once the host source may be
+ *     reused (every host copy out of it has finished) -- except with
+ *     TC_HOST_PINNED, where the source must stay unchanged until `stream`
+ *     has passed the call (as for hipMemcpyAsync).
+ *   tc_stage_d2h / tc_publish_to_host return when host_dst holds the bytes.
+ *
+ * tc_hydrate_from_host: host_src holds n * num_regions * block_bytes bytes in
+ *   the layout tc_gather_blocks writes (id-major, then region); the blocks
+ *   are scattered into the pool exactly as tc_scatter_blocks would (ids
+ *   distinct).  tc_publish_to_host is the inverse: the pool's blocks of ids,
+ *   gathered, land in host_dst.
+ *
+ * Errors: TC_ERR_INVALID_ARGUMENT for null pointers with work to do, unknown
+ * flags, a bad pool, a call from another device than the stager's;
+ * TC_ERR_WORKSPACE if one id's blocks (num_regions * block_bytes) exceed a
+ * slot or dev_stage cannot hold one chunk; validation-mode errors as for the
+ * block calls, checked over the whole id list.
+ * ------------------------------------------------------------------------ */
+#define TC_HOST_PINNED 1
+typedef struct tc_stager tc_stager;
+tc_status tc_stager_create(size_t slot_bytes, int32_t slots, int32_t host_threads,
+                           tc_stager** out);
+/* Waits for the stager's copies, then frees everything it owns. */
+tc_status tc_stager_destroy(tc_stager* stager);
+/* host_src (bytes) -> dev_dst (bytes). */
+tc_status tc_stage_h2d(tc_stager* stager, const void* host_src, void* dev_dst, size_t bytes,
+                       int32_t flags, hipStream_t stream);
+/* dev_src (bytes) -> host_dst (bytes); blocks until host_dst is complete. */
+tc_status tc_stage_d2h(tc_stager* stager, const void* dev_src, void* host_dst, size_t bytes,
+                       int32_t flags, hipStream_t stream);
+tc_status tc_hydrate_from_host(tc_stager* stager, const tc_block_pool* pool, const int32_t* ids,
+                               int64_t n, const void* host_src, int32_t flags, void* dev_stage,
+                               size_t dev_stage_bytes, hipStream_t stream);
+tc_status tc_publish_to_host(tc_stager* stager, const tc_block_pool* pool, const int32_t* ids,
+                             int64_t n, void* host_dst, int32_t flags, void* dev_stage,
+                             size_t dev_stage_bytes, hipStream_t stream);
+
 /* ------------------------------------------------------------------------ */
 const char* tc_status_string(tc_status status);
 /* hipError_t of the most recent TC_ERR_HIP on the calling thread. */

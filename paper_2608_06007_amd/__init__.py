@@ -15,6 +15,8 @@ Entry points (see include/tensorcast_hip.h for the contracts):
   transfer stage (Table 2, Sec. 5).
 * ``tc_copy_planned_digest`` / ``tc_digest_planned`` -- the same copies with
   a per-fragment integrity digest (the verify stage of Sec. 5).
+* ``tc_stager_create`` ... ``tc_hydrate_from_host`` / ``tc_publish_to_host`` --
+  pinned-ring staging between host memory and the device (Sec. 5).
 * ``tc_tp_fragments`` / ``tc_tp_cast_item`` -- host builders that describe a
   tensor-parallel rank's view(slice) of each weight (Table 2, Sec. 6.1-6.2).
 * ``tc_cast_fp8_blockscaled`` / ``tc_cast_fp8_scaled`` -- a transform_into
@@ -36,6 +38,8 @@ __all__ = [
     "tc_reshard_fragment_count", "tc_reshard_fragments",
     "tc_cast_fp8_workspace", "tc_cast_fp8_blockscaled", "tc_cast_fp8_scaled",
     "tc_dequant_fp8_workspace", "tc_dequant_fp8_blockscaled", "DEQUANT_ITEM_DTYPE",
+    "tc_stager_create", "tc_stager_destroy", "tc_stage_h2d", "tc_stage_d2h",
+    "tc_hydrate_from_host", "tc_publish_to_host", "Stager", "HOST_PINNED",
     "tc_status_string", "tc_last_hip_error", "tc_set_validate", "tc_get_validate",
     "FRAGMENT_DTYPE", "TP_VIEW_DTYPE", "CAST_ITEM_DTYPE",
     "SPLIT_NONE", "SPLIT_ROWS", "SPLIT_COLS", "MAX_REGIONS",
@@ -47,6 +51,7 @@ lib_path = os.path.join(_HERE, "libtchip.so")
 MAX_REGIONS = 256
 SPLIT_NONE, SPLIT_ROWS, SPLIT_COLS = 0, 1, 2
 DIGEST_SRC, DIGEST_DST = 0, 1
+HOST_PINNED = 1
 TC_OK = 0
 _STATUS = {0: "TC_OK", 1: "TC_ERR_INVALID_ARGUMENT", 2: "TC_ERR_OUT_OF_RANGE", 3: "TC_ERR_ALIAS",
            4: "TC_ERR_HIP", 5: "TC_ERR_WORKSPACE"}
@@ -126,6 +131,14 @@ def load():
     L.tc_dequant_fp8_workspace.argtypes = [c.c_int64]
     L.tc_dequant_fp8_workspace.restype = c.c_size_t
     L.tc_dequant_fp8_blockscaled.argtypes = [P, P, P, P, c.c_int64, c.c_int32, P, c.c_size_t, P]
+    L.tc_stager_create.argtypes = [c.c_size_t, c.c_int32, c.c_int32, c.POINTER(c.c_void_p)]
+    L.tc_stager_destroy.argtypes = [P]
+    L.tc_stage_h2d.argtypes = [P, P, P, c.c_size_t, c.c_int32, P]
+    L.tc_stage_d2h.argtypes = [P, P, P, c.c_size_t, c.c_int32, P]
+    L.tc_hydrate_from_host.argtypes = [P, c.POINTER(_BlockPool), P, c.c_int64, P, c.c_int32, P,
+                                       c.c_size_t, P]
+    L.tc_publish_to_host.argtypes = [P, c.POINTER(_BlockPool), P, c.c_int64, P, c.c_int32, P,
+                                     c.c_size_t, P]
     L.tc_status_string.argtypes = [c.c_int]
     L.tc_status_string.restype = c.c_char_p
     L.tc_last_hip_error.restype = c.c_int
@@ -134,7 +147,8 @@ def load():
     for name in ("tc_gather_blocks", "tc_scatter_blocks", "tc_copy_fragments", "tc_plan_fragments",
                  "tc_copy_planned", "tc_copy_planned_digest", "tc_digest_planned", "tc_tp_fragments", "tc_tp_cast_item", "tc_reshard_fragments",
                  "tc_cast_fp8_blockscaled", "tc_dequant_fp8_blockscaled",
-                 "tc_cast_fp8_scaled"):
+                 "tc_cast_fp8_scaled", "tc_stager_create", "tc_stager_destroy", "tc_stage_h2d",
+                 "tc_stage_d2h", "tc_hydrate_from_host", "tc_publish_to_host"):
         getattr(L, name).restype = c.c_int
     _lib = L
     return L
@@ -278,6 +292,112 @@ def tc_digest_planned(base, side: int, workspace, total_tasks: int, n: int, dige
                                  _nbytes(workspace), int(total_tasks), int(n),
                                  _digest_out(digests, n), _stream(stream)),
         "tc_digest_planned")
+
+
+# ---------------------------------------------------------------------------
+# host <-> device staging
+# ---------------------------------------------------------------------------
+
+def _host(buf):
+    """(address, bytes, pinned) of a host buffer: a numpy array (pageable) or
+    a CPU torch tensor (pinned when it was allocated with pin_memory)."""
+    if isinstance(buf, np.ndarray):
+        if not buf.flags["C_CONTIGUOUS"]:
+            raise ValueError("host buffer must be contiguous")
+        return buf.ctypes.data, buf.nbytes, False
+    if buf.is_cuda:
+        raise ValueError("expected a host buffer")
+    if not buf.is_contiguous():
+        raise ValueError("host buffer must be contiguous")
+    return buf.data_ptr(), _nbytes(buf), bool(buf.is_pinned())
+
+
+def _flags(pinned_detected: bool, pinned) -> int:
+    use = pinned_detected if pinned is None else bool(pinned)
+    return HOST_PINNED if use else 0
+
+
+def tc_stager_create(slot_bytes: int = 0, slots: int = 0, host_threads: int = 0) -> int:
+    """A stager bound to the current device; returns its handle."""
+    h = ctypes.c_void_p(0)
+    _ok(load().tc_stager_create(int(slot_bytes), int(slots), int(host_threads), ctypes.byref(h)),
+        "tc_stager_create")
+    return int(h.value)
+
+
+def tc_stager_destroy(stager: int) -> None:
+    _ok(load().tc_stager_destroy(stager), "tc_stager_destroy")
+
+
+def tc_stage_h2d(stager: int, host_src, dev_dst, nbytes=None, pinned=None, stream=None) -> None:
+    """Copy host bytes to the device through the pinned ring (or directly if pinned)."""
+    a, n, det = _host(host_src)
+    n = n if nbytes is None else int(nbytes)
+    if n > _nbytes(dev_dst):
+        raise ValueError("device buffer too small")
+    _ok(load().tc_stage_h2d(stager, a, _dev_ptr(dev_dst), n, _flags(det, pinned), _stream(stream)),
+        "tc_stage_h2d")
+
+
+def tc_stage_d2h(stager: int, dev_src, host_dst, nbytes=None, pinned=None, stream=None) -> None:
+    """Copy device bytes into host memory; returns when host_dst holds them."""
+    a, n, det = _host(host_dst)
+    n = n if nbytes is None else int(nbytes)
+    if n > _nbytes(dev_src):
+        raise ValueError("device buffer too small")
+    _ok(load().tc_stage_d2h(stager, _dev_ptr(dev_src), a, n, _flags(det, pinned), _stream(stream)),
+        "tc_stage_d2h")
+
+
+def tc_hydrate_from_host(stager: int, regions, num_blocks: int, block_bytes: int, block_stride: int,
+                         ids, host_src, dev_stage, pinned=None, stream=None) -> None:
+    """Scatter a host-resident transfer buffer (layout of tc_gather_blocks)
+    into the device block pool, staged through ``dev_stage``."""
+    pool, keep = _pool(regions, num_blocks, block_bytes, block_stride)
+    n = ids.numel()
+    a, hb, det = _host(host_src)
+    if n and hb < n * len(keep) * block_bytes:
+        raise ValueError("host buffer too small")
+    _ok(load().tc_hydrate_from_host(stager, ctypes.byref(pool), _dev_ptr(ids) if n else None, n, a,
+                                    _flags(det, pinned), _dev_ptr(dev_stage), _nbytes(dev_stage),
+                                    _stream(stream)), "tc_hydrate_from_host")
+
+
+def tc_publish_to_host(stager: int, regions, num_blocks: int, block_bytes: int, block_stride: int,
+                       ids, host_dst, dev_stage, pinned=None, stream=None) -> None:
+    """Gather the pool's blocks of ``ids`` into host memory (blocks until done)."""
+    pool, keep = _pool(regions, num_blocks, block_bytes, block_stride)
+    n = ids.numel()
+    a, hb, det = _host(host_dst)
+    if n and hb < n * len(keep) * block_bytes:
+        raise ValueError("host buffer too small")
+    _ok(load().tc_publish_to_host(stager, ctypes.byref(pool), _dev_ptr(ids) if n else None, n, a,
+                                  _flags(det, pinned), _dev_ptr(dev_stage), _nbytes(dev_stage),
+                                  _stream(stream)), "tc_publish_to_host")
+
+
+class Stager:
+    """Owns a stager handle (``with Stager() as st: ...``)."""
+
+    def __init__(self, slot_bytes: int = 0, slots: int = 0, host_threads: int = 0):
+        self.handle = tc_stager_create(slot_bytes, slots, host_threads)
+
+    def close(self) -> None:
+        if self.handle:
+            tc_stager_destroy(self.handle)
+            self.handle = 0
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 # ---------------------------------------------------------------------------

@@ -289,6 +289,10 @@ void reshard_fragments(const tc_reshard_view& v, int32_t dst_tp, int32_t d, Emit
 }  // namespace
 
 namespace tc {
+tc_status hip_status(hipError_t e) { return check(e); }
+}  // namespace tc
+
+namespace tc {
 hipError_t device_info(DeviceInfo* out) {
   static int cus[64] = {0};
   int dev = 0;

@@ -51,6 +51,10 @@ PlanLayout plan_layout(int64_t n, size_t ws_bytes);
 size_t frag_workspace_bytes(int64_t n);
 size_t frag_workspace_min_bytes(int64_t n);
 
+// TC_OK for hipSuccess; otherwise records the error for tc_last_hip_error()
+// and returns TC_ERR_HIP.
+tc_status hip_status(hipError_t e);
+
 // Launch geometry of the current device.
 struct DeviceInfo {
   int device;

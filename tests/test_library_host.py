@@ -81,6 +81,15 @@ def test_argument_errors_need_no_gpu(lib):
     assert lib.tc_copy_planned_digest(P(16), None, P(4096), 1 << 20, U64(1), 1, P(16), None) == 1
     assert lib.tc_copy_planned_digest(P(16), P(16), P(4096), 4096, U64(1000), 1, P(16), None) == 5
     assert lib.tc_copy_planned_digest(None, None, None, 0, U64(0), 0, None, None) == 0
+    # staging: bad ring shapes and flags are refused before any HIP call
+    h = ctypes.c_void_p(0)
+    assert lib.tc_stager_create(0, 1, 0, ctypes.byref(h)) == 1        # one slot cannot overlap
+    assert lib.tc_stager_create(100, 2, 0, ctypes.byref(h)) == 1      # slot below 4 KiB
+    assert lib.tc_stager_create(0, -1, 0, ctypes.byref(h)) == 1
+    assert lib.tc_stager_create(0, 0, 0, None) == 1
+    assert lib.tc_stager_destroy(None) == 0
+    assert lib.tc_stage_h2d(None, P(16), P(16), 10, 0, None) == 1
+    assert lib.tc_stage_d2h(None, P(16), P(16), 10, 0, None) == 1
     # cast items are checked on the host before anything is staged
     items = np.zeros(1, dtype=tc.CAST_ITEM_DTYPE)
     items[0] = (0, 128, 256, 100, 0, 256, 0, 2)          # src_ld < cols
