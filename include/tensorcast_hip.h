@@ -132,7 +132,8 @@ tc_status tc_copy_fragments(const void* src_base, void* dst_base, const tc_fragm
  * returns its task count in *total_tasks (host); it synchronizes the stream
  * once.  tc_copy_planned then copies with that plan -- asynchronously, as
  * often as wanted -- for any src/dst bases, while the workspace is kept
- * unchanged.  total_tasks == 0 means there is nothing to copy. */
+ * unchanged.  total_tasks == 0 means there is nothing to copy; a count
+ * larger than the workspace's task table can hold is TC_ERR_WORKSPACE. */
 tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace,
                             size_t workspace_bytes, uint64_t* total_tasks /* host, out */,
                             hipStream_t stream);

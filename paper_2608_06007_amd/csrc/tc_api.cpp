@@ -386,7 +386,7 @@ tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
     if (e != hipSuccess) return hip_fail(e);
     if (hdr.total_tasks <= L.capacity) break;
-    // Too many 4 KiB pieces for the workspace: larger pieces bound the count
+    // Too many 1 KiB pieces for the workspace: larger pieces bound the count
     // by n + payload / piece <= capacity.
     const uint64_t room = L.capacity - uint64_t(n);
     piece = pow2_at_least(std::max<uint64_t>(tc::kMinPiece, (hdr.payload + room - 1) / room));
@@ -405,6 +405,11 @@ tc_status tc_copy_planned(const void* src_base, void* dst_base, const void* work
   if (total_tasks == 0) return TC_OK;
   if (!src_base || !dst_base || !workspace || (uintptr_t)workspace % 256)
     return TC_ERR_INVALID_ARGUMENT;
+  // Whatever the plan's fragment count, its task table lies inside the
+  // workspace: a larger count cannot come from a plan made in it.
+  if (workspace_bytes < tc::kTasksOffset ||
+      total_tasks > (workspace_bytes - tc::kTasksOffset) / tc::kTaskBytes)
+    return TC_ERR_WORKSPACE;
   // The plan's own fragment count sizes its layout.
   tc::PlanHeader hdr;
   hipError_t e = hipSuccess;

@@ -68,6 +68,9 @@ def test_argument_errors_need_no_gpu(lib):
     assert lib.tc_copy_fragments(P(16), P(16), P(16), 10, P(4100), 1 << 20, None) == 1  # misaligned
     assert lib.tc_copy_fragments(P(16), P(16), P(16), -1, P(16), 1 << 20, None) == 1
     assert lib.tc_copy_fragments(None, None, None, 0, None, 0, None) == 0
+    # a task count the workspace's table cannot hold is refused before any launch
+    assert lib.tc_copy_planned(P(16), P(16), P(4096), 256 + 32 * 10, ctypes.c_uint64(11), None) == 5
+    assert lib.tc_copy_planned(P(16), P(16), P(4096), 100, ctypes.c_uint64(1), None) == 5
     # cast: tile other than 128
     assert lib.tc_cast_fp8_blockscaled(P(16), P(16), P(16), P(16), 1, 64, P(16), 1 << 20, None) == 1
     assert lib.tc_cast_fp8_scaled(P(16), -5, ctypes.c_float(1.0), P(16), None) == 1
