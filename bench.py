@@ -196,7 +196,24 @@ def cpu_baseline_kv(torch, synth, s, regions_dev, ids_np, n_sample=512, min_seco
         if el >= min_seconds:
             break
     gbs = per_rep * reps / el / 1e9
-    return {"value": round(gbs, 2), "unit": "GB/s", "cores": oracle.threads(), "kind": "oracle",
+    # the same oracle on one thread, over a quarter of the time
+    cores = oracle.threads()
+    oracle.set_threads(1)
+    try:
+        reps1 = 0
+        t1 = time.perf_counter()
+        while True:
+            buf = oracle.gather_blocks(host_a, B, B, pos)
+            oracle.scatter_blocks(host_b, B, B, pos, buf)
+            reps1 += 1
+            el1 = time.perf_counter() - t1
+            if el1 >= min_seconds / 4:
+                break
+    finally:
+        oracle.set_threads(cores)
+    gbs1 = per_rep * reps1 / el1 / 1e9
+    return {"value": round(gbs, 2), "unit": "GB/s", "cores": cores, "kind": "oracle",
+            "value_1_thread": round(gbs1, 2),
             "sample": (f"gather+scatter of the first {n_sample} of the 4096 ids x {R} regions x "
                        f"{B} B ({per_rep / 1e9:.2f} GB algorithmic per repetition) between host pools of "
                        f"{nbh} blocks per region; {reps} repetitions in {el:.1f} s"),
@@ -418,8 +435,16 @@ def run_calib(torch, tc, synth, args, stream):
     src = synth.random_bytes(n, 41, device="cuda")
     dst = torch.empty_like(src)
     ms = _time_calls(torch, stream, lambda: dst.copy_(src), args.warmup, args.cast_steps)
-    out = {"bytes_each_way": n, "torch_copy": _stats(ms, 2 * n)}
-    del src, dst
+    # this library's own streaming copy of the same bytes (one 4 GiB fragment,
+    # planned into 1 KiB tasks): the copy ceiling the workloads are set against
+    _log("[calib] planned copy of one 4 GiB fragment")
+    frags = torch.tensor([[0, 0, n]], dtype=torch.int64, device="cuda")
+    ws = torch.empty(tc.tc_copy_fragments_workspace(1), dtype=torch.uint8, device="cuda")
+    total = tc.tc_plan_fragments(frags, ws, stream=stream)
+    own = _time_calls(torch, stream, lambda: tc.tc_copy_planned(src, dst, ws, total, stream=stream),
+                      args.warmup, args.cast_steps)
+    out = {"bytes_each_way": n, "torch_copy": _stats(ms, 2 * n), "library_copy": _stats(own, 2 * n)}
+    del src, dst, ws, frags
     torch.cuda.empty_cache()
     return out
 
@@ -480,6 +505,10 @@ def main():
         if "cpu" in kv:
             result["cpu_baseline"] = kv["cpu"]
     result["workloads"] = extra
+    if "roofline" in result and "calib" in extra:
+        ceiling = extra["calib"]["library_copy"]["GBps"]
+        result["roofline"]["copy_ceiling_GBps"] = ceiling
+        result["roofline"]["frac_of_copy_ceiling"] = round(result["roofline"]["achieved"] / ceiling, 4)
     result["kernel_source_sha256"] = src_hash
     print(json.dumps(result), flush=True)
 
