@@ -31,6 +31,13 @@
  *   also copy the descriptors to the host, synchronize the stream, and
  *   report ids out of range (TC_ERR_OUT_OF_RANGE) and aliasing writes
  *   (TC_ERR_ALIAS) before launching; without it those are preconditions.
+ * - HIP graph capture: with validation off, tc_gather_blocks,
+ *   tc_scatter_blocks, tc_copy_planned, tc_copy_planned_digest,
+ *   tc_digest_planned and tc_cast_fp8_scaled only launch kernels on `stream`
+ *   (no memset, no host synchronization), so they may be captured and the
+ *   graph replayed.  tc_plan_fragments / tc_copy_fragments (they read the
+ *   task count back), the block-scaled cast and inverse cast (they stage their
+ *   host item table at call time) and the staging calls must not be captured.
  */
 #ifndef TENSORCAST_HIP_H
 #define TENSORCAST_HIP_H

@@ -1,0 +1,122 @@
+"""GPU: stream ordering and HIP-graph capture of the entry points.
+
+Each call runs on a side stream right behind a device fill that produces its
+input on that same stream, so a call that ignored its stream argument would
+read stale bytes.  The calls that do no host-side staging or synchronization
+(block gather/scatter, planned copies with and without digests, the scaled
+cast) are also captured into a HIP graph and replayed several times, with the
+input changed eagerly between replays; every replay is checked against the
+oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+import paper_2608_06007_amd as tc
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _pool(R, nb, B):
+    flat = torch.zeros(R * nb * B, dtype=torch.uint8, device=DEV)
+    return flat, [flat[r * nb * B:(r + 1) * nb * B] for r in range(R)]
+
+
+def test_side_stream_ordering():
+    R, nb, B = 8, 512, 16384
+    ids_np = synth.ids_without_replacement(nb, 300, seed=61)
+    ids = torch.from_numpy(ids_np).to(DEV)
+    src_flat, src = _pool(R, nb, B)
+    dst_flat, dst = _pool(R, nb, B)
+    buf = torch.empty(300 * R * B, dtype=torch.uint8, device=DEV)
+    frags_np = synth.fragment_storm(3000, 32 << 20, seed=62)
+    frags = torch.from_numpy(frags_np.view(np.int64)).to(DEV)
+    fsrc = torch.empty(32 << 20, dtype=torch.uint8, device=DEV)
+    fdst = torch.zeros(32 << 20, dtype=torch.uint8, device=DEV)
+    ws = torch.empty(tc.tc_copy_fragments_workspace(len(frags_np)), dtype=torch.uint8, device=DEV)
+    dg = torch.empty(2 * len(frags_np), dtype=torch.int64, device=DEV)
+    total = tc.tc_plan_fragments(frags, ws)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        # inputs produced on the side stream, consumed there without a sync
+        src_flat.copy_(synth.random_bytes(src_flat.numel(), 63, device=DEV))
+        tc.tc_gather_blocks(src, nb, B, B, ids, buf, stream=side)
+        tc.tc_scatter_blocks(dst, nb, B, B, ids, buf, stream=side)
+        fsrc.copy_(synth.random_bytes(fsrc.numel(), 64, device=DEV))
+        tc.tc_copy_planned_digest(fsrc, fdst, ws, total, len(frags_np), dg, stream=side)
+    side.synchronize()
+    hs = [r.cpu().numpy() for r in src]
+    want = oracle.gather_blocks(hs, B, B, ids_np)
+    assert np.array_equal(buf.cpu().numpy(), want.reshape(-1))
+    hd = [np.zeros(nb * B, np.uint8) for _ in range(R)]
+    oracle.scatter_blocks(hd, B, B, ids_np, want.reshape(-1))
+    assert np.array_equal(dst_flat.cpu().numpy(), np.concatenate(hd))
+    hf = fsrc.cpu().numpy()
+    wf = np.zeros(32 << 20, np.uint8)
+    oracle.copy_fragments(hf, wf, frags_np)
+    assert np.array_equal(fdst.cpu().numpy(), wf)
+    assert np.array_equal(dg.cpu().numpy().view(np.uint64).reshape(-1, 2),
+                          oracle.fragment_digests(hf, frags_np))
+
+
+def test_graph_capture_and_replay():
+    R, nb, B = 4, 256, 8192
+    ids_np = synth.ids_without_replacement(nb, 100, seed=65)
+    ids = torch.from_numpy(ids_np).to(DEV)
+    src_flat, src = _pool(R, nb, B)
+    dst_flat, dst = _pool(R, nb, B)
+    buf = torch.empty(100 * R * B, dtype=torch.uint8, device=DEV)
+    frags_np = synth.fragment_storm(1000, 16 << 20, seed=66)
+    frags = torch.from_numpy(frags_np.view(np.int64)).to(DEV)
+    fsrc = torch.empty(16 << 20, dtype=torch.uint8, device=DEV)
+    fdst = torch.zeros(16 << 20, dtype=torch.uint8, device=DEV)
+    ws = torch.empty(tc.tc_copy_fragments_workspace(len(frags_np)), dtype=torch.uint8, device=DEV)
+    dg = torch.empty(2 * len(frags_np), dtype=torch.int64, device=DEV)
+    x = torch.empty(65536 + 77, dtype=torch.bfloat16, device=DEV)
+    q = torch.empty(x.numel(), dtype=torch.uint8, device=DEV)
+    total = tc.tc_plan_fragments(frags, ws)
+    n = len(frags_np)
+    torch.cuda.synchronize()
+
+    g = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(g, stream=cap):
+            s = torch.cuda.current_stream()
+            tc.tc_gather_blocks(src, nb, B, B, ids, buf, stream=s)
+            tc.tc_scatter_blocks(dst, nb, B, B, ids, buf, stream=s)
+            tc.tc_copy_planned_digest(fsrc, fdst, ws, total, n, dg, stream=s)
+            tc.tc_copy_planned(fsrc, fdst, ws, total, stream=s)
+            tc.tc_cast_fp8_scaled(x, 0.25, q, stream=s)
+    torch.cuda.synchronize()
+
+    for rep in range(4):
+        # new inputs, written eagerly between replays
+        src_flat.copy_(synth.random_bytes(src_flat.numel(), 70 + rep, device=DEV))
+        fsrc.copy_(synth.random_bytes(fsrc.numel(), 80 + rep, device=DEV))
+        x.copy_(synth.bf16_normal(x.numel(), 1.0, 90 + rep, device=DEV))
+        dst_flat.zero_()
+        fdst.zero_()
+        dg.fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        hs = [r.cpu().numpy() for r in src]
+        want = oracle.gather_blocks(hs, B, B, ids_np)
+        assert np.array_equal(buf.cpu().numpy(), want.reshape(-1)), rep
+        hd = [np.zeros(nb * B, np.uint8) for _ in range(R)]
+        oracle.scatter_blocks(hd, B, B, ids_np, want.reshape(-1))
+        assert np.array_equal(dst_flat.cpu().numpy(), np.concatenate(hd)), rep
+        hf = fsrc.cpu().numpy()
+        wf = np.zeros(16 << 20, np.uint8)
+        oracle.copy_fragments(hf, wf, frags_np)
+        assert np.array_equal(fdst.cpu().numpy(), wf), rep
+        assert np.array_equal(dg.cpu().numpy().view(np.uint64).reshape(-1, 2),
+                              oracle.fragment_digests(hf, frags_np)), rep
+        xb = x.view(torch.int16).cpu().numpy().view(np.uint16)
+        assert np.array_equal(q.cpu().numpy(), oracle.cast_fp8_scaled(xb, 0.25)), rep
