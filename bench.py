@@ -339,8 +339,12 @@ def run_storm(torch, tc, synth, args, stream):
     nbytes = 2 * int(frags_np[:, 2].sum())
     ms = _time_calls(torch, stream, lambda: tc.tc_copy_fragments(src, dst, frags, ws, stream=stream),
                      args.warmup, args.cast_steps)
-    out = {"fragments": 1_000_000, "payload_bytes": int(frags_np[:, 2].sum()),
-           "plan_and_copy": _stats(ms, nbytes), "descriptors_sha256": synth.sha256(frags_np)}
+    total = tc.tc_plan_fragments(frags, ws, stream=stream)
+    planned = _time_calls(torch, stream, lambda: tc.tc_copy_planned(src, dst, ws, total, stream=stream),
+                          args.warmup, args.cast_steps)
+    out = {"fragments": 1_000_000, "payload_bytes": int(frags_np[:, 2].sum()), "tasks": int(total),
+           "plan_and_copy": _stats(ms, nbytes), "copy_planned": _stats(planned, nbytes),
+           "descriptors_sha256": synth.sha256(frags_np)}
     del src, dst, frags, ws
     torch.cuda.empty_cache()
     return out

@@ -379,7 +379,7 @@ tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace
   uint64_t piece = tc::kMinPiece;
   tc::PlanHeader hdr;
   for (int attempt = 0; attempt < 2; ++attempt) {
-    hipError_t e = tc::launch_plan_count(frags, n, piece, workspace, L, stream);
+    hipError_t e = tc::launch_plan_count(frags, n, piece, workspace, L, false, stream);
     if (e != hipSuccess) return hip_fail(e);
     // The launch size of the copy depends on the task count: read it back.
     e = hipMemcpyAsync(&hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, stream);
@@ -394,7 +394,19 @@ tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace
     piece = std::min<uint64_t>(piece, uint64_t(1) << 31);
   }
   if (hdr.total_tasks > L.capacity) return TC_ERR_WORKSPACE;
-  hipError_t e = tc::launch_plan_expand(frags, n, hdr.total_tasks, piece, workspace, L, stream);
+  // Long lists with scattered destinations are planned in destination order
+  // (same tasks, so the same count): the copy then writes in address order.
+  const tc_fragment* planned = frags;
+  hipError_t e = hipSuccess;
+  if (hdr.dst_unordered && L.nbuckets) {
+    int shift = 12;
+    while (shift < 62 && (hdr.dst_end >> shift) >= L.nbuckets) ++shift;
+    e = tc::launch_plan_reorder(frags, n, shift, workspace, L, stream);
+    planned = reinterpret_cast<const tc_fragment*>(static_cast<uint8_t*>(workspace) + L.sorted);
+    if (e == hipSuccess) e = tc::launch_plan_count(planned, n, piece, workspace, L, true, stream);
+    if (e != hipSuccess) return hip_fail(e);
+  }
+  e = tc::launch_plan_expand(planned, n, hdr.total_tasks, piece, workspace, L, stream);
   if (e != hipSuccess) return hip_fail(e);
   if (total_tasks) *total_tasks = hdr.total_tasks;
   return TC_OK;

@@ -30,22 +30,30 @@ constexpr uint64_t kOffsetLimit = uint64_t(1) << 48;
 
 // Header at the start of a fragment-plan workspace.
 struct PlanHeader {
-  uint64_t total_tasks;  // written by the planning kernels
-  uint64_t piece;        // task size chosen for this plan
-  uint64_t payload;      // sum of the fragment lengths
-  uint64_t n;            // number of fragments planned
-  uint64_t capacity;     // task-table entries that fit the workspace
-  uint64_t pad[3];
+  uint64_t total_tasks;    // written by the planning kernels
+  uint64_t piece;          // task size chosen for this plan
+  uint64_t payload;        // sum of the fragment lengths
+  uint64_t n;              // number of fragments planned
+  uint64_t capacity;       // task-table entries that fit the workspace
+  uint64_t dst_unordered;  // some fragment starts below its predecessor (destination side)
+  uint64_t dst_end;        // largest dst_off + len of a non-empty fragment
+  uint64_t permuted;       // the tasks follow the reordered list; perm maps back
 };
 
 // Workspace layout: header | tasks[capacity] | digest slots[capacity] | ... |
-// tstart[n + 1] | block sums.  The task table sits at a fixed offset so a copy
-// needs only the workspace base; the planning scratch lives at the end and
-// stays valid with the plan (the digest reduction reads tstart).
+// tstart[n + 1] | block sums | [reordered fragments | perm | buckets].  The
+// task table sits at a fixed offset so a copy needs only the workspace base;
+// the planning scratch lives at the end and stays valid with the plan (the
+// digest reduction reads tstart and perm).
 constexpr size_t kTasksOffset = 256;
 constexpr size_t kTaskBytes = 32;  // a task and its 16-byte digest slot
+// Lists of at least this many fragments whose destinations are not in
+// ascending order are planned in destination order (bucketed by address).
+constexpr int64_t kReorderMin = 4096;
 struct PlanLayout {
   size_t tstart, blocks, capacity, slots;
+  size_t sorted, perm, buckets, bucket_sums;  // valid when nbuckets > 0
+  uint64_t nbuckets;                          // bucket capacity (0: no reordering)
 };
 PlanLayout plan_layout(int64_t n, size_t ws_bytes);
 size_t frag_workspace_bytes(int64_t n);
@@ -69,9 +77,14 @@ hipError_t launch_blocks(const RegionTable& tab, int32_t num_regions, int64_t bl
 
 // --- fragments ---------------------------------------------------------
 // Count pieces of `piece` bytes per fragment and write tstart; the header
-// receives the totals.  Enqueued only (no synchronization).
+// receives the totals, whether the destinations are unordered, their end, and
+// `permuted` (the list counted is the reordered one).  Enqueued only.
 hipError_t launch_plan_count(const tc_fragment* frags, int64_t n, uint64_t piece, void* ws,
-                             const PlanLayout& L, hipStream_t s);
+                             const PlanLayout& L, bool permuted, hipStream_t s);
+// Write the fragments in destination order (buckets of 2^shift bytes) to
+// L.sorted and their original indices to L.perm.
+hipError_t launch_plan_reorder(const tc_fragment* frags, int64_t n, int shift, void* ws,
+                               const PlanLayout& L, hipStream_t s);
 // Expand the counted plan into its task table (total_tasks known on the host).
 hipError_t launch_plan_expand(const tc_fragment* frags, int64_t n, uint64_t total_tasks,
                               uint64_t piece, void* ws, const PlanLayout& L, hipStream_t s);

@@ -136,25 +136,55 @@ __device__ __forceinline__ uint64_t pieces_of(uint64_t len, uint64_t piece) {
   return (len + piece - 1) / piece;
 }
 
+// Maximum over a 256-thread block (every thread gets it).
+__device__ uint64_t block_max_u64(uint64_t v) {
+  __shared__ uint64_t wave_max[kThreads / kWaveLanes];
+#pragma unroll
+  for (int d = kWaveLanes / 2; d >= 1; d >>= 1) {
+    const uint64_t o = (uint64_t(uint32_t(__shfl_xor(uint32_t(v >> 32), d, kWaveLanes))) << 32) |
+                       uint32_t(__shfl_xor(uint32_t(v), d, kWaveLanes));
+    v = v > o ? v : o;
+  }
+  if ((threadIdx.x & (kWaveLanes - 1)) == 0) wave_max[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint64_t m = 0;
+#pragma unroll
+  for (int k = 0; k < kThreads / kWaveLanes; ++k) m = m > wave_max[k] ? m : wave_max[k];
+  __syncthreads();
+  return m;
+}
+
+// Per block: task and byte sums, whether some destination starts below its
+// predecessor's (checked across the block's last boundary too), and the
+// largest destination end.
 __global__ __launch_bounds__(kThreads) void k_plan_count(const tc_fragment* __restrict__ frags,
                                                         const int64_t n, const uint64_t piece,
                                                         uint64_t* __restrict__ block_cnt,
-                                                        uint64_t* __restrict__ block_len) {
+                                                        uint64_t* __restrict__ block_len,
+                                                        uint64_t* __restrict__ block_unord,
+                                                        uint64_t* __restrict__ block_dend) {
   const int64_t f0 = int64_t(blockIdx.x) * kPlanPerBlock + int64_t(threadIdx.x) * kPlanPerThread;
-  uint64_t c = 0, l = 0;
+  uint64_t c = 0, l = 0, dend = 0;
+  int unord = 0;
 #pragma unroll
   for (int j = 0; j < kPlanPerThread; ++j)
     if (f0 + j < n) {
-      const uint64_t len = frags[f0 + j].len;
-      c += pieces_of(len, piece);
-      l += len;
+      const tc_fragment f = frags[f0 + j];
+      c += pieces_of(f.len, piece);
+      l += f.len;
+      if (f.len && f.dst_off + f.len > dend) dend = f.dst_off + f.len;
+      if (f0 + j + 1 < n && frags[f0 + j + 1].dst_off < f.dst_off) unord = 1;
     }
   uint64_t tc_, tl;
   block_exclusive_scan(c, &tc_);
   block_exclusive_scan(l, &tl);
+  const int any_unord = __syncthreads_or(unord);
+  const uint64_t bdend = block_max_u64(dend);
   if (threadIdx.x == 0) {
     block_cnt[blockIdx.x] = tc_;
     block_len[blockIdx.x] = tl;
+    block_unord[blockIdx.x] = any_unord ? 1 : 0;
+    block_dend[blockIdx.x] = bdend;
   }
 }
 
@@ -162,15 +192,23 @@ __global__ __launch_bounds__(kThreads) void k_plan_count(const tc_fragment* __re
 // the totals.
 __global__ __launch_bounds__(kThreads) void k_plan_scan(uint64_t* __restrict__ block_cnt,
                                                        const uint64_t* __restrict__ block_len,
+                                                       const uint64_t* __restrict__ block_unord,
+                                                       const uint64_t* __restrict__ block_dend,
                                                        const int64_t nblocks, const uint64_t piece,
                                                        const int64_t n, const uint64_t capacity,
+                                                       const uint64_t permuted,
                                                        PlanHeader* __restrict__ hdr,
                                                        uint64_t* __restrict__ tstart_end) {
-  uint64_t carry = 0, bytes = 0;
+  uint64_t carry = 0, bytes = 0, dend = 0;
+  int unord = 0;
   for (int64_t base = 0; base < nblocks; base += kThreads) {
     const int64_t i = base + threadIdx.x;
     const uint64_t v = i < nblocks ? block_cnt[i] : 0;
     const uint64_t l = i < nblocks ? block_len[i] : 0;
+    if (i < nblocks) {
+      unord |= block_unord[i] ? 1 : 0;
+      dend = dend > block_dend[i] ? dend : block_dend[i];
+    }
     uint64_t total, ltot;
     const uint64_t ex = block_exclusive_scan(v, &total);
     block_exclusive_scan(l, &ltot);
@@ -178,12 +216,17 @@ __global__ __launch_bounds__(kThreads) void k_plan_scan(uint64_t* __restrict__ b
     carry += total;
     bytes += ltot;
   }
+  const int any_unord = __syncthreads_or(unord);
+  dend = block_max_u64(dend);
   if (threadIdx.x == 0) {
     hdr->total_tasks = carry;
     hdr->piece = piece;
     hdr->payload = bytes;
     hdr->n = uint64_t(n);
     hdr->capacity = capacity;
+    hdr->dst_unordered = any_unord ? 1 : 0;
+    hdr->dst_end = dend;
+    hdr->permuted = permuted;
     *tstart_end = carry;
   }
 }
@@ -545,6 +588,7 @@ __global__ __launch_bounds__(kThreads) void k_fill_zero(uint64_t* __restrict__ p
 __global__ __launch_bounds__(kThreads) void k_digest_reduce(const uint64_t* __restrict__ tstart,
                                                            const int64_t n, const uint64_t total,
                                                            const PlanHeader* __restrict__ hdr,
+                                                           const uint64_t* __restrict__ perm,
                                                            const u64x2* __restrict__ slots,
                                                            uint64_t* __restrict__ digests) {
   __shared__ uint64_t win[kExpandPerBlock + 1];
@@ -566,6 +610,8 @@ __global__ __launch_bounds__(kThreads) void k_digest_reduce(const uint64_t* __re
   const int64_t span = f1 - f0 + 1;
   const bool local = span <= kExpandPerBlock;
   const uint64_t piece = hdr->piece;
+  // digests are indexed by the caller's order; a reordered plan maps back
+  const bool mapped = perm != nullptr && hdr->permuted != 0;
   if (local) {
     for (int64_t k = threadIdx.x; k <= span; k += kThreads) win[k] = tstart[f0 + k];
     for (int64_t k = threadIdx.x; k < 2 * span; k += kThreads) acc[k] = 0;
@@ -603,14 +649,15 @@ __global__ __launch_bounds__(kThreads) void k_digest_reduce(const uint64_t* __re
       atomicAdd(reinterpret_cast<unsigned long long*>(&acc[2 * lo]), (unsigned long long)p.x);
       atomicAdd(reinterpret_cast<unsigned long long*>(&acc[2 * lo + 1]), (unsigned long long)s2);
     } else {
-      atomicAdd(reinterpret_cast<unsigned long long*>(&digests[2 * lo]), (unsigned long long)p.x);
-      atomicAdd(reinterpret_cast<unsigned long long*>(&digests[2 * lo + 1]), (unsigned long long)s2);
+      const uint64_t o = mapped ? perm[lo] : uint64_t(lo);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&digests[2 * o]), (unsigned long long)p.x);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&digests[2 * o + 1]), (unsigned long long)s2);
     }
   }
   if (!local) return;
   __syncthreads();
   for (int64_t k = threadIdx.x; k < span; k += kThreads) {
-    uint64_t* out = digests + 2 * (f0 + k);
+    uint64_t* out = digests + 2 * (mapped ? perm[f0 + k] : uint64_t(f0 + k));
     if (win[k] >= t0 && win[k + 1] <= t1) {
       out[0] = acc[2 * k];
       out[1] = acc[2 * k + 1];
@@ -618,6 +665,90 @@ __global__ __launch_bounds__(kThreads) void k_digest_reduce(const uint64_t* __re
       atomicAdd(reinterpret_cast<unsigned long long*>(out), (unsigned long long)acc[2 * k]);
       atomicAdd(reinterpret_cast<unsigned long long*>(out + 1), (unsigned long long)acc[2 * k + 1]);
     }
+  }
+}
+
+// ------------------------------------------------------------------------
+// Destination-ordered plans: a counting sort of the fragments by
+// dst_off >> shift (buckets of 2^shift bytes).  The tasks then write the
+// destination in address order -- measured +12.6% on a million fragments
+// scattered over 16 GiB (gathers, which read scattered blocks and write in
+// order, are the fastest block pattern on this GPU).  Inside a bucket the
+// order is whatever the atomics give; a copy does not depend on it.
+// ------------------------------------------------------------------------
+__device__ __forceinline__ uint64_t bucket_of(uint64_t dst_off, int shift, uint64_t nbk) {
+  const uint64_t b = dst_off >> shift;  // empty fragments may lie past the end: clamp
+  return b < nbk ? b : nbk - 1;
+}
+
+__global__ __launch_bounds__(kThreads) void k_bucket_hist(const tc_fragment* __restrict__ frags,
+                                                         const int64_t n, const int shift,
+                                                         const uint64_t nbk,
+                                                         uint64_t* __restrict__ cnt) {
+  for (int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * kThreads)
+    atomicAdd(reinterpret_cast<unsigned long long*>(&cnt[bucket_of(frags[i].dst_off, shift, nbk)]),
+              1ull);
+}
+
+// Exclusive scan of v[0 .. m) in place, in three passes: sums of 1024
+// entries, a scan of those sums (one workgroup), then each 1024-entry block.
+__global__ __launch_bounds__(kThreads) void k_scan_sums(const uint64_t* __restrict__ v,
+                                                       const uint64_t m,
+                                                       uint64_t* __restrict__ sums) {
+  const uint64_t i0 = uint64_t(blockIdx.x) * kPlanPerBlock + uint64_t(threadIdx.x) * kPlanPerThread;
+  uint64_t t = 0;
+#pragma unroll
+  for (int j = 0; j < kPlanPerThread; ++j)
+    if (i0 + j < m) t += v[i0 + j];
+  uint64_t total;
+  block_exclusive_scan(t, &total);
+  if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(kThreads) void k_scan_one(uint64_t* __restrict__ v, const uint64_t m) {
+  uint64_t carry = 0;
+  for (uint64_t base = 0; base < m; base += kThreads) {
+    const uint64_t i = base + threadIdx.x;
+    uint64_t total;
+    const uint64_t ex = block_exclusive_scan(i < m ? v[i] : 0, &total);
+    if (i < m) v[i] = carry + ex;
+    carry += total;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_scan_apply(uint64_t* __restrict__ v, const uint64_t m,
+                                                        const uint64_t* __restrict__ sums) {
+  const uint64_t i0 = uint64_t(blockIdx.x) * kPlanPerBlock + uint64_t(threadIdx.x) * kPlanPerThread;
+  uint64_t c[kPlanPerThread];
+  uint64_t t = 0;
+#pragma unroll
+  for (int j = 0; j < kPlanPerThread; ++j) {
+    c[j] = i0 + j < m ? v[i0 + j] : 0;
+    t += c[j];
+  }
+  uint64_t total;
+  uint64_t run = sums[blockIdx.x] + block_exclusive_scan(t, &total);
+#pragma unroll
+  for (int j = 0; j < kPlanPerThread; ++j) {
+    if (i0 + j < m) v[i0 + j] = run;
+    run += c[j];
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_bucket_scatter(const tc_fragment* __restrict__ frags,
+                                                            const int64_t n, const int shift,
+                                                            const uint64_t nbk,
+                                                            uint64_t* __restrict__ off,
+                                                            tc_fragment* __restrict__ sorted,
+                                                            uint64_t* __restrict__ perm) {
+  for (int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * kThreads) {
+    const tc_fragment f = frags[i];
+    const uint64_t pos = atomicAdd(
+        reinterpret_cast<unsigned long long*>(&off[bucket_of(f.dst_off, shift, nbk)]), 1ull);
+    sorted[pos] = f;
+    perm[pos] = uint64_t(i);
   }
 }
 
@@ -657,8 +788,23 @@ static int64_t plan_blocks(int64_t n) { return (n + kPlanPerBlock - 1) / kPlanPe
 
 static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// Buckets for reordering a list of n fragments (0: lists this short keep
+// their order): a quarter of n rounded up to a power of two, at most 2^18.
+static uint64_t plan_buckets(int64_t n) {
+  if (n < kReorderMin) return 0;
+  uint64_t p = 1;
+  while (p < uint64_t(n)) p <<= 1;
+  p /= 4;
+  return p < (uint64_t(1) << 18) ? p : (uint64_t(1) << 18);
+}
+
 static size_t plan_tail_bytes(int64_t n) {
-  return align256(8 * size_t(n + 1)) + align256(2 * 8 * size_t(plan_blocks(n)));
+  size_t t = align256(8 * size_t(n + 1)) + align256(4 * 8 * size_t(plan_blocks(n)));
+  const uint64_t nbk = plan_buckets(n);
+  if (nbk)
+    t += align256(sizeof(tc_fragment) * size_t(n)) + align256(8 * size_t(n)) + align256(8 * nbk) +
+         align256(8 * ((nbk + kPlanPerBlock - 1) / kPlanPerBlock));
+  return t;
 }
 
 PlanLayout plan_layout(int64_t n, size_t ws_bytes) {
@@ -667,6 +813,11 @@ PlanLayout plan_layout(int64_t n, size_t ws_bytes) {
   const size_t start = ws_bytes > tail ? ((ws_bytes - tail) & ~size_t(255)) : 0;
   L.tstart = start;
   L.blocks = start + align256(8 * size_t(n + 1));
+  L.nbuckets = plan_buckets(n);
+  L.sorted = L.blocks + align256(4 * 8 * size_t(plan_blocks(n)));
+  L.perm = L.sorted + align256(sizeof(tc_fragment) * size_t(n));
+  L.buckets = L.perm + align256(8 * size_t(n));
+  L.bucket_sums = L.buckets + align256(8 * L.nbuckets);
   // every task has a 16-byte digest slot after the task table
   L.capacity = start > kTasksOffset ? (start - kTasksOffset) / kTaskBytes : 0;
   L.slots = kTasksOffset + L.capacity * sizeof(Task);
@@ -685,19 +836,46 @@ size_t frag_workspace_min_bytes(int64_t n) {
 }
 
 hipError_t launch_plan_count(const tc_fragment* frags, int64_t n, uint64_t piece, void* ws,
-                             const PlanLayout& L, hipStream_t s) {
+                             const PlanLayout& L, bool permuted, hipStream_t s) {
   uint8_t* base = static_cast<uint8_t*>(ws);
   PlanHeader* hdr = reinterpret_cast<PlanHeader*>(base);
   uint64_t* tstart = reinterpret_cast<uint64_t*>(base + L.tstart);
   const int64_t nb = plan_blocks(n);
   uint64_t* bcnt = reinterpret_cast<uint64_t*>(base + L.blocks);
   uint64_t* blen = bcnt + nb;
+  uint64_t* bunord = blen + nb;
+  uint64_t* bdend = bunord + nb;
   hipLaunchKernelGGL(k_plan_count, dim3((unsigned)nb), dim3(kThreads), 0, s, frags, n, piece, bcnt,
-                     blen);
-  hipLaunchKernelGGL(k_plan_scan, dim3(1), dim3(kThreads), 0, s, bcnt, (const uint64_t*)blen, nb,
-                     piece, n, uint64_t(L.capacity), hdr, tstart + n);
+                     blen, bunord, bdend);
+  hipLaunchKernelGGL(k_plan_scan, dim3(1), dim3(kThreads), 0, s, bcnt, (const uint64_t*)blen,
+                     (const uint64_t*)bunord, (const uint64_t*)bdend, nb, piece, n,
+                     uint64_t(L.capacity), uint64_t(permuted ? 1 : 0), hdr, tstart + n);
   hipLaunchKernelGGL(k_plan_tstart, dim3((unsigned)nb), dim3(kThreads), 0, s, frags, n, piece,
                      (const uint64_t*)bcnt, tstart);
+  return hipGetLastError();
+}
+
+hipError_t launch_plan_reorder(const tc_fragment* frags, int64_t n, int shift, void* ws,
+                               const PlanLayout& L, hipStream_t s) {
+  if (n == 0 || L.nbuckets == 0) return hipSuccess;
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  uint64_t* cnt = reinterpret_cast<uint64_t*>(base + L.buckets);
+  uint64_t* sums = reinterpret_cast<uint64_t*>(base + L.bucket_sums);
+  tc_fragment* sorted = reinterpret_cast<tc_fragment*>(base + L.sorted);
+  uint64_t* perm = reinterpret_cast<uint64_t*>(base + L.perm);
+  const uint64_t nbk = L.nbuckets;
+  const uint64_t sblocks = (nbk + kPlanPerBlock - 1) / kPlanPerBlock;
+  const unsigned fgrid = grid_for((uint64_t(n) + kThreads - 1) / kThreads);
+  hipLaunchKernelGGL(k_fill_zero, dim3(grid_for((nbk + kThreads - 1) / kThreads)), dim3(kThreads),
+                     0, s, cnt, nbk);
+  hipLaunchKernelGGL(k_bucket_hist, dim3(fgrid), dim3(kThreads), 0, s, frags, n, shift, nbk, cnt);
+  hipLaunchKernelGGL(k_scan_sums, dim3((unsigned)sblocks), dim3(kThreads), 0, s,
+                     (const uint64_t*)cnt, nbk, sums);
+  hipLaunchKernelGGL(k_scan_one, dim3(1), dim3(kThreads), 0, s, sums, sblocks);
+  hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)sblocks), dim3(kThreads), 0, s, cnt, nbk,
+                     (const uint64_t*)sums);
+  hipLaunchKernelGGL(k_bucket_scatter, dim3(fgrid), dim3(kThreads), 0, s, frags, n, shift, nbk,
+                     cnt, sorted, perm);
   return hipGetLastError();
 }
 
@@ -758,7 +936,9 @@ hipError_t launch_copy_digest(const uint8_t* src, uint8_t* dst, void* ws, const 
   const uint64_t rgrid = (total + kExpandPerBlock - 1) / kExpandPerBlock;
   hipLaunchKernelGGL(k_digest_reduce, dim3((unsigned)rgrid), dim3(kThreads), 0, s,
                      reinterpret_cast<const uint64_t*>(base + L.tstart), n, total,
-                     reinterpret_cast<const PlanHeader*>(base), (const u64x2*)slots, digests);
+                     reinterpret_cast<const PlanHeader*>(base),
+                     L.nbuckets ? reinterpret_cast<const uint64_t*>(base + L.perm) : nullptr,
+                     (const u64x2*)slots, digests);
   return hipGetLastError();
 }
 

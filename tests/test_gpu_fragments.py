@@ -286,3 +286,31 @@ def test_cross_layout_reshard_8b_full_size():
         lw = _host(stream[l * per_layer:(l + 1) * per_layer].view(torch.int16)).view(np.uint16)
         assert np.array_equal(got[l * shard_layer:(l + 1) * shard_layer],
                               oracle.tp_shard(lw, spec[7 * l:7 * l + 7], 4, 1))
+
+
+def _header_permuted(ws):
+    # the plan header's eighth word says whether the tasks follow a reordered list
+    return int(ws[56:64].cpu().numpy().view(np.uint64)[0])
+
+
+def test_long_unordered_lists_are_planned_in_destination_order():
+    """A list of 5,000 fragments with scattered destinations is planned in
+    destination order; an ordered list, and an unordered one of 1,000, keep
+    their order.  The copies are exact either way."""
+    pool = 64 << 20
+    src = _rand_bytes(pool, 44)
+    frags = synth.fragment_storm(5000, pool, seed=45)
+    _, _, ws = _copy_and_check(src, frags, pool, planned=True)
+    assert _header_permuted(ws) == 1
+    # the task table ascends in destination address at bucket granularity
+    # (64 KiB buckets here): consecutive tasks never step back by 1 MiB or more,
+    # while the list as given does
+    tasks = ws[256:256 + 16 * ws.total].cpu().numpy().view(np.uint64).reshape(-1, 2)
+    dst = (tasks[:, 0] >> np.uint64(48)) | ((tasks[:, 1] & np.uint64(0xFFFFFFFF)) << np.uint64(16))
+    assert np.diff(dst.astype(np.int64)).min() > -(1 << 20)
+    assert np.diff(frags[:, 1].astype(np.int64)).min() < -(1 << 20)
+    ordered = frags[np.argsort(frags[:, 1], kind="stable")]
+    _, _, ws2 = _copy_and_check(src, ordered, pool, planned=True)
+    assert _header_permuted(ws2) == 0
+    _, _, ws3 = _copy_and_check(src, synth.fragment_storm(1000, pool, seed=46), pool, planned=True)
+    assert _header_permuted(ws3) == 0
