@@ -394,6 +394,11 @@ class Stager:
         self.close()
 
     def __del__(self):
+        # at interpreter shutdown the HIP runtime may already be gone: leave
+        # the stager to the process exit then
+        import sys
+        if sys.is_finalizing():
+            return
         try:
             self.close()
         except Exception:
