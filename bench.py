@@ -328,6 +328,32 @@ def run_cast(torch, tc, synth, args, stream):
     return out
 
 
+def run_reshard_cast(torch, tc, synth, args, stream):
+    """Reshard + transform_into in one pass: 70B-shaped weights held as the 8
+    bf16 shards of a TP=8 split (rank-major) cast straight into rank 1 of a
+    TP=4 split as e4m3 + tile scales.  The source values are drawn directly in
+    the shard layout (seeded N(0, 0.02))."""
+    from paper_2608_06007_amd import views as tcv
+    src_tp, dst_tp, rank = 8, 4, 1
+    spec = synth.spec_70b(80)
+    n = synth.spec_elems(spec)
+    _log(f"[reshard_cast] 70B-shaped TP={src_tp} bf16 shards ({n * 2 / 1e9:.1f} GB) -> TP={dst_tp} rank {rank} e4m3")
+    src = synth.bf16_normal(n, 0.02, synth.SEED_CAST_70B, device="cuda")
+    items = tcv.reshard_cast_items(spec, src_tp, dst_tp, rank)
+    shard_n = tcv.shard_elems(spec, dst_tp)
+    n_scales = tcv.scale_elems(spec, dst_tp)
+    q = torch.empty(shard_n, dtype=torch.uint8, device="cuda")
+    sc = torch.empty(n_scales, dtype=torch.float32, device="cuda")
+    ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device="cuda")
+    nbytes = 2 * shard_n + shard_n + 4 * n_scales
+    ms = _time_calls(torch, stream, lambda: tc.tc_cast_fp8_blockscaled(src, q, sc, items, ws, stream=stream),
+                     args.warmup, args.cast_steps)
+    out = {"items": int(len(items)), "tiles": int(n_scales), "reshard_cast": _stats(ms, nbytes)}
+    del src, q, sc, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def run_storm(torch, tc, synth, args, stream):
     pool = 16 << 30
     frags_np = synth.fragment_storm(1_000_000, pool, seed=synth.SEED_STORM)
@@ -454,6 +480,7 @@ def run_calib(torch, tc, synth, args, stream):
 
 
 RUNNERS = {"reshard": run_reshard, "reshard_tp8_tp4": run_reshard44, "cast": run_cast,
+           "reshard_cast": run_reshard_cast,
            "storm": run_storm, "moe": run_moe, "stage": run_stage, "calib": run_calib}
 
 
@@ -465,7 +492,7 @@ def main():
     ap.add_argument("--cast-steps", type=int, default=20, help="timed launches per extra workload")
     # the host staging workload ("stage") runs only when named: it launches the
     # block kernels once per chunk, which would mix into their profiles
-    ap.add_argument("--workloads", default="kv,reshard,reshard_tp8_tp4,cast,storm,moe,calib")
+    ap.add_argument("--workloads", default="kv,reshard,reshard_tp8_tp4,cast,reshard_cast,storm,moe,calib")
     ap.add_argument("--skip-cpu", action="store_true", help="skip the CPU oracle baseline")
     args = ap.parse_args()
     if args.gpus != 1:

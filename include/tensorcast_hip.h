@@ -293,6 +293,28 @@ typedef struct {
 tc_status tc_tp_cast_item(const tc_tp_view* view /* host */, int32_t tp, int32_t rank,
                           uint64_t scale_off, tc_cast_item* out /* host */);
 
+/* Host: cast items (for tc_cast_fp8_blockscaled) that build rank dst_rank's
+ * fp8 slices of a dst_tp-way split straight from bf16 source slices of a
+ * src_tp-way split: the reshard and the transform_into rule in one pass
+ * (rank-specific resharding with view() + transform_into(), Sec. 7).  Views
+ * as for tc_reshard_fragments with elem_bytes 2 and BYTE offsets: src_off[s]
+ * of each bf16 source slice (even), dst_off of the fp8 destination slice
+ * (one byte per element, densely row-major); scale_off[i] (host) is the
+ * float offset of view i's scale grid, ceil(rows_d/128) x ceil(cols_d/128)
+ * row-major for the destination slice's shape rows_d x cols_d.  One item per
+ * overlapping source slice.  The destination's tiles are those of its own
+ * slice, so every boundary between two source slices must lie on a multiple
+ * of 128 from the destination slice's first row (row split) or column (column
+ * split); otherwise, and for elem_bytes != 2 or an odd src_off, the count is
+ * -1 and the builder returns TC_ERR_INVALID_ARGUMENT.  TC_ERR_WORKSPACE if
+ * `capacity` items do not fit. */
+int64_t tc_reshard_cast_item_count(const tc_reshard_view* views /* host */, int64_t n_views,
+                                   int32_t dst_tp, int32_t dst_rank);
+tc_status tc_reshard_cast_items(const tc_reshard_view* views /* host */,
+                                const uint64_t* scale_off /* host [n_views] */, int64_t n_views,
+                                int32_t dst_tp, int32_t dst_rank, tc_cast_item* out /* host */,
+                                int64_t capacity, int64_t* written);
+
 /* Bytes of device workspace tc_cast_fp8_blockscaled needs for n items. */
 size_t tc_cast_fp8_workspace(int64_t n_items);
 

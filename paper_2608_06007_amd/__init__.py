@@ -36,6 +36,7 @@ __all__ = [
     "tc_copy_planned_digest", "tc_digest_planned", "DIGEST_SRC", "DIGEST_DST",
     "tc_tp_fragment_count", "tc_tp_fragments", "tc_tp_cast_item",
     "tc_reshard_fragment_count", "tc_reshard_fragments",
+    "tc_reshard_cast_item_count", "tc_reshard_cast_items",
     "tc_cast_fp8_workspace", "tc_cast_fp8_blockscaled", "tc_cast_fp8_scaled",
     "tc_dequant_fp8_workspace", "tc_dequant_fp8_blockscaled", "DEQUANT_ITEM_DTYPE",
     "tc_stager_create", "tc_stager_destroy", "tc_stage_h2d", "tc_stage_d2h",
@@ -124,6 +125,10 @@ def load():
     L.tc_reshard_fragment_count.restype = c.c_int64
     L.tc_reshard_fragments.argtypes = [P, c.c_int64, c.c_int32, c.c_int32, P, c.c_int64,
                                        c.POINTER(c.c_int64)]
+    L.tc_reshard_cast_item_count.argtypes = [P, c.c_int64, c.c_int32, c.c_int32]
+    L.tc_reshard_cast_item_count.restype = c.c_int64
+    L.tc_reshard_cast_items.argtypes = [P, P, c.c_int64, c.c_int32, c.c_int32, P, c.c_int64,
+                                        c.POINTER(c.c_int64)]
     L.tc_cast_fp8_workspace.argtypes = [c.c_int64]
     L.tc_cast_fp8_workspace.restype = c.c_size_t
     L.tc_cast_fp8_blockscaled.argtypes = [P, P, P, P, c.c_int64, c.c_int32, P, c.c_size_t, P]
@@ -145,7 +150,7 @@ def load():
     L.tc_set_validate.argtypes = [c.c_int]
     L.tc_get_validate.restype = c.c_int
     for name in ("tc_gather_blocks", "tc_scatter_blocks", "tc_copy_fragments", "tc_plan_fragments",
-                 "tc_copy_planned", "tc_copy_planned_digest", "tc_digest_planned", "tc_tp_fragments", "tc_tp_cast_item", "tc_reshard_fragments",
+                 "tc_copy_planned", "tc_copy_planned_digest", "tc_digest_planned", "tc_tp_fragments", "tc_tp_cast_item", "tc_reshard_fragments", "tc_reshard_cast_items",
                  "tc_cast_fp8_blockscaled", "tc_dequant_fp8_blockscaled",
                  "tc_cast_fp8_scaled", "tc_stager_create", "tc_stager_destroy", "tc_stage_h2d",
                  "tc_stage_d2h", "tc_hydrate_from_host", "tc_publish_to_host"):
@@ -474,6 +479,32 @@ def tc_reshard_fragments(views, dst_tp: int, dst_rank: int) -> np.ndarray:
     _ok(load().tc_reshard_fragments(arr if len(views) else None, len(views), dst_tp, dst_rank,
                                     out.ctypes.data if m else None, m, ctypes.byref(written)),
         "tc_reshard_fragments")
+    return out[:written.value]
+
+
+def tc_reshard_cast_item_count(views, dst_tp: int, dst_rank: int) -> int:
+    arr, _keep = _reshard_array(views)
+    n = int(load().tc_reshard_cast_item_count(arr if len(views) else None, len(views), dst_tp, dst_rank))
+    if n < 0:
+        raise TcError(1, "tc_reshard_cast_item_count")
+    return n
+
+
+def tc_reshard_cast_items(views, scale_off, dst_tp: int, dst_rank: int) -> np.ndarray:
+    """CAST_ITEM_DTYPE records that cast rank ``dst_rank``'s slices of a
+    ``dst_tp``-way split straight from the bf16 source slices of ``views``
+    (byte offsets; fp8 destination offsets) into fp8 with per-view scale
+    grids at ``scale_off`` (floats)."""
+    arr, _keep = _reshard_array(views)
+    so = np.ascontiguousarray(scale_off, dtype=np.uint64).reshape(-1)
+    if so.size != len(views):
+        raise ValueError("one scale offset per view")
+    m = tc_reshard_cast_item_count(views, dst_tp, dst_rank)
+    out = np.zeros(m, dtype=CAST_ITEM_DTYPE)
+    written = ctypes.c_int64(0)
+    _ok(load().tc_reshard_cast_items(arr if len(views) else None, so.ctypes.data if so.size else None,
+                                     len(views), dst_tp, dst_rank, out.ctypes.data if m else None, m,
+                                     ctypes.byref(written)), "tc_reshard_cast_items")
     return out[:written.value]
 
 

@@ -286,6 +286,45 @@ void reshard_fragments(const tc_reshard_view& v, int32_t dst_tp, int32_t d, Emit
   }
 }
 
+// Cast items that fill the destination rank's fp8 slice from the
+// overlapping bf16 source slices, one item per source slice; each writes its
+// part of the slice's scale grid.  A boundary between two source slices must
+// fall on a 128-element tile edge of the destination slice (a tile cannot
+// take its amax from two sources); returns false otherwise, and for views
+// that are not bf16.
+template <typename Emit>
+bool reshard_cast_items(const tc_reshard_view& v, uint64_t scale_off, int32_t dst_tp, int32_t d,
+                        Emit emit) {
+  if (v.elem_bytes != 2) return false;
+  const int32_t nsrc = v.split == TC_SPLIT_NONE ? 1 : v.src_tp;
+  for (int32_t s = 0; s < nsrc; ++s)
+    if (v.src_off[s] % 2) return false;
+  if (v.rows == 0 || v.cols == 0) return true;
+  if (v.split == TC_SPLIT_NONE) {
+    emit(tc_cast_item{v.src_off[0] / 2, v.rows, v.cols, v.cols, v.dst_off, v.cols, scale_off,
+                      (v.cols + 127) / 128});
+    return true;
+  }
+  const bool by_rows = v.split == TC_SPLIT_ROWS;
+  const int64_t extent = by_rows ? v.rows : v.cols;
+  const int64_t ns = extent / v.src_tp, nd = extent / dst_tp;
+  const int64_t d0 = int64_t(d) * nd, d1 = d0 + nd;
+  const int64_t dcols = by_rows ? v.cols : nd;  // destination slice width
+  const int64_t sld = (dcols + 127) / 128;
+  for (int64_t s = d0 / ns; s <= (d1 - 1) / ns; ++s) {
+    const int64_t a = std::max(d0, s * ns), b = std::min(d1, (s + 1) * ns);
+    if ((a - d0) % 128) return false;
+    if (by_rows)
+      emit(tc_cast_item{v.src_off[s] / 2 + uint64_t(a - s * ns) * uint64_t(v.cols), b - a, v.cols,
+                        v.cols, v.dst_off + uint64_t(a - d0) * uint64_t(v.cols), v.cols,
+                        scale_off + uint64_t((a - d0) / 128) * uint64_t(sld), sld});
+    else
+      emit(tc_cast_item{v.src_off[s] / 2 + uint64_t(a - s * ns), v.rows, b - a, ns,
+                        v.dst_off + uint64_t(a - d0), nd, scale_off + uint64_t((a - d0) / 128), sld});
+  }
+  return true;
+}
+
 }  // namespace
 
 namespace tc {
@@ -579,6 +618,34 @@ tc_status tc_reshard_fragments(const tc_reshard_view* views, int64_t n_views, in
   int64_t k = 0;
   for (int64_t i = 0; i < n_views; ++i)
     reshard_fragments(views[i], dst_tp, dst_rank, [&](const tc_fragment& f) { out[k++] = f; });
+  *written = k;
+  return TC_OK;
+}
+
+int64_t tc_reshard_cast_item_count(const tc_reshard_view* views, int64_t n_views, int32_t dst_tp,
+                                   int32_t dst_rank) {
+  if (n_views < 0 || (n_views > 0 && !views)) return -1;
+  int64_t count = 0;
+  for (int64_t i = 0; i < n_views; ++i) {
+    if (!reshard_ok(views[i], dst_tp, dst_rank)) return -1;
+    if (!reshard_cast_items(views[i], 0, dst_tp, dst_rank, [&](const tc_cast_item&) { ++count; }))
+      return -1;
+  }
+  return count;
+}
+
+tc_status tc_reshard_cast_items(const tc_reshard_view* views, const uint64_t* scale_off,
+                                int64_t n_views, int32_t dst_tp, int32_t dst_rank, tc_cast_item* out,
+                                int64_t capacity, int64_t* written) {
+  if (!written || n_views < 0 || (n_views > 0 && (!views || !scale_off)) || capacity < 0)
+    return TC_ERR_INVALID_ARGUMENT;
+  const int64_t need = tc_reshard_cast_item_count(views, n_views, dst_tp, dst_rank);
+  if (need < 0) return TC_ERR_INVALID_ARGUMENT;
+  if (need > capacity || (need > 0 && !out)) return TC_ERR_WORKSPACE;
+  int64_t k = 0;
+  for (int64_t i = 0; i < n_views; ++i)
+    reshard_cast_items(views[i], scale_off[i], dst_tp, dst_rank,
+                       [&](const tc_cast_item& it) { out[k++] = it; });
   *written = k;
   return TC_OK;
 }

@@ -81,12 +81,13 @@ def shard_slice_offsets(spec, tp: int, elem_bytes: int = 2):
     return offs, off
 
 
-def reshard_views(spec, src_tp: int, dst_tp: int, elem_bytes: int = 2):
+def reshard_views(spec, src_tp: int, dst_tp: int, elem_bytes: int = 2, dst_elem_bytes: int | None = None):
     """Views for tc_reshard_fragments: the source buffer holds the src_tp
     shards one after another (rank-major, each packed in spec order); the
-    destination is one rank's packed shard of the dst_tp split."""
+    destination is one rank's packed shard of the dst_tp split
+    (``dst_elem_bytes`` per element there; 1 for an fp8 destination)."""
     soffs, sbytes = shard_slice_offsets(spec, src_tp, elem_bytes)
-    doffs, _ = shard_slice_offsets(spec, dst_tp, elem_bytes)
+    doffs, _ = shard_slice_offsets(spec, dst_tp, elem_bytes if dst_elem_bytes is None else dst_elem_bytes)
     out = []
     for k, (_name, rows, cols, split) in enumerate(spec):
         src = [r * sbytes + soffs[k] for r in range(src_tp)]
@@ -107,3 +108,24 @@ def dequant_items(spec, tp: int):
         q_off += sr * sc
         s_off += ((sr + 127) // 128) * tcn
     return items
+
+
+def scale_offsets(spec, tp: int, tile: int = 128):
+    """Float offset of every matrix's scale grid inside one rank's packed
+    scale buffer (spec order)."""
+    offs = []
+    off = 0
+    for (_name, rows, cols, split) in spec:
+        sr, sc = slice_shape(rows, cols, split, tp)
+        offs.append(off)
+        off += ((sr + tile - 1) // tile) * ((sc + tile - 1) // tile)
+    return offs
+
+
+def reshard_cast_items(spec, src_tp: int, dst_tp: int, rank: int) -> np.ndarray:
+    """Cast items that build rank ``rank``'s packed fp8 shard of the
+    ``dst_tp`` split (with packed scale grids) directly from a buffer holding
+    the ``src_tp`` bf16 shards rank-major."""
+    from . import tc_reshard_cast_items
+    views = reshard_views(spec, src_tp, dst_tp, elem_bytes=2, dst_elem_bytes=1)
+    return tc_reshard_cast_items(views, scale_offsets(spec, dst_tp), dst_tp, rank)

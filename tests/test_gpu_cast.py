@@ -348,3 +348,52 @@ def test_cast_then_dequant_70b_layers():
         assert np.array_equal(hy[dit["dst_off"]:dit["dst_off"] + r * c].reshape(r, c), want_y)
     del stream
     torch.cuda.empty_cache()
+
+
+def _torch_shards(stream, spec, tp):
+    """All tp shards of a contiguous stream, rank-major (torch slicing on the device)."""
+    parts = []
+    for r in range(tp):
+        off = 0
+        for (_, rows, cols, split) in spec:
+            w = stream[off:off + rows * cols].view(rows, cols)
+            off += rows * cols
+            sl = w[r * rows // tp:(r + 1) * rows // tp] if split == "rows" else \
+                w[:, r * cols // tp:(r + 1) * cols // tp]
+            parts.append(sl.reshape(-1))
+    return torch.cat(parts)
+
+
+@pytest.mark.parametrize("src_tp,dst_tp,ranks", [(8, 4, [1, 2]), (4, 8, [5]), (8, 1, [0])])
+def test_reshard_cast_70b_layers(src_tp, dst_tp, ranks):
+    """Two 70B-shaped layers held as src_tp bf16 shards, cast straight into
+    rank r of a dst_tp fp8 split: every code and scale equals the oracle's cast
+    of that rank's slices of the full weights."""
+    spec = synth.spec_70b(2)
+    n = synth.spec_elems(spec)
+    stream = synth.bf16_normal(n, 0.02, synth.SEED_CAST_70B, device=DEV)
+    host = _host(stream.view(torch.int16)).view(np.uint16)
+    src = _torch_shards(stream, spec, src_tp)
+    del stream
+    for rank in ranks:
+        items = tcv.reshard_cast_items(spec, src_tp, dst_tp, rank)
+        q = torch.empty(tcv.shard_elems(spec, dst_tp), dtype=torch.uint8, device=DEV)
+        s = torch.empty(tcv.scale_elems(spec, dst_tp), dtype=torch.float32, device=DEV)
+        ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device=DEV)
+        tc.tc_cast_fp8_blockscaled(src, q, s, items, ws)
+        torch.cuda.synchronize()
+        hq, hs = _host(q), _host(s).view(np.uint32)
+        qoffs, _ = tcv.shard_slice_offsets(spec, dst_tp, 1)
+        soffs = tcv.scale_offsets(spec, dst_tp)
+        off = 0
+        for k, (_, rows, cols, split) in enumerate(spec):
+            w = host[off:off + rows * cols].reshape(rows, cols)
+            off += rows * cols
+            want_q, want_s = oracle.cast_fp8_blockscaled(oracle.tp_slice(w, split, dst_tp, rank))
+            r, c = want_q.shape
+            assert np.array_equal(hq[qoffs[k]:qoffs[k] + r * c].reshape(r, c), want_q), (k, rank)
+            tr, tcn = want_s.shape
+            assert np.array_equal(hs[soffs[k]:soffs[k] + tr * tcn].reshape(tr, tcn),
+                                  want_s.view(np.uint32)), (k, rank)
+    del src
+    torch.cuda.empty_cache()

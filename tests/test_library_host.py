@@ -222,3 +222,85 @@ def test_reshard_round_trip_and_fragment_counts(lib):
     assert tc.tc_reshard_fragment_count(tcv.reshard_views(SPEC, 8, 4), 4, 1) == 2 * (5 * 2 + 2 * 256 * 2)
     with pytest.raises(tc.TcError):
         tc.tc_reshard_fragments(tcv.reshard_views(SPEC, 8, 3), 3, 0)   # 3 does not divide
+
+
+def test_header_compiles_as_plain_c(tmp_path):
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "abi.c"
+    src.write_text('#include "tensorcast_hip.h"\nint main(void) { return TC_OK; }\n')
+    r = subprocess.run([gcc, "-std=c99", "-Wall", "-Werror", "-fsyntax-only", "-D__HIP_PLATFORM_AMD__",
+                        f"-I{os.path.dirname(HEADER)}", "-I/opt/rocm/include", str(src)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+
+
+# Dimensions that are multiples of 128 x tp for tp up to 8, small enough for the oracle.
+SPEC_TILED = synth.spec_scaled(layers=1, hidden=1024, q_heads=8, kv_heads=8, head_dim=128, mlp=2048)
+
+
+def _apply_cast_items_with_oracle(src_bits, items, q_size, s_size):
+    """Cast every item's sub-matrix with the oracle and place codes and scales
+    where the item says (a CPU stand-in for the cast kernel's addressing)."""
+    q = np.full(q_size, 0xEE, np.uint8)
+    sc = np.full(s_size, np.nan, np.float32)
+    for it in items:
+        rows, cols = int(it["rows"]), int(it["cols"])
+        so, sld = int(it["src_off"]), int(it["src_ld"])
+        m = np.lib.stride_tricks.as_strided(src_bits[so:], shape=(rows, cols), strides=(2 * sld, 2))
+        codes, scales = oracle.cast_fp8_blockscaled(np.ascontiguousarray(m))
+        do, dld = int(it["dst_off"]), int(it["dst_ld"])
+        for r in range(rows):
+            q[do + r * dld:do + r * dld + cols] = codes[r]
+        s0, sl = int(it["scale_off"]), int(it["scale_ld"])
+        for r in range(scales.shape[0]):
+            sc[s0 + r * sl:s0 + r * sl + scales.shape[1]] = scales[r]
+    return q, sc
+
+
+@pytest.mark.parametrize("src_tp,dst_tp,rank", [(8, 4, 1), (4, 8, 6), (8, 1, 0), (1, 8, 3), (2, 4, 2),
+                                                 (8, 8, 5)])
+def test_reshard_cast_items_reproduce_the_oracle_cast(lib, src_tp, dst_tp, rank):
+    """Items built for a reshard into fp8, applied by the oracle, equal the
+    oracle's cast of the destination rank's slices of the full weights."""
+    spec = SPEC_TILED
+    n = synth.spec_elems(spec)
+    rng = np.random.default_rng(21)
+    stream = (rng.standard_normal(n).astype(np.float32) * 0.02).view(np.uint32) >> 16
+    stream = stream.astype(np.uint16)
+    # source buffer: the src_tp shards, rank-major
+    src = np.concatenate([oracle.tp_shard(stream, spec, src_tp, r) for r in range(src_tp)])
+    items = tcv.reshard_cast_items(spec, src_tp, dst_tp, rank)
+    q_size = tcv.shard_elems(spec, dst_tp)
+    s_size = tcv.scale_elems(spec, dst_tp)
+    q, sc = _apply_cast_items_with_oracle(src, items, q_size, s_size)
+    # the oracle's cast of each destination slice, packed the same way
+    want_q, want_s = [], []
+    off = 0
+    for (_n, rows, cols, split) in spec:
+        w = stream[off:off + rows * cols].reshape(rows, cols)
+        off += rows * cols
+        codes, scales = oracle.cast_fp8_blockscaled(
+            np.ascontiguousarray(oracle.tp_slice(w, split, dst_tp, rank)))
+        want_q.append(codes.reshape(-1))
+        want_s.append(scales.reshape(-1))
+    assert np.array_equal(q, np.concatenate(want_q))
+    assert np.array_equal(sc.view(np.uint32), np.concatenate(want_s).view(np.uint32))
+
+
+def test_reshard_cast_items_refuse_tiles_across_sources(lib):
+    # 192 rows from 3 source ranks of 64 rows: a destination tile would span two sources
+    bad = [((0, 192 * 256 * 2 // 3, 2 * 192 * 256 * 2 // 3), 192, 256, 2, tc.SPLIT_ROWS, 0)]
+    with pytest.raises(tc.TcError):
+        tc.tc_reshard_cast_item_count(bad, 1, 0)
+    # odd source offsets cannot hold bf16
+    odd = [((1,), 128, 128, 2, tc.SPLIT_NONE, 0)]
+    with pytest.raises(tc.TcError):
+        tc.tc_reshard_cast_item_count(odd, 1, 0)
+    # fp32 views are not castable
+    f32 = [((0,), 128, 128, 4, tc.SPLIT_NONE, 0)]
+    with pytest.raises(tc.TcError):
+        tc.tc_reshard_cast_item_count(f32, 1, 0)
