@@ -184,3 +184,28 @@ def _full_size_body(s, B, nb, R):
         assert torch.equal(torch.index_select(a, 0, idl), bufv[:, r])
         assert torch.equal(b[idl], a[idl])
         assert bool((b[~mask] == 0xA5).all())
+
+
+def test_region_larger_than_4gib():
+    """One region of 100,000 blocks of 64 KiB (6.55 GB): block addresses past
+    2^32, ids at both ends of the region."""
+    nb, B = 100_000, 65536
+    region = synth.random_bytes(nb * B, 48, device=DEV)
+    ids_np = np.array([nb - 1, 0, 65536, 65535, nb - 2, 70000], dtype=np.int32)
+    ids = torch.from_numpy(ids_np).to(DEV)
+    buf = torch.empty(len(ids_np) * B, dtype=torch.uint8, device=DEV)
+    tc.tc_gather_blocks([region], nb, B, B, ids, buf)
+    torch.cuda.synchronize()
+    for k, i in enumerate(ids_np):
+        want = oracle.gather_blocks([_host(region[int(i) * B:(int(i) + 1) * B])], B, B,
+                                    np.array([0], np.int32))
+        assert np.array_equal(_host(buf[k * B:(k + 1) * B]), want.reshape(-1)), int(i)
+    # scatter them back shifted by one slot, then gather again
+    ids2 = torch.from_numpy(np.array([1, 2, 3, 4, 5, 6], np.int32)).to(DEV)
+    tc.tc_scatter_blocks([region], nb, B, B, ids2, buf)
+    back = torch.empty_like(buf)
+    tc.tc_gather_blocks([region], nb, B, B, ids2, back)
+    torch.cuda.synchronize()
+    assert torch.equal(back, buf)
+    del region
+    torch.cuda.empty_cache()

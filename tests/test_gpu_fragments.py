@@ -314,3 +314,31 @@ def test_long_unordered_lists_are_planned_in_destination_order():
     assert _header_permuted(ws2) == 0
     _, _, ws3 = _copy_and_check(src, synth.fragment_storm(1000, pool, seed=46), pool, planned=True)
     assert _header_permuted(ws3) == 0
+
+
+def test_fragment_longer_than_4gib_beyond_4gib():
+    """One fragment of 4 GiB + 17 bytes, read from and written to offsets past
+    2^32, beside two small ones: 64-bit offsets and lengths in the plan and
+    the copy.  Checked in full on the device and, in sampled windows, against
+    the oracle."""
+    big = (4 << 30) + 17
+    src_size, dst_size = (5 << 30) + 4096, (6 << 30) + 4096
+    src = _rand_bytes(src_size, 47)
+    rows = np.array([((1 << 30) + 3, (3 << 30) // 2 + 3, big),   # same residue: vector body
+                     (100, 200, 1000), (5 << 30, 8192, 4096)], dtype=np.uint64)
+    frags = torch.from_numpy(rows.view(np.int64)).to(DEV)
+    dst = torch.full((dst_size,), 0x5A, dtype=torch.uint8, device=DEV)
+    ws = torch.empty(tc.tc_copy_fragments_workspace(3), dtype=torch.uint8, device=DEV)
+    tc.tc_copy_fragments(src, dst, frags, ws)
+    torch.cuda.synchronize()
+    s0, d0 = int(rows[0, 0]), int(rows[0, 1])
+    assert torch.equal(dst[d0:d0 + big], src[s0:s0 + big])
+    assert torch.equal(dst[200:1200], src[100:1100]) and torch.equal(dst[8192:12288], src[5 << 30:(5 << 30) + 4096])
+    for a, b in ((0, 200), (1200, 8192), (12288, d0), (d0 + big, dst_size)):
+        assert int((dst[a:b] != 0x5A).sum()) == 0, (a, b)
+    for off in (0, (1 << 32) - 8192, big - 4096):
+        w = np.zeros(4096, np.uint8)
+        oracle.copy_fragments(_host(src[s0 + off:s0 + off + 4096]), w, np.array([[0, 0, 4096]], np.uint64))
+        assert np.array_equal(_host(dst[d0 + off:d0 + off + 4096]), w)
+    del src, dst
+    torch.cuda.empty_cache()
