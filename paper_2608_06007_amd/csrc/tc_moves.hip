@@ -425,6 +425,19 @@ __device__ __forceinline__ uint32_t wave_sum32(uint32_t v) {
          (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
 }
 
+// The same sum left in lane 63 only (other lanes hold partial sums): the row
+// reduction, then row 0 added into row 1 and row 2 into row 3, then lane 31
+// (rows 0 + 1) into rows 2 and 3.  No scalar work.
+__device__ __forceinline__ uint32_t wave_sum32_lane63(uint32_t v) {
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);   // quad_perm 1,0,3,2
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);   // quad_perm 2,3,0,1
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false);  // row_half_mirror
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false);  // row_mirror
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return v;
+}
+
 // A task is summed in chunks of 256 vectors (4 KiB) of its 16-byte-aligned
 // body: chunk 0 also takes the head bytes, the last chunk the tail bytes.
 // Inside a chunk every weight is the byte's position relative to the chunk's
@@ -439,7 +452,7 @@ constexpr uint64_t kChunkVecs = 256;
 template <int kMode>
 __device__ __forceinline__ void task_sums(const uint8_t* s, uint8_t* d, const uint64_t len,
                                           const int lane, const bool preloaded, const u32x4 pre,
-                                          uint64_t* A_out, uint64_t* W_out) {
+                                          u64x2* slot) {
   uint64_t A = 0, W = 0;
   const uintptr_t sa = reinterpret_cast<uintptr_t>(s);
   const uintptr_t mis = kMode == kCopyDigest ? (sa ^ reinterpret_cast<uintptr_t>(d)) & 15 : 0;
@@ -461,8 +474,9 @@ __device__ __forceinline__ void task_sums(const uint8_t* s, uint8_t* d, const ui
       a += x;
       ws += uint32_t(body_end + lane) * x;
     }
-    A = wave_sum32(a);
-    W = wave_sum32(ws);
+    const uint32_t ta = wave_sum32_lane63(a), tw = wave_sum32_lane63(ws);
+    if (lane == kWaveLanes - 1) *slot = u64x2{ta, uint64_t(tw) + ta};
+    return;
   } else if (mis == 0) {
     uint64_t head = (16 - (sa & 15)) & 15;
     if (head > len) head = len;
@@ -516,8 +530,7 @@ __device__ __forceinline__ void task_sums(const uint8_t* s, uint8_t* d, const ui
       W += cw + base * ca;
     }
   }
-  *A_out = A;
-  *W_out = W;
+  if (lane == 0) *slot = u64x2{A, W + A};
 }
 
 // kPerWave consecutive tasks per wave.  The first body vector of every task
@@ -565,9 +578,7 @@ __global__ __launch_bounds__(kThreads) void k_copy_digest(const uint8_t* __restr
 #pragma unroll
     for (int k = 0; k < kPerWave; ++k) {
       if (t0 + k >= total) break;
-      uint64_t A, W;
-      task_sums<kMode>(s[k], d[k], len[k], lane, pre[k], v[k], &A, &W);
-      if (lane == 0) slots[t0 + k] = u64x2{A, W + A};
+      task_sums<kMode>(s[k], d[k], len[k], lane, pre[k], v[k], slots + t0 + k);
     }
   }
 }
