@@ -26,6 +26,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import sys as _sys
 
 import numpy as np
 
@@ -401,8 +402,7 @@ class Stager:
     def __del__(self):
         # at interpreter shutdown the HIP runtime may already be gone: leave
         # the stager to the process exit then
-        import sys
-        if sys.is_finalizing():
+        if not self.handle or _sys.is_finalizing():
             return
         try:
             self.close()
