@@ -25,7 +25,9 @@
  *   failure is safe (the paper's idempotent retry, Sec. 3.2 "Plan").
  * - Errors: TC_ERR_INVALID_ARGUMENT for null pointers, negative sizes and
  *   geometry that cannot be valid; TC_ERR_WORKSPACE for a workspace that is
- *   too small; TC_ERR_HIP when the HIP runtime rejects a launch (the HIP
+ *   too small; TC_ERR_HOST_RESOURCES when host memory (for validation or
+ *   host tables) or host threads cannot be had; no C++ exception leaves the
+ *   library; TC_ERR_HIP when the HIP runtime rejects a launch (the HIP
  *   error code is then available from tc_last_hip_error()).  With validation
  *   on (tc_set_validate(1) or TC_VALIDATE=1 in the environment) the calls
  *   also copy the descriptors to the host, synchronize the stream, and
@@ -56,7 +58,8 @@ typedef enum {
   TC_ERR_OUT_OF_RANGE = 2,
   TC_ERR_ALIAS = 3,
   TC_ERR_HIP = 4,
-  TC_ERR_WORKSPACE = 5
+  TC_ERR_WORKSPACE = 5,
+  TC_ERR_HOST_RESOURCES = 6 /* host memory or threads could not be had */
 } tc_status;
 
 /* Largest number of regions a block pool may have. */
@@ -119,7 +122,7 @@ typedef struct {
  * digest slot, plus 16 bytes per descriptor of planning scratch); this size
  * keeps 1 KiB pieces for payloads up to ~3 KiB per fragment plus 8 GiB.  Offsets plus lengths must stay
  * below 2^48. */
-size_t tc_copy_fragments_workspace(int64_t n);
+size_t tc_copy_fragments_workspace(int64_t n); /* 0 for n < 0 or n > 2^40 */
 /* Smallest workspace a plan of n descriptors accepts (room for n + 1 tasks;
  * the task size then grows to fit). */
 size_t tc_copy_fragments_workspace_min(int64_t n);

@@ -56,7 +56,7 @@ DIGEST_SRC, DIGEST_DST = 0, 1
 HOST_PINNED = 1
 TC_OK = 0
 _STATUS = {0: "TC_OK", 1: "TC_ERR_INVALID_ARGUMENT", 2: "TC_ERR_OUT_OF_RANGE", 3: "TC_ERR_ALIAS",
-           4: "TC_ERR_HIP", 5: "TC_ERR_WORKSPACE"}
+           4: "TC_ERR_HIP", 5: "TC_ERR_WORKSPACE", 6: "TC_ERR_HOST_RESOURCES"}
 
 # Host layouts of the C structs.
 FRAGMENT_DTYPE = np.dtype([("src_off", "<u8"), ("dst_off", "<u8"), ("len", "<u8")])

@@ -354,21 +354,32 @@ extern "C" {
 
 tc_status tc_gather_blocks(const tc_block_pool* pool, const int32_t* ids, int64_t n, void* out,
                            hipStream_t stream) {
-  return blocks_common(pool, ids, n, out, true, stream);
+  try {
+    return blocks_common(pool, ids, n, out, true, stream);
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
+  }
 }
 
 tc_status tc_scatter_blocks(const tc_block_pool* pool, const int32_t* ids, int64_t n,
                             const void* in, hipStream_t stream) {
-  return blocks_common(pool, ids, n, const_cast<void*>(in), false, stream);
+  try {
+    return blocks_common(pool, ids, n, const_cast<void*>(in), false, stream);
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
+  }
 }
 
+// Counts above this are refused: the workspace sizes would not fit size_t.
+constexpr int64_t kMaxCount = int64_t(1) << 40;
+
 size_t tc_copy_fragments_workspace(int64_t n) {
-  if (n < 0) return 0;
+  if (n < 0 || n > kMaxCount) return 0;
   return tc::frag_workspace_bytes(n);
 }
 
 size_t tc_copy_fragments_workspace_min(int64_t n) {
-  if (n < 0) return 0;
+  if (n < 0 || n > kMaxCount) return 0;
   return tc::frag_workspace_min_bytes(n);
 }
 
@@ -402,92 +413,100 @@ static uint64_t pow2_at_least(uint64_t x) {
 
 tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace,
                             size_t workspace_bytes, uint64_t* total_tasks, hipStream_t stream) {
-  if (n < 0) return TC_ERR_INVALID_ARGUMENT;
-  if (total_tasks) *total_tasks = 0;
-  if (n == 0) return TC_OK;
-  if (!frags || !workspace || (uintptr_t)workspace % 256) return TC_ERR_INVALID_ARGUMENT;
-  const tc::PlanLayout L = tc::plan_layout(n, workspace_bytes);
-  if (L.capacity < uint64_t(n) + 1) return TC_ERR_WORKSPACE;
-  if (validating()) {
-    std::vector<tc_fragment> h;
-    tc_status st = fetch(frags, n, &h, stream);
-    if (st != TC_OK) return st;
-    st = check_ranges(nullptr, nullptr, h);
-    if (st != TC_OK) return st;
-  }
-  uint64_t piece = tc::kMinPiece;
-  tc::PlanHeader hdr;
-  for (int attempt = 0; attempt < 2; ++attempt) {
-    hipError_t e = tc::launch_plan_count(frags, n, piece, workspace, L, false, stream);
+  try {
+    if (n < 0 || n > kMaxCount) return TC_ERR_INVALID_ARGUMENT;
+    if (total_tasks) *total_tasks = 0;
+    if (n == 0) return TC_OK;
+    if (!frags || !workspace || (uintptr_t)workspace % 256) return TC_ERR_INVALID_ARGUMENT;
+    const tc::PlanLayout L = tc::plan_layout(n, workspace_bytes);
+    if (L.capacity < uint64_t(n) + 1) return TC_ERR_WORKSPACE;
+    if (validating()) {
+      std::vector<tc_fragment> h;
+      tc_status st = fetch(frags, n, &h, stream);
+      if (st != TC_OK) return st;
+      st = check_ranges(nullptr, nullptr, h);
+      if (st != TC_OK) return st;
+    }
+    uint64_t piece = tc::kMinPiece;
+    tc::PlanHeader hdr;
+    for (int attempt = 0; attempt < 2; ++attempt) {
+      hipError_t e = tc::launch_plan_count(frags, n, piece, workspace, L, false, stream);
+      if (e != hipSuccess) return hip_fail(e);
+      // The launch size of the copy depends on the task count: read it back.
+      e = hipMemcpyAsync(&hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, stream);
+      if (e == hipSuccess) e = hipStreamSynchronize(stream);
+      if (e != hipSuccess) return hip_fail(e);
+      if (hdr.total_tasks <= L.capacity) break;
+      // Too many 1 KiB pieces for the workspace: larger pieces bound the count
+      // by n + payload / piece <= capacity.
+      const uint64_t room = L.capacity - uint64_t(n);
+      piece = pow2_at_least(std::max<uint64_t>(tc::kMinPiece, (hdr.payload + room - 1) / room));
+      // a task's length is stored in 32 bits
+      piece = std::min<uint64_t>(piece, uint64_t(1) << 31);
+    }
+    if (hdr.total_tasks > L.capacity) return TC_ERR_WORKSPACE;
+    // Long lists with scattered destinations are planned in destination order
+    // (same tasks, so the same count): the copy then writes in address order.
+    const tc_fragment* planned = frags;
+    hipError_t e = hipSuccess;
+    if (hdr.dst_unordered && L.nbuckets) {
+      int shift = 12;
+      while (shift < 62 && (hdr.dst_end >> shift) >= L.nbuckets) ++shift;
+      e = tc::launch_plan_reorder(frags, n, shift, workspace, L, stream);
+      planned = reinterpret_cast<const tc_fragment*>(static_cast<uint8_t*>(workspace) + L.sorted);
+      if (e == hipSuccess) e = tc::launch_plan_count(planned, n, piece, workspace, L, true, stream);
+      if (e != hipSuccess) return hip_fail(e);
+    }
+    e = tc::launch_plan_expand(planned, n, hdr.total_tasks, piece, workspace, L, stream);
     if (e != hipSuccess) return hip_fail(e);
-    // The launch size of the copy depends on the task count: read it back.
-    e = hipMemcpyAsync(&hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, stream);
-    if (e == hipSuccess) e = hipStreamSynchronize(stream);
-    if (e != hipSuccess) return hip_fail(e);
-    if (hdr.total_tasks <= L.capacity) break;
-    // Too many 1 KiB pieces for the workspace: larger pieces bound the count
-    // by n + payload / piece <= capacity.
-    const uint64_t room = L.capacity - uint64_t(n);
-    piece = pow2_at_least(std::max<uint64_t>(tc::kMinPiece, (hdr.payload + room - 1) / room));
-    // a task's length is stored in 32 bits
-    piece = std::min<uint64_t>(piece, uint64_t(1) << 31);
+    if (total_tasks) *total_tasks = hdr.total_tasks;
+    return TC_OK;
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }
-  if (hdr.total_tasks > L.capacity) return TC_ERR_WORKSPACE;
-  // Long lists with scattered destinations are planned in destination order
-  // (same tasks, so the same count): the copy then writes in address order.
-  const tc_fragment* planned = frags;
-  hipError_t e = hipSuccess;
-  if (hdr.dst_unordered && L.nbuckets) {
-    int shift = 12;
-    while (shift < 62 && (hdr.dst_end >> shift) >= L.nbuckets) ++shift;
-    e = tc::launch_plan_reorder(frags, n, shift, workspace, L, stream);
-    planned = reinterpret_cast<const tc_fragment*>(static_cast<uint8_t*>(workspace) + L.sorted);
-    if (e == hipSuccess) e = tc::launch_plan_count(planned, n, piece, workspace, L, true, stream);
-    if (e != hipSuccess) return hip_fail(e);
-  }
-  e = tc::launch_plan_expand(planned, n, hdr.total_tasks, piece, workspace, L, stream);
-  if (e != hipSuccess) return hip_fail(e);
-  if (total_tasks) *total_tasks = hdr.total_tasks;
-  return TC_OK;
 }
 
 tc_status tc_copy_planned(const void* src_base, void* dst_base, const void* workspace,
                           size_t workspace_bytes, uint64_t total_tasks, hipStream_t stream) {
-  if (total_tasks == 0) return TC_OK;
-  if (!src_base || !dst_base || !workspace || (uintptr_t)workspace % 256)
-    return TC_ERR_INVALID_ARGUMENT;
-  // Whatever the plan's fragment count, its task table lies inside the
-  // workspace: a larger count cannot come from a plan made in it.
-  if (workspace_bytes < tc::kTasksOffset ||
-      total_tasks > (workspace_bytes - tc::kTasksOffset) / tc::kTaskBytes)
-    return TC_ERR_WORKSPACE;
-  // The plan's own fragment count sizes its layout.
-  tc::PlanHeader hdr;
-  hipError_t e = hipSuccess;
-  if (validating()) {
-    e = hipMemcpyAsync(&hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, stream);
-    if (e == hipSuccess) e = hipStreamSynchronize(stream);
-    if (e != hipSuccess) return hip_fail(e);
-    if (hdr.total_tasks != total_tasks) return TC_ERR_INVALID_ARGUMENT;
-    const tc::PlanLayout L = tc::plan_layout((int64_t)hdr.n, workspace_bytes);
-    if (total_tasks > L.capacity) return TC_ERR_WORKSPACE;
-    std::vector<tc::Task> packed;
-    tc_status st = fetch(reinterpret_cast<const tc::Task*>(static_cast<const uint8_t*>(workspace) +
-                                                           tc::kTasksOffset),
-                         (int64_t)total_tasks, &packed, stream);
-    if (st != TC_OK) return st;
-    std::vector<tc_fragment> tasks(packed.size());
-    for (size_t i = 0; i < packed.size(); ++i) {
-      const tc::Task& t = packed[i];
-      tasks[i] = tc_fragment{t.lo & (tc::kOffsetLimit - 1),
-                             (t.lo >> 48) | ((t.hi & 0xFFFFFFFFu) << 16), t.hi >> 32};
+  try {
+    if (total_tasks == 0) return TC_OK;
+    if (!src_base || !dst_base || !workspace || (uintptr_t)workspace % 256)
+      return TC_ERR_INVALID_ARGUMENT;
+    // Whatever the plan's fragment count, its task table lies inside the
+    // workspace: a larger count cannot come from a plan made in it.
+    if (workspace_bytes < tc::kTasksOffset ||
+        total_tasks > (workspace_bytes - tc::kTasksOffset) / tc::kTaskBytes)
+      return TC_ERR_WORKSPACE;
+    // The plan's own fragment count sizes its layout.
+    tc::PlanHeader hdr;
+    hipError_t e = hipSuccess;
+    if (validating()) {
+      e = hipMemcpyAsync(&hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, stream);
+      if (e == hipSuccess) e = hipStreamSynchronize(stream);
+      if (e != hipSuccess) return hip_fail(e);
+      if (hdr.total_tasks != total_tasks) return TC_ERR_INVALID_ARGUMENT;
+      const tc::PlanLayout L = tc::plan_layout((int64_t)hdr.n, workspace_bytes);
+      if (total_tasks > L.capacity) return TC_ERR_WORKSPACE;
+      std::vector<tc::Task> packed;
+      tc_status st = fetch(reinterpret_cast<const tc::Task*>(static_cast<const uint8_t*>(workspace) +
+                                                             tc::kTasksOffset),
+                           (int64_t)total_tasks, &packed, stream);
+      if (st != TC_OK) return st;
+      std::vector<tc_fragment> tasks(packed.size());
+      for (size_t i = 0; i < packed.size(); ++i) {
+        const tc::Task& t = packed[i];
+        tasks[i] = tc_fragment{t.lo & (tc::kOffsetLimit - 1),
+                               (t.lo >> 48) | ((t.hi & 0xFFFFFFFFu) << 16), t.hi >> 32};
+      }
+      st = check_ranges(src_base, dst_base, tasks);
+      if (st != TC_OK) return st;
     }
-    st = check_ranges(src_base, dst_base, tasks);
-    if (st != TC_OK) return st;
+    return check(tc::launch_copy_tasks(static_cast<const uint8_t*>(src_base),
+                                       static_cast<uint8_t*>(dst_base), workspace, total_tasks,
+                                       stream));
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }
-  return check(tc::launch_copy_tasks(static_cast<const uint8_t*>(src_base),
-                                     static_cast<uint8_t*>(dst_base), workspace, total_tasks,
-                                     stream));
 }
 
 // Shared by the digest entry points: argument checks, the plan's layout for
@@ -496,7 +515,7 @@ tc_status tc_copy_planned(const void* src_base, void* dst_base, const void* work
 static tc_status digest_common(const void* read_base, void* workspace, size_t workspace_bytes,
                                uint64_t total_tasks, int64_t n, const uint64_t* digests,
                                hipStream_t stream, tc::PlanLayout* L) {
-  if (n < 0) return TC_ERR_INVALID_ARGUMENT;
+  if (n < 0 || n > kMaxCount) return TC_ERR_INVALID_ARGUMENT;
   if (n == 0) return total_tasks == 0 ? TC_OK : TC_ERR_INVALID_ARGUMENT;
   if (!digests || !workspace || (uintptr_t)workspace % 256 || (uintptr_t)digests % 8)
     return TC_ERR_INVALID_ARGUMENT;
@@ -516,61 +535,73 @@ static tc_status digest_common(const void* read_base, void* workspace, size_t wo
 tc_status tc_copy_planned_digest(const void* src_base, void* dst_base, void* workspace,
                                  size_t workspace_bytes, uint64_t total_tasks, int64_t n,
                                  uint64_t* digests, hipStream_t stream) {
-  if (total_tasks && !dst_base) return TC_ERR_INVALID_ARGUMENT;
-  tc::PlanLayout L;
-  tc_status st =
-      digest_common(src_base, workspace, workspace_bytes, total_tasks, n, digests, stream, &L);
-  if (st != TC_OK || n == 0) return st;
-  if (validating() && total_tasks) {
-    // the planned ranges must not alias, as for tc_copy_planned
-    std::vector<tc::Task> packed;
-    st = fetch(reinterpret_cast<const tc::Task*>(static_cast<const uint8_t*>(workspace) +
-                                                 tc::kTasksOffset),
-               (int64_t)total_tasks, &packed, stream);
-    if (st != TC_OK) return st;
-    std::vector<tc_fragment> tasks(packed.size());
-    for (size_t i = 0; i < packed.size(); ++i) {
-      const tc::Task& t = packed[i];
-      tasks[i] = tc_fragment{t.lo & (tc::kOffsetLimit - 1),
-                             (t.lo >> 48) | ((t.hi & 0xFFFFFFFFu) << 16), t.hi >> 32};
+  try {
+    if (total_tasks && !dst_base) return TC_ERR_INVALID_ARGUMENT;
+    tc::PlanLayout L;
+    tc_status st =
+        digest_common(src_base, workspace, workspace_bytes, total_tasks, n, digests, stream, &L);
+    if (st != TC_OK || n == 0) return st;
+    if (validating() && total_tasks) {
+      // the planned ranges must not alias, as for tc_copy_planned
+      std::vector<tc::Task> packed;
+      st = fetch(reinterpret_cast<const tc::Task*>(static_cast<const uint8_t*>(workspace) +
+                                                   tc::kTasksOffset),
+                 (int64_t)total_tasks, &packed, stream);
+      if (st != TC_OK) return st;
+      std::vector<tc_fragment> tasks(packed.size());
+      for (size_t i = 0; i < packed.size(); ++i) {
+        const tc::Task& t = packed[i];
+        tasks[i] = tc_fragment{t.lo & (tc::kOffsetLimit - 1),
+                               (t.lo >> 48) | ((t.hi & 0xFFFFFFFFu) << 16), t.hi >> 32};
+      }
+      st = check_ranges(src_base, dst_base, tasks);
+      if (st != TC_OK) return st;
     }
-    st = check_ranges(src_base, dst_base, tasks);
-    if (st != TC_OK) return st;
+    return check(tc::launch_copy_digest(static_cast<const uint8_t*>(src_base),
+                                        static_cast<uint8_t*>(dst_base), workspace, L, n,
+                                        total_tasks, 0, digests, stream));
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }
-  return check(tc::launch_copy_digest(static_cast<const uint8_t*>(src_base),
-                                      static_cast<uint8_t*>(dst_base), workspace, L, n,
-                                      total_tasks, 0, digests, stream));
 }
 
 tc_status tc_digest_planned(const void* base, int32_t side, void* workspace,
                             size_t workspace_bytes, uint64_t total_tasks, int64_t n,
                             uint64_t* digests, hipStream_t stream) {
-  if (side != TC_DIGEST_SRC && side != TC_DIGEST_DST) return TC_ERR_INVALID_ARGUMENT;
-  tc::PlanLayout L;
-  tc_status st = digest_common(base, workspace, workspace_bytes, total_tasks, n, digests, stream, &L);
-  if (st != TC_OK || n == 0) return st;
-  return check(tc::launch_copy_digest(static_cast<const uint8_t*>(base), nullptr, workspace, L, n,
-                                      total_tasks, side == TC_DIGEST_SRC ? 1 : 2, digests,
-                                      stream));
+  try {
+    if (side != TC_DIGEST_SRC && side != TC_DIGEST_DST) return TC_ERR_INVALID_ARGUMENT;
+    tc::PlanLayout L;
+    tc_status st = digest_common(base, workspace, workspace_bytes, total_tasks, n, digests, stream, &L);
+    if (st != TC_OK || n == 0) return st;
+    return check(tc::launch_copy_digest(static_cast<const uint8_t*>(base), nullptr, workspace, L, n,
+                                        total_tasks, side == TC_DIGEST_SRC ? 1 : 2, digests,
+                                        stream));
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
+  }
 }
 
 tc_status tc_copy_fragments(const void* src_base, void* dst_base, const tc_fragment* frags,
                             int64_t n, void* workspace, size_t workspace_bytes,
                             hipStream_t stream) {
-  if (n < 0) return TC_ERR_INVALID_ARGUMENT;
-  if (n == 0) return TC_OK;
-  if (!src_base || !dst_base || !frags || !workspace) return TC_ERR_INVALID_ARGUMENT;
-  if (validating()) {
-    std::vector<tc_fragment> h;
-    tc_status st = fetch(frags, n, &h, stream);
+  try {
+    if (n < 0 || n > kMaxCount) return TC_ERR_INVALID_ARGUMENT;
+    if (n == 0) return TC_OK;
+    if (!src_base || !dst_base || !frags || !workspace) return TC_ERR_INVALID_ARGUMENT;
+    if (validating()) {
+      std::vector<tc_fragment> h;
+      tc_status st = fetch(frags, n, &h, stream);
+      if (st != TC_OK) return st;
+      st = check_ranges(src_base, dst_base, h);
+      if (st != TC_OK) return st;
+    }
+    uint64_t total = 0;
+    tc_status st = tc_plan_fragments(frags, n, workspace, workspace_bytes, &total, stream);
     if (st != TC_OK) return st;
-    st = check_ranges(src_base, dst_base, h);
-    if (st != TC_OK) return st;
+    return tc_copy_planned(src_base, dst_base, workspace, workspace_bytes, total, stream);
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }
-  uint64_t total = 0;
-  tc_status st = tc_plan_fragments(frags, n, workspace, workspace_bytes, &total, stream);
-  if (st != TC_OK) return st;
-  return tc_copy_planned(src_base, dst_base, workspace, workspace_bytes, total, stream);
 }
 
 int64_t tc_tp_fragment_count(const tc_tp_view* views, int64_t n_views, int32_t tp, int32_t rank) {
@@ -585,15 +616,19 @@ int64_t tc_tp_fragment_count(const tc_tp_view* views, int64_t n_views, int32_t t
 
 tc_status tc_tp_fragments(const tc_tp_view* views, int64_t n_views, int32_t tp, int32_t rank,
                           tc_fragment* out, int64_t capacity, int64_t* written) {
-  if (!written || n_views < 0 || (n_views > 0 && !views) || capacity < 0) return TC_ERR_INVALID_ARGUMENT;
-  const int64_t need = tc_tp_fragment_count(views, n_views, tp, rank);
-  if (need < 0) return TC_ERR_INVALID_ARGUMENT;
-  if (need > capacity || (need > 0 && !out)) return TC_ERR_WORKSPACE;
-  int64_t k = 0;
-  for (int64_t i = 0; i < n_views; ++i)
-    view_fragments(views[i], tp, rank, [&](const tc_fragment& f) { out[k++] = f; });
-  *written = k;
-  return TC_OK;
+  try {
+    if (!written || n_views < 0 || (n_views > 0 && !views) || capacity < 0) return TC_ERR_INVALID_ARGUMENT;
+    const int64_t need = tc_tp_fragment_count(views, n_views, tp, rank);
+    if (need < 0) return TC_ERR_INVALID_ARGUMENT;
+    if (need > capacity || (need > 0 && !out)) return TC_ERR_WORKSPACE;
+    int64_t k = 0;
+    for (int64_t i = 0; i < n_views; ++i)
+      view_fragments(views[i], tp, rank, [&](const tc_fragment& f) { out[k++] = f; });
+    *written = k;
+    return TC_OK;
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
+  }
 }
 
 int64_t tc_reshard_fragment_count(const tc_reshard_view* views, int64_t n_views, int32_t dst_tp,
@@ -610,16 +645,20 @@ int64_t tc_reshard_fragment_count(const tc_reshard_view* views, int64_t n_views,
 tc_status tc_reshard_fragments(const tc_reshard_view* views, int64_t n_views, int32_t dst_tp,
                                int32_t dst_rank, tc_fragment* out, int64_t capacity,
                                int64_t* written) {
-  if (!written || n_views < 0 || (n_views > 0 && !views) || capacity < 0)
-    return TC_ERR_INVALID_ARGUMENT;
-  const int64_t need = tc_reshard_fragment_count(views, n_views, dst_tp, dst_rank);
-  if (need < 0) return TC_ERR_INVALID_ARGUMENT;
-  if (need > capacity || (need > 0 && !out)) return TC_ERR_WORKSPACE;
-  int64_t k = 0;
-  for (int64_t i = 0; i < n_views; ++i)
-    reshard_fragments(views[i], dst_tp, dst_rank, [&](const tc_fragment& f) { out[k++] = f; });
-  *written = k;
-  return TC_OK;
+  try {
+    if (!written || n_views < 0 || (n_views > 0 && !views) || capacity < 0)
+      return TC_ERR_INVALID_ARGUMENT;
+    const int64_t need = tc_reshard_fragment_count(views, n_views, dst_tp, dst_rank);
+    if (need < 0) return TC_ERR_INVALID_ARGUMENT;
+    if (need > capacity || (need > 0 && !out)) return TC_ERR_WORKSPACE;
+    int64_t k = 0;
+    for (int64_t i = 0; i < n_views; ++i)
+      reshard_fragments(views[i], dst_tp, dst_rank, [&](const tc_fragment& f) { out[k++] = f; });
+    *written = k;
+    return TC_OK;
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
+  }
 }
 
 int64_t tc_reshard_cast_item_count(const tc_reshard_view* views, int64_t n_views, int32_t dst_tp,
@@ -637,17 +676,21 @@ int64_t tc_reshard_cast_item_count(const tc_reshard_view* views, int64_t n_views
 tc_status tc_reshard_cast_items(const tc_reshard_view* views, const uint64_t* scale_off,
                                 int64_t n_views, int32_t dst_tp, int32_t dst_rank, tc_cast_item* out,
                                 int64_t capacity, int64_t* written) {
-  if (!written || n_views < 0 || (n_views > 0 && (!views || !scale_off)) || capacity < 0)
-    return TC_ERR_INVALID_ARGUMENT;
-  const int64_t need = tc_reshard_cast_item_count(views, n_views, dst_tp, dst_rank);
-  if (need < 0) return TC_ERR_INVALID_ARGUMENT;
-  if (need > capacity || (need > 0 && !out)) return TC_ERR_WORKSPACE;
-  int64_t k = 0;
-  for (int64_t i = 0; i < n_views; ++i)
-    reshard_cast_items(views[i], scale_off[i], dst_tp, dst_rank,
-                       [&](const tc_cast_item& it) { out[k++] = it; });
-  *written = k;
-  return TC_OK;
+  try {
+    if (!written || n_views < 0 || (n_views > 0 && (!views || !scale_off)) || capacity < 0)
+      return TC_ERR_INVALID_ARGUMENT;
+    const int64_t need = tc_reshard_cast_item_count(views, n_views, dst_tp, dst_rank);
+    if (need < 0) return TC_ERR_INVALID_ARGUMENT;
+    if (need > capacity || (need > 0 && !out)) return TC_ERR_WORKSPACE;
+    int64_t k = 0;
+    for (int64_t i = 0; i < n_views; ++i)
+      reshard_cast_items(views[i], scale_off[i], dst_tp, dst_rank,
+                         [&](const tc_cast_item& it) { out[k++] = it; });
+    *written = k;
+    return TC_OK;
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
+  }
 }
 
 tc_status tc_tp_cast_item(const tc_tp_view* view, int32_t tp, int32_t rank, uint64_t scale_off,
@@ -670,85 +713,89 @@ tc_status tc_tp_cast_item(const tc_tp_view* view, int32_t tp, int32_t rank, uint
 }
 
 size_t tc_cast_fp8_workspace(int64_t n_items) {
-  if (n_items < 0) return 0;
+  if (n_items < 0 || n_items > kMaxCount) return 0;
   return tc::cast_workspace_bytes(n_items);
 }
 
 tc_status tc_cast_fp8_blockscaled(const void* src_base, void* dst_base, float* scale_base,
                                   const tc_cast_item* items, int64_t n_items, int32_t tile,
                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  if (n_items < 0 || tile != 128) return TC_ERR_INVALID_ARGUMENT;
-  if (n_items == 0) return TC_OK;
-  if (!src_base || !dst_base || !scale_base || !items || !workspace) return TC_ERR_INVALID_ARGUMENT;
-  if (workspace_bytes < tc::cast_workspace_bytes(n_items)) return TC_ERR_WORKSPACE;
-  if ((uintptr_t)workspace % 256 || (uintptr_t)src_base % 2 || (uintptr_t)scale_base % 4)
-    return TC_ERR_INVALID_ARGUMENT;
-  // Geometry and the tile ranges, on the host: full tiles of vector-aligned
-  // items go to the streaming kernel, every other tile to the edge kernel.
-  const size_t N = (size_t)n_items;
-  std::vector<uint64_t> fprefix(N + 1), eprefix(N + 1);
-  std::vector<uint8_t> aligned(N);
-  uint64_t full = 0, edge = 0;
-  for (size_t i = 0; i < N; ++i) {
-    const tc_cast_item& it = items[i];
-    if (it.rows < 0 || it.cols < 0 || it.src_ld < it.cols || it.dst_ld < it.cols)
+  try {
+    if (n_items < 0 || n_items > kMaxCount || tile != 128) return TC_ERR_INVALID_ARGUMENT;
+    if (n_items == 0) return TC_OK;
+    if (!src_base || !dst_base || !scale_base || !items || !workspace) return TC_ERR_INVALID_ARGUMENT;
+    if (workspace_bytes < tc::cast_workspace_bytes(n_items)) return TC_ERR_WORKSPACE;
+    if ((uintptr_t)workspace % 256 || (uintptr_t)src_base % 2 || (uintptr_t)scale_base % 4)
       return TC_ERR_INVALID_ARGUMENT;
-    const uint64_t tr = uint64_t((it.rows + 127) / 128), tcn = uint64_t((it.cols + 127) / 128);
-    if (it.rows > 0 && it.cols > 0 && it.scale_ld < int64_t(tcn)) return TC_ERR_INVALID_ARGUMENT;
-    const uint64_t x = (uint64_t)(uintptr_t)src_base + 2 * it.src_off;
-    const uint64_t q = (uint64_t)(uintptr_t)dst_base + it.dst_off;
-    aligned[i] = (x % 16 == 0 && (2 * uint64_t(it.src_ld)) % 16 == 0 && q % 8 == 0 &&
-                  uint64_t(it.dst_ld) % 8 == 0) ? 1 : 0;
-    const uint64_t all = (it.rows > 0 && it.cols > 0) ? tr * tcn : 0;
-    const uint64_t f = aligned[i] ? uint64_t(it.rows / 128) * uint64_t(it.cols / 128) : 0;
-    fprefix[i] = full;
-    eprefix[i] = edge;
-    full += f;
-    edge += all - f;
-  }
-  fprefix[N] = full;
-  eprefix[N] = edge;
-  if (full + edge == 0) return TC_OK;
-  if (validating()) {
-    std::vector<Range> q, sc, srcr;
-    const uint64_t db = (uint64_t)(uintptr_t)dst_base, sb = (uint64_t)(uintptr_t)scale_base;
-    const uint64_t xb = (uint64_t)(uintptr_t)src_base;
-    for (int64_t i = 0; i < n_items; ++i) {
+    // Geometry and the tile ranges, on the host: full tiles of vector-aligned
+    // items go to the streaming kernel, every other tile to the edge kernel.
+    const size_t N = (size_t)n_items;
+    std::vector<uint64_t> fprefix(N + 1), eprefix(N + 1);
+    std::vector<uint8_t> aligned(N);
+    uint64_t full = 0, edge = 0;
+    for (size_t i = 0; i < N; ++i) {
       const tc_cast_item& it = items[i];
-      if (it.rows == 0 || it.cols == 0) continue;
-      const int64_t tcn = (it.cols + 127) / 128, tr = (it.rows + 127) / 128;
-      for (int64_t r = 0; r < it.rows; ++r) {
-        const uint64_t a = db + it.dst_off + uint64_t(r) * uint64_t(it.dst_ld);
-        q.push_back({a, a + uint64_t(it.cols)});
-        const uint64_t x = xb + 2 * (it.src_off + uint64_t(r) * uint64_t(it.src_ld));
-        srcr.push_back({x, x + 2 * uint64_t(it.cols)});
-      }
-      for (int64_t r = 0; r < tr; ++r) {
-        const uint64_t a = sb + 4 * (it.scale_off + uint64_t(r) * uint64_t(it.scale_ld));
-        sc.push_back({a, a + 4 * uint64_t(tcn)});
-      }
+      if (it.rows < 0 || it.cols < 0 || it.src_ld < it.cols || it.dst_ld < it.cols)
+        return TC_ERR_INVALID_ARGUMENT;
+      const uint64_t tr = uint64_t((it.rows + 127) / 128), tcn = uint64_t((it.cols + 127) / 128);
+      if (it.rows > 0 && it.cols > 0 && it.scale_ld < int64_t(tcn)) return TC_ERR_INVALID_ARGUMENT;
+      const uint64_t x = (uint64_t)(uintptr_t)src_base + 2 * it.src_off;
+      const uint64_t q = (uint64_t)(uintptr_t)dst_base + it.dst_off;
+      aligned[i] = (x % 16 == 0 && (2 * uint64_t(it.src_ld)) % 16 == 0 && q % 8 == 0 &&
+                    uint64_t(it.dst_ld) % 8 == 0) ? 1 : 0;
+      const uint64_t all = (it.rows > 0 && it.cols > 0) ? tr * tcn : 0;
+      const uint64_t f = aligned[i] ? uint64_t(it.rows / 128) * uint64_t(it.cols / 128) : 0;
+      fprefix[i] = full;
+      eprefix[i] = edge;
+      full += f;
+      edge += all - f;
     }
-    std::vector<Range> outs = q;
-    outs.insert(outs.end(), sc.begin(), sc.end());
-    if (any_overlap(outs)) return TC_ERR_ALIAS;
-    if (cross_overlap(outs, srcr)) return TC_ERR_ALIAS;
+    fprefix[N] = full;
+    eprefix[N] = edge;
+    if (full + edge == 0) return TC_OK;
+    if (validating()) {
+      std::vector<Range> q, sc, srcr;
+      const uint64_t db = (uint64_t)(uintptr_t)dst_base, sb = (uint64_t)(uintptr_t)scale_base;
+      const uint64_t xb = (uint64_t)(uintptr_t)src_base;
+      for (int64_t i = 0; i < n_items; ++i) {
+        const tc_cast_item& it = items[i];
+        if (it.rows == 0 || it.cols == 0) continue;
+        const int64_t tcn = (it.cols + 127) / 128, tr = (it.rows + 127) / 128;
+        for (int64_t r = 0; r < it.rows; ++r) {
+          const uint64_t a = db + it.dst_off + uint64_t(r) * uint64_t(it.dst_ld);
+          q.push_back({a, a + uint64_t(it.cols)});
+          const uint64_t x = xb + 2 * (it.src_off + uint64_t(r) * uint64_t(it.src_ld));
+          srcr.push_back({x, x + 2 * uint64_t(it.cols)});
+        }
+        for (int64_t r = 0; r < tr; ++r) {
+          const uint64_t a = sb + 4 * (it.scale_off + uint64_t(r) * uint64_t(it.scale_ld));
+          sc.push_back({a, a + 4 * uint64_t(tcn)});
+        }
+      }
+      std::vector<Range> outs = q;
+      outs.insert(outs.end(), sc.begin(), sc.end());
+      if (any_overlap(outs)) return TC_ERR_ALIAS;
+      if (cross_overlap(outs, srcr)) return TC_ERR_ALIAS;
+    }
+    // Items and tile tables go to the workspace through pinned staging memory,
+    // so the caller's host array is free as soon as this call returns.
+    const tc::CastLayout L = tc::cast_layout(n_items);
+    tc_status st = stage_to_device(workspace, stream,
+                                   {{items, sizeof(tc_cast_item) * N, L.items},
+                                    {fprefix.data(), 8 * (N + 1), L.full_prefix},
+                                    {eprefix.data(), 8 * (N + 1), L.edge_prefix},
+                                    {aligned.data(), N, L.aligned}});
+    if (st != TC_OK) return st;
+    return check(tc::launch_cast_blockscaled(static_cast<const uint16_t*>(src_base),
+                                             static_cast<uint8_t*>(dst_base), scale_base, workspace,
+                                             n_items, full, edge, stream));
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }
-  // Items and tile tables go to the workspace through pinned staging memory,
-  // so the caller's host array is free as soon as this call returns.
-  const tc::CastLayout L = tc::cast_layout(n_items);
-  tc_status st = stage_to_device(workspace, stream,
-                                 {{items, sizeof(tc_cast_item) * N, L.items},
-                                  {fprefix.data(), 8 * (N + 1), L.full_prefix},
-                                  {eprefix.data(), 8 * (N + 1), L.edge_prefix},
-                                  {aligned.data(), N, L.aligned}});
-  if (st != TC_OK) return st;
-  return check(tc::launch_cast_blockscaled(static_cast<const uint16_t*>(src_base),
-                                           static_cast<uint8_t*>(dst_base), scale_base, workspace,
-                                           n_items, full, edge, stream));
 }
 
 size_t tc_dequant_fp8_workspace(int64_t n_items) {
-  if (n_items < 0) return 0;
+  if (n_items < 0 || n_items > kMaxCount) return 0;
   return tc::cast_workspace_bytes(n_items);
 }
 
@@ -758,68 +805,72 @@ tc_status tc_dequant_fp8_blockscaled(const void* codes_base, const float* scale_
                                      void* dst_base, const tc_dequant_item* items, int64_t n_items,
                                      int32_t tile, void* workspace, size_t workspace_bytes,
                                      hipStream_t stream) {
-  if (n_items < 0 || tile != 128) return TC_ERR_INVALID_ARGUMENT;
-  if (n_items == 0) return TC_OK;
-  if (!codes_base || !scale_base || !dst_base || !items || !workspace) return TC_ERR_INVALID_ARGUMENT;
-  if (workspace_bytes < tc::cast_workspace_bytes(n_items)) return TC_ERR_WORKSPACE;
-  if ((uintptr_t)workspace % 256 || (uintptr_t)dst_base % 2 || (uintptr_t)scale_base % 4)
-    return TC_ERR_INVALID_ARGUMENT;
-  const size_t N = (size_t)n_items;
-  std::vector<uint64_t> fprefix(N + 1), eprefix(N + 1);
-  std::vector<uint8_t> aligned(N);
-  uint64_t full = 0, edge = 0;
-  for (size_t i = 0; i < N; ++i) {
-    const tc_dequant_item& it = items[i];
-    if (it.rows < 0 || it.cols < 0 || it.src_ld < it.cols || it.dst_ld < it.cols)
+  try {
+    if (n_items < 0 || n_items > kMaxCount || tile != 128) return TC_ERR_INVALID_ARGUMENT;
+    if (n_items == 0) return TC_OK;
+    if (!codes_base || !scale_base || !dst_base || !items || !workspace) return TC_ERR_INVALID_ARGUMENT;
+    if (workspace_bytes < tc::cast_workspace_bytes(n_items)) return TC_ERR_WORKSPACE;
+    if ((uintptr_t)workspace % 256 || (uintptr_t)dst_base % 2 || (uintptr_t)scale_base % 4)
       return TC_ERR_INVALID_ARGUMENT;
-    const uint64_t tr = uint64_t((it.rows + 127) / 128), tcn = uint64_t((it.cols + 127) / 128);
-    if (it.rows > 0 && it.cols > 0 && it.scale_ld < int64_t(tcn)) return TC_ERR_INVALID_ARGUMENT;
-    const uint64_t q = (uint64_t)(uintptr_t)codes_base + it.src_off;
-    const uint64_t y = (uint64_t)(uintptr_t)dst_base + 2 * it.dst_off;
-    aligned[i] = (q % 8 == 0 && uint64_t(it.src_ld) % 8 == 0 && y % 16 == 0 &&
-                  (2 * uint64_t(it.dst_ld)) % 16 == 0) ? 1 : 0;
-    const uint64_t all = (it.rows > 0 && it.cols > 0) ? tr * tcn : 0;
-    const uint64_t f = aligned[i] ? uint64_t(it.rows / 128) * uint64_t(it.cols / 128) : 0;
-    fprefix[i] = full;
-    eprefix[i] = edge;
-    full += f;
-    edge += all - f;
-  }
-  fprefix[N] = full;
-  eprefix[N] = edge;
-  if (full + edge == 0) return TC_OK;
-  if (validating()) {
-    std::vector<Range> outs, srcs;
-    const uint64_t db = (uint64_t)(uintptr_t)dst_base, qb = (uint64_t)(uintptr_t)codes_base;
-    const uint64_t sb = (uint64_t)(uintptr_t)scale_base;
+    const size_t N = (size_t)n_items;
+    std::vector<uint64_t> fprefix(N + 1), eprefix(N + 1);
+    std::vector<uint8_t> aligned(N);
+    uint64_t full = 0, edge = 0;
     for (size_t i = 0; i < N; ++i) {
       const tc_dequant_item& it = items[i];
-      if (it.rows == 0 || it.cols == 0) continue;
-      const int64_t tcn = (it.cols + 127) / 128, tr = (it.rows + 127) / 128;
-      for (int64_t r = 0; r < it.rows; ++r) {
-        const uint64_t a = db + 2 * (it.dst_off + uint64_t(r) * uint64_t(it.dst_ld));
-        outs.push_back({a, a + 2 * uint64_t(it.cols)});
-        const uint64_t x = qb + it.src_off + uint64_t(r) * uint64_t(it.src_ld);
-        srcs.push_back({x, x + uint64_t(it.cols)});
-      }
-      for (int64_t r = 0; r < tr; ++r) {
-        const uint64_t a = sb + 4 * (it.scale_off + uint64_t(r) * uint64_t(it.scale_ld));
-        srcs.push_back({a, a + 4 * uint64_t(tcn)});
-      }
+      if (it.rows < 0 || it.cols < 0 || it.src_ld < it.cols || it.dst_ld < it.cols)
+        return TC_ERR_INVALID_ARGUMENT;
+      const uint64_t tr = uint64_t((it.rows + 127) / 128), tcn = uint64_t((it.cols + 127) / 128);
+      if (it.rows > 0 && it.cols > 0 && it.scale_ld < int64_t(tcn)) return TC_ERR_INVALID_ARGUMENT;
+      const uint64_t q = (uint64_t)(uintptr_t)codes_base + it.src_off;
+      const uint64_t y = (uint64_t)(uintptr_t)dst_base + 2 * it.dst_off;
+      aligned[i] = (q % 8 == 0 && uint64_t(it.src_ld) % 8 == 0 && y % 16 == 0 &&
+                    (2 * uint64_t(it.dst_ld)) % 16 == 0) ? 1 : 0;
+      const uint64_t all = (it.rows > 0 && it.cols > 0) ? tr * tcn : 0;
+      const uint64_t f = aligned[i] ? uint64_t(it.rows / 128) * uint64_t(it.cols / 128) : 0;
+      fprefix[i] = full;
+      eprefix[i] = edge;
+      full += f;
+      edge += all - f;
     }
-    if (any_overlap(outs)) return TC_ERR_ALIAS;
-    if (cross_overlap(outs, srcs)) return TC_ERR_ALIAS;
+    fprefix[N] = full;
+    eprefix[N] = edge;
+    if (full + edge == 0) return TC_OK;
+    if (validating()) {
+      std::vector<Range> outs, srcs;
+      const uint64_t db = (uint64_t)(uintptr_t)dst_base, qb = (uint64_t)(uintptr_t)codes_base;
+      const uint64_t sb = (uint64_t)(uintptr_t)scale_base;
+      for (size_t i = 0; i < N; ++i) {
+        const tc_dequant_item& it = items[i];
+        if (it.rows == 0 || it.cols == 0) continue;
+        const int64_t tcn = (it.cols + 127) / 128, tr = (it.rows + 127) / 128;
+        for (int64_t r = 0; r < it.rows; ++r) {
+          const uint64_t a = db + 2 * (it.dst_off + uint64_t(r) * uint64_t(it.dst_ld));
+          outs.push_back({a, a + 2 * uint64_t(it.cols)});
+          const uint64_t x = qb + it.src_off + uint64_t(r) * uint64_t(it.src_ld);
+          srcs.push_back({x, x + uint64_t(it.cols)});
+        }
+        for (int64_t r = 0; r < tr; ++r) {
+          const uint64_t a = sb + 4 * (it.scale_off + uint64_t(r) * uint64_t(it.scale_ld));
+          srcs.push_back({a, a + 4 * uint64_t(tcn)});
+        }
+      }
+      if (any_overlap(outs)) return TC_ERR_ALIAS;
+      if (cross_overlap(outs, srcs)) return TC_ERR_ALIAS;
+    }
+    const tc::CastLayout L = tc::cast_layout(n_items);
+    tc_status st = stage_to_device(workspace, stream,
+                                   {{items, sizeof(tc_dequant_item) * N, L.items},
+                                    {fprefix.data(), 8 * (N + 1), L.full_prefix},
+                                    {eprefix.data(), 8 * (N + 1), L.edge_prefix},
+                                    {aligned.data(), N, L.aligned}});
+    if (st != TC_OK) return st;
+    return check(tc::launch_dequant_blockscaled(static_cast<const uint8_t*>(codes_base), scale_base,
+                                                static_cast<uint16_t*>(dst_base), workspace, n_items,
+                                                full, edge, stream));
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }
-  const tc::CastLayout L = tc::cast_layout(n_items);
-  tc_status st = stage_to_device(workspace, stream,
-                                 {{items, sizeof(tc_dequant_item) * N, L.items},
-                                  {fprefix.data(), 8 * (N + 1), L.full_prefix},
-                                  {eprefix.data(), 8 * (N + 1), L.edge_prefix},
-                                  {aligned.data(), N, L.aligned}});
-  if (st != TC_OK) return st;
-  return check(tc::launch_dequant_blockscaled(static_cast<const uint8_t*>(codes_base), scale_base,
-                                              static_cast<uint16_t*>(dst_base), workspace, n_items,
-                                              full, edge, stream));
 }
 
 tc_status tc_cast_fp8_scaled(const void* src_bf16, int64_t n, float scale, void* dst_e4m3,
@@ -839,6 +890,7 @@ const char* tc_status_string(tc_status s) {
     case TC_ERR_ALIAS: return "aliasing writes";
     case TC_ERR_HIP: return "HIP runtime error";
     case TC_ERR_WORKSPACE: return "workspace too small";
+    case TC_ERR_HOST_RESOURCES: return "host memory or threads unavailable";
   }
   return "unknown status";
 }

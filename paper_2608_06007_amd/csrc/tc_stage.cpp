@@ -23,6 +23,7 @@
 #include <cstring>
 #include <functional>
 #include <mutex>
+#include <new>
 #include <thread>
 #include <vector>
 
@@ -253,12 +254,16 @@ tc_status tc_stager_create(size_t slot_bytes, int32_t slots, int32_t host_thread
   if (slots == 0) slots = kDefaultSlots;
   if (host_threads == 0) host_threads = kDefaultThreads;
   if (slots < 2 || slot_bytes < 4096) return TC_ERR_INVALID_ARGUMENT;
-  tc_stager* st = new tc_stager;
+  tc_stager* st = new (std::nothrow) tc_stager;
+  if (!st) return TC_ERR_HOST_RESOURCES;
   st->slot_bytes = slot_bytes;
   hipError_t e = hipGetDevice(&st->device);
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&st->copy, hipStreamNonBlocking);
   if (e == hipSuccess) e = new_event(&st->start);
   if (e == hipSuccess) e = new_event(&st->end);
+  st->pinned.reserve(size_t(slots));
+  st->pinned_free.reserve(size_t(slots));
+  st->pinned_used.reserve(size_t(slots));
   for (int32_t j = 0; e == hipSuccess && j < slots; ++j) {
     void* p = nullptr;
     hipEvent_t ev = nullptr;
@@ -274,7 +279,12 @@ tc_status tc_stager_create(size_t slot_bytes, int32_t slots, int32_t host_thread
     release(st);
     return fail(e);
   }
-  st->workers = new Workers(host_threads);
+  try {
+    st->workers = new Workers(host_threads);
+  } catch (...) {  // threads or memory unavailable
+    release(st);
+    return TC_ERR_HOST_RESOURCES;
+  }
   *out = st;
   return TC_OK;
 }
@@ -287,185 +297,201 @@ tc_status tc_stager_destroy(tc_stager* st) {
 
 tc_status tc_stage_h2d(tc_stager* st, const void* host_src, void* dev_dst, size_t bytes,
                        int32_t flags, hipStream_t stream) {
-  if (!st || (flags & ~TC_HOST_PINNED)) return TC_ERR_INVALID_ARGUMENT;
-  if (bytes == 0) return TC_OK;
-  if (!host_src || !dev_dst) return TC_ERR_INVALID_ARGUMENT;
-  std::lock_guard<std::mutex> lock(st->mu);
-  tc_status s = same_device(st);
-  if (s == TC_OK) s = copy_after(st, stream);
-  if (s != TC_OK) return s;
-  const uint8_t* src = static_cast<const uint8_t*>(host_src);
-  uint8_t* dst = static_cast<uint8_t*>(dev_dst);
-  const bool pinned = flags & TC_HOST_PINNED;
-  const size_t C = st->slot_bytes, S = st->pinned.size();
-  for (size_t k = 0, off = 0; off < bytes; ++k, off += C) {
-    const size_t j = k % S, len = std::min(C, bytes - off);
-    if ((s = pace(st, k)) != TC_OK) return s;
-    const void* from = src + off;
-    if (!pinned) {
-      par_copy(st, st->pinned[j], from, len);
-      from = st->pinned[j];
+  try {
+    if (!st || (flags & ~TC_HOST_PINNED)) return TC_ERR_INVALID_ARGUMENT;
+    if (bytes == 0) return TC_OK;
+    if (!host_src || !dev_dst) return TC_ERR_INVALID_ARGUMENT;
+    std::lock_guard<std::mutex> lock(st->mu);
+    tc_status s = same_device(st);
+    if (s == TC_OK) s = copy_after(st, stream);
+    if (s != TC_OK) return s;
+    const uint8_t* src = static_cast<const uint8_t*>(host_src);
+    uint8_t* dst = static_cast<uint8_t*>(dev_dst);
+    const bool pinned = flags & TC_HOST_PINNED;
+    const size_t C = st->slot_bytes, S = st->pinned.size();
+    for (size_t k = 0, off = 0; off < bytes; ++k, off += C) {
+      const size_t j = k % S, len = std::min(C, bytes - off);
+      if ((s = pace(st, k)) != TC_OK) return s;
+      const void* from = src + off;
+      if (!pinned) {
+        par_copy(st, st->pinned[j], from, len);
+        from = st->pinned[j];
+      }
+      hipError_t e = hipMemcpyAsync(dst + off, from, len, hipMemcpyHostToDevice, st->copy);
+      if (e == hipSuccess) e = hipEventRecord(st->pinned_free[j], st->copy);
+      if (e != hipSuccess) return fail(e);
+      st->pinned_used[j] = true;
     }
-    hipError_t e = hipMemcpyAsync(dst + off, from, len, hipMemcpyHostToDevice, st->copy);
-    if (e == hipSuccess) e = hipEventRecord(st->pinned_free[j], st->copy);
-    if (e != hipSuccess) return fail(e);
-    st->pinned_used[j] = true;
+    return stream_after_copy(st, stream);
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }
-  return stream_after_copy(st, stream);
 }
 
 tc_status tc_stage_d2h(tc_stager* st, const void* dev_src, void* host_dst, size_t bytes,
                        int32_t flags, hipStream_t stream) {
-  if (!st || (flags & ~TC_HOST_PINNED)) return TC_ERR_INVALID_ARGUMENT;
-  if (bytes == 0) return TC_OK;
-  if (!host_dst || !dev_src) return TC_ERR_INVALID_ARGUMENT;
-  std::lock_guard<std::mutex> lock(st->mu);
-  tc_status s = same_device(st);
-  if (s == TC_OK) s = copy_after(st, stream);
-  if (s != TC_OK) return s;
-  const uint8_t* src = static_cast<const uint8_t*>(dev_src);
-  uint8_t* dst = static_cast<uint8_t*>(host_dst);
-  const bool pinned = flags & TC_HOST_PINNED;
-  const size_t C = st->slot_bytes, S = st->pinned.size();
-  const size_t chunks = (bytes + C - 1) / C;
-  // Pageable: chunk k lands in slot k % S and is copied out by the host once
-  // its DMA is done; the host drains chunk k - S before chunk k reuses the
-  // slot, so later DMAs stay queued while the host copies.
-  auto drain = [&](size_t k) -> tc_status {
-    const size_t j = k % S, off = k * C, len = std::min(C, bytes - off);
-    tc_status r = fail(hipEventSynchronize(st->pinned_free[j]));
-    if (r != TC_OK) return r;
-    par_copy(st, dst + off, st->pinned[j], len);
+  try {
+    if (!st || (flags & ~TC_HOST_PINNED)) return TC_ERR_INVALID_ARGUMENT;
+    if (bytes == 0) return TC_OK;
+    if (!host_dst || !dev_src) return TC_ERR_INVALID_ARGUMENT;
+    std::lock_guard<std::mutex> lock(st->mu);
+    tc_status s = same_device(st);
+    if (s == TC_OK) s = copy_after(st, stream);
+    if (s != TC_OK) return s;
+    const uint8_t* src = static_cast<const uint8_t*>(dev_src);
+    uint8_t* dst = static_cast<uint8_t*>(host_dst);
+    const bool pinned = flags & TC_HOST_PINNED;
+    const size_t C = st->slot_bytes, S = st->pinned.size();
+    const size_t chunks = (bytes + C - 1) / C;
+    // Pageable: chunk k lands in slot k % S and is copied out by the host once
+    // its DMA is done; the host drains chunk k - S before chunk k reuses the
+    // slot, so later DMAs stay queued while the host copies.
+    auto drain = [&](size_t k) -> tc_status {
+      const size_t j = k % S, off = k * C, len = std::min(C, bytes - off);
+      tc_status r = fail(hipEventSynchronize(st->pinned_free[j]));
+      if (r != TC_OK) return r;
+      par_copy(st, dst + off, st->pinned[j], len);
+      return TC_OK;
+    };
+    for (size_t k = 0; k < chunks; ++k) {
+      const size_t j = k % S, off = k * C, len = std::min(C, bytes - off);
+      if (!pinned && k >= S && (s = drain(k - S)) != TC_OK) return s;
+      if ((s = pace(st, k)) != TC_OK) return s;
+      void* to = pinned ? static_cast<void*>(dst + off) : st->pinned[j];
+      hipError_t e = hipMemcpyAsync(to, src + off, len, hipMemcpyDeviceToHost, st->copy);
+      if (e == hipSuccess) e = hipEventRecord(st->pinned_free[j], st->copy);
+      if (e != hipSuccess) return fail(e);
+      st->pinned_used[j] = true;
+    }
+    if (pinned) return fail(hipStreamSynchronize(st->copy));
+    for (size_t k = chunks > S ? chunks - S : 0; k < chunks; ++k)
+      if ((s = drain(k)) != TC_OK) return s;
     return TC_OK;
-  };
-  for (size_t k = 0; k < chunks; ++k) {
-    const size_t j = k % S, off = k * C, len = std::min(C, bytes - off);
-    if (!pinned && k >= S && (s = drain(k - S)) != TC_OK) return s;
-    if ((s = pace(st, k)) != TC_OK) return s;
-    void* to = pinned ? static_cast<void*>(dst + off) : st->pinned[j];
-    hipError_t e = hipMemcpyAsync(to, src + off, len, hipMemcpyDeviceToHost, st->copy);
-    if (e == hipSuccess) e = hipEventRecord(st->pinned_free[j], st->copy);
-    if (e != hipSuccess) return fail(e);
-    st->pinned_used[j] = true;
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }
-  if (pinned) return fail(hipStreamSynchronize(st->copy));
-  for (size_t k = chunks > S ? chunks - S : 0; k < chunks; ++k)
-    if ((s = drain(k)) != TC_OK) return s;
-  return TC_OK;
 }
 
 tc_status tc_hydrate_from_host(tc_stager* st, const tc_block_pool* pool, const int32_t* ids,
                                int64_t n, const void* host_src, int32_t flags, void* dev_stage,
                                size_t dev_stage_bytes, hipStream_t stream) {
-  if (!st || n < 0 || !pool_shape_ok(pool) || (flags & ~TC_HOST_PINNED))
-    return TC_ERR_INVALID_ARGUMENT;
-  if (n == 0) return TC_OK;
-  if (!ids || !host_src || !dev_stage) return TC_ERR_INVALID_ARGUMENT;
-  const uint64_t per_id = uint64_t(pool->num_regions) * uint64_t(pool->block_bytes);
-  const uint64_t m = std::min<uint64_t>(st->slot_bytes / per_id, uint64_t(n));  // ids per chunk
-  if (m == 0) return TC_ERR_WORKSPACE;
-  const uint64_t chunk = m * per_id;
-  const uint64_t D = std::min<uint64_t>(dev_stage_bytes / chunk, 8);  // device slots
-  if (D == 0) return TC_ERR_WORKSPACE;
-  std::lock_guard<std::mutex> lock(st->mu);
-  tc_status s = same_device(st);
-  if (s == TC_OK && tc_get_validate()) s = check_ids(pool, ids, n, true, stream);
-  if (s == TC_OK) s = ensure_dev_slots(st, D);
-  if (s == TC_OK) s = copy_after(st, stream);
-  if (s != TC_OK) return s;
-  const bool pinned = flags & TC_HOST_PINNED;
-  const size_t S = st->pinned.size();
-  const uint8_t* src = static_cast<const uint8_t*>(host_src);
-  uint8_t* stage = static_cast<uint8_t*>(dev_stage);
-  for (uint64_t k = 0, i0 = 0; i0 < uint64_t(n); ++k, i0 += m) {
-    const uint64_t cnt = std::min<uint64_t>(m, uint64_t(n) - i0), bytes = cnt * per_id;
-    const size_t j = k % S, dj = k % D;
-    const uint8_t* from = src + i0 * per_id;
-    if ((s = pace(st, k)) != TC_OK) return s;
-    if (!pinned) {
-      par_copy(st, st->pinned[j], from, bytes);
-      from = static_cast<const uint8_t*>(st->pinned[j]);
-    }
-    hipError_t e = hipSuccess;
-    if (st->dev_used[dj]) e = hipStreamWaitEvent(st->copy, st->dev_free[dj], 0);
-    if (e == hipSuccess)
-      e = hipMemcpyAsync(stage + dj * chunk, from, bytes, hipMemcpyHostToDevice, st->copy);
-    if (e == hipSuccess) e = hipEventRecord(st->pinned_free[j], st->copy);
-    if (e == hipSuccess) e = hipEventRecord(st->dev_ready[dj], st->copy);
-    if (e == hipSuccess) e = hipStreamWaitEvent(stream, st->dev_ready[dj], 0);
-    if (e != hipSuccess) return fail(e);
-    st->pinned_used[j] = true;
-    s = tc_scatter_blocks(pool, ids + i0, int64_t(cnt), stage + dj * chunk, stream);
+  try {
+    if (!st || n < 0 || !pool_shape_ok(pool) || (flags & ~TC_HOST_PINNED))
+      return TC_ERR_INVALID_ARGUMENT;
+    if (n == 0) return TC_OK;
+    if (!ids || !host_src || !dev_stage) return TC_ERR_INVALID_ARGUMENT;
+    const uint64_t per_id = uint64_t(pool->num_regions) * uint64_t(pool->block_bytes);
+    const uint64_t m = std::min<uint64_t>(st->slot_bytes / per_id, uint64_t(n));  // ids per chunk
+    if (m == 0) return TC_ERR_WORKSPACE;
+    const uint64_t chunk = m * per_id;
+    const uint64_t D = std::min<uint64_t>(dev_stage_bytes / chunk, 8);  // device slots
+    if (D == 0) return TC_ERR_WORKSPACE;
+    std::lock_guard<std::mutex> lock(st->mu);
+    tc_status s = same_device(st);
+    if (s == TC_OK && tc_get_validate()) s = check_ids(pool, ids, n, true, stream);
+    if (s == TC_OK) s = ensure_dev_slots(st, D);
+    if (s == TC_OK) s = copy_after(st, stream);
     if (s != TC_OK) return s;
-    if ((e = hipEventRecord(st->dev_free[dj], stream)) != hipSuccess) return fail(e);
-    st->dev_used[dj] = true;
+    const bool pinned = flags & TC_HOST_PINNED;
+    const size_t S = st->pinned.size();
+    const uint8_t* src = static_cast<const uint8_t*>(host_src);
+    uint8_t* stage = static_cast<uint8_t*>(dev_stage);
+    for (uint64_t k = 0, i0 = 0; i0 < uint64_t(n); ++k, i0 += m) {
+      const uint64_t cnt = std::min<uint64_t>(m, uint64_t(n) - i0), bytes = cnt * per_id;
+      const size_t j = k % S, dj = k % D;
+      const uint8_t* from = src + i0 * per_id;
+      if ((s = pace(st, k)) != TC_OK) return s;
+      if (!pinned) {
+        par_copy(st, st->pinned[j], from, bytes);
+        from = static_cast<const uint8_t*>(st->pinned[j]);
+      }
+      hipError_t e = hipSuccess;
+      if (st->dev_used[dj]) e = hipStreamWaitEvent(st->copy, st->dev_free[dj], 0);
+      if (e == hipSuccess)
+        e = hipMemcpyAsync(stage + dj * chunk, from, bytes, hipMemcpyHostToDevice, st->copy);
+      if (e == hipSuccess) e = hipEventRecord(st->pinned_free[j], st->copy);
+      if (e == hipSuccess) e = hipEventRecord(st->dev_ready[dj], st->copy);
+      if (e == hipSuccess) e = hipStreamWaitEvent(stream, st->dev_ready[dj], 0);
+      if (e != hipSuccess) return fail(e);
+      st->pinned_used[j] = true;
+      s = tc_scatter_blocks(pool, ids + i0, int64_t(cnt), stage + dj * chunk, stream);
+      if (s != TC_OK) return s;
+      if ((e = hipEventRecord(st->dev_free[dj], stream)) != hipSuccess) return fail(e);
+      st->dev_used[dj] = true;
+    }
+    return TC_OK;
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }
-  return TC_OK;
 }
 
 tc_status tc_publish_to_host(tc_stager* st, const tc_block_pool* pool, const int32_t* ids,
                              int64_t n, void* host_dst, int32_t flags, void* dev_stage,
                              size_t dev_stage_bytes, hipStream_t stream) {
-  if (!st || n < 0 || !pool_shape_ok(pool) || (flags & ~TC_HOST_PINNED))
-    return TC_ERR_INVALID_ARGUMENT;
-  if (n == 0) return TC_OK;
-  if (!ids || !host_dst || !dev_stage) return TC_ERR_INVALID_ARGUMENT;
-  const uint64_t per_id = uint64_t(pool->num_regions) * uint64_t(pool->block_bytes);
-  const uint64_t m = std::min<uint64_t>(st->slot_bytes / per_id, uint64_t(n));
-  if (m == 0) return TC_ERR_WORKSPACE;
-  const uint64_t chunk = m * per_id;
-  const uint64_t D = std::min<uint64_t>(dev_stage_bytes / chunk, 8);
-  if (D == 0) return TC_ERR_WORKSPACE;
-  std::lock_guard<std::mutex> lock(st->mu);
-  tc_status s = same_device(st);
-  if (s == TC_OK && tc_get_validate()) s = check_ids(pool, ids, n, false, stream);
-  if (s == TC_OK) s = ensure_dev_slots(st, D);
-  if (s != TC_OK) return s;
-  const bool pinned = flags & TC_HOST_PINNED;
-  const size_t S = st->pinned.size();
-  uint8_t* dst = static_cast<uint8_t*>(host_dst);
-  uint8_t* stage = static_cast<uint8_t*>(dev_stage);
-  const uint64_t chunks = (uint64_t(n) + m - 1) / m;
-  auto chunk_of = [&](uint64_t k, uint64_t* off, uint64_t* bytes) {
-    const uint64_t i0 = k * m, cnt = std::min<uint64_t>(m, uint64_t(n) - i0);
-    *off = i0 * per_id;
-    *bytes = cnt * per_id;
-  };
-  auto drain = [&](uint64_t k) -> tc_status {
-    uint64_t off, bytes;
-    chunk_of(k, &off, &bytes);
-    const size_t j = k % S;
-    tc_status r = fail(hipEventSynchronize(st->pinned_free[j]));
-    if (r != TC_OK) return r;
-    par_copy(st, dst + off, st->pinned[j], bytes);
-    return TC_OK;
-  };
-  for (uint64_t k = 0; k < chunks; ++k) {
-    uint64_t off, bytes;
-    chunk_of(k, &off, &bytes);
-    const size_t j = k % S, dj = k % D;
-    hipError_t e = hipSuccess;
-    if (st->dev_used[dj]) e = hipStreamWaitEvent(stream, st->dev_free[dj], 0);
-    if (e != hipSuccess) return fail(e);
-    s = tc_gather_blocks(pool, ids + k * m, int64_t(bytes / per_id), stage + dj * chunk, stream);
+  try {
+    if (!st || n < 0 || !pool_shape_ok(pool) || (flags & ~TC_HOST_PINNED))
+      return TC_ERR_INVALID_ARGUMENT;
+    if (n == 0) return TC_OK;
+    if (!ids || !host_dst || !dev_stage) return TC_ERR_INVALID_ARGUMENT;
+    const uint64_t per_id = uint64_t(pool->num_regions) * uint64_t(pool->block_bytes);
+    const uint64_t m = std::min<uint64_t>(st->slot_bytes / per_id, uint64_t(n));
+    if (m == 0) return TC_ERR_WORKSPACE;
+    const uint64_t chunk = m * per_id;
+    const uint64_t D = std::min<uint64_t>(dev_stage_bytes / chunk, 8);
+    if (D == 0) return TC_ERR_WORKSPACE;
+    std::lock_guard<std::mutex> lock(st->mu);
+    tc_status s = same_device(st);
+    if (s == TC_OK && tc_get_validate()) s = check_ids(pool, ids, n, false, stream);
+    if (s == TC_OK) s = ensure_dev_slots(st, D);
     if (s != TC_OK) return s;
-    e = hipEventRecord(st->dev_ready[dj], stream);
-    if (e == hipSuccess) e = hipStreamWaitEvent(st->copy, st->dev_ready[dj], 0);
-    if (e != hipSuccess) return fail(e);
-    if (!pinned && k >= S && (s = drain(k - S)) != TC_OK) return s;
-    if ((s = pace(st, k)) != TC_OK) return s;
-    void* to = pinned ? static_cast<void*>(dst + off) : st->pinned[j];
-    e = hipMemcpyAsync(to, stage + dj * chunk, bytes, hipMemcpyDeviceToHost, st->copy);
-    if (e == hipSuccess) e = hipEventRecord(st->pinned_free[j], st->copy);
-    if (e == hipSuccess) e = hipEventRecord(st->dev_free[dj], st->copy);
-    if (e != hipSuccess) return fail(e);
-    st->pinned_used[j] = true;
-    st->dev_used[dj] = true;
+    const bool pinned = flags & TC_HOST_PINNED;
+    const size_t S = st->pinned.size();
+    uint8_t* dst = static_cast<uint8_t*>(host_dst);
+    uint8_t* stage = static_cast<uint8_t*>(dev_stage);
+    const uint64_t chunks = (uint64_t(n) + m - 1) / m;
+    auto chunk_of = [&](uint64_t k, uint64_t* off, uint64_t* bytes) {
+      const uint64_t i0 = k * m, cnt = std::min<uint64_t>(m, uint64_t(n) - i0);
+      *off = i0 * per_id;
+      *bytes = cnt * per_id;
+    };
+    auto drain = [&](uint64_t k) -> tc_status {
+      uint64_t off, bytes;
+      chunk_of(k, &off, &bytes);
+      const size_t j = k % S;
+      tc_status r = fail(hipEventSynchronize(st->pinned_free[j]));
+      if (r != TC_OK) return r;
+      par_copy(st, dst + off, st->pinned[j], bytes);
+      return TC_OK;
+    };
+    for (uint64_t k = 0; k < chunks; ++k) {
+      uint64_t off, bytes;
+      chunk_of(k, &off, &bytes);
+      const size_t j = k % S, dj = k % D;
+      hipError_t e = hipSuccess;
+      if (st->dev_used[dj]) e = hipStreamWaitEvent(stream, st->dev_free[dj], 0);
+      if (e != hipSuccess) return fail(e);
+      s = tc_gather_blocks(pool, ids + k * m, int64_t(bytes / per_id), stage + dj * chunk, stream);
+      if (s != TC_OK) return s;
+      e = hipEventRecord(st->dev_ready[dj], stream);
+      if (e == hipSuccess) e = hipStreamWaitEvent(st->copy, st->dev_ready[dj], 0);
+      if (e != hipSuccess) return fail(e);
+      if (!pinned && k >= S && (s = drain(k - S)) != TC_OK) return s;
+      if ((s = pace(st, k)) != TC_OK) return s;
+      void* to = pinned ? static_cast<void*>(dst + off) : st->pinned[j];
+      e = hipMemcpyAsync(to, stage + dj * chunk, bytes, hipMemcpyDeviceToHost, st->copy);
+      if (e == hipSuccess) e = hipEventRecord(st->pinned_free[j], st->copy);
+      if (e == hipSuccess) e = hipEventRecord(st->dev_free[dj], st->copy);
+      if (e != hipSuccess) return fail(e);
+      st->pinned_used[j] = true;
+      st->dev_used[dj] = true;
+    }
+    if (pinned) return fail(hipStreamSynchronize(st->copy));
+    for (uint64_t k = chunks > S ? chunks - S : 0; k < chunks; ++k)
+      if ((s = drain(k)) != TC_OK) return s;
+    return TC_OK;
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }
-  if (pinned) return fail(hipStreamSynchronize(st->copy));
-  for (uint64_t k = chunks > S ? chunks - S : 0; k < chunks; ++k)
-    if ((s = drain(k)) != TC_OK) return s;
-  return TC_OK;
 }
 
 }  // extern "C"

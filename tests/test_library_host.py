@@ -46,6 +46,20 @@ def test_exports_every_declared_function(lib):
 def test_status_strings(lib):
     assert tc.tc_status_string(0) == "ok"
     assert tc.tc_status_string(5) == "workspace too small"
+    assert tc.tc_status_string(6) == "host memory or threads unavailable"
+
+
+def test_absurd_counts_are_refused_not_wrapped(lib):
+    P = ctypes.c_void_p
+    huge = 1 << 58                       # sizes for this many would not fit size_t
+    assert tc.tc_copy_fragments_workspace(huge) == 0
+    assert tc.tc_copy_fragments_workspace_min(huge) == 0
+    assert tc.tc_cast_fp8_workspace(huge) == 0
+    assert tc.tc_dequant_fp8_workspace(huge) == 0
+    assert lib.tc_cast_fp8_blockscaled(P(16), P(16), P(16), P(16), huge, 128, P(4096), 1 << 20, None) == 1
+    assert lib.tc_dequant_fp8_blockscaled(P(16), P(16), P(16), P(16), huge, 128, P(4096), 1 << 20, None) == 1
+    assert lib.tc_plan_fragments(P(16), huge, P(4096), 1 << 20, None, None) == 1
+    assert lib.tc_copy_fragments(P(16), P(16), P(16), huge, P(4096), 1 << 20, None) == 1
 
 
 def test_argument_errors_need_no_gpu(lib):
