@@ -1,0 +1,36 @@
+"""Compile abi_demo.c with the host C compiler against libtchip.so.
+
+The program includes only tensorcast_hip.h and the HIP runtime API header,
+and links the library and the HIP runtime: nothing from Python or torch.
+"""
+import os
+import shutil
+import subprocess
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(os.path.dirname(HERE))
+LIBDIR = os.path.join(ROOT, "paper_2608_06007_amd")
+EXE = os.path.join(HERE, "abi_demo")
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
+
+
+def build(verbose: bool = False) -> str:
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        raise RuntimeError("no host C compiler for the C ABI demo")
+    cmd = [cc, "-std=c99", "-O2", "-Wall", "-Werror", "-D__HIP_PLATFORM_AMD__",
+           f"-I{os.path.join(ROOT, 'include')}", f"-I{os.path.join(ROCM, 'include')}",
+           os.path.join(HERE, "abi_demo.c"), "-o", EXE + ".tmp",
+           f"-L{LIBDIR}", "-ltchip", "-Wl,-rpath,$ORIGIN/../../paper_2608_06007_amd",
+           f"-L{os.path.join(ROCM, 'lib')}", "-lamdhip64", f"-Wl,-rpath,{os.path.join(ROCM, 'lib')}"]
+    if verbose:
+        print(" ".join(cmd))
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"C ABI demo failed to build:\n{r.stderr}")
+    os.replace(EXE + ".tmp", EXE)
+    return EXE
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

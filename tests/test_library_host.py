@@ -252,6 +252,27 @@ def test_header_compiles_as_plain_c(tmp_path):
     assert r.returncode == 0, r.stderr
 
 
+def test_c_program_links_against_the_library(tmp_path):
+    """tests/c_abi/abi_demo.c builds with a plain C compiler and every library
+    symbol it calls resolves at link time (running it needs a GPU)."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no C compiler")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    libdir = os.path.join(root, "paper_2608_06007_amd")
+    exe = tmp_path / "abi_demo"
+    r = subprocess.run([gcc, "-std=c99", "-O1", "-Wall", "-Werror", "-D__HIP_PLATFORM_AMD__",
+                        f"-I{os.path.dirname(HEADER)}", "-I/opt/rocm/include",
+                        os.path.join(root, "tests", "c_abi", "abi_demo.c"), "-o", str(exe),
+                        f"-L{libdir}", "-ltchip", "-L/opt/rocm/lib", "-lamdhip64",
+                        "-Wl,--no-undefined", "-Wl,--no-allow-shlib-undefined"],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    assert exe.exists()
+
+
 # Dimensions that are multiples of 128 x tp for tp up to 8, small enough for the oracle.
 SPEC_TILED = synth.spec_scaled(layers=1, hidden=1024, q_heads=8, kv_heads=8, head_dim=128, mlp=2048)
 
