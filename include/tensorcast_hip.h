@@ -116,15 +116,18 @@ typedef struct {
 
 /* Recommended bytes of device workspace for a plan of n descriptors.  A
  * plan cuts every fragment into tasks of at most `piece` bytes (1 KiB, or the
- * next power of two that keeps the task table inside the workspace) and
- * spreads the tasks over the whole GPU, one task per wave.  Any workspace
- * holding at least n + 1 tasks works (32 bytes each: the packed task and its
- * digest slot, plus 16 bytes per descriptor of planning scratch); this size
- * keeps 1 KiB pieces for payloads up to ~3 KiB per fragment plus 8 GiB.  Offsets plus lengths must stay
- * below 2^48. */
+ * next power of two, at most 2^30, that keeps the task table inside the
+ * workspace) and spreads the tasks over the whole GPU, one task per wave.  A
+ * task costs 32 bytes (the packed task and its digest slot) plus 16 bytes per
+ * 1024 tasks; a descriptor costs at most ~48 bytes of planning scratch.  A
+ * workspace with room for T >= n + 1 tasks accepts payloads up to
+ * (T - n) * 2^30 bytes (beyond that the plan returns TC_ERR_WORKSPACE); this
+ * size has room for 4n + 2^23 tasks, which keeps 1 KiB pieces for payloads
+ * up to ~3 KiB per fragment plus 8 GiB.  Offsets plus lengths must stay below
+ * 2^48. */
 size_t tc_copy_fragments_workspace(int64_t n); /* 0 for n < 0 or n > 2^40 */
 /* Smallest workspace a plan of n descriptors accepts (room for n + 1 tasks;
- * the task size then grows to fit). */
+ * the task size then grows to fit, so payloads up to 2^30 bytes always fit). */
 size_t tc_copy_fragments_workspace_min(int64_t n);
 
 /* Copy every fragment: tc_plan_fragments + tc_copy_planned.  frags: device

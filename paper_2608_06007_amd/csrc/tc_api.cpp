@@ -441,8 +441,8 @@ tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace
       // by n + payload / piece <= capacity.
       const uint64_t room = L.capacity - uint64_t(n);
       piece = pow2_at_least(std::max<uint64_t>(tc::kMinPiece, (hdr.payload + room - 1) / room));
-      // a task's length is stored in 32 bits
-      piece = std::min<uint64_t>(piece, uint64_t(1) << 31);
+      // a task's length is stored in 31 bits
+      piece = std::min<uint64_t>(piece, tc::kMaxPiece);
     }
     if (hdr.total_tasks > L.capacity) return TC_ERR_WORKSPACE;
     // Long lists with scattered destinations are planned in destination order
@@ -495,8 +495,7 @@ tc_status tc_copy_planned(const void* src_base, void* dst_base, const void* work
       std::vector<tc_fragment> tasks(packed.size());
       for (size_t i = 0; i < packed.size(); ++i) {
         const tc::Task& t = packed[i];
-        tasks[i] = tc_fragment{t.lo & (tc::kOffsetLimit - 1),
-                               (t.lo >> 48) | ((t.hi & 0xFFFFFFFFu) << 16), t.hi >> 32};
+        tasks[i] = tc_fragment{tc::task_src(t), tc::task_dst(t), tc::task_len(t)};
       }
       st = check_ranges(src_base, dst_base, tasks);
       if (st != TC_OK) return st;
@@ -551,8 +550,7 @@ tc_status tc_copy_planned_digest(const void* src_base, void* dst_base, void* wor
       std::vector<tc_fragment> tasks(packed.size());
       for (size_t i = 0; i < packed.size(); ++i) {
         const tc::Task& t = packed[i];
-        tasks[i] = tc_fragment{t.lo & (tc::kOffsetLimit - 1),
-                               (t.lo >> 48) | ((t.hi & 0xFFFFFFFFu) << 16), t.hi >> 32};
+        tasks[i] = tc_fragment{tc::task_src(t), tc::task_dst(t), tc::task_len(t)};
       }
       st = check_ranges(src_base, dst_base, tasks);
       if (st != TC_OK) return st;

@@ -10,8 +10,10 @@ namespace tc {
 
 // Fragment plans cut fragments into tasks of at most `piece` bytes, one task
 // per wave (64 lanes x 16 B = 1 KiB per pass); the piece is the smallest
-// power of two >= kMinPiece that keeps the task table within the workspace.
+// power of two >= kMinPiece that keeps the task table within the workspace,
+// at most kMaxPiece.
 constexpr uint64_t kMinPiece = 1024;
+constexpr uint64_t kMaxPiece = uint64_t(1) << 30;
 // Descriptors handled by one workgroup of the planning kernels.
 constexpr int kPlanPerBlock = 1024;
 
@@ -20,13 +22,20 @@ struct RegionTable {
 };
 
 // One task of a fragment plan, a byte run of at most `piece` bytes, packed in
-// 16 bytes: src_off (48 bits) | dst_off (48 bits) | len (32 bits).  Offsets
-// must stay below 2^48 (256 TiB).
+// 16 bytes: src_off (48 bits) | dst_off (48 bits) | len (31 bits) | a flag
+// set on the first task of each fragment.  Offsets must stay below 2^48
+// (256 TiB).
 struct Task {
   uint64_t lo;  // src_off | dst_off << 48
-  uint64_t hi;  // dst_off >> 16 | len << 32
+  uint64_t hi;  // dst_off >> 16 | len << 32 | first << 63
 };
 constexpr uint64_t kOffsetLimit = uint64_t(1) << 48;
+constexpr uint64_t kTaskFirst = uint64_t(1) << 63;
+__host__ __device__ inline uint64_t task_src(const Task& t) { return t.lo & (kOffsetLimit - 1); }
+__host__ __device__ inline uint64_t task_dst(const Task& t) {
+  return (t.lo >> 48) | ((t.hi & 0xFFFFFFFFu) << 16);
+}
+__host__ __device__ inline uint64_t task_len(const Task& t) { return (t.hi >> 32) & 0x7FFFFFFFu; }
 
 // Header at the start of a fragment-plan workspace.
 struct PlanHeader {
@@ -40,18 +49,22 @@ struct PlanHeader {
   uint64_t permuted;       // the tasks follow the reordered list; perm maps back
 };
 
-// Workspace layout: header | tasks[capacity] | digest slots[capacity] | ... |
-// tstart[n + 1] | block sums | [reordered fragments | perm | buckets].  The
-// task table sits at a fixed offset so a copy needs only the workspace base;
-// the planning scratch lives at the end and stays valid with the plan (the
-// digest reduction reads tstart and perm).
+// Workspace layout: header | tasks[capacity] | digest slots[capacity] |
+// windows[ceil(capacity / 1024)] | ... | tstart[n + 1] | block sums |
+// [reordered fragments | perm | buckets].  The task table sits at a fixed
+// offset so a copy needs only the workspace base; windows[j] holds the first
+// and last fragment of tasks [1024 j, 1024 (j + 1)), written by the plan's
+// expansion.  The planning scratch lives at the end and stays valid with the
+// plan (the digest reduction reads tstart, windows and perm).
 constexpr size_t kTasksOffset = 256;
 constexpr size_t kTaskBytes = 32;  // a task and its 16-byte digest slot
+constexpr uint64_t kWindowTasks = 1024;  // tasks per window of the expansion and the reduction
+constexpr size_t kWindowBytes = 16;      // first and last fragment of a window
 // Lists of at least this many fragments whose destinations are not in
 // ascending order are planned in destination order (bucketed by address).
 constexpr int64_t kReorderMin = 4096;
 struct PlanLayout {
-  size_t tstart, blocks, capacity, slots;
+  size_t tstart, blocks, capacity, slots, windows;
   size_t sorted, perm, buckets, bucket_sums;  // valid when nbuckets > 0
   uint64_t nbuckets;                          // bucket capacity (0: no reordering)
 };

@@ -266,21 +266,23 @@ __device__ int64_t wave_find(const uint64_t* __restrict__ tstart, int64_t lo, in
   return lo;
 }
 
-__device__ __forceinline__ Task pack_task(uint64_t src, uint64_t dst, uint64_t len) {
-  return Task{src | (dst << 48), (dst >> 16) | (len << 32)};
+__device__ __forceinline__ Task pack_task(uint64_t src, uint64_t dst, uint64_t len, bool first) {
+  return Task{src | (dst << 48), (dst >> 16) | (len << 32) | (first ? kTaskFirst : 0)};
 }
 
-constexpr int kExpandPerBlock = 1024;  // tasks written by one workgroup
+constexpr int kExpandPerBlock = int(kWindowTasks);  // tasks written by one workgroup
 
 // Block j writes tasks [j * 1024, (j + 1) * 1024).  Wave 0 finds the first
-// and last task's fragments; if they span at most 1024 fragments their
-// tstart entries go to LDS and every task finds its fragment there,
-// otherwise (long runs of empty fragments) each task searches globally.
+// and last task's fragments and records them in windows[j]; if they span at
+// most 1024 fragments their tstart entries go to LDS and every task finds its
+// fragment there, otherwise (long runs of empty fragments) each task searches
+// globally.
 __global__ __launch_bounds__(kThreads) void k_plan_expand(const tc_fragment* __restrict__ frags,
                                                          const int64_t n,
                                                          const uint64_t* __restrict__ tstart,
                                                          const uint64_t total, const uint64_t piece,
-                                                         Task* __restrict__ tasks) {
+                                                         Task* __restrict__ tasks,
+                                                         int64_t* __restrict__ windows) {
   __shared__ uint64_t win[kExpandPerBlock + 1];
   __shared__ int64_t range[2];
   const int lane = threadIdx.x & (kWaveLanes - 1);
@@ -292,6 +294,8 @@ __global__ __launch_bounds__(kThreads) void k_plan_expand(const tc_fragment* __r
     if (lane == 0) {
       range[0] = f0;
       range[1] = f1;
+      windows[2 * uint64_t(blockIdx.x)] = f0;
+      windows[2 * uint64_t(blockIdx.x) + 1] = f1;
     }
   }
   __syncthreads();
@@ -331,7 +335,7 @@ __global__ __launch_bounds__(kThreads) void k_plan_expand(const tc_fragment* __r
     const tc_fragment f = frags[lo];
     const uint64_t off = (t - start) * piece;
     const uint64_t rem = f.len - off;
-    tasks[t] = pack_task(f.src_off + off, f.dst_off + off, rem < piece ? rem : piece);
+    tasks[t] = pack_task(f.src_off + off, f.dst_off + off, rem < piece ? rem : piece, off == 0);
   }
 }
 
@@ -352,9 +356,9 @@ __global__ __launch_bounds__(kThreads) void k_copy_tasks(const uint8_t* __restri
     const uint64_t t = xcd_grouped(b, nblocks, kXcdGroup) * kTasksPerBlock + w;
     if (t >= total) continue;
     const Task tk = tasks[t];
-    const uint8_t* s = src + (tk.lo & (kOffsetLimit - 1));
-    uint8_t* d = dst + ((tk.lo >> 48) | ((tk.hi & 0xFFFFFFFFu) << 16));
-    uint64_t len = tk.hi >> 32;
+    const uint8_t* s = src + task_src(tk);
+    uint8_t* d = dst + task_dst(tk);
+    uint64_t len = task_len(tk);
     const uintptr_t sa = reinterpret_cast<uintptr_t>(s), da = reinterpret_cast<uintptr_t>(d);
     if (((sa ^ da) & 15) == 0) {
       // byte head up to 16-byte alignment, 16-byte body, byte tail
@@ -564,16 +568,56 @@ __global__ __launch_bounds__(kThreads) void k_copy_digest(const uint8_t* __restr
     for (int k = 0; k < kPerWave; ++k) tk[k] = tasks[min(t0 + k, total - 1)];  // one scalar load
 #pragma unroll
     for (int k = 0; k < kPerWave; ++k) {
-      const uint64_t so = tk[k].lo & (kOffsetLimit - 1);
-      const uint64_t dof = (tk[k].lo >> 48) | ((tk[k].hi & 0xFFFFFFFFu) << 16);
+      const uint64_t so = task_src(tk[k]);
+      const uint64_t dof = task_dst(tk[k]);
       s[k] = src + (kMode == kDigestDst ? dof : so);
       d[k] = kMode == kCopyDigest ? dst + dof : nullptr;
-      len[k] = t0 + k < total ? tk[k].hi >> 32 : 0;
+      len[k] = t0 + k < total ? task_len(tk[k]) : 0;
       const uintptr_t sa = reinterpret_cast<uintptr_t>(s[k]);
       const uintptr_t al = kMode == kCopyDigest ? (sa | reinterpret_cast<uintptr_t>(d[k])) & 15 : sa & 15;
       pre[k] = al == 0 && len[k] <= uint64_t(kWaveLanes) * 16 + 15;
       v[k] = u32x4{0, 0, 0, 0};
       if (pre[k] && uint64_t(lane) < (len[k] >> 4)) v[k] = ld_nt(reinterpret_cast<const u32x4*>(s[k]) + lane);
+    }
+    // The group is one run of a fragment when no task after the first starts
+    // a fragment, every task is one aligned vector per lane and all but the
+    // last are full 1 KiB pieces.  Its bytes then sit at positions below
+    // kPerWave * 1024 <= 4096 from the first task's start, so the run's two
+    // sums are exact in 32 bits and one wave reduction serves the group: the
+    // first task's slot takes the run's sums and the others zeros, which the
+    // reduction by fragment adds up to the same digest.
+    bool run = t0 + kPerWave <= total;
+#pragma unroll
+    for (int k = 0; k < kPerWave; ++k) {
+      run = run && pre[k] && (k == 0 || (tk[k].hi & kTaskFirst) == 0) &&
+            (k == kPerWave - 1 || len[k] == uint64_t(kWaveLanes) * 16);
+    }
+    if (run) {
+      uint32_t a = 0, ws = 0;
+#pragma unroll
+      for (int k = 0; k < kPerWave; ++k) {
+        if (uint64_t(lane) < (len[k] >> 4)) {
+          if (kMode == kCopyDigest) st_sc1_nt(reinterpret_cast<u32x4*>(d[k]) + lane, v[k]);
+          uint32_t vs, vw;
+          vec_sums(v[k], &vs, &vw);
+          a += vs;
+          ws += uint32_t(k * kWaveLanes * 16 + lane * 16) * vs + vw;
+        }
+      }
+      constexpr int kLast = kPerWave - 1;
+      const uint64_t body_end = (len[kLast] >> 4) << 4;
+      if (uint64_t(lane) < len[kLast] - body_end) {
+        const uint8_t x = s[kLast][body_end + lane];
+        if (kMode == kCopyDigest) d[kLast][body_end + lane] = x;
+        a += x;
+        ws += uint32_t(kLast * kWaveLanes * 16 + body_end + lane) * x;
+      }
+      const uint32_t ta = wave_sum32_lane63(a), tw = wave_sum32_lane63(ws);
+      if (lane == kWaveLanes - 1)
+        slots[t0] = u64x2{ta, uint64_t(tw) + ta};
+      else if (lane >= kWaveLanes - kPerWave)
+        slots[t0 + (kWaveLanes - 1 - lane)] = u64x2{0, 0};
+      continue;
     }
 #pragma unroll
     for (int k = 0; k < kPerWave; ++k) {
@@ -592,32 +636,33 @@ __global__ __launch_bounds__(kThreads) void k_fill_zero(uint64_t* __restrict__ p
 }
 
 // Reduce-by-fragment of the task slots.  Block j owns tasks
-// [j * 1024, (j + 1) * 1024) and finds their fragments as k_plan_expand does.
-// A fragment whose tasks all lie in the block is written with a plain store;
-// one that crosses the block's edges (at most the first and the last) is
-// added atomically into the zeroed digest.
+// [j * 1024, (j + 1) * 1024), whose first and last fragment the plan recorded
+// in windows[j]; each thread takes four consecutive tasks, whose slots it
+// loads first, and adds them per fragment in registers.  A fragment whose tasks
+// all lie in the block is written with a plain store; one that crosses the
+// block's edges (at most the first and the last) is added atomically into the
+// zeroed digest.
+constexpr int kReducePerThread = kExpandPerBlock / kThreads;
+static_assert(kReducePerThread * kThreads == kExpandPerBlock, "whole tasks per thread");
+
 __global__ __launch_bounds__(kThreads) void k_digest_reduce(const uint64_t* __restrict__ tstart,
-                                                           const int64_t n, const uint64_t total,
+                                                           const uint64_t total,
                                                            const PlanHeader* __restrict__ hdr,
                                                            const uint64_t* __restrict__ perm,
                                                            const u64x2* __restrict__ slots,
+                                                           const int64_t* __restrict__ windows,
                                                            uint64_t* __restrict__ digests) {
   __shared__ uint64_t win[kExpandPerBlock + 1];
   __shared__ uint64_t acc[2 * kExpandPerBlock];
-  __shared__ int64_t range[2];
-  const int lane = threadIdx.x & (kWaveLanes - 1);
   const uint64_t t0 = uint64_t(blockIdx.x) * kExpandPerBlock;
   const uint64_t t1 = min(total, t0 + kExpandPerBlock);
-  if (threadIdx.x < kWaveLanes) {
-    const int64_t f0 = wave_find(tstart, 0, n, t0, lane);
-    const int64_t f1 = wave_find(tstart, f0, n, t1 - 1, lane);
-    if (lane == 0) {
-      range[0] = f0;
-      range[1] = f1;
-    }
-  }
-  __syncthreads();
-  const int64_t f0 = range[0], f1 = range[1];
+  const uint64_t tb = t0 + uint64_t(threadIdx.x) * kReducePerThread;
+  u64x2 p[kReducePerThread];
+#pragma unroll
+  for (int j = 0; j < kReducePerThread; ++j)
+    p[j] = tb + j < t1 ? slots[tb + j] : u64x2{0, 0};
+  const int64_t f0 = windows[2 * uint64_t(blockIdx.x)];
+  const int64_t f1 = windows[2 * uint64_t(blockIdx.x) + 1];
   const int64_t span = f1 - f0 + 1;
   const bool local = span <= kExpandPerBlock;
   const uint64_t piece = hdr->piece;
@@ -628,23 +673,46 @@ __global__ __launch_bounds__(kThreads) void k_digest_reduce(const uint64_t* __re
     for (int64_t k = threadIdx.x; k < 2 * span; k += kThreads) acc[k] = 0;
   }
   __syncthreads();
-  for (uint64_t t = t0 + threadIdx.x; t < t1; t += kThreads) {
-    int64_t lo, hi;
-    uint64_t start;
-    if (local) {
-      lo = 0;
-      hi = span;
+  if (local) {
+    if (tb < t1) {
+      // fragment of the first task: win[lo] <= tb < win[hi], relative to f0
+      int64_t lo = 0, hi = span;
       while (hi - lo > 1) {
         const int64_t mid = (lo + hi) >> 1;
-        if (win[mid] <= t)
+        if (win[mid] <= tb)
           lo = mid;
         else
           hi = mid;
       }
-      start = win[lo];
-    } else {
-      lo = f0;
-      hi = f1 + 1;
+      uint64_t s1 = 0, s2 = 0;
+#pragma unroll
+      for (int j = 0; j < kReducePerThread; ++j) {
+        const uint64_t t = tb + j;
+        if (t >= t1) break;
+        // win[span] > t1 - 1 >= t, so lo stays below span
+        while (win[lo + 1] <= t) {
+          if (s1 | s2) {
+            atomicAdd(reinterpret_cast<unsigned long long*>(&acc[2 * lo]), (unsigned long long)s1);
+            atomicAdd(reinterpret_cast<unsigned long long*>(&acc[2 * lo + 1]), (unsigned long long)s2);
+          }
+          s1 = s2 = 0;
+          ++lo;
+        }
+        s1 += p[j].x;
+        s2 += p[j].y + (t - win[lo]) * piece * p[j].x;
+      }
+      if (s1 | s2) {
+        atomicAdd(reinterpret_cast<unsigned long long*>(&acc[2 * lo]), (unsigned long long)s1);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&acc[2 * lo + 1]), (unsigned long long)s2);
+      }
+    }
+  } else {
+    // long runs of empty fragments: each task searches the global table
+#pragma unroll
+    for (int j = 0; j < kReducePerThread; ++j) {
+      const uint64_t t = tb + j;
+      if (t >= t1) break;
+      int64_t lo = f0, hi = f1 + 1;
       while (hi - lo > 1) {
         const int64_t mid = (lo + hi) >> 1;
         if (tstart[mid] <= t)
@@ -652,20 +720,13 @@ __global__ __launch_bounds__(kThreads) void k_digest_reduce(const uint64_t* __re
         else
           hi = mid;
       }
-      start = tstart[lo];
-    }
-    const u64x2 p = slots[t];
-    const uint64_t s2 = p.y + (t - start) * piece * p.x;
-    if (local) {
-      atomicAdd(reinterpret_cast<unsigned long long*>(&acc[2 * lo]), (unsigned long long)p.x);
-      atomicAdd(reinterpret_cast<unsigned long long*>(&acc[2 * lo + 1]), (unsigned long long)s2);
-    } else {
+      const uint64_t s2 = p[j].y + (t - tstart[lo]) * piece * p[j].x;
       const uint64_t o = mapped ? perm[lo] : uint64_t(lo);
-      atomicAdd(reinterpret_cast<unsigned long long*>(&digests[2 * o]), (unsigned long long)p.x);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&digests[2 * o]), (unsigned long long)p[j].x);
       atomicAdd(reinterpret_cast<unsigned long long*>(&digests[2 * o + 1]), (unsigned long long)s2);
     }
+    return;
   }
-  if (!local) return;
   __syncthreads();
   for (int64_t k = threadIdx.x; k < span; k += kThreads) {
     uint64_t* out = digests + 2 * (mapped ? perm[f0 + k] : uint64_t(f0 + k));
@@ -818,6 +879,11 @@ static size_t plan_tail_bytes(int64_t n) {
   return t;
 }
 
+// Bytes of the task table, digest slots and window entries for cap tasks.
+static size_t task_area_bytes(size_t cap) {
+  return kTaskBytes * cap + kWindowBytes * ((cap + kWindowTasks - 1) / kWindowTasks);
+}
+
 PlanLayout plan_layout(int64_t n, size_t ws_bytes) {
   PlanLayout L;
   const size_t tail = plan_tail_bytes(n);
@@ -829,21 +895,26 @@ PlanLayout plan_layout(int64_t n, size_t ws_bytes) {
   L.perm = L.sorted + align256(sizeof(tc_fragment) * size_t(n));
   L.buckets = L.perm + align256(8 * size_t(n));
   L.bucket_sums = L.buckets + align256(8 * L.nbuckets);
-  // every task has a 16-byte digest slot after the task table
-  L.capacity = start > kTasksOffset ? (start - kTasksOffset) / kTaskBytes : 0;
-  L.slots = kTasksOffset + L.capacity * sizeof(Task);
+  // every task has a 16-byte digest slot after the task table, and every
+  // 1024 tasks a window entry after the slots
+  const size_t avail = start > kTasksOffset ? start - kTasksOffset : 0;
+  size_t cap = avail / (kTaskBytes * kWindowTasks + kWindowBytes) * kWindowTasks;
+  while (task_area_bytes(cap + 1) <= avail) ++cap;
+  L.capacity = cap;
+  L.slots = kTasksOffset + cap * sizeof(Task);
+  L.windows = kTasksOffset + cap * kTaskBytes;
   return L;
 }
 
 // Room for 4n + 2^23 tasks: pieces stay at 1 KiB while the payload is below
 // ~3 KiB per fragment plus 8 GiB.
 size_t frag_workspace_bytes(int64_t n) {
-  return kTasksOffset + kTaskBytes * (4 * size_t(n) + (size_t(1) << 23)) + plan_tail_bytes(n) +
+  return kTasksOffset + task_area_bytes(4 * size_t(n) + (size_t(1) << 23)) + plan_tail_bytes(n) +
          256;
 }
 
 size_t frag_workspace_min_bytes(int64_t n) {
-  return kTasksOffset + kTaskBytes * (size_t(n) + 1) + plan_tail_bytes(n) + 256;
+  return kTasksOffset + task_area_bytes(size_t(n) + 1) + plan_tail_bytes(n) + 256;
 }
 
 hipError_t launch_plan_count(const tc_fragment* frags, int64_t n, uint64_t piece, void* ws,
@@ -897,8 +968,9 @@ hipError_t launch_plan_expand(const tc_fragment* frags, int64_t n, uint64_t tota
   const uint64_t* tstart = reinterpret_cast<const uint64_t*>(base + L.tstart);
   Task* tasks = reinterpret_cast<Task*>(base + kTasksOffset);
   const uint64_t grid = (total + kExpandPerBlock - 1) / kExpandPerBlock;
+  int64_t* windows = reinterpret_cast<int64_t*>(base + L.windows);
   hipLaunchKernelGGL(k_plan_expand, dim3((unsigned)grid), dim3(kThreads), 0, s, frags, n, tstart,
-                     total, piece, tasks);
+                     total, piece, tasks, windows);
   return hipGetLastError();
 }
 
@@ -946,10 +1018,11 @@ hipError_t launch_copy_digest(const uint8_t* src, uint8_t* dst, void* ws, const 
                        slots, total, nblocks, digests, words);
   const uint64_t rgrid = (total + kExpandPerBlock - 1) / kExpandPerBlock;
   hipLaunchKernelGGL(k_digest_reduce, dim3((unsigned)rgrid), dim3(kThreads), 0, s,
-                     reinterpret_cast<const uint64_t*>(base + L.tstart), n, total,
+                     reinterpret_cast<const uint64_t*>(base + L.tstart), total,
                      reinterpret_cast<const PlanHeader*>(base),
                      L.nbuckets ? reinterpret_cast<const uint64_t*>(base + L.perm) : nullptr,
-                     (const u64x2*)slots, digests);
+                     (const u64x2*)slots, reinterpret_cast<const int64_t*>(base + L.windows),
+                     digests);
   return hipGetLastError();
 }
 

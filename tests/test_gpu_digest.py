@@ -2,8 +2,8 @@
 
 The copy-with-digest and digest-only entry points against the oracle's
 per-fragment digests and its copy, on the same seeded inputs: storms
-(aligned and byte-granular), empty fragments, fragments spanning many
-reduction windows, long runs of empty descriptors, plans with pieces larger
+(aligned and byte-granular), empty fragments, fragments laid back to back,
+fragments spanning many reduction windows, long runs of empty descriptors, plans with pieces larger
 than 1 KiB, and the full-size cross-layout shard copy.
 """
 import numpy as np
@@ -104,6 +104,30 @@ def test_digest_long_runs_of_empty_descriptors():
     rows += [(7, 7, 0)] * 3000
     rows += [(2 << 20, 2 << 20, 700 << 10), (3 << 20, 3 << 20, 3)]
     _check(src, np.array(rows, dtype=np.uint64), 4 << 20)
+
+
+def _back_to_back(n, seed, reverse_dst):
+    """n fragments of 1-8 KiB, some ragged, laid end to end in the source and
+    in the destination (in reverse order when reverse_dst), so consecutive
+    tasks of different fragments are contiguous on the side being summed."""
+    rng = np.random.default_rng(seed)
+    lens = 1024 * rng.integers(1, 9, size=n) + rng.choice([0, 0, 0, 16, 5, 1000 - 1024], size=n)
+    src = np.concatenate([[0], np.cumsum(lens)[:-1]])
+    order = np.arange(n)[::-1] if reverse_dst else np.arange(n)
+    dst = np.empty(n, dtype=np.int64)
+    dst[order] = np.concatenate([[0], np.cumsum(lens[order])[:-1]])
+    return np.stack([src, dst, lens], axis=1).astype(np.uint64), int(lens.sum())
+
+
+@pytest.mark.parametrize("n,reverse_dst", [(2000, False), (5000, True)])
+def test_digest_adjacent_fragments_stay_separate(n, reverse_dst):
+    """Tasks summed as one run must belong to one fragment: with fragments
+    back to back, a group of consecutive tasks crossing a fragment boundary
+    covers contiguous bytes, and only the fragment boundary keeps the two
+    digests apart.  5000 fragments with descending destinations take the
+    destination-ordered plan."""
+    frags, payload = _back_to_back(n, 81 + n, reverse_dst)
+    _check(synth.random_bytes(payload, 82, device=DEV), frags, payload)
 
 
 @pytest.mark.parametrize("extra_tasks", [1, 300])
