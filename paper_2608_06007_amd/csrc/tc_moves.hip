@@ -34,10 +34,11 @@ __device__ __forceinline__ uint64_t xcd_grouped(uint64_t b, uint64_t N, uint64_t
 
 __device__ __forceinline__ u32x4 ld_nt(const u32x4* p) { return __builtin_nontemporal_load(p); }
 // Vector stores with the SC1 scope bit, alone (gather's contiguous output) or
-// with NT (hydrate's scattered blocks, planned task copies): measured +1-4%
-// over plain non-temporal stores on those streams.  (For a storm of small
-// random fragments plain NT stores are ~10% faster; the shard and expert
-// copies, which matter more, prefer SC1 NT.)
+// with NT (hydrate's scattered blocks, planned copies of ordered lists):
+// measured +1-4% over plain non-temporal stores on those streams.  Plans
+// built from unordered destination lists (small fragments with scattered
+// sources, copied in destination order) store with plain NT: +8% there.
+__device__ __forceinline__ void st_nt(u32x4* p, u32x4 v) { __builtin_nontemporal_store(v, p); }
 __device__ __forceinline__ void st_sc1(u32x4* p, u32x4 v) {
   asm volatile("global_store_dwordx4 %0, %1, off sc1" ::"v"(p), "v"(v) : "memory");
 }
@@ -347,11 +348,13 @@ constexpr int kTasksPerBlock = kThreads / kWaveLanes;
 
 __global__ __launch_bounds__(kThreads) void k_copy_tasks(const uint8_t* __restrict__ src,
                                                         uint8_t* __restrict__ dst,
+                                                        const PlanHeader* __restrict__ hdr,
                                                         const Task* __restrict__ tasks,
                                                         const uint64_t total,
                                                         const uint64_t nblocks) {
   const int lane = threadIdx.x & (kWaveLanes - 1);
   const uint64_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const bool reordered = hdr->permuted != 0;
   for (uint64_t b = blockIdx.x; b < nblocks; b += gridDim.x) {
     const uint64_t t = xcd_grouped(b, nblocks, kXcdGroup) * kTasksPerBlock + w;
     if (t >= total) continue;
@@ -371,7 +374,10 @@ __global__ __launch_bounds__(kThreads) void k_copy_tasks(const uint8_t* __restri
       const uint64_t n16 = len >> 4;
       const u32x4* sv = reinterpret_cast<const u32x4*>(s);
       u32x4* dv = reinterpret_cast<u32x4*>(d);
-      for (uint64_t i = lane; i < n16; i += kWaveLanes) st_sc1_nt(dv + i, ld_nt(sv + i));
+      if (reordered)
+        for (uint64_t i = lane; i < n16; i += kWaveLanes) st_nt(dv + i, ld_nt(sv + i));
+      else
+        for (uint64_t i = lane; i < n16; i += kWaveLanes) st_sc1_nt(dv + i, ld_nt(sv + i));
       const uint64_t tail = len & 15;
       if (uint64_t(lane) < tail) d[(n16 << 4) + lane] = s[(n16 << 4) + lane];
     } else {
@@ -979,8 +985,8 @@ hipError_t launch_copy_tasks(const uint8_t* src, uint8_t* dst, const void* ws, u
   if (total == 0) return hipSuccess;
   const Task* tasks = reinterpret_cast<const Task*>(static_cast<const uint8_t*>(ws) + kTasksOffset);
   const uint64_t nblocks = (total + kTasksPerBlock - 1) / kTasksPerBlock;
-  hipLaunchKernelGGL(k_copy_tasks, dim3(grid_for(nblocks)), dim3(kThreads), 0, s, src, dst, tasks,
-                     total, nblocks);
+  hipLaunchKernelGGL(k_copy_tasks, dim3(grid_for(nblocks)), dim3(kThreads), 0, s, src, dst,
+                     static_cast<const PlanHeader*>(ws), tasks, total, nblocks);
   return hipGetLastError();
 }
 
