@@ -255,7 +255,8 @@ bool reshard_ok(const tc_reshard_view& v, int32_t dst_tp, int32_t dst_rank) {
 }
 
 // Fragments that fill the destination rank's slice from the overlapping
-// source slices.
+// source slices, in ascending destination order (so a plan keeps the list's
+// order and the copy writes the slice front to back).
 template <typename Emit>
 void reshard_fragments(const tc_reshard_view& v, int32_t dst_tp, int32_t d, Emit emit) {
   if (v.rows == 0 || v.cols == 0) return;
@@ -268,21 +269,26 @@ void reshard_fragments(const tc_reshard_view& v, int32_t dst_tp, int32_t d, Emit
   const int64_t extent = by_rows ? v.rows : v.cols;
   const int64_t ns = extent / v.src_tp, nd = extent / dst_tp;  // slice widths
   const int64_t d0 = int64_t(d) * nd, d1 = d0 + nd;
-  for (int64_t s = d0 / ns; s <= (d1 - 1) / ns; ++s) {
-    const int64_t a = std::max(d0, s * ns), b = std::min(d1, (s + 1) * ns);
-    if (by_rows) {
-      const uint64_t row = uint64_t(v.cols) * eb;
+  const int64_t s0 = d0 / ns, s1 = (d1 - 1) / ns;  // overlapping source slices
+  if (by_rows) {
+    const uint64_t row = uint64_t(v.cols) * eb;
+    for (int64_t s = s0; s <= s1; ++s) {
+      const int64_t a = std::max(d0, s * ns), b = std::min(d1, (s + 1) * ns);
       emit(tc_fragment{v.src_off[s] + uint64_t(a - s * ns) * row, v.dst_off + uint64_t(a - d0) * row,
                        uint64_t(b - a) * row});
-    } else if (ns == nd && a == s * ns && b - a == ns) {
-      // identical column blocks: the whole slice is one contiguous run
-      emit(tc_fragment{v.src_off[s], v.dst_off, uint64_t(v.rows) * uint64_t(ns) * eb});
-    } else {
-      for (int64_t r = 0; r < v.rows; ++r)
+    }
+  } else if (ns == nd) {
+    // identical column blocks: the whole slice is one contiguous run
+    emit(tc_fragment{v.src_off[s0], v.dst_off, uint64_t(v.rows) * uint64_t(ns) * eb});
+  } else {
+    // row by row; within a row, the source slices left to right
+    for (int64_t r = 0; r < v.rows; ++r)
+      for (int64_t s = s0; s <= s1; ++s) {
+        const int64_t a = std::max(d0, s * ns), b = std::min(d1, (s + 1) * ns);
         emit(tc_fragment{v.src_off[s] + (uint64_t(r) * uint64_t(ns) + uint64_t(a - s * ns)) * eb,
                          v.dst_off + (uint64_t(r) * uint64_t(nd) + uint64_t(a - d0)) * eb,
                          uint64_t(b - a) * eb});
-    }
+      }
   }
 }
 

@@ -151,6 +151,8 @@ def test_tp_fragments_reproduce_oracle_shard(lib, tp):
         oracle.copy_fragments(src, dst, frags)
         want = oracle.tp_shard(stream, SPEC, tp, rank)
         assert np.array_equal(dst.view(np.uint16), want)
+        d = frags[:, 1].astype(np.int64)                 # ascending, no holes
+        assert d[0] == 0 and np.array_equal(d[1:], d[:-1] + frags[:-1, 2].astype(np.int64))
 
 
 def test_tp_fragments_merge_contiguous_rows(lib):
@@ -212,6 +214,12 @@ def test_reshard_fragments_reproduce_oracle_shard(lib, src_tp, dst_tp):
         dst = np.full(tcv.shard_elems(SPEC, dst_tp), 0xBEEF, dtype=np.uint16)
         oracle.copy_fragments(src.view(np.uint8), dst.view(np.uint8), frags)
         assert np.array_equal(dst, oracle.tp_shard(stream, SPEC, dst_tp, rank))
+        # the list ascends in destination and tiles the shard without holes,
+        # so a plan keeps its order
+        d = frags[:, 1].astype(np.int64)
+        ln = frags[:, 2].astype(np.int64)
+        assert d[0] == 0 and np.array_equal(d[1:], d[:-1] + ln[:-1])
+        assert int(ln.sum()) == 2 * tcv.shard_elems(SPEC, dst_tp)
 
 
 def test_reshard_round_trip_and_fragment_counts(lib):
