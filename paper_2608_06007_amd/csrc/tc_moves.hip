@@ -235,7 +235,9 @@ __global__ __launch_bounds__(kThreads) void k_plan_scan(uint64_t* __restrict__ b
 __global__ __launch_bounds__(kThreads) void k_plan_tstart(const tc_fragment* __restrict__ frags,
                                                          const int64_t n, const uint64_t piece,
                                                          const uint64_t* __restrict__ block_off,
-                                                         uint64_t* __restrict__ tstart) {
+                                                         uint64_t* __restrict__ tstart,
+                                                         int64_t* __restrict__ windows,
+                                                         const uint64_t capacity) {
   const int64_t f0 = int64_t(blockIdx.x) * kPlanPerBlock + int64_t(threadIdx.x) * kPlanPerThread;
   uint64_t c[kPlanPerThread];
   uint64_t s = 0;
@@ -244,27 +246,33 @@ __global__ __launch_bounds__(kThreads) void k_plan_tstart(const tc_fragment* __r
     c[j] = f0 + j < n ? pieces_of(frags[f0 + j].len, piece) : 0;
     s += c[j];
   }
-  uint64_t total;
-  uint64_t run = block_off[blockIdx.x] + block_exclusive_scan(s, &total);
+  uint64_t block_total;
+  uint64_t run = block_off[blockIdx.x] + block_exclusive_scan(s, &block_total);
+  // the plan's total (written by k_plan_scan); the window table only has
+  // room for a plan that fits the workspace
+  const uint64_t total = tstart[n];
+  const bool fits = total <= capacity;
+  const uint64_t nwin = (total + kWindowTasks - 1) / kWindowTasks;
 #pragma unroll
   for (int j = 0; j < kPlanPerThread; ++j) {
-    if (f0 + j < n) tstart[f0 + j] = run;
+    if (f0 + j < n) {
+      tstart[f0 + j] = run;
+      // Every task lies in exactly one non-empty fragment, which is therefore
+      // the first fragment of each window whose first task it holds and the
+      // last fragment of each window whose last task it holds.
+      if (fits && c[j]) {
+        const uint64_t te = run + c[j];  // tasks [run, te)
+        for (uint64_t w = (run + kWindowTasks - 1) / kWindowTasks; w * kWindowTasks < te; ++w)
+          windows[2 * w] = f0 + j;
+        for (uint64_t w = run / kWindowTasks; w < nwin; ++w) {
+          const uint64_t last = min(w * kWindowTasks + kWindowTasks - 1, total - 1);
+          if (last >= te) break;
+          windows[2 * w + 1] = f0 + j;
+        }
+      }
+    }
     run += c[j];
   }
-}
-
-// Last f in [lo, hi) with tstart[f] <= t, given tstart[lo] <= t < tstart[hi]
-// (64-way search by one wave).
-__device__ int64_t wave_find(const uint64_t* __restrict__ tstart, int64_t lo, int64_t hi,
-                             uint64_t t, int lane) {
-  while (hi - lo > 1) {
-    const int64_t step = (hi - lo + kWaveLanes - 1) / kWaveLanes;
-    const int64_t p = lo + (int64_t(lane) + 1) * step;
-    const bool pred = lane < kWaveLanes - 1 && p < hi && tstart[p] <= t;
-    lo += int64_t(__popcll(__ballot(pred))) * step;
-    hi = min(hi, lo + step);
-  }
-  return lo;
 }
 
 __device__ __forceinline__ Task pack_task(uint64_t src, uint64_t dst, uint64_t len, bool first) {
@@ -273,42 +281,39 @@ __device__ __forceinline__ Task pack_task(uint64_t src, uint64_t dst, uint64_t l
 
 constexpr int kExpandPerBlock = int(kWindowTasks);  // tasks written by one workgroup
 
-// Block j writes tasks [j * 1024, (j + 1) * 1024).  Wave 0 finds the first
-// and last task's fragments and records them in windows[j]; if they span at
-// most 1024 fragments their tstart entries go to LDS and every task finds its
-// fragment there, otherwise (long runs of empty fragments) each task searches
-// globally.
+// Block j writes tasks [j * 1024, (j + 1) * 1024), whose first and last
+// fragment k_plan_tstart recorded in windows[j].  If they span at most 1024
+// fragments their tstart entries go to LDS and every task finds its fragment
+// there, otherwise (long runs of empty fragments) each task searches
+// globally.  A thread's four tasks are found first and their descriptors
+// loaded together, so the loads overlap.
+constexpr int kExpandPerThread = kExpandPerBlock / kThreads;
+static_assert(kExpandPerThread * kThreads == kExpandPerBlock, "whole tasks per thread");
+
 __global__ __launch_bounds__(kThreads) void k_plan_expand(const tc_fragment* __restrict__ frags,
-                                                         const int64_t n,
                                                          const uint64_t* __restrict__ tstart,
+                                                         const int64_t* __restrict__ windows,
                                                          const uint64_t total, const uint64_t piece,
-                                                         Task* __restrict__ tasks,
-                                                         int64_t* __restrict__ windows) {
+                                                         Task* __restrict__ tasks) {
   __shared__ uint64_t win[kExpandPerBlock + 1];
-  __shared__ int64_t range[2];
-  const int lane = threadIdx.x & (kWaveLanes - 1);
   const uint64_t t0 = uint64_t(blockIdx.x) * kExpandPerBlock;
   const uint64_t t1 = min(total, t0 + kExpandPerBlock);
-  if (threadIdx.x < kWaveLanes) {
-    const int64_t f0 = wave_find(tstart, 0, n, t0, lane);
-    const int64_t f1 = wave_find(tstart, f0, n, t1 - 1, lane);
-    if (lane == 0) {
-      range[0] = f0;
-      range[1] = f1;
-      windows[2 * uint64_t(blockIdx.x)] = f0;
-      windows[2 * uint64_t(blockIdx.x) + 1] = f1;
-    }
-  }
-  __syncthreads();
-  const int64_t f0 = range[0], f1 = range[1];
+  const int64_t f0 = windows[2 * uint64_t(blockIdx.x)];
+  const int64_t f1 = windows[2 * uint64_t(blockIdx.x) + 1];
   const int64_t span = f1 - f0 + 1;
   const bool local = span <= kExpandPerBlock;
   if (local)
     for (int64_t k = threadIdx.x; k <= span; k += kThreads) win[k] = tstart[f0 + k];
   __syncthreads();
-  for (uint64_t t = t0 + threadIdx.x; t < t1; t += kThreads) {
+  int64_t frag[kExpandPerThread];
+  uint64_t start[kExpandPerThread];
+#pragma unroll
+  for (int j = 0; j < kExpandPerThread; ++j) {
+    const uint64_t t = t0 + threadIdx.x + uint64_t(j) * kThreads;
+    frag[j] = -1;
+    start[j] = 0;
+    if (t >= t1) continue;
     int64_t lo, hi;
-    uint64_t start;
     if (local) {  // win[lo] <= t < win[hi], indices relative to f0
       lo = 0;
       hi = span;
@@ -319,8 +324,8 @@ __global__ __launch_bounds__(kThreads) void k_plan_expand(const tc_fragment* __r
         else
           hi = mid;
       }
-      start = win[lo];
-      lo += f0;
+      start[j] = win[lo];
+      frag[j] = f0 + lo;
     } else {
       lo = f0;
       hi = f1 + 1;
@@ -331,12 +336,21 @@ __global__ __launch_bounds__(kThreads) void k_plan_expand(const tc_fragment* __r
         else
           hi = mid;
       }
-      start = tstart[lo];
+      start[j] = tstart[lo];
+      frag[j] = lo;
     }
-    const tc_fragment f = frags[lo];
-    const uint64_t off = (t - start) * piece;
-    const uint64_t rem = f.len - off;
-    tasks[t] = pack_task(f.src_off + off, f.dst_off + off, rem < piece ? rem : piece, off == 0);
+  }
+  tc_fragment f[kExpandPerThread];
+#pragma unroll
+  for (int j = 0; j < kExpandPerThread; ++j)
+    if (frag[j] >= 0) f[j] = frags[frag[j]];
+#pragma unroll
+  for (int j = 0; j < kExpandPerThread; ++j) {
+    if (frag[j] < 0) continue;
+    const uint64_t t = t0 + threadIdx.x + uint64_t(j) * kThreads;
+    const uint64_t off = (t - start[j]) * piece;
+    const uint64_t rem = f[j].len - off;
+    tasks[t] = pack_task(f[j].src_off + off, f[j].dst_off + off, rem < piece ? rem : piece, off == 0);
   }
 }
 
@@ -939,7 +953,8 @@ hipError_t launch_plan_count(const tc_fragment* frags, int64_t n, uint64_t piece
                      (const uint64_t*)bunord, (const uint64_t*)bdend, nb, piece, n,
                      uint64_t(L.capacity), uint64_t(permuted ? 1 : 0), hdr, tstart + n);
   hipLaunchKernelGGL(k_plan_tstart, dim3((unsigned)nb), dim3(kThreads), 0, s, frags, n, piece,
-                     (const uint64_t*)bcnt, tstart);
+                     (const uint64_t*)bcnt, tstart, reinterpret_cast<int64_t*>(base + L.windows),
+                     uint64_t(L.capacity));
   return hipGetLastError();
 }
 
@@ -974,9 +989,9 @@ hipError_t launch_plan_expand(const tc_fragment* frags, int64_t n, uint64_t tota
   const uint64_t* tstart = reinterpret_cast<const uint64_t*>(base + L.tstart);
   Task* tasks = reinterpret_cast<Task*>(base + kTasksOffset);
   const uint64_t grid = (total + kExpandPerBlock - 1) / kExpandPerBlock;
-  int64_t* windows = reinterpret_cast<int64_t*>(base + L.windows);
-  hipLaunchKernelGGL(k_plan_expand, dim3((unsigned)grid), dim3(kThreads), 0, s, frags, n, tstart,
-                     total, piece, tasks, windows);
+  const int64_t* windows = reinterpret_cast<const int64_t*>(base + L.windows);
+  hipLaunchKernelGGL(k_plan_expand, dim3((unsigned)grid), dim3(kThreads), 0, s, frags, tstart,
+                     windows, total, piece, tasks);
   return hipGetLastError();
 }
 
