@@ -123,7 +123,7 @@ typedef struct {
  * workspace with room for T >= n + 1 tasks accepts payloads up to
  * (T - n) * 2^30 bytes (beyond that the plan returns TC_ERR_WORKSPACE); this
  * size has room for 4n + 2^23 tasks, which keeps 1 KiB pieces for payloads
- * up to ~3 KiB per fragment plus 8 GiB.  Offsets plus lengths must stay below
+ * up to ~2 KiB per fragment plus 8 GiB.  Offsets plus lengths must stay below
  * 2^48. */
 size_t tc_copy_fragments_workspace(int64_t n); /* 0 for n < 0 or n > 2^40 */
 /* Smallest workspace a plan of n descriptors accepts (room for n + 1 tasks;

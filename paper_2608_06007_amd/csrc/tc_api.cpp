@@ -433,10 +433,12 @@ tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace
       st = check_ranges(nullptr, nullptr, h);
       if (st != TC_OK) return st;
     }
-    uint64_t piece = tc::kMinPiece;
+    // 1 KiB pieces cut on 128-byte destination lines; if that overflows the
+    // workspace, larger pieces at plain multiples (which fit by construction)
+    uint64_t piece = tc::kMinPiece, cut = 127;
     tc::PlanHeader hdr;
     for (int attempt = 0; attempt < 2; ++attempt) {
-      hipError_t e = tc::launch_plan_count(frags, n, piece, workspace, L, false, stream);
+      hipError_t e = tc::launch_plan_count(frags, n, piece, cut, workspace, L, false, stream);
       if (e != hipSuccess) return hip_fail(e);
       // The launch size of the copy depends on the task count: read it back.
       e = hipMemcpyAsync(&hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, stream);
@@ -449,6 +451,7 @@ tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace
       piece = pow2_at_least(std::max<uint64_t>(tc::kMinPiece, (hdr.payload + room - 1) / room));
       // a task's length is stored in 31 bits
       piece = std::min<uint64_t>(piece, tc::kMaxPiece);
+      cut = 0;
     }
     if (hdr.total_tasks > L.capacity) return TC_ERR_WORKSPACE;
     // Long lists with scattered destinations are planned in destination order
@@ -460,10 +463,10 @@ tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace
       while (shift < 62 && (hdr.dst_end >> shift) >= L.nbuckets) ++shift;
       e = tc::launch_plan_reorder(frags, n, shift, workspace, L, stream);
       planned = reinterpret_cast<const tc_fragment*>(static_cast<uint8_t*>(workspace) + L.sorted);
-      if (e == hipSuccess) e = tc::launch_plan_count(planned, n, piece, workspace, L, true, stream);
+      if (e == hipSuccess) e = tc::launch_plan_count(planned, n, piece, cut, workspace, L, true, stream);
       if (e != hipSuccess) return hip_fail(e);
     }
-    e = tc::launch_plan_expand(planned, n, hdr.total_tasks, piece, workspace, L, stream);
+    e = tc::launch_plan_expand(planned, n, hdr.total_tasks, piece, cut, workspace, L, stream);
     if (e != hipSuccess) return hip_fail(e);
     if (total_tasks) *total_tasks = hdr.total_tasks;
     return TC_OK;

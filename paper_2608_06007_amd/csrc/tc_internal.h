@@ -47,6 +47,8 @@ struct PlanHeader {
   uint64_t dst_unordered;  // some fragment starts below its predecessor (destination side)
   uint64_t dst_end;        // largest dst_off + len of a non-empty fragment
   uint64_t permuted;       // the tasks follow the reordered list; perm maps back
+  uint64_t cut;            // 127: tasks after a fragment's first start on a 128-byte
+                           // destination line; 0: tasks start at multiples of the piece
 };
 
 // Workspace layout: header | tasks[capacity] | digest slots[capacity] |
@@ -57,6 +59,7 @@ struct PlanHeader {
 // expansion.  The planning scratch lives at the end and stays valid with the
 // plan (the digest reduction reads tstart, windows and perm).
 constexpr size_t kTasksOffset = 256;
+static_assert(sizeof(PlanHeader) <= kTasksOffset, "the header fits before the task table");
 constexpr size_t kTaskBytes = 32;  // a task and its 16-byte digest slot
 constexpr uint64_t kWindowTasks = 1024;  // tasks per window of the expansion and the reduction
 constexpr size_t kWindowBytes = 16;      // first and last fragment of a window
@@ -92,15 +95,16 @@ hipError_t launch_blocks(const RegionTable& tab, int32_t num_regions, int64_t bl
 // Count pieces of `piece` bytes per fragment and write tstart; the header
 // receives the totals, whether the destinations are unordered, their end, and
 // `permuted` (the list counted is the reordered one).  Enqueued only.
-hipError_t launch_plan_count(const tc_fragment* frags, int64_t n, uint64_t piece, void* ws,
-                             const PlanLayout& L, bool permuted, hipStream_t s);
+hipError_t launch_plan_count(const tc_fragment* frags, int64_t n, uint64_t piece, uint64_t cut,
+                             void* ws, const PlanLayout& L, bool permuted, hipStream_t s);
 // Write the fragments in destination order (buckets of 2^shift bytes) to
 // L.sorted and their original indices to L.perm.
 hipError_t launch_plan_reorder(const tc_fragment* frags, int64_t n, int shift, void* ws,
                                const PlanLayout& L, hipStream_t s);
 // Expand the counted plan into its task table (total_tasks known on the host).
 hipError_t launch_plan_expand(const tc_fragment* frags, int64_t n, uint64_t total_tasks,
-                              uint64_t piece, void* ws, const PlanLayout& L, hipStream_t s);
+                              uint64_t piece, uint64_t cut, void* ws, const PlanLayout& L,
+                              hipStream_t s);
 hipError_t launch_copy_tasks(const uint8_t* src, uint8_t* dst, const void* ws,
                              uint64_t total_tasks, hipStream_t s);
 // Copy (mode 0) or only read (1: at the tasks' source offsets, 2: at their

@@ -96,8 +96,11 @@ __global__ __launch_bounds__(kThreads) void k_blocks_bytes(const RegionTable tab
 }
 
 // ------------------------------------------------------------------------
-// Fragment plan.  Fragment f becomes ceil(len / piece) tasks; tstart[f] is
-// its first task, tstart[n] the total.  Passes: per-block task and byte sums,
+// Fragment plan.  Fragment f becomes ceil((len + h) / piece) tasks, where
+// h = dst_off & cut: with cut = 127 every task after a fragment's first starts
+// on a 128-byte destination line (no line is split between two waves inside
+// a fragment); cut = 0 gives plain multiples of the piece.  tstart[f] is its
+// first task, tstart[n] the total.  Passes: per-block task and byte sums,
 // an exclusive scan of the block sums (one workgroup), the per-fragment
 // prefix, then (after the host has read the total) the task table.
 // ------------------------------------------------------------------------
@@ -133,8 +136,8 @@ __device__ uint64_t block_exclusive_scan(uint64_t v, uint64_t* block_total) {
 
 constexpr int kPlanPerThread = kPlanPerBlock / kThreads;  // 4
 
-__device__ __forceinline__ uint64_t pieces_of(uint64_t len, uint64_t piece) {
-  return (len + piece - 1) / piece;
+__device__ __forceinline__ uint64_t pieces_of(const tc_fragment& f, uint64_t piece, uint64_t cut) {
+  return f.len ? (f.len + (f.dst_off & cut) + piece - 1) / piece : 0;
 }
 
 // Maximum over a 256-thread block (every thread gets it).
@@ -160,6 +163,7 @@ __device__ uint64_t block_max_u64(uint64_t v) {
 // largest destination end.
 __global__ __launch_bounds__(kThreads) void k_plan_count(const tc_fragment* __restrict__ frags,
                                                         const int64_t n, const uint64_t piece,
+                                                        const uint64_t cut,
                                                         uint64_t* __restrict__ block_cnt,
                                                         uint64_t* __restrict__ block_len,
                                                         uint64_t* __restrict__ block_unord,
@@ -171,7 +175,7 @@ __global__ __launch_bounds__(kThreads) void k_plan_count(const tc_fragment* __re
   for (int j = 0; j < kPlanPerThread; ++j)
     if (f0 + j < n) {
       const tc_fragment f = frags[f0 + j];
-      c += pieces_of(f.len, piece);
+      c += pieces_of(f, piece, cut);
       l += f.len;
       if (f.len && f.dst_off + f.len > dend) dend = f.dst_off + f.len;
       if (f0 + j + 1 < n && frags[f0 + j + 1].dst_off < f.dst_off) unord = 1;
@@ -196,6 +200,7 @@ __global__ __launch_bounds__(kThreads) void k_plan_scan(uint64_t* __restrict__ b
                                                        const uint64_t* __restrict__ block_unord,
                                                        const uint64_t* __restrict__ block_dend,
                                                        const int64_t nblocks, const uint64_t piece,
+                                                       const uint64_t cut,
                                                        const int64_t n, const uint64_t capacity,
                                                        const uint64_t permuted,
                                                        PlanHeader* __restrict__ hdr,
@@ -228,12 +233,14 @@ __global__ __launch_bounds__(kThreads) void k_plan_scan(uint64_t* __restrict__ b
     hdr->dst_unordered = any_unord ? 1 : 0;
     hdr->dst_end = dend;
     hdr->permuted = permuted;
+    hdr->cut = cut;
     *tstart_end = carry;
   }
 }
 
 __global__ __launch_bounds__(kThreads) void k_plan_tstart(const tc_fragment* __restrict__ frags,
                                                          const int64_t n, const uint64_t piece,
+                                                         const uint64_t cut,
                                                          const uint64_t* __restrict__ block_off,
                                                          uint64_t* __restrict__ tstart,
                                                          int64_t* __restrict__ windows,
@@ -243,7 +250,7 @@ __global__ __launch_bounds__(kThreads) void k_plan_tstart(const tc_fragment* __r
   uint64_t s = 0;
 #pragma unroll
   for (int j = 0; j < kPlanPerThread; ++j) {
-    c[j] = f0 + j < n ? pieces_of(frags[f0 + j].len, piece) : 0;
+    c[j] = f0 + j < n ? pieces_of(frags[f0 + j], piece, cut) : 0;
     s += c[j];
   }
   uint64_t block_total;
@@ -294,6 +301,7 @@ __global__ __launch_bounds__(kThreads) void k_plan_expand(const tc_fragment* __r
                                                          const uint64_t* __restrict__ tstart,
                                                          const int64_t* __restrict__ windows,
                                                          const uint64_t total, const uint64_t piece,
+                                                         const uint64_t cut,
                                                          Task* __restrict__ tasks) {
   __shared__ uint64_t win[kExpandPerBlock + 1];
   const uint64_t t0 = uint64_t(blockIdx.x) * kExpandPerBlock;
@@ -348,9 +356,12 @@ __global__ __launch_bounds__(kThreads) void k_plan_expand(const tc_fragment* __r
   for (int j = 0; j < kExpandPerThread; ++j) {
     if (frag[j] < 0) continue;
     const uint64_t t = t0 + threadIdx.x + uint64_t(j) * kThreads;
-    const uint64_t off = (t - start[j]) * piece;
-    const uint64_t rem = f[j].len - off;
-    tasks[t] = pack_task(f[j].src_off + off, f[j].dst_off + off, rem < piece ? rem : piece, off == 0);
+    // task k covers [k * piece - h, (k + 1) * piece - h) of the fragment,
+    // clipped to [0, len)
+    const uint64_t k = t - start[j], h = f[j].dst_off & cut;
+    const uint64_t off = k ? k * piece - h : 0;
+    const uint64_t end = min(f[j].len, (k + 1) * piece - h);
+    tasks[t] = pack_task(f[j].src_off + off, f[j].dst_off + off, end - off, k == 0);
   }
 }
 
@@ -404,11 +415,12 @@ __global__ __launch_bounds__(kThreads) void k_copy_tasks(const uint8_t* __restri
 // Integrity digests (the verify stage of the materialization pipeline).
 // A fragment's digest is S1 = sum b_i and S2 = sum (i + 1) b_i (mod 2^64)
 // over its bytes.  The copy kernel, with the same launch shape as
-// k_copy_tasks, also writes each task's partial sums -- P1 = sum c_j and
-// P2 = sum (j + 1) c_j over its own bytes c_j -- into the task's digest slot;
-// k_digest_reduce then adds the tasks of each fragment: task k of a fragment
-// starts at byte k * piece, so it contributes P1 to S1 and
-// P2 + k * piece * P1 to S2.  No two tasks add into the same word during the
+// k_copy_tasks, also writes each task's partial sums into the task's digest
+// slot: P1 = sum c_j and P2 = sum (a_j + 1) c_j over its own bytes c_j, where
+// a_j is the byte's destination offset.  A fragment whose destination starts
+// at D then has S1 = sum P1 and S2 = sum P2 - D * S1 over its tasks, however
+// the plan cut it; k_digest_reduce adds the tasks of each fragment and
+// subtracts D * S1 once.  No two tasks add into the same word during the
 // copy, and the reduction adds at most a few words per window atomically.
 // ------------------------------------------------------------------------
 enum DigestMode { kCopyDigest = 0, kDigestSrc = 1, kDigestDst = 2 };
@@ -470,13 +482,14 @@ __device__ __forceinline__ uint32_t wave_sum32_lane63(uint32_t v) {
 // the wave-uniform 64-bit totals add base * sum on top.
 constexpr uint64_t kChunkVecs = 256;
 
-// Sums of one task's bytes at s (copied to d in kCopyDigest mode); pre holds
-// this lane's first body vector when the caller has loaded it already
+// Sums of one task's bytes at s (copied to d in kCopyDigest mode), weighted
+// by destination position (the task starts at destination offset dof); pre
+// holds this lane's first body vector when the caller has loaded it already
 // (tasks of one aligned vector per lane at most, no head).
 template <int kMode>
 __device__ __forceinline__ void task_sums(const uint8_t* s, uint8_t* d, const uint64_t len,
-                                          const int lane, const bool preloaded, const u32x4 pre,
-                                          u64x2* slot) {
+                                          const uint64_t dof, const int lane, const bool preloaded,
+                                          const u32x4 pre, u64x2* slot) {
   uint64_t A = 0, W = 0;
   const uintptr_t sa = reinterpret_cast<uintptr_t>(s);
   const uintptr_t mis = kMode == kCopyDigest ? (sa ^ reinterpret_cast<uintptr_t>(d)) & 15 : 0;
@@ -499,7 +512,7 @@ __device__ __forceinline__ void task_sums(const uint8_t* s, uint8_t* d, const ui
       ws += uint32_t(body_end + lane) * x;
     }
     const uint32_t ta = wave_sum32_lane63(a), tw = wave_sum32_lane63(ws);
-    if (lane == kWaveLanes - 1) *slot = u64x2{ta, uint64_t(tw) + ta};
+    if (lane == kWaveLanes - 1) *slot = u64x2{ta, uint64_t(tw) + (dof + 1) * ta};
     return;
   } else if (mis == 0) {
     uint64_t head = (16 - (sa & 15)) & 15;
@@ -554,7 +567,7 @@ __device__ __forceinline__ void task_sums(const uint8_t* s, uint8_t* d, const ui
       W += cw + base * ca;
     }
   }
-  if (lane == 0) *slot = u64x2{A, W + A};
+  if (lane == 0) *slot = u64x2{A, W + (dof + 1) * A};
 }
 
 // kPerWave consecutive tasks per wave.  The first body vector of every task
@@ -634,7 +647,7 @@ __global__ __launch_bounds__(kThreads) void k_copy_digest(const uint8_t* __restr
       }
       const uint32_t ta = wave_sum32_lane63(a), tw = wave_sum32_lane63(ws);
       if (lane == kWaveLanes - 1)
-        slots[t0] = u64x2{ta, uint64_t(tw) + ta};
+        slots[t0] = u64x2{ta, uint64_t(tw) + (task_dst(tk[0]) + 1) * ta};
       else if (lane >= kWaveLanes - kPerWave)
         slots[t0 + (kWaveLanes - 1 - lane)] = u64x2{0, 0};
       continue;
@@ -642,7 +655,7 @@ __global__ __launch_bounds__(kThreads) void k_copy_digest(const uint8_t* __restr
 #pragma unroll
     for (int k = 0; k < kPerWave; ++k) {
       if (t0 + k >= total) break;
-      task_sums<kMode>(s[k], d[k], len[k], lane, pre[k], v[k], slots + t0 + k);
+      task_sums<kMode>(s[k], d[k], len[k], task_dst(tk[k]), lane, pre[k], v[k], slots + t0 + k);
     }
   }
 }
@@ -658,10 +671,11 @@ __global__ __launch_bounds__(kThreads) void k_fill_zero(uint64_t* __restrict__ p
 // Reduce-by-fragment of the task slots.  Block j owns tasks
 // [j * 1024, (j + 1) * 1024), whose first and last fragment the plan recorded
 // in windows[j]; each thread takes four consecutive tasks, whose slots it
-// loads first, and adds them per fragment in registers.  A fragment whose tasks
-// all lie in the block is written with a plain store; one that crosses the
-// block's edges (at most the first and the last) is added atomically into the
-// zeroed digest.
+// loads first, and adds them per fragment in registers.  A fragment whose
+// tasks all lie in the block is written with a plain store; one that crosses
+// the block's edges (at most the first and the last) is added atomically into
+// the zeroed digest.  Each partial sum subtracts D * S1 for its own S1, D
+// being the fragment's destination offset (its first task's).
 constexpr int kReducePerThread = kExpandPerBlock / kThreads;
 static_assert(kReducePerThread * kThreads == kExpandPerBlock, "whole tasks per thread");
 
@@ -669,6 +683,7 @@ __global__ __launch_bounds__(kThreads) void k_digest_reduce(const uint64_t* __re
                                                            const uint64_t total,
                                                            const PlanHeader* __restrict__ hdr,
                                                            const uint64_t* __restrict__ perm,
+                                                           const Task* __restrict__ tasks,
                                                            const u64x2* __restrict__ slots,
                                                            const int64_t* __restrict__ windows,
                                                            uint64_t* __restrict__ digests) {
@@ -685,7 +700,6 @@ __global__ __launch_bounds__(kThreads) void k_digest_reduce(const uint64_t* __re
   const int64_t f1 = windows[2 * uint64_t(blockIdx.x) + 1];
   const int64_t span = f1 - f0 + 1;
   const bool local = span <= kExpandPerBlock;
-  const uint64_t piece = hdr->piece;
   // digests are indexed by the caller's order; a reordered plan maps back
   const bool mapped = perm != nullptr && hdr->permuted != 0;
   if (local) {
@@ -694,6 +708,13 @@ __global__ __launch_bounds__(kThreads) void k_digest_reduce(const uint64_t* __re
   }
   __syncthreads();
   if (local) {
+    // destination offsets of the fragments this thread writes out below
+    uint64_t dbase[kReducePerThread];
+#pragma unroll
+    for (int j = 0; j < kReducePerThread; ++j) {
+      const int64_t k = threadIdx.x + int64_t(j) * kThreads;
+      dbase[j] = k < span && win[k] < win[k + 1] ? task_dst(tasks[win[k]]) : 0;
+    }
     if (tb < t1) {
       // fragment of the first task: win[lo] <= tb < win[hi], relative to f0
       int64_t lo = 0, hi = span;
@@ -719,11 +740,26 @@ __global__ __launch_bounds__(kThreads) void k_digest_reduce(const uint64_t* __re
           ++lo;
         }
         s1 += p[j].x;
-        s2 += p[j].y + (t - win[lo]) * piece * p[j].x;
+        s2 += p[j].y;
       }
       if (s1 | s2) {
         atomicAdd(reinterpret_cast<unsigned long long*>(&acc[2 * lo]), (unsigned long long)s1);
         atomicAdd(reinterpret_cast<unsigned long long*>(&acc[2 * lo + 1]), (unsigned long long)s2);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kReducePerThread; ++j) {
+      const int64_t k = threadIdx.x + int64_t(j) * kThreads;
+      if (k >= span) break;
+      uint64_t* out = digests + 2 * (mapped ? perm[f0 + k] : uint64_t(f0 + k));
+      const uint64_t a = acc[2 * k], b = acc[2 * k + 1] - dbase[j] * acc[2 * k];
+      if (win[k] >= t0 && win[k + 1] <= t1) {
+        out[0] = a;
+        out[1] = b;
+      } else {
+        atomicAdd(reinterpret_cast<unsigned long long*>(out), (unsigned long long)a);
+        atomicAdd(reinterpret_cast<unsigned long long*>(out + 1), (unsigned long long)b);
       }
     }
   } else {
@@ -740,22 +776,10 @@ __global__ __launch_bounds__(kThreads) void k_digest_reduce(const uint64_t* __re
         else
           hi = mid;
       }
-      const uint64_t s2 = p[j].y + (t - tstart[lo]) * piece * p[j].x;
+      const uint64_t s2 = p[j].y - task_dst(tasks[tstart[lo]]) * p[j].x;
       const uint64_t o = mapped ? perm[lo] : uint64_t(lo);
       atomicAdd(reinterpret_cast<unsigned long long*>(&digests[2 * o]), (unsigned long long)p[j].x);
       atomicAdd(reinterpret_cast<unsigned long long*>(&digests[2 * o + 1]), (unsigned long long)s2);
-    }
-    return;
-  }
-  __syncthreads();
-  for (int64_t k = threadIdx.x; k < span; k += kThreads) {
-    uint64_t* out = digests + 2 * (mapped ? perm[f0 + k] : uint64_t(f0 + k));
-    if (win[k] >= t0 && win[k + 1] <= t1) {
-      out[0] = acc[2 * k];
-      out[1] = acc[2 * k + 1];
-    } else {
-      atomicAdd(reinterpret_cast<unsigned long long*>(out), (unsigned long long)acc[2 * k]);
-      atomicAdd(reinterpret_cast<unsigned long long*>(out + 1), (unsigned long long)acc[2 * k + 1]);
     }
   }
 }
@@ -927,7 +951,7 @@ PlanLayout plan_layout(int64_t n, size_t ws_bytes) {
 }
 
 // Room for 4n + 2^23 tasks: pieces stay at 1 KiB while the payload is below
-// ~3 KiB per fragment plus 8 GiB.
+// ~2 KiB per fragment plus 8 GiB (a fragment's line offset can add a task).
 size_t frag_workspace_bytes(int64_t n) {
   return kTasksOffset + task_area_bytes(4 * size_t(n) + (size_t(1) << 23)) + plan_tail_bytes(n) +
          256;
@@ -937,7 +961,7 @@ size_t frag_workspace_min_bytes(int64_t n) {
   return kTasksOffset + task_area_bytes(size_t(n) + 1) + plan_tail_bytes(n) + 256;
 }
 
-hipError_t launch_plan_count(const tc_fragment* frags, int64_t n, uint64_t piece, void* ws,
+hipError_t launch_plan_count(const tc_fragment* frags, int64_t n, uint64_t piece, uint64_t cut, void* ws,
                              const PlanLayout& L, bool permuted, hipStream_t s) {
   uint8_t* base = static_cast<uint8_t*>(ws);
   PlanHeader* hdr = reinterpret_cast<PlanHeader*>(base);
@@ -947,12 +971,12 @@ hipError_t launch_plan_count(const tc_fragment* frags, int64_t n, uint64_t piece
   uint64_t* blen = bcnt + nb;
   uint64_t* bunord = blen + nb;
   uint64_t* bdend = bunord + nb;
-  hipLaunchKernelGGL(k_plan_count, dim3((unsigned)nb), dim3(kThreads), 0, s, frags, n, piece, bcnt,
+  hipLaunchKernelGGL(k_plan_count, dim3((unsigned)nb), dim3(kThreads), 0, s, frags, n, piece, cut, bcnt,
                      blen, bunord, bdend);
   hipLaunchKernelGGL(k_plan_scan, dim3(1), dim3(kThreads), 0, s, bcnt, (const uint64_t*)blen,
-                     (const uint64_t*)bunord, (const uint64_t*)bdend, nb, piece, n,
+                     (const uint64_t*)bunord, (const uint64_t*)bdend, nb, piece, cut, n,
                      uint64_t(L.capacity), uint64_t(permuted ? 1 : 0), hdr, tstart + n);
-  hipLaunchKernelGGL(k_plan_tstart, dim3((unsigned)nb), dim3(kThreads), 0, s, frags, n, piece,
+  hipLaunchKernelGGL(k_plan_tstart, dim3((unsigned)nb), dim3(kThreads), 0, s, frags, n, piece, cut,
                      (const uint64_t*)bcnt, tstart, reinterpret_cast<int64_t*>(base + L.windows),
                      uint64_t(L.capacity));
   return hipGetLastError();
@@ -983,6 +1007,7 @@ hipError_t launch_plan_reorder(const tc_fragment* frags, int64_t n, int shift, v
 }
 
 hipError_t launch_plan_expand(const tc_fragment* frags, int64_t n, uint64_t total, uint64_t piece,
+                              uint64_t cut,
                               void* ws, const PlanLayout& L, hipStream_t s) {
   if (total == 0) return hipSuccess;
   uint8_t* base = static_cast<uint8_t*>(ws);
@@ -991,7 +1016,7 @@ hipError_t launch_plan_expand(const tc_fragment* frags, int64_t n, uint64_t tota
   const uint64_t grid = (total + kExpandPerBlock - 1) / kExpandPerBlock;
   const int64_t* windows = reinterpret_cast<const int64_t*>(base + L.windows);
   hipLaunchKernelGGL(k_plan_expand, dim3((unsigned)grid), dim3(kThreads), 0, s, frags, tstart,
-                     windows, total, piece, tasks);
+                     windows, total, piece, cut, tasks);
   return hipGetLastError();
 }
 
@@ -1042,7 +1067,7 @@ hipError_t launch_copy_digest(const uint8_t* src, uint8_t* dst, void* ws, const 
                      reinterpret_cast<const uint64_t*>(base + L.tstart), total,
                      reinterpret_cast<const PlanHeader*>(base),
                      L.nbuckets ? reinterpret_cast<const uint64_t*>(base + L.perm) : nullptr,
-                     (const u64x2*)slots, reinterpret_cast<const int64_t*>(base + L.windows),
+                     tasks, (const u64x2*)slots, reinterpret_cast<const int64_t*>(base + L.windows),
                      digests);
   return hipGetLastError();
 }

@@ -119,6 +119,7 @@ def test_small_workspace_grows_the_task_size(extra_tasks):
     src = _rand_bytes(pool, 43)
     dst, fr, ws = _copy_and_check(src, frags, pool, planned=True, ws_bytes=ws_bytes)
     assert ws.total <= n + extra_tasks + 32      # capacity rounds to 256-byte alignment
+    assert _header_word(ws, 8) == 0               # larger pieces: plain multiples
     with pytest.raises(tc.TcError) as e:          # below the minimum
         tc.tc_plan_fragments(fr, torch.empty(tc.tc_copy_fragments_workspace_min(n) - 4096,
                                              dtype=torch.uint8, device=DEV))
@@ -291,6 +292,46 @@ def test_cross_layout_reshard_8b_full_size():
 def _header_permuted(ws):
     # the plan header's eighth word says whether the tasks follow a reordered list
     return int(ws[56:64].cpu().numpy().view(np.uint64)[0])
+
+
+def _header_word(ws, k):
+    return int(ws[8 * k:8 * k + 8].cpu().numpy().view(np.uint64)[0])
+
+
+def _task_table(ws):
+    t = ws[256:256 + 16 * ws.total].cpu().numpy().view(np.uint64).reshape(-1, 2)
+    src = t[:, 0] & np.uint64((1 << 48) - 1)
+    dst = (t[:, 0] >> np.uint64(48)) | ((t[:, 1] & np.uint64(0xFFFFFFFF)) << np.uint64(16))
+    ln = (t[:, 1] >> np.uint64(32)) & np.uint64(0x7FFFFFFF)
+    first = (t[:, 1] >> np.uint64(63)).astype(bool)
+    return src.astype(np.int64), dst.astype(np.int64), ln.astype(np.int64), first
+
+
+@pytest.mark.parametrize("align", [16, 1])
+def test_tasks_start_on_destination_lines(align):
+    """1 KiB pieces are cut on 128-byte destination lines: every task after a
+    fragment's first starts at a multiple of 128 in the destination, the
+    first is the shorter by the fragment's offset into its line, and the
+    tasks of each fragment tile it exactly (checked from the task table)."""
+    pool = 64 << 20
+    frags = synth.fragment_storm(3000, pool, seed=47 + align, align=align)
+    _, _, ws = _copy_and_check(_rand_bytes(pool, 48), frags, pool, planned=True)
+    assert _header_word(ws, 1) == 1024 and _header_word(ws, 8) == 127
+    src, dst, ln, first = _task_table(ws)
+    assert np.all(dst[~first] % 128 == 0)
+    assert first.sum() == np.count_nonzero(frags[:, 2])
+    assert np.all(ln > 0) and np.all(ln <= 1024)
+    # each fragment's tasks, in plan order, tile its bytes
+    fid = np.cumsum(first) - 1
+    nz = np.nonzero(frags[:, 2])[0]
+    f = frags[nz].astype(np.int64)[fid]
+    off = dst - f[:, 1]
+    assert np.array_equal(src - f[:, 0], off)
+    nxt = np.append(off[1:], 0)
+    last = np.append(first[1:], True)
+    assert np.array_equal(np.where(last, f[:, 2], nxt), off + ln)
+    h = f[:, 1] % 128
+    assert np.array_equal(ln[first], np.minimum(f[first, 2], 1024 - h[first]))
 
 
 def test_long_unordered_lists_are_planned_in_destination_order():
