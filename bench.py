@@ -220,6 +220,59 @@ def cpu_baseline_kv(torch, synth, s, regions_dev, ids_np, n_sample=512, min_seco
             "cpu_model": _cpu_model()}
 
 
+def _repeat_for(fn, min_seconds):
+    """Call fn until min_seconds have passed; returns (repetitions, seconds)."""
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        fn()
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds:
+            return reps, el
+
+
+def oracle_copy_sample(torch, src_dev, frags_np, src_lim, dst_lim, label, min_seconds=3.0):
+    """The oracle's fragment copy on host copies of the first src_lim /
+    dst_lim bytes of the source and destination: the fragments of the list
+    that lie entirely inside both."""
+    import oracle
+    inside = ((frags_np[:, 0] + frags_np[:, 2] <= src_lim) & (frags_np[:, 1] + frags_np[:, 2] <= dst_lim))
+    fr = np.ascontiguousarray(frags_np[inside])
+    src_h = src_dev.view(torch.uint8)[:src_lim].cpu().numpy()
+    dst_h = np.zeros(dst_lim, dtype=np.uint8)
+    nbytes = 2 * int(fr[:, 2].sum())
+    reps, el = _repeat_for(lambda: oracle.copy_fragments(src_h, dst_h, fr), min_seconds)
+    return {"value": round(nbytes * reps / el / 1e9, 2), "unit": "GB/s", "threads": oracle.threads(),
+            "kind": "oracle",
+            "sample": (f"{label}: {len(fr)} of {len(frags_np)} fragments ({nbytes / 1e9:.3f} GB algorithmic); "
+                       f"{reps} repetitions in {el:.1f} s")}
+
+
+def oracle_cast_sample(torch, src_dev, items, n_items, label, min_seconds=3.0):
+    """The oracle's block-scaled cast of the first n_items cast items, each
+    read from a host copy of its strided source rows."""
+    import oracle
+    mats = []
+    nbytes = 0
+    flat = src_dev.view(torch.int16)
+    for it in items[:n_items]:
+        rows, cols, ld, off = int(it["rows"]), int(it["cols"]), int(it["src_ld"]), int(it["src_off"])
+        h = flat[off:off + (rows - 1) * ld + cols].cpu().numpy().view(np.uint16)
+        mats.append(np.lib.stride_tricks.as_strided(h, shape=(rows, cols), strides=(2 * ld, 2),
+                                                    writeable=False))
+        tiles = ((rows + 127) // 128) * ((cols + 127) // 128)
+        nbytes += 3 * rows * cols + 4 * tiles
+
+    def run():
+        for m in mats:
+            oracle.cast_fp8_blockscaled(m)
+    reps, el = _repeat_for(run, min_seconds)
+    return {"value": round(nbytes * reps / el / 1e9, 2), "unit": "GB/s", "threads": oracle.threads(),
+            "kind": "oracle",
+            "sample": (f"{label}: the first {n_items} of {len(items)} cast items ({nbytes / 1e9:.3f} GB "
+                       f"algorithmic); {reps} repetitions in {el:.1f} s")}
+
+
 def _cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -259,6 +312,10 @@ def run_reshard(torch, tc, synth, args, stream):
     out = {"fragments": int(nf), "tasks": int(total), "copy_planned": _stats(planned, nbytes),
            "plan_and_copy": _stats(full, nbytes), "copy_planned_digest": _stats(with_digest, nbytes),
            "digest_only_read": _stats(digest_only, nbytes // 2)}
+    if not args.skip_cpu:
+        # the whole shard copy: host working sets beyond any CPU cache
+        out["cpu_oracle"] = oracle_copy_sample(torch, stream_t, frags_np, 2 * n, 2 * tcv.shard_elems(spec, tp),
+                                               "the whole shard copy")
     del stream_t, shard, frags, ws, digests
     torch.cuda.empty_cache()
     return out
@@ -314,6 +371,8 @@ def run_cast(torch, tc, synth, args, stream):
     ms = _time_calls(torch, stream, lambda: tc.tc_cast_fp8_blockscaled(src, q, sc, it, ws, stream=stream),
                      args.warmup, args.cast_steps)
     out = {"items": int(len(items)), "tiles": int(n_scales), "cast": _stats(ms, nbytes)}
+    if not args.skip_cpu:
+        out["cpu_oracle"] = oracle_cast_sample(torch, src, items, 7, "layer 0 of the shard cast")
     del src
     torch.cuda.empty_cache()
     # the inverse rule on the shard just produced: e4m3 + scales -> bf16
@@ -371,6 +430,9 @@ def run_storm(torch, tc, synth, args, stream):
     out = {"fragments": 1_000_000, "payload_bytes": int(frags_np[:, 2].sum()), "tasks": int(total),
            "plan_and_copy": _stats(ms, nbytes), "copy_planned": _stats(planned, nbytes),
            "descriptors_sha256": synth.sha256(frags_np)}
+    if not args.skip_cpu:
+        out["cpu_oracle"] = oracle_copy_sample(torch, src, frags_np, 8 << 30, 8 << 30,
+                                               "fragments inside the first 8 GiB of both pools")
     del src, dst, frags, ws
     torch.cuda.empty_cache()
     return out
