@@ -797,14 +797,17 @@ __device__ __forceinline__ uint64_t bucket_of(uint64_t dst_off, int shift, uint6
   return b < nbk ? b : nbk - 1;
 }
 
+// Bucket sizes; each fragment keeps the count it found as its rank inside
+// its bucket (in no particular order), so the scatter needs no atomics.
 __global__ __launch_bounds__(kThreads) void k_bucket_hist(const tc_fragment* __restrict__ frags,
                                                          const int64_t n, const int shift,
                                                          const uint64_t nbk,
-                                                         uint64_t* __restrict__ cnt) {
+                                                         uint64_t* __restrict__ cnt,
+                                                         uint64_t* __restrict__ rank) {
   for (int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x; i < n;
        i += int64_t(gridDim.x) * kThreads)
-    atomicAdd(reinterpret_cast<unsigned long long*>(&cnt[bucket_of(frags[i].dst_off, shift, nbk)]),
-              1ull);
+    rank[i] = atomicAdd(
+        reinterpret_cast<unsigned long long*>(&cnt[bucket_of(frags[i].dst_off, shift, nbk)]), 1ull);
 }
 
 // Exclusive scan of v[0 .. m) in place, in three passes: sums of 1024
@@ -852,17 +855,18 @@ __global__ __launch_bounds__(kThreads) void k_scan_apply(uint64_t* __restrict__ 
   }
 }
 
+// Fragment i goes to its bucket's start plus its rank.
 __global__ __launch_bounds__(kThreads) void k_bucket_scatter(const tc_fragment* __restrict__ frags,
                                                             const int64_t n, const int shift,
                                                             const uint64_t nbk,
-                                                            uint64_t* __restrict__ off,
+                                                            const uint64_t* __restrict__ off,
+                                                            const uint64_t* __restrict__ rank,
                                                             tc_fragment* __restrict__ sorted,
                                                             uint64_t* __restrict__ perm) {
   for (int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x; i < n;
        i += int64_t(gridDim.x) * kThreads) {
     const tc_fragment f = frags[i];
-    const uint64_t pos = atomicAdd(
-        reinterpret_cast<unsigned long long*>(&off[bucket_of(f.dst_off, shift, nbk)]), 1ull);
+    const uint64_t pos = off[bucket_of(f.dst_off, shift, nbk)] + rank[i];
     sorted[pos] = f;
     perm[pos] = uint64_t(i);
   }
@@ -990,19 +994,22 @@ hipError_t launch_plan_reorder(const tc_fragment* frags, int64_t n, int shift, v
   uint64_t* sums = reinterpret_cast<uint64_t*>(base + L.bucket_sums);
   tc_fragment* sorted = reinterpret_cast<tc_fragment*>(base + L.sorted);
   uint64_t* perm = reinterpret_cast<uint64_t*>(base + L.perm);
+  // ranks live in tstart's room, which the recount after the reorder rewrites
+  uint64_t* rank = reinterpret_cast<uint64_t*>(base + L.tstart);
   const uint64_t nbk = L.nbuckets;
   const uint64_t sblocks = (nbk + kPlanPerBlock - 1) / kPlanPerBlock;
   const unsigned fgrid = grid_for((uint64_t(n) + kThreads - 1) / kThreads);
   hipLaunchKernelGGL(k_fill_zero, dim3(grid_for((nbk + kThreads - 1) / kThreads)), dim3(kThreads),
                      0, s, cnt, nbk);
-  hipLaunchKernelGGL(k_bucket_hist, dim3(fgrid), dim3(kThreads), 0, s, frags, n, shift, nbk, cnt);
+  hipLaunchKernelGGL(k_bucket_hist, dim3(fgrid), dim3(kThreads), 0, s, frags, n, shift, nbk, cnt,
+                     rank);
   hipLaunchKernelGGL(k_scan_sums, dim3((unsigned)sblocks), dim3(kThreads), 0, s,
                      (const uint64_t*)cnt, nbk, sums);
   hipLaunchKernelGGL(k_scan_one, dim3(1), dim3(kThreads), 0, s, sums, sblocks);
   hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)sblocks), dim3(kThreads), 0, s, cnt, nbk,
                      (const uint64_t*)sums);
   hipLaunchKernelGGL(k_bucket_scatter, dim3(fgrid), dim3(kThreads), 0, s, frags, n, shift, nbk,
-                     cnt, sorted, perm);
+                     (const uint64_t*)cnt, (const uint64_t*)rank, sorted, perm);
   return hipGetLastError();
 }
 
