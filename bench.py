@@ -160,6 +160,19 @@ def run_kv(torch, tc, synth, args, stream):
         "ids_sha256": synth.sha256(ids_np),
         "ids_distinct": int(len(np.unique(ids_np))),
     }
+    # one request's pages at a time (the first ids of the same stream), as a
+    # serving engine publishes and hydrates them; context for the batch above
+    req = {}
+    for tokens in (512, 4096, 16384, 35000):
+        k = -(-tokens // s.block_tokens)
+        ids_k = ids[:k]
+        nbytes = 2 * k * R * B
+        gk = _time_calls(torch, stream, lambda: tc.tc_gather_blocks(ra, nb, B, B, ids_k, buf, stream=stream),
+                         args.warmup, args.steps)
+        sk = _time_calls(torch, stream, lambda: tc.tc_scatter_blocks(rb, nb, B, B, ids_k, buf, stream=stream),
+                         args.warmup, args.steps)
+        req[f"{tokens}_tokens"] = {"blocks": k, "gather": _stats(gk, nbytes), "scatter": _stats(sk, nbytes)}
+    out["requests"] = req
     # CPU oracle on a bounded sample of the same workload
     if not args.skip_cpu:
         out["cpu"] = cpu_baseline_kv(torch, synth, s, ra, ids_np)
@@ -601,6 +614,8 @@ def main():
         })
         if "cpu" in kv:
             result["cpu_baseline"] = kv["cpu"]
+    if kv is not None:
+        extra = {"kv_requests": kv["requests"], **extra}
     result["workloads"] = extra
     if "roofline" in result and "calib" in extra:
         ceiling = extra["calib"]["library_copy"]["GBps"]
