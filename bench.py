@@ -440,13 +440,19 @@ def run_storm(torch, tc, synth, args, stream):
     total = tc.tc_plan_fragments(frags, ws, stream=stream)
     planned = _time_calls(torch, stream, lambda: tc.tc_copy_planned(src, dst, ws, total, stream=stream),
                           args.warmup, args.cast_steps)
+    nf = len(frags_np)
+    digests = torch.empty(2 * nf, dtype=torch.int64, device="cuda")
+    with_digest = _time_calls(
+        torch, stream, lambda: tc.tc_copy_planned_digest(src, dst, ws, total, nf, digests, stream=stream),
+        args.warmup, args.cast_steps)
     out = {"fragments": 1_000_000, "payload_bytes": int(frags_np[:, 2].sum()), "tasks": int(total),
            "plan_and_copy": _stats(ms, nbytes), "copy_planned": _stats(planned, nbytes),
+           "copy_planned_digest": _stats(with_digest, nbytes),
            "descriptors_sha256": synth.sha256(frags_np)}
     if not args.skip_cpu:
         out["cpu_oracle"] = oracle_copy_sample(torch, src, frags_np, 8 << 30, 8 << 30,
                                                "fragments inside the first 8 GiB of both pools")
-    del src, dst, frags, ws
+    del src, dst, frags, ws, digests
     torch.cuda.empty_cache()
     return out
 

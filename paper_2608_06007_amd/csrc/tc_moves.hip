@@ -45,6 +45,14 @@ __device__ __forceinline__ void st_sc1(u32x4* p, u32x4 v) {
 __device__ __forceinline__ void st_sc1_nt(u32x4* p, u32x4 v) {
   asm volatile("global_store_dwordx4 %0, %1, off sc1 nt" ::"v"(p), "v"(v) : "memory");
 }
+// The planned copies' store: plain NT for a reordered plan, SC1 NT otherwise
+// (plain is wave-uniform, read from the plan header).
+__device__ __forceinline__ void st_task(u32x4* p, u32x4 v, bool plain) {
+  if (plain)
+    st_nt(p, v);
+  else
+    st_sc1_nt(p, v);
+}
 
 // ------------------------------------------------------------------------
 // Block gather / scatter: work item w = 4 KiB tile k of chunk c = i*R + r
@@ -489,7 +497,7 @@ constexpr uint64_t kChunkVecs = 256;
 template <int kMode>
 __device__ __forceinline__ void task_sums(const uint8_t* s, uint8_t* d, const uint64_t len,
                                           const uint64_t dof, const int lane, const bool preloaded,
-                                          const u32x4 pre, u64x2* slot) {
+                                          const u32x4 pre, const bool plain, u64x2* slot) {
   uint64_t A = 0, W = 0;
   const uintptr_t sa = reinterpret_cast<uintptr_t>(s);
   const uintptr_t mis = kMode == kCopyDigest ? (sa ^ reinterpret_cast<uintptr_t>(d)) & 15 : 0;
@@ -498,7 +506,7 @@ __device__ __forceinline__ void task_sums(const uint8_t* s, uint8_t* d, const ui
     const uint64_t n16 = len >> 4;
     uint32_t a = 0, ws = 0;
     if (uint64_t(lane) < n16) {
-      if (kMode == kCopyDigest) st_sc1_nt(reinterpret_cast<u32x4*>(d) + lane, pre);
+      if (kMode == kCopyDigest) st_task(reinterpret_cast<u32x4*>(d) + lane, pre, plain);
       uint32_t vs, vw;
       vec_sums(pre, &vs, &vw);
       a = vs;
@@ -534,7 +542,7 @@ __device__ __forceinline__ void task_sums(const uint8_t* s, uint8_t* d, const ui
       const uint64_t i_end = min(n16, (c + 1) * kChunkVecs);
       for (uint64_t i = c * kChunkVecs + lane; i < i_end; i += kWaveLanes) {
         const u32x4 v = ld_nt(sv + i);
-        if (kMode == kCopyDigest) st_sc1_nt(dv + i, v);
+        if (kMode == kCopyDigest) st_task(dv + i, v, plain);
         uint32_t vs, vw;
         vec_sums(v, &vs, &vw);
         a += vs;
@@ -576,12 +584,14 @@ __device__ __forceinline__ void task_sums(const uint8_t* s, uint8_t* d, const ui
 template <int kMode, int kPerWave>
 __global__ __launch_bounds__(kThreads) void k_copy_digest(const uint8_t* __restrict__ src,
                                                          uint8_t* __restrict__ dst,
+                                                         const PlanHeader* __restrict__ hdr,
                                                          const Task* __restrict__ tasks,
                                                          u64x2* __restrict__ slots,
                                                          const uint64_t total,
                                                          const uint64_t nblocks,
                                                          uint64_t* __restrict__ digests,
                                                          const uint64_t words) {
+  const bool plain = kMode == kCopyDigest && hdr->permuted != 0;
   // clear the digests for the reduction that follows (it adds into them)
   for (uint64_t i = uint64_t(blockIdx.x) * kThreads + threadIdx.x; i < words;
        i += uint64_t(gridDim.x) * kThreads)
@@ -630,7 +640,7 @@ __global__ __launch_bounds__(kThreads) void k_copy_digest(const uint8_t* __restr
 #pragma unroll
       for (int k = 0; k < kPerWave; ++k) {
         if (uint64_t(lane) < (len[k] >> 4)) {
-          if (kMode == kCopyDigest) st_sc1_nt(reinterpret_cast<u32x4*>(d[k]) + lane, v[k]);
+          if (kMode == kCopyDigest) st_task(reinterpret_cast<u32x4*>(d[k]) + lane, v[k], plain);
           uint32_t vs, vw;
           vec_sums(v[k], &vs, &vw);
           a += vs;
@@ -655,7 +665,8 @@ __global__ __launch_bounds__(kThreads) void k_copy_digest(const uint8_t* __restr
 #pragma unroll
     for (int k = 0; k < kPerWave; ++k) {
       if (t0 + k >= total) break;
-      task_sums<kMode>(s[k], d[k], len[k], task_dst(tk[k]), lane, pre[k], v[k], slots + t0 + k);
+      task_sums<kMode>(s[k], d[k], len[k], task_dst(tk[k]), lane, pre[k], v[k], plain,
+                       slots + t0 + k);
     }
   }
 }
@@ -1054,6 +1065,7 @@ hipError_t launch_copy_digest(const uint8_t* src, uint8_t* dst, void* ws, const 
   uint8_t* base = static_cast<uint8_t*>(ws);
   const Task* tasks = reinterpret_cast<const Task*>(base + kTasksOffset);
   u64x2* slots = reinterpret_cast<u64x2*>(base + L.slots);
+  const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(base);
   // Tasks per wave: two for the copy (measured 6.1 vs 5.9 TB/s with one on a
   // TP=8 shard of 1 KiB pieces), four when only reading (4.9 vs 4.75; eight
   // gives no more).
@@ -1061,13 +1073,13 @@ hipError_t launch_copy_digest(const uint8_t* src, uint8_t* dst, void* ws, const 
   const uint64_t nblocks = (total + per_block - 1) / per_block;
   const dim3 grid(grid_for(nblocks)), block(kThreads);
   if (mode == kCopyDigest)
-    hipLaunchKernelGGL((k_copy_digest<kCopyDigest, 2>), grid, block, 0, s, src, dst, tasks, slots,
+    hipLaunchKernelGGL((k_copy_digest<kCopyDigest, 2>), grid, block, 0, s, src, dst, hdr, tasks, slots,
                        total, nblocks, digests, words);
   else if (mode == kDigestSrc)
-    hipLaunchKernelGGL((k_copy_digest<kDigestSrc, 4>), grid, block, 0, s, src, nullptr, tasks,
+    hipLaunchKernelGGL((k_copy_digest<kDigestSrc, 4>), grid, block, 0, s, src, nullptr, hdr, tasks,
                        slots, total, nblocks, digests, words);
   else
-    hipLaunchKernelGGL((k_copy_digest<kDigestDst, 4>), grid, block, 0, s, src, nullptr, tasks,
+    hipLaunchKernelGGL((k_copy_digest<kDigestDst, 4>), grid, block, 0, s, src, nullptr, hdr, tasks,
                        slots, total, nblocks, digests, words);
   const uint64_t rgrid = (total + kExpandPerBlock - 1) / kExpandPerBlock;
   hipLaunchKernelGGL(k_digest_reduce, dim3((unsigned)rgrid), dim3(kThreads), 0, s,
