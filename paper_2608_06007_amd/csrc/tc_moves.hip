@@ -21,6 +21,7 @@ constexpr int64_t kTileBytes = int64_t(kThreads) * 16;  // 4 KiB per workgroup
 constexpr int kXcds = 8;
 constexpr uint64_t kXcdGroup = 64;           // consecutive tiles per XCD run
 constexpr uint64_t kXcdGroupScatter = 512;   // hydrate: longer runs stream its reads better
+constexpr uint64_t kXcdGroupReordered = 256;  // task copies of destination-ordered plans
 
 // Work item of block b when the 8 XCDs each take runs of G consecutive items
 // (a bijection on [0, N); the last partial round keeps the identity order).
@@ -388,8 +389,9 @@ __global__ __launch_bounds__(kThreads) void k_copy_tasks(const uint8_t* __restri
   const int lane = threadIdx.x & (kWaveLanes - 1);
   const uint64_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const bool reordered = hdr->permuted != 0;
+  const uint64_t group = reordered ? kXcdGroupReordered : kXcdGroup;
   for (uint64_t b = blockIdx.x; b < nblocks; b += gridDim.x) {
-    const uint64_t t = xcd_grouped(b, nblocks, kXcdGroup) * kTasksPerBlock + w;
+    const uint64_t t = xcd_grouped(b, nblocks, group) * kTasksPerBlock + w;
     if (t >= total) continue;
     const Task tk = tasks[t];
     const uint8_t* s = src + task_src(tk);
@@ -592,6 +594,7 @@ __global__ __launch_bounds__(kThreads) void k_copy_digest(const uint8_t* __restr
                                                          uint64_t* __restrict__ digests,
                                                          const uint64_t words) {
   const bool plain = kMode == kCopyDigest && hdr->permuted != 0;
+  const uint64_t group = plain ? kXcdGroupReordered : kXcdGroup;
   // clear the digests for the reduction that follows (it adds into them)
   for (uint64_t i = uint64_t(blockIdx.x) * kThreads + threadIdx.x; i < words;
        i += uint64_t(gridDim.x) * kThreads)
@@ -599,7 +602,7 @@ __global__ __launch_bounds__(kThreads) void k_copy_digest(const uint8_t* __restr
   const int lane = threadIdx.x & (kWaveLanes - 1);
   const uint64_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   for (uint64_t b = blockIdx.x; b < nblocks; b += gridDim.x) {
-    const uint64_t t0 = (xcd_grouped(b, nblocks, kXcdGroup) * kTasksPerBlock + w) * kPerWave;
+    const uint64_t t0 = (xcd_grouped(b, nblocks, group) * kTasksPerBlock + w) * kPerWave;
     if (t0 >= total) continue;
     const uint8_t* s[kPerWave];
     uint8_t* d[kPerWave];
