@@ -117,7 +117,9 @@ typedef struct {
 /* Recommended bytes of device workspace for a plan of n descriptors.  A
  * plan cuts every fragment into tasks of at most `piece` bytes (1 KiB, or the
  * next power of two, at most 2^30, that keeps the task table inside the
- * workspace) and spreads the tasks over the whole GPU, one task per wave.  A
+ * workspace) and spreads the tasks over the whole GPU, one task per wave.
+ * With 1 KiB pieces every task after a fragment's first starts on a 128-byte
+ * line of the destination, so a fragment may take one task more.  A
  * task costs 32 bytes (the packed task and its digest slot) plus 16 bytes per
  * 1024 tasks; a descriptor costs at most ~48 bytes of planning scratch.  A
  * workspace with room for T >= n + 1 tasks accepts payloads up to
