@@ -200,12 +200,51 @@ def test_tp_shard_cast_70b_layers(layers, ranks):
     torch.cuda.empty_cache()
 
 
+def _sampled_tiles_match_oracle(src, q, s, items, rng, count):
+    """count random 128x128 tiles of random items: codes and scale bits of
+    the GPU cast against the oracle's cast of the same source tile."""
+    for k in rng.choice(len(items), size=min(count, len(items)), replace=False):
+        it = items[k]
+        rows, cols = int(it["rows"]), int(it["cols"])
+        tr, tcn = (rows + 127) // 128, (cols + 127) // 128
+        ti, tj = int(rng.integers(0, tr)), int(rng.integers(0, tcn))
+        r0, c0 = ti * 128, tj * 128
+        ld = int(it["src_ld"])
+        base = int(it["src_off"]) + r0 * ld + c0
+        tile = _host(src[base:base + 127 * ld + 128].view(torch.int16)).view(np.uint16)
+        view = np.lib.stride_tricks.as_strided(tile, shape=(128, 128), strides=(2 * ld, 2))
+        want_q, want_s = oracle.cast_fp8_blockscaled(view)
+        dld = int(it["dst_ld"])
+        dq = int(it["dst_off"]) + r0 * dld + c0
+        got_q = _host(q[dq:dq + 127 * dld + 128])
+        got_q = np.lib.stride_tricks.as_strided(got_q, shape=(128, 128), strides=(dld, 1))
+        assert np.array_equal(got_q, want_q), (k, ti, tj)
+        got_s = _host(s[int(it["scale_off"]) + ti * int(it["scale_ld"]) + tj])
+        assert got_s.view(np.uint32) == want_s.view(np.uint32)[0, 0]
+
+
+def _every_tile_reaches_448(q, items):
+    """The element with |x| = amax encodes to +-448 (0x7E / 0xFE): the
+    largest code magnitude of every tile is 0x7E.  Item sizes here are
+    multiples of 128."""
+    for it in items:
+        rows, cols, ld, off = int(it["rows"]), int(it["cols"]), int(it["dst_ld"]), int(it["dst_off"])
+        assert rows % 128 == 0 and cols % 128 == 0
+        m = q[off:off + (rows - 1) * ld + cols].as_strided((rows, cols), (ld, 1))
+        mag = torch.bitwise_and(m, 0x7F).contiguous().view(rows // 128, 128, cols // 128, 128)
+        tmax = mag.amax(dim=(1, 3))
+        assert bool((tmax == 0x7E).all()), int(tmax.min())
+
+
 def test_tp_shard_cast_70b_full_size():
     """All 80 layers (136.9 GB of bf16 in HBM), rank 3 of TP=8: the shard
     slices hold N(0, 0.02) values and everything outside them is poisoned with
     a huge value, so a read outside the slice would change the scales.
     Sampled tiles against the oracle; every scale is checked to be a normal
-    N(0, 0.02) tile scale (no poison), and every tile's largest code is +-448."""
+    N(0, 0.02) tile scale (no poison), and every tile's largest code is +-448.
+    Then the inverse rule over the whole shard: sampled tiles against the
+    oracle, and every element within the E4M3 + bf16 rounding bound of its
+    source value."""
     tp, rank = 8, 3
     spec = synth.spec_70b(80)
     n = synth.spec_elems(spec)
@@ -231,27 +270,62 @@ def test_tp_shard_cast_70b_full_size():
     torch.cuda.synchronize()
     # no poisoned tile: every scale is what an N(0, 0.02) tile gives
     assert bool(((s > 1e-5) & (s < 1e-3)).all())
-    # sampled tiles against the oracle
+    _every_tile_reaches_448(q, items)
     rng = np.random.default_rng(55)
-    for k in rng.choice(len(items), size=40, replace=False):
-        it = items[k]
+    _sampled_tiles_match_oracle(stream, q, s, items, rng, 40)
+
+    # the inverse rule over the whole shard
+    ditems = tcv.dequant_items(spec, tp)
+    y = torch.empty(tcv.shard_elems(spec, tp), dtype=torch.bfloat16, device=DEV)
+    dws = torch.empty(tc.tc_dequant_fp8_workspace(len(ditems)), dtype=torch.uint8, device=DEV)
+    tc.tc_dequant_fp8_blockscaled(q, s, y, ditems, dws)
+    torch.cuda.synchronize()
+    smax = float(s.max())
+    for it, dit in zip(items, ditems):
         rows, cols = int(it["rows"]), int(it["cols"])
-        tr, tcn = (rows + 127) // 128, (cols + 127) // 128
-        ti, tj = int(rng.integers(0, tr)), int(rng.integers(0, tcn))
-        r0, c0 = ti * 128, tj * 128
-        ld = int(it["src_ld"])
-        base = int(it["src_off"]) + r0 * ld + c0
-        rows_t = stream[base:base + 127 * ld + 128].view(torch.int16)
-        tile = _host(rows_t).view(np.uint16)
-        view = np.lib.stride_tricks.as_strided(tile, shape=(128, 128), strides=(2 * ld, 2))
-        want_q, want_s = oracle.cast_fp8_blockscaled(view)
-        dq = int(it["dst_off"]) + r0 * int(it["dst_ld"]) + c0
-        got_q = _host(q[dq:dq + 127 * int(it["dst_ld"]) + 128])
-        got_q = np.lib.stride_tricks.as_strided(got_q, shape=(128, 128), strides=(int(it["dst_ld"]), 1))
-        assert np.array_equal(got_q, want_q), (k, ti, tj)
-        got_s = _host(s[int(it["scale_off"]) + ti * int(it["scale_ld"]) + tj])
-        assert got_s.view(np.uint32) == want_s.view(np.uint32)[0, 0]
-    del stream, q, s
+        x = stream[int(it["src_off"]):int(it["src_off"]) + (rows - 1) * int(it["src_ld"]) + cols]
+        x = x.as_strided((rows, cols), (int(it["src_ld"]), 1)).float()
+        yy = y[int(dit["dst_off"]):int(dit["dst_off"]) + rows * cols].view(rows, cols).float()
+        # E4M3 keeps 3 mantissa bits (half an ulp: 2^-4 relative), bf16 adds
+        # 2^-8; below the normal range the step is s * 2^-9 (half: s * 2^-10)
+        bound = (2.0 ** -4 + 2.0 ** -8 + 2.0 ** -12) * x.abs() + smax * 2.0 ** -10
+        assert bool(((yy - x).abs() <= bound).all()), it
+    for k in rng.choice(len(ditems), size=20, replace=False):
+        dit = ditems[k]
+        rows, cols = int(dit["rows"]), int(dit["cols"])
+        ti, tj = int(rng.integers(0, rows // 128)), int(rng.integers(0, cols // 128))
+        qo = int(dit["src_off"]) + ti * 128 * int(dit["src_ld"]) + tj * 128
+        qt = _host(q[qo:qo + 127 * int(dit["src_ld"]) + 128])
+        qt = np.lib.stride_tricks.as_strided(qt, shape=(128, 128), strides=(int(dit["src_ld"]), 1))
+        st = _host(s[int(dit["scale_off"]) + ti * int(dit["scale_ld"]) + tj]).reshape(1, 1)
+        want = oracle.dequant_fp8_blockscaled(np.ascontiguousarray(qt), st)
+        yo = int(dit["dst_off"]) + ti * 128 * int(dit["dst_ld"]) + tj * 128
+        got = _host(y[yo:yo + 127 * int(dit["dst_ld"]) + 128].view(torch.int16)).view(np.uint16)
+        got = np.lib.stride_tricks.as_strided(got, shape=(128, 128), strides=(2 * int(dit["dst_ld"]), 2))
+        assert np.array_equal(got, want), (k, ti, tj)
+    del stream, q, s, y
+    torch.cuda.empty_cache()
+
+
+def test_reshard_cast_70b_full_size():
+    """The timed reshard into fp8 at full size: 70B-shaped weights held as the
+    eight bf16 shards of a TP=8 split (136.9 GB, N(0, 0.02)) cast into rank 1
+    of a TP=4 split.  Sampled tiles against the oracle; every scale in the
+    N(0, 0.02) range; every tile's largest code is +-448."""
+    src_tp, dst_tp, rank = 8, 4, 1
+    spec = synth.spec_70b(80)
+    n = synth.spec_elems(spec)
+    src = synth.bf16_normal(n, 0.02, synth.SEED_CAST_70B, device=DEV)
+    items = tcv.reshard_cast_items(spec, src_tp, dst_tp, rank)
+    q = torch.empty(tcv.shard_elems(spec, dst_tp), dtype=torch.uint8, device=DEV)
+    s = torch.full((tcv.scale_elems(spec, dst_tp),), float("nan"), dtype=torch.float32, device=DEV)
+    ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device=DEV)
+    tc.tc_cast_fp8_blockscaled(src, q, s, items, ws)
+    torch.cuda.synchronize()
+    assert bool(((s > 1e-5) & (s < 1e-3)).all())      # every scale written, none poisoned
+    _every_tile_reaches_448(q, items)
+    _sampled_tiles_match_oracle(src, q, s, items, np.random.default_rng(56), 40)
+    del src, q, s
     torch.cuda.empty_cache()
 
 
