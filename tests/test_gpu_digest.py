@@ -203,3 +203,28 @@ def test_digest_reshard_8b_full_size():
     del want_dst
     hsrc = _host(src.view(torch.uint8))
     assert np.array_equal(_as_u64(dg, n), oracle.fragment_digests(hsrc, frags_np, use_src=True))
+
+
+def test_digest_storm_full_size():
+    """The timed storm with digests: 1,000,000 fragments in two 16 GiB pools,
+    planned in destination order with the line cut; every digest of the
+    copy and of a read of the destination against the oracle over the host
+    copy of the source."""
+    pool = 16 << 30
+    frags_np = synth.fragment_storm(1_000_000, pool, seed=synth.SEED_STORM)
+    n = len(frags_np)
+    src = synth.random_bytes(pool, synth.SEED_STORM, device=DEV)
+    frags, ws, total = _plan(frags_np)
+    dst = torch.empty(pool, dtype=torch.uint8, device=DEV)
+    dg, dd = _digests(n), _digests(n)
+    tc.tc_copy_planned_digest(src, dst, ws, total, n, dg)
+    tc.tc_digest_planned(dst, tc.DIGEST_DST, ws, total, n, dd)
+    torch.cuda.synchronize()
+    del dst
+    want = oracle.fragment_digests(_host(src), frags_np, use_src=True)
+    got = _as_u64(dg, n)
+    bad = np.nonzero(np.any(got != want, axis=1))[0]
+    assert bad.size == 0, f"{bad.size} digests differ, first fragments {bad[:5]}"
+    assert np.array_equal(_as_u64(dd, n), want)
+    del src
+    torch.cuda.empty_cache()
