@@ -34,6 +34,13 @@ __device__ __forceinline__ uint64_t xcd_grouped(uint64_t b, uint64_t N, uint64_t
 }
 
 __device__ __forceinline__ u32x4 ld_nt(const u32x4* p) { return __builtin_nontemporal_load(p); }
+// The same load through a global-address-space pointer, for addresses the
+// compiler cannot prove global (pool bases passed as integers): a global
+// rather than a flat load.
+typedef const u32x4 __attribute__((address_space(1))) global_u32x4;
+__device__ __forceinline__ u32x4 ld_nt_global(const void* p) {
+  return __builtin_nontemporal_load((global_u32x4*)p);
+}
 // Vector stores with the SC1 scope bit, alone (gather's contiguous output) or
 // with NT (hydrate's scattered blocks, planned copies of ordered lists):
 // measured +1-4% over plain non-temporal stores on those streams.  Plans
@@ -78,7 +85,7 @@ __global__ __launch_bounds__(kThreads) void k_blocks_vec(const RegionTable tab, 
     const int64_t off = int64_t(k) * kTileBytes + int64_t(threadIdx.x) * 16;
     if (off < B) {
       if (kGather)
-        st_sc1(reinterpret_cast<u32x4*>(xfer + off), ld_nt(reinterpret_cast<const u32x4*>(pool + off)));
+        st_sc1(reinterpret_cast<u32x4*>(xfer + off), ld_nt_global(pool + off));
       else
         st_sc1_nt(reinterpret_cast<u32x4*>(pool + off), ld_nt(reinterpret_cast<const u32x4*>(xfer + off)));
     }
