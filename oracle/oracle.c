@@ -10,6 +10,12 @@
  *   block-scaled E4M3 cast ............. a transform_into `spec` rule
  *                                        (Table 2); encoding per the OCP
  *                                        8-bit floating point definition.
+ *   inverse cast ....................... E4M3 codes and tile scales back to
+ *                                        bf16 (the training-side rule of
+ *                                        Sec. 7)
+ *   fragment digests ................... the pipeline's verify-integrity
+ *                                        stage (Sec. 5): a byte sum and a
+ *                                        position-weighted byte sum
  * Build: gcc -O2 -fno-fast-math -fopenmp -shared -fPIC.
  */
 #include "oracle.h"

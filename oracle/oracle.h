@@ -17,7 +17,12 @@
  *     concrete `spec` rule for transform_into (Table 2, Sec. 3.2).  The paper
  *     gives no numeric format; the E4M3 encoding follows the OCP 8-bit
  *     floating point definition (bias 7, largest finite 448, NaN S.1111.111,
- *     no infinities), rounding to nearest with ties to even, saturating.
+ *     no infinities), rounding to nearest with ties to even, saturating;
+ *   - the inverse cast: codes times the tile's scale, rounded to binary32 and
+ *     then to bf16 (the training-side transform_into of Sec. 7);
+ *   - fragment digests for the pipeline's verify-integrity stage (Sec. 5):
+ *     S1 = sum of the fragment's bytes, S2 = sum of (i + 1) * byte i, both
+ *     mod 2^64.
  *
  * Threads: OpenMP over independent units (blocks, fragments, tiles).
  * Floating point: IEEE binary32 division and comparisons; the library is
