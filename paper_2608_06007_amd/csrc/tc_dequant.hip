@@ -17,6 +17,14 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
+// bf16 stores with the SC1 scope bit and NT (measured on the 70B shard:
+// 5809 against 5709 GB/s with plain NT stores).  The store reads its 16 data
+// bytes after issue, and a VALU write to those registers needs 2 wait states;
+// the compiler cannot see into inline asm, so s_nop 1 provides them.
+__device__ __forceinline__ void st_sc1_nt(u32x4* p, u32x4 v) {
+  asm volatile("global_store_dwordx4 %0, %1, off sc1 nt\n\ts_nop 1" ::"v"(p), "v"(v) : "memory");
+}
+
 constexpr int kWaveLanes = 64;
 constexpr int kTile = 128;
 constexpr int kThreads = 512;
@@ -88,9 +96,8 @@ __global__ __launch_bounds__(kThreads) void k_dequant_full(const uint8_t* __rest
 #pragma unroll
   for (int p = 0; p < kPasses; ++p) {
     const u32x2 lo = dequant4(v[p].x, s), hi = dequant4(v[p].y, s);
-    __builtin_nontemporal_store(
-        u32x4{lo.x, lo.y, hi.x, hi.y},
-        reinterpret_cast<u32x4*>(ys + int64_t(p * kRowsPerPass + prow) * item.dst_ld + seg * 8));
+    st_sc1_nt(reinterpret_cast<u32x4*>(ys + int64_t(p * kRowsPerPass + prow) * item.dst_ld + seg * 8),
+              u32x4{lo.x, lo.y, hi.x, hi.y});
   }
 }
 

@@ -47,11 +47,16 @@ __device__ __forceinline__ u32x4 ld_nt_global(const void* p) {
 // built from unordered destination lists (small fragments with scattered
 // sources, copied in destination order) store with plain NT: +8% there.
 __device__ __forceinline__ void st_nt(u32x4* p, u32x4 v) { __builtin_nontemporal_store(v, p); }
+//
+// A store of more than 8 bytes reads its data registers after issue: a VALU
+// write to them needs 2 wait states on this GPU.  The compiler inserts them
+// for its own stores but cannot see into inline asm, so each asm store ends
+// with s_nop 1 (2 wait states) before any later instruction of the wave.
 __device__ __forceinline__ void st_sc1(u32x4* p, u32x4 v) {
-  asm volatile("global_store_dwordx4 %0, %1, off sc1" ::"v"(p), "v"(v) : "memory");
+  asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_nop 1" ::"v"(p), "v"(v) : "memory");
 }
 __device__ __forceinline__ void st_sc1_nt(u32x4* p, u32x4 v) {
-  asm volatile("global_store_dwordx4 %0, %1, off sc1 nt" ::"v"(p), "v"(v) : "memory");
+  asm volatile("global_store_dwordx4 %0, %1, off sc1 nt\n\ts_nop 1" ::"v"(p), "v"(v) : "memory");
 }
 // The planned copies' store: plain NT for a reordered plan, SC1 NT otherwise
 // (plain is wave-uniform, read from the plan header).
