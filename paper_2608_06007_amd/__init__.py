@@ -166,11 +166,14 @@ def _ok(status: int, what: str) -> None:
 
 
 def _dev_ptr(x) -> int:
-    """Device address of a torch tensor (must live on a GPU) or a raw int."""
+    """Device address of a torch tensor (must live on a GPU and be contiguous:
+    the library addresses it as one flat byte range) or a raw int."""
     if isinstance(x, int):
         return x
     if not x.is_cuda:
         raise ValueError("expected a device tensor")
+    if not x.is_contiguous():
+        raise ValueError("expected a contiguous device tensor")
     return x.data_ptr()
 
 

@@ -88,6 +88,26 @@ def test_gather_repeated_ids_and_empty():
     tc.tc_scatter_blocks(regions, nb, B, B, empty, out)
 
 
+def test_binding_refuses_host_and_strided_tensors():
+    """The library addresses every buffer as one flat device byte range, so
+    the binding refuses host tensors and non-contiguous views before any
+    launch (a strided view's flat range would reach past the view)."""
+    nb, B = 8, 256
+    regions = _regions_random(2, nb, B, B, 11)
+    ids = torch.tensor([1, 3], dtype=torch.int32, device=DEV)
+    out = torch.empty(2 * 2 * B, dtype=torch.uint8, device=DEV)
+    with pytest.raises(ValueError):
+        tc.tc_gather_blocks(regions, nb, B, B, ids, out.cpu())
+    strided = torch.empty(2 * 2 * B * 2, dtype=torch.uint8, device=DEV)[::2]
+    with pytest.raises(ValueError):
+        tc.tc_gather_blocks(regions, nb, B, B, ids, strided)
+    with pytest.raises(ValueError):
+        tc.tc_gather_blocks(regions, nb, B, B, torch.tensor([1, 0, 3, 0], dtype=torch.int32,
+                                                            device=DEV)[::2], out)
+    tc.tc_gather_blocks(regions, nb, B, B, ids, out)         # the same call, contiguous
+    torch.cuda.synchronize()
+
+
 def test_interleaved_engine_layout():
     """One allocation laid out [blocks][2][...]: K and V of a layer are two
     regions with base offset block_bytes apart and stride 2*block_bytes."""
