@@ -466,7 +466,7 @@ tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace
       if (e == hipSuccess) e = tc::launch_plan_count(planned, n, piece, cut, workspace, L, true, stream);
       if (e != hipSuccess) return hip_fail(e);
     }
-    e = tc::launch_plan_expand(planned, n, hdr.total_tasks, piece, cut, workspace, L, stream);
+    e = tc::launch_plan_expand(planned, hdr.total_tasks, piece, cut, workspace, L, stream);
     if (e != hipSuccess) return hip_fail(e);
     if (total_tasks) *total_tasks = hdr.total_tasks;
     return TC_OK;

@@ -218,7 +218,7 @@ __global__ __launch_bounds__(kCastThreads) void k_cast_edge(const uint16_t* __re
                                                            const uint64_t* __restrict__ prefix,
                                                            const uint8_t* __restrict__ aligned,
                                                            const int64_t n_items,
-                                                           const uint64_t t0, const uint64_t count) {
+                                                           const uint64_t t0) {
   __shared__ uint32_t red[kCastWaves];
   const int lane = threadIdx.x & (kWaveLanes - 1);
   const uint64_t t = t0 + blockIdx.x;
@@ -345,7 +345,7 @@ hipError_t launch_cast_blockscaled(const uint16_t* src, uint8_t* dst, float* sca
   for (uint64_t t0 = 0; t0 < edge_tiles; t0 += kMaxGrid) {
     const uint64_t cnt = edge_tiles - t0 < kMaxGrid ? edge_tiles - t0 : kMaxGrid;
     hipLaunchKernelGGL(k_cast_edge, dim3((unsigned)cnt), dim3(kCastThreads), 0, s, src, dst, scales,
-                       items, ep, al, n_items, t0, cnt);
+                       items, ep, al, n_items, t0);
   }
   return hipGetLastError();
 }

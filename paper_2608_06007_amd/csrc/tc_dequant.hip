@@ -109,8 +109,7 @@ __global__ __launch_bounds__(kThreads) void k_dequant_edge(const uint8_t* __rest
                                                           const tc_dequant_item* __restrict__ items,
                                                           const uint64_t* __restrict__ prefix,
                                                           const uint8_t* __restrict__ aligned,
-                                                          const int64_t n_items, const uint64_t t0,
-                                                          const uint64_t count) {
+                                                          const int64_t n_items, const uint64_t t0) {
   const int lane = threadIdx.x & (kWaveLanes - 1);
   const uint64_t t = t0 + blockIdx.x;
   const int64_t it = find_item(prefix, n_items, t, lane);
@@ -160,7 +159,7 @@ hipError_t launch_dequant_blockscaled(const uint8_t* codes, const float* scales,
   for (uint64_t t0 = 0; t0 < edge_tiles; t0 += kMaxGrid) {
     const uint64_t cnt = edge_tiles - t0 < kMaxGrid ? edge_tiles - t0 : kMaxGrid;
     hipLaunchKernelGGL(k_dequant_edge, dim3((unsigned)cnt), dim3(kThreads), 0, s, codes, scales, dst,
-                       items, ep, al, n_items, t0, cnt);
+                       items, ep, al, n_items, t0);
   }
   return hipGetLastError();
 }

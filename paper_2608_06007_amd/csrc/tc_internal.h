@@ -102,9 +102,8 @@ hipError_t launch_plan_count(const tc_fragment* frags, int64_t n, uint64_t piece
 hipError_t launch_plan_reorder(const tc_fragment* frags, int64_t n, int shift, void* ws,
                                const PlanLayout& L, hipStream_t s);
 // Expand the counted plan into its task table (total_tasks known on the host).
-hipError_t launch_plan_expand(const tc_fragment* frags, int64_t n, uint64_t total_tasks,
-                              uint64_t piece, uint64_t cut, void* ws, const PlanLayout& L,
-                              hipStream_t s);
+hipError_t launch_plan_expand(const tc_fragment* frags, uint64_t total_tasks, uint64_t piece,
+                              uint64_t cut, void* ws, const PlanLayout& L, hipStream_t s);
 hipError_t launch_copy_tasks(const uint8_t* src, uint8_t* dst, const void* ws,
                              uint64_t total_tasks, hipStream_t s);
 // Copy (mode 0) or only read (1: at the tasks' source offsets, 2: at their

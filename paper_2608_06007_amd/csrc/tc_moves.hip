@@ -1039,8 +1039,7 @@ hipError_t launch_plan_reorder(const tc_fragment* frags, int64_t n, int shift, v
   return hipGetLastError();
 }
 
-hipError_t launch_plan_expand(const tc_fragment* frags, int64_t n, uint64_t total, uint64_t piece,
-                              uint64_t cut,
+hipError_t launch_plan_expand(const tc_fragment* frags, uint64_t total, uint64_t piece, uint64_t cut,
                               void* ws, const PlanLayout& L, hipStream_t s) {
   if (total == 0) return hipSuccess;
   uint8_t* base = static_cast<uint8_t*>(ws);
