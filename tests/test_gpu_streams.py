@@ -120,3 +120,45 @@ def test_graph_capture_and_replay():
                               oracle.fragment_digests(hf, frags_np)), rep
         xb = x.view(torch.int16).cpu().numpy().view(np.uint16)
         assert np.array_equal(q.cpu().numpy(), oracle.cast_fp8_scaled(xb, 0.25)), rep
+
+
+def test_concurrent_streams_independent_plans():
+    """Three streams at once, none waiting for another: two planned copies
+    with digests on their own workspaces (one plan reordered, one not) and a
+    block gather.  Each result against the oracle."""
+    pool = 64 << 20
+    fa = synth.fragment_storm(6000, pool, seed=65)                   # unordered: reordered plan
+    fb = fa[np.argsort(fa[:, 1], kind="stable")]                      # the same, ordered
+    src = synth.random_bytes(pool, 66, device=DEV)
+    outs, plans = [], []
+    for fr in (fa, fb):
+        frags = torch.from_numpy(fr.view(np.int64)).to(DEV)
+        ws = torch.empty(tc.tc_copy_fragments_workspace(len(fr)), dtype=torch.uint8, device=DEV)
+        plans.append((fr, ws, tc.tc_plan_fragments(frags, ws),
+                      torch.zeros(pool, dtype=torch.uint8, device=DEV),
+                      torch.empty(2 * len(fr), dtype=torch.int64, device=DEV)))
+    R, nb, B = 4, 256, 32768
+    ids_np = synth.ids_without_replacement(nb, 200, seed=67)
+    ids = torch.from_numpy(ids_np).to(DEV)
+    kv_flat, kv = _pool(R, nb, B)
+    kv_flat.copy_(synth.random_bytes(kv_flat.numel(), 68, device=DEV))
+    buf = torch.empty(200 * R * B, dtype=torch.uint8, device=DEV)
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream() for _ in range(3)]
+    for _ in range(3):                          # repeated, so the calls overlap in time
+        for (fr, ws, total, dst, dg), st in zip(plans, streams):
+            tc.tc_copy_planned_digest(src, dst, ws, total, len(fr), dg, stream=st)
+        tc.tc_gather_blocks(kv, nb, B, B, ids, buf, stream=streams[2])
+    for st in streams:
+        st.synchronize()
+    hsrc = src.cpu().numpy()
+    for fr, ws, total, dst, dg in plans:
+        want = np.zeros(pool, np.uint8)
+        oracle.copy_fragments(hsrc, want, fr)
+        assert np.array_equal(dst.cpu().numpy(), want)
+        got = dg.cpu().numpy().view(np.uint64).reshape(-1, 2)
+        assert np.array_equal(got, oracle.fragment_digests(hsrc, fr, use_src=True))
+    want = oracle.gather_blocks([r.cpu().numpy() for r in kv], B, B, ids_np)
+    assert np.array_equal(buf.cpu().numpy(), want.reshape(-1))
+    assert int(plans[0][1][56:64].cpu().numpy().view(np.uint64)[0]) == 1   # reordered
+    assert int(plans[1][1][56:64].cpu().numpy().view(np.uint64)[0]) == 0
