@@ -416,7 +416,8 @@ tc_status tc_dequant_fp8_blockscaled(const void* codes_base, const float* scale_
 typedef struct tc_stager tc_stager;
 tc_status tc_stager_create(size_t slot_bytes, int32_t slots, int32_t host_threads,
                            tc_stager** out);
-/* Waits for the stager's copies, then frees everything it owns. */
+/* Waits for the stager's copies, then frees everything it owns.  No other
+ * thread may be inside a call on this stager (its lock is freed too). */
 tc_status tc_stager_destroy(tc_stager* stager);
 /* host_src (bytes) -> dev_dst (bytes). */
 tc_status tc_stage_h2d(tc_stager* stager, const void* host_src, void* dev_dst, size_t bytes,
