@@ -129,7 +129,9 @@ typedef struct {
  * 2^48. */
 size_t tc_copy_fragments_workspace(int64_t n); /* 0 for n < 0 or n > 2^40 */
 /* Smallest workspace a plan of n descriptors accepts (room for n + 1 tasks;
- * the task size then grows to fit, so payloads up to 2^30 bytes always fit). */
+ * the task size then grows to fit, so payloads up to 2^30 bytes always fit).
+ * Fewer, longer tasks use fewer waves: a copy needs tens of thousands of
+ * tasks to fill the GPU, which the recommended size provides. */
 size_t tc_copy_fragments_workspace_min(int64_t n);
 
 /* Copy every fragment: tc_plan_fragments + tc_copy_planned.  frags: device
