@@ -524,6 +524,37 @@ def run_stage(torch, tc, synth, args, stream):
         out["publish_pinned"] = wall(lambda: tc.tc_publish_to_host(h, regions, nb, B, B, ids, pinned, stage, stream=stream))
         out["hydrate_pinned"] = wall(lambda: tc.tc_hydrate_from_host(h, regions, nb, B, B, ids, pinned, stage, stream=stream))
 
+    # Both directions at once (PCIe is full duplex): one stager publishes the
+    # first half of the ids while a second, on its own stream and thread,
+    # hydrates the other half; the rate is over all bytes moved.
+    import threading
+    half = len(ids) // 2
+    ids_a, ids_b = ids[:half], ids[half:]
+    part = half * R * B
+    host_a, host_b = host[:part], host[part:2 * part]
+    stage2 = torch.empty_like(stage)
+    s_a, s_b = torch.cuda.Stream(), torch.cuda.Stream()
+    with tc.Stager() as sa, tc.Stager() as sb:
+        def duplex(dst_a, src_b):
+            err = []
+
+            def publish():
+                try:
+                    tc.tc_publish_to_host(sa.handle, regions, nb, B, B, ids_a, dst_a, stage, stream=s_a)
+                except Exception as e:  # reported after the join
+                    err.append(e)
+            t = threading.Thread(target=publish)
+            t.start()
+            tc.tc_hydrate_from_host(sb.handle, regions, nb, B, B, ids_b, src_b, stage2, stream=s_b)
+            t.join()
+            if err:
+                raise err[0]
+        for key, (dst_a, src_b) in (("duplex_pageable", (host_a, host_b)),
+                                    ("duplex_pinned", (pinned[:part], pinned[part:2 * part]))):
+            d = wall(lambda: duplex(dst_a, src_b))
+            d["frac_of_pcie"] = round(d["GBps"] / (2 * PEAK_PCIE_GBS), 4)   # both directions' peak
+            out[key] = d
+
     def runtime_publish():
         tc.tc_gather_blocks(regions, nb, B, B, ids, buf, stream=stream)
         host_t.copy_(buf)
@@ -534,7 +565,7 @@ def run_stage(torch, tc, synth, args, stream):
 
     out["runtime_publish_pageable"] = wall(runtime_publish)
     out["runtime_hydrate_pageable"] = wall(runtime_hydrate)
-    del pool, regions, pinned, stage, buf, host_t, host
+    del pool, regions, pinned, stage, stage2, buf, host_t, host
     torch.cuda.empty_cache()
     return out
 

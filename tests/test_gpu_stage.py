@@ -169,3 +169,41 @@ def test_hydrate_publish_full_size_kv():
         assert int(rb[r].count_nonzero()) == int(blocks_a.count_nonzero())
     del a, b, ra, rb
     torch.cuda.empty_cache()
+
+
+def test_duplex_publish_and_hydrate_on_two_stagers():
+    """Two stagers at once, from two host threads on two streams: one
+    publishes some ids' blocks to host memory while the other hydrates other
+    ids from host memory into the same pool.  Both results against the
+    oracle; the blocks of neither call's ids change."""
+    import threading
+    R, nb, B = 4, 256, 16384
+    rng = np.random.default_rng(120)
+    host_pool = [rng.integers(0, 256, size=nb * B, dtype=np.uint8) for _ in range(R)]
+    flat = torch.from_numpy(np.concatenate(host_pool)).to(DEV)
+    regions = [flat[r * nb * B:(r + 1) * nb * B] for r in range(R)]
+    ids_np = synth.ids_without_replacement(nb, 200, seed=121)
+    pub_np, hyd_np = ids_np[:100], ids_np[100:]
+    pub, hyd = torch.from_numpy(pub_np).to(DEV), torch.from_numpy(hyd_np).to(DEV)
+    out = np.zeros(100 * R * B, np.uint8)
+    src = rng.integers(0, 256, size=100 * R * B, dtype=np.uint8)
+    st_a = torch.empty(4 << 20, dtype=torch.uint8, device=DEV)
+    st_b = torch.empty(4 << 20, dtype=torch.uint8, device=DEV)
+    s_a, s_b = torch.cuda.Stream(), torch.cuda.Stream()
+    err = []
+    with tc.Stager(slot_bytes=1 << 20) as a, tc.Stager(slot_bytes=1 << 20) as b:
+        def publish():
+            try:
+                tc.tc_publish_to_host(a.handle, regions, nb, B, B, pub, out, st_a, stream=s_a)
+            except Exception as e:
+                err.append(e)
+        t = threading.Thread(target=publish)
+        t.start()
+        tc.tc_hydrate_from_host(b.handle, regions, nb, B, B, hyd, src, st_b, stream=s_b)
+        t.join()
+        torch.cuda.synchronize()
+    assert not err, err
+    assert np.array_equal(out, oracle.gather_blocks(host_pool, B, B, pub_np).reshape(-1))
+    want = [h.copy() for h in host_pool]
+    oracle.scatter_blocks(want, B, B, hyd_np, src)
+    assert np.array_equal(flat.cpu().numpy(), np.concatenate(want))
