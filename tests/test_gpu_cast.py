@@ -169,6 +169,43 @@ def test_blockscaled_rounding_midpoints():
 _E4M3_POS = sorted({abs(oracle.e4m3_decode(c)) for c in range(0x7F)})
 
 
+def test_blockscaled_every_value_under_each_amax():
+    """For 64 tile maxima A (normal and subnormal bf16), every bf16 pattern
+    with |x| <= A, both signs, goes through the full-tile kernel's fast
+    quotient path in tiles whose amax is exactly A, so each tile's scale is
+    A / 448 and every representable quotient at that scale is encoded once.
+    Codes and scales against the oracle."""
+    rng = np.random.default_rng(57)
+    amaxes = np.concatenate([rng.integers(0x0080, 0x7F80, size=56), rng.integers(1, 0x0080, size=6),
+                             [0x7F7F, 0x0001]]).astype(np.uint16)
+    per_tile = 128 * 128
+    tiles = []
+    for a in amaxes:
+        mags = np.arange(0, int(a) + 1, dtype=np.uint32)
+        vals = np.concatenate([mags, mags | 0x8000]).astype(np.uint16)
+        for k in range(0, vals.size, per_tile - 1):
+            t = np.zeros(per_tile, np.uint16)
+            t[0] = a                                   # the tile's amax, exactly
+            chunk = vals[k:k + per_tile - 1]
+            t[1:1 + chunk.size] = chunk
+            tiles.append(t.reshape(128, 128))
+    m = np.concatenate(tiles, axis=1)                  # 128 x (128 * tiles)
+    rows, cols = m.shape
+    src = _to_dev_bits(np.ascontiguousarray(m).reshape(-1))
+    items = np.zeros(1, dtype=tc.CAST_ITEM_DTYPE)
+    items[0] = (0, rows, cols, cols, 0, cols, 0, cols // 128)
+    q = torch.empty(rows * cols, dtype=torch.uint8, device=DEV)
+    sc = torch.empty(cols // 128, dtype=torch.float32, device=DEV)
+    ws = torch.empty(tc.tc_cast_fp8_workspace(1), dtype=torch.uint8, device=DEV)
+    tc.tc_cast_fp8_blockscaled(src, q, sc, items, ws)
+    torch.cuda.synchronize()
+    want_q, want_s = oracle.cast_fp8_blockscaled(m)
+    assert np.array_equal(_host(sc).view(np.uint32), want_s.reshape(-1).view(np.uint32))
+    got = _host(q).reshape(rows, cols)
+    bad = np.argwhere(got != want_q)
+    assert bad.size == 0, f"{len(bad)} codes differ, first at {tuple(bad[0])}"
+
+
 @pytest.mark.parametrize("layers,ranks", [(2, [0, 3, 7])])
 def test_tp_shard_cast_70b_layers(layers, ranks):
     """70B-shaped layers (hidden 8192, 64 q / 8 kv heads, MLP 28672), N(0, 0.02),
