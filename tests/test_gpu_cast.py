@@ -169,41 +169,60 @@ def test_blockscaled_rounding_midpoints():
 _E4M3_POS = sorted({abs(oracle.e4m3_decode(c)) for c in range(0x7F)})
 
 
-def test_blockscaled_every_value_under_each_amax():
-    """For 64 tile maxima A (normal and subnormal bf16), every bf16 pattern
-    with |x| <= A, both signs, goes through the full-tile kernel's fast
-    quotient path in tiles whose amax is exactly A, so each tile's scale is
-    A / 448 and every representable quotient at that scale is encoded once.
-    Codes and scales against the oracle."""
-    rng = np.random.default_rng(57)
-    amaxes = np.concatenate([rng.integers(0x0080, 0x7F80, size=56), rng.integers(1, 0x0080, size=6),
-                             [0x7F7F, 0x0001]]).astype(np.uint16)
-    per_tile = 128 * 128
-    tiles = []
-    for a in amaxes:
-        mags = np.arange(0, int(a) + 1, dtype=np.uint32)
-        vals = np.concatenate([mags, mags | 0x8000]).astype(np.uint16)
-        for k in range(0, vals.size, per_tile - 1):
-            t = np.zeros(per_tile, np.uint16)
-            t[0] = a                                   # the tile's amax, exactly
-            chunk = vals[k:k + per_tile - 1]
-            t[1:1 + chunk.size] = chunk
-            tiles.append(t.reshape(128, 128))
-    m = np.concatenate(tiles, axis=1)                  # 128 x (128 * tiles)
-    rows, cols = m.shape
-    src = _to_dev_bits(np.ascontiguousarray(m).reshape(-1))
-    items = np.zeros(1, dtype=tc.CAST_ITEM_DTYPE)
-    items[0] = (0, rows, cols, cols, 0, cols, 0, cols // 128)
-    q = torch.empty(rows * cols, dtype=torch.uint8, device=DEV)
-    sc = torch.empty(cols // 128, dtype=torch.float32, device=DEV)
+def _tiles_under_amax(a_lo, a_hi):
+    """For every tile maximum A in [a_lo, a_hi): tiles whose element 0 is A
+    and whose other elements run through every bf16 pattern with magnitude
+    <= A, both signs (zero-padded), as one 128-row matrix."""
+    per = 128 * 128 - 1
+    blocks = []
+    for a in range(a_lo, a_hi):
+        mags = np.arange(a + 1, dtype=np.uint16)
+        vals = np.concatenate([mags, mags | np.uint16(0x8000)])
+        t = -(-vals.size // per)
+        body = np.zeros(t * per, np.uint16)
+        body[:vals.size] = vals
+        tiles = np.empty((t, per + 1), np.uint16)
+        tiles[:, 0] = a
+        tiles[:, 1:] = body.reshape(t, per)
+        blocks.append(tiles)
+    tiles = np.concatenate(blocks)
+    return np.ascontiguousarray(tiles.reshape(-1, 128, 128).transpose(1, 0, 2).reshape(128, -1))
+
+
+@pytest.mark.parametrize("part", range(4))
+def test_blockscaled_exhaustive_amax_and_value(part):
+    """Every finite positive tile maximum A (bf16 0x0001 .. 0x7F7F, in four
+    parts) with every bf16 value |x| <= A of both signs: all pairs of element
+    and tile scale that a finite, non-zero tile can present to the full-tile
+    kernel (its quotient and its choice of fast or dividing path depend on
+    nothing else).  Codes and scales against the oracle, in chunks."""
+    bounds = [1, 0x3F80, 0x5A00, 0x6D00, 0x7F80]     # about equal work per part
+    a0, a1 = bounds[part], bounds[part + 1]
     ws = torch.empty(tc.tc_cast_fp8_workspace(1), dtype=torch.uint8, device=DEV)
-    tc.tc_cast_fp8_blockscaled(src, q, sc, items, ws)
-    torch.cuda.synchronize()
-    want_q, want_s = oracle.cast_fp8_blockscaled(m)
-    assert np.array_equal(_host(sc).view(np.uint32), want_s.reshape(-1).view(np.uint32))
-    got = _host(q).reshape(rows, cols)
-    bad = np.argwhere(got != want_q)
-    assert bad.size == 0, f"{len(bad)} codes differ, first at {tuple(bad[0])}"
+    step = 512 if part == 0 else 128
+    checked = 0
+    for lo in range(a0, a1, step):
+        m = _tiles_under_amax(lo, min(a1, lo + step))
+        rows, cols = m.shape
+        items = np.zeros(1, dtype=tc.CAST_ITEM_DTYPE)
+        items[0] = (0, rows, cols, cols, 0, cols, 0, cols // 128)
+        src = _to_dev_bits(m.reshape(-1))
+        q = torch.empty(rows * cols, dtype=torch.uint8, device=DEV)
+        sc = torch.empty(cols // 128, dtype=torch.float32, device=DEV)
+        tc.tc_cast_fp8_blockscaled(src, q, sc, items, ws)
+        torch.cuda.synchronize()
+        want_q, want_s = oracle.cast_fp8_blockscaled(m)
+        assert np.array_equal(_host(sc).view(np.uint32), want_s.reshape(-1).view(np.uint32)), lo
+        got = _host(q).reshape(rows, cols)
+        if not np.array_equal(got, want_q):
+            r, c = np.argwhere(got != want_q)[0]
+            raise AssertionError(f"A in [{lo}, {lo + step}): x={hex(int(m[r, c]))} gpu={hex(int(got[r, c]))} "
+                                 f"oracle={hex(int(want_q[r, c]))}")
+        checked += m.size
+        del src, q, sc
+    # every (A, x) pair of the part was cast: sum over A of 2 (A + 1) values
+    assert checked >= sum(2 * (a + 1) for a in range(a0, a1))
+    print(f"A in [{a0:#x}, {a1:#x}): {checked / 1e6:.0f} M elements checked")
 
 
 @pytest.mark.parametrize("layers,ranks", [(2, [0, 3, 7])])
