@@ -432,6 +432,22 @@ def test_dequant_every_code_many_scales():
     _dequant_matrices(codes, sgrid, mats)
 
 
+@pytest.mark.parametrize("part", range(4))
+def test_dequant_every_code_at_every_cast_scale(part):
+    """Every E4M3 code at every scale a cast can produce for a finite,
+    non-zero tile, s = RN_f32(A / 448) for bf16 A = 0x0001 .. 0x7F7F (in four
+    parts): one full 128x128 tile per scale holding each code 64 times,
+    through the full-tile kernel, against the oracle."""
+    a = np.arange(1, 0x7F80, dtype=np.uint32)
+    a = np.array_split(a, 4)[part]
+    scales = (a << np.uint32(16)).view(np.float32) / np.float32(448.0)   # IEEE single division
+    tile = np.tile(np.arange(256, dtype=np.uint8), 64).reshape(128, 128)
+    for chunk in np.array_split(scales, 8):
+        t = len(chunk)
+        codes = np.ascontiguousarray(np.broadcast_to(tile, (t, 128, 128)).transpose(1, 0, 2)).reshape(-1)
+        _dequant_matrices(codes, chunk, [(0, 128, 128 * t, 128 * t, 0, t)])
+
+
 def test_dequant_ragged_strided_unaligned():
     rng = np.random.default_rng(71)
     codes = rng.integers(0, 256, size=700 * 600, dtype=np.int64).astype(np.uint8)
