@@ -60,6 +60,36 @@ def test_storm_small(align):
     _copy_and_check(_rand_bytes(pool, 32), frags, pool)
 
 
+def test_every_residue_pair_and_ragged_length():
+    """Every source offset mod 16 against every destination offset mod 128
+    (the vector path's and the line cut's residues), each with lengths
+    around the vector, piece and line boundaries: 26,624 fragments, copied
+    with digests, against the oracle."""
+    lens = [0, 1, 15, 16, 17, 127, 128, 129, 1023, 1024, 1025, 2175, 4097]
+    rows = []
+    so = do = 0
+    for rs in range(16):
+        for rd in range(128):
+            for ln in lens:
+                so = (so + 15) // 16 * 16 + rs
+                do = (do + 127) // 128 * 128 + rd
+                rows.append((so, do, ln))
+                so += ln + 5
+                do += ln + 7
+    frags = np.array(rows, dtype=np.uint64)
+    n = len(frags)
+    src = _rand_bytes(so + 16, 95)
+    dst_size = do + 16
+    dst, fr, ws = _copy_and_check(src, frags, dst_size, planned=True)
+    dg = torch.empty(2 * n, dtype=torch.int64, device=DEV)
+    dst2 = torch.full((dst_size,), 0x5A, dtype=torch.uint8, device=DEV)
+    tc.tc_copy_planned_digest(src, dst2, ws, ws.total, n, dg)
+    torch.cuda.synchronize()
+    assert torch.equal(dst2, dst)
+    got = _host(dg).view(np.uint64).reshape(n, 2)
+    assert np.array_equal(got, oracle.fragment_digests(_host(src), frags, use_src=True))
+
+
 def test_mixed_misalignment():
     """src and dst with different residues mod 16 (byte path), and equal
     residues that are not 0 (vector body with byte head/tail)."""
