@@ -65,6 +65,18 @@ def test_block_geometries(B, stride):
     _run_pair(regions, nb, B, stride, ids)
 
 
+def test_every_small_block_size_and_stride_pad():
+    """Block sizes 1 .. 48 bytes and 4080 .. 4112 (around the 4 KiB tile), each
+    with stride pads 0, 1, 15 and 16: the byte path and the vector path's
+    tiles and tails, through gather and scatter, against the oracle."""
+    nb = 12
+    ids = synth.ids_without_replacement(nb, 7, seed=12)
+    for B in list(range(1, 49)) + list(range(4080, 4113)):
+        for pad in (0, 1, 15, 16):
+            regions = _regions_random(2, nb, B, B + pad, 13 + B + pad)
+            _run_pair(regions, nb, B, B + pad, ids)
+
+
 def test_edge_ids():
     nb, B = 64, 4096
     regions = _regions_random(4, nb, B, B, 9)
