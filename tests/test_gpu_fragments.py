@@ -389,9 +389,9 @@ def test_long_unordered_lists_are_planned_in_destination_order():
 
 def test_fragment_longer_than_4gib_beyond_4gib():
     """One fragment of 4 GiB + 17 bytes, read from and written to offsets past
-    2^32, beside two small ones: 64-bit offsets and lengths in the plan and
-    the copy.  Checked in full on the device and, in sampled windows, against
-    the oracle."""
+    2^32, beside two small ones: 64-bit offsets and lengths in the plan, the
+    copy and the digests.  The copy checked in full on the device and, in
+    sampled windows, against the oracle; the digests against the oracle."""
     big = (4 << 30) + 17
     src_size, dst_size = (5 << 30) + 4096, (6 << 30) + 4096
     src = _rand_bytes(src_size, 47)
@@ -411,5 +411,16 @@ def test_fragment_longer_than_4gib_beyond_4gib():
         w = np.zeros(4096, np.uint8)
         oracle.copy_fragments(_host(src[s0 + off:s0 + off + 4096]), w, np.array([[0, 0, 4096]], np.uint64))
         assert np.array_equal(_host(dst[d0 + off:d0 + off + 4096]), w)
+    # digests over the same fragments: byte positions past 2^32 in a fragment
+    # and destination offsets past 2^32 in the weights
+    total = tc.tc_plan_fragments(frags, ws)
+    dg = torch.empty(6, dtype=torch.int64, device=DEV)
+    dd = torch.empty(6, dtype=torch.int64, device=DEV)
+    tc.tc_digest_planned(src, tc.DIGEST_SRC, ws, total, 3, dg)
+    tc.tc_digest_planned(dst, tc.DIGEST_DST, ws, total, 3, dd)
+    torch.cuda.synchronize()
+    want = oracle.fragment_digests(_host(src), rows, use_src=True)
+    assert np.array_equal(_host(dg).view(np.uint64).reshape(3, 2), want)
+    assert np.array_equal(_host(dd).view(np.uint64).reshape(3, 2), want)
     del src, dst
     torch.cuda.empty_cache()
