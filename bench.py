@@ -77,7 +77,7 @@ def _stats(ms, nbytes):
             "frac_of_peak": round(nbytes / (med * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
 
 
-KERNEL_SOURCES = {"gather": "tc_moves.hip", "scatter": "tc_moves.hip", "reshard": "tc_moves.hip",
+KERNEL_SOURCES = {"gather": "tc_blocks.hip", "scatter": "tc_blocks.hip", "reshard": "tc_copy.hip",
                   "cast": "tc_cast.hip"}
 
 

@@ -12,7 +12,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libtchip.so")
-SOURCES = ["tc_moves.hip", "tc_cast.hip", "tc_dequant.hip", "tc_api.cpp", "tc_stage.cpp"]
+SOURCES = ["tc_blocks.hip", "tc_plan.hip", "tc_copy.hip", "tc_cast.hip", "tc_dequant.hip", "tc_api.cpp", "tc_stage.cpp"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

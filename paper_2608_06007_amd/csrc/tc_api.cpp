@@ -1,5 +1,6 @@
 // C ABI of the data path: argument checks, optional validation, launches.
-// Host-only code; the kernels live in tc_moves.hip and tc_cast.hip.
+// Host-only code; the kernels live in tc_blocks.hip, tc_plan.hip, tc_copy.hip,
+// tc_cast.hip and tc_dequant.hip.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
