@@ -9,9 +9,12 @@
  * in batches through prefetch_many(); transform_into() transforms a tensor by
  * a `spec` rule while filling an instance-owned buffer (Sec. 3.2, Table 2).
  * This library is the device-side hot path of those operations: descriptor
- * driven gathers and scatters between device layouts and contiguous buffers,
- * plus a bf16 -> fp8 E4M3 cast with one fp32 scale per 128x128 tile as one
- * concrete transform_into rule.
+ * driven gathers and scatters between device layouts and contiguous buffers
+ * (including resharding between tensor-parallel layouts), a bf16 -> fp8 E4M3
+ * cast with one fp32 scale per 128x128 tile as one concrete transform_into
+ * rule, and its inverse; per-fragment integrity digests for the pipeline's
+ * verify stage; and the pinned staging that moves such bytes between host
+ * memory and the device (Sec. 5).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
