@@ -82,10 +82,10 @@ KERNEL_SOURCES = {"gather": "tc_blocks.hip", "scatter": "tc_blocks.hip", "reshar
 
 
 def _source_hash(*names):
-    """sha256 over the named files of the HIP sources plus their shared header."""
+    """sha256 over the named files of the HIP sources plus their shared headers."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_06007_amd", "csrc")
-    for name in sorted(set(names) | {"tc_internal.h"}):
+    for name in sorted(set(names) | {"tc_internal.h", "tc_device.h"}):
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode() + f.read())
     return h.hexdigest()

@@ -107,10 +107,12 @@ constexpr int kDefaultSlots = 4;
 constexpr int kDefaultThreads = 4;
 constexpr size_t kMinPart = size_t(1) << 20;  // smallest share of a host copy per thread
 // Chunks in flight on the copy stream at most.  The host waits for chunk
-// k - kDepth before it enqueues chunk k, in every path: with the host far
+// k - kDepth before it enqueues chunk k, in every path.  With the host far
 // ahead (pinned buffers, rings of six slots) the same copies measured 15-30
-// GB/s instead of 54 on MI355X.
-constexpr size_t kDepth = 4;
+// GB/s instead of 54 on MI355X.  Two stagers moving opposite directions at
+// once reach 94-96 GB/s together at depths 2 and 3 but 63-71 at depth 4; at
+// depth 1 a lone hydrate from pageable memory falls from 54 to 34 GB/s.
+constexpr size_t kDepth = 2;
 
 }  // namespace
 
