@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
+#include <cstdint>
 #include <cstdlib>
 #include <cstring>
 #include <initializer_list>
@@ -15,14 +17,19 @@
 namespace {
 
 thread_local int g_last_hip_error = 0;
-int g_validate = -1;  // -1: not yet read from the environment
+std::atomic<int> g_validate{-1};  // -1: not yet read from the environment
 
 bool validating() {
-  if (g_validate < 0) {
+  int v = g_validate.load(std::memory_order_relaxed);
+  if (v < 0) {
     const char* e = std::getenv("TC_VALIDATE");
-    g_validate = (e && e[0] && e[0] != '0') ? 1 : 0;
+    int expected = -1;
+    // tc_set_validate may have run meanwhile: only an unset flag takes the environment
+    g_validate.compare_exchange_strong(expected, (e && e[0] && e[0] != '0') ? 1 : 0,
+                                       std::memory_order_relaxed);
+    v = g_validate.load(std::memory_order_relaxed);
   }
-  return g_validate == 1;
+  return v == 1;
 }
 
 tc_status hip_fail(hipError_t e) {
@@ -85,6 +92,8 @@ bool pool_ok(const tc_block_pool* p) {
   if (!p || !p->region_base) return false;
   if (p->num_regions < 1 || p->num_regions > TC_MAX_REGIONS) return false;
   if (p->num_blocks < 1 || p->block_bytes < 1 || p->block_stride < p->block_bytes) return false;
+  // a region's byte extent must fit in 63 bits
+  if (p->num_blocks > INT64_MAX / p->block_stride) return false;
   for (int r = 0; r < p->num_regions; ++r)
     if (p->region_base[r] == 0) return false;
   return true;
@@ -97,6 +106,8 @@ tc_status blocks_common(const tc_block_pool* pool, const int32_t* ids, int64_t n
   if (!ids || !buf) return TC_ERR_INVALID_ARGUMENT;
   const int32_t R = pool->num_regions;
   const int64_t B = pool->block_bytes, stride = pool->block_stride;
+  // so does the transfer buffer's, n * R * B bytes
+  if (n > INT64_MAX / R / B) return TC_ERR_INVALID_ARGUMENT;
   if (validating()) {
     std::vector<int32_t> h;
     tc_status st = fetch(ids, n, &h, s);
@@ -905,7 +916,7 @@ const char* tc_status_string(tc_status s) {
 
 int tc_last_hip_error(void) { return g_last_hip_error; }
 
-void tc_set_validate(int on) { g_validate = on ? 1 : 0; }
+void tc_set_validate(int on) { g_validate.store(on ? 1 : 0, std::memory_order_relaxed); }
 
 int tc_get_validate(void) { return validating() ? 1 : 0; }
 

@@ -77,6 +77,11 @@ def test_argument_errors_need_no_gpu(lib):
     big = (ctypes.c_uint64 * 300)(*([4096] * 300))
     pool_big = tc._BlockPool(ctypes.cast(big, ctypes.POINTER(ctypes.c_uint64)), 300, 4, 64, 64)
     assert lib.tc_gather_blocks(ctypes.byref(pool_big), P(16), 1, P(16), None) == 1
+    # byte extents beyond 63 bits: a region (blocks x stride), the transfer buffer (n x R x B)
+    pool_wide = tc._BlockPool(ctypes.cast(arr, ctypes.POINTER(ctypes.c_uint64)), 1, 1 << 40, 1 << 23, 1 << 23)
+    assert lib.tc_gather_blocks(ctypes.byref(pool_wide), P(16), 1, P(16), None) == 1
+    pool_huge = tc._BlockPool(ctypes.cast(big, ctypes.POINTER(ctypes.c_uint64)), 64, 4, 1 << 30, 1 << 30)
+    assert lib.tc_scatter_blocks(ctypes.byref(pool_huge), P(16), 1 << 27, P(16), None) == 1
     # fragments: workspace too small, negative count
     assert lib.tc_copy_fragments(P(16), P(16), P(16), 10, P(4096), 8, None) == 5
     assert lib.tc_copy_fragments(P(16), P(16), P(16), 10, P(4100), 1 << 20, None) == 1  # misaligned
