@@ -88,20 +88,9 @@ bool cross_overlap(std::vector<Range> a, std::vector<Range> b) {
   return false;
 }
 
-bool pool_ok(const tc_block_pool* p) {
-  if (!p || !p->region_base) return false;
-  if (p->num_regions < 1 || p->num_regions > TC_MAX_REGIONS) return false;
-  if (p->num_blocks < 1 || p->block_bytes < 1 || p->block_stride < p->block_bytes) return false;
-  // a region's byte extent must fit in 63 bits
-  if (p->num_blocks > INT64_MAX / p->block_stride) return false;
-  for (int r = 0; r < p->num_regions; ++r)
-    if (p->region_base[r] == 0) return false;
-  return true;
-}
-
 tc_status blocks_common(const tc_block_pool* pool, const int32_t* ids, int64_t n, void* buf,
                         bool gather, hipStream_t s) {
-  if (n < 0 || !pool_ok(pool)) return TC_ERR_INVALID_ARGUMENT;
+  if (n < 0 || !tc::pool_valid(pool)) return TC_ERR_INVALID_ARGUMENT;
   if (n == 0) return TC_OK;
   if (!ids || !buf) return TC_ERR_INVALID_ARGUMENT;
   const int32_t R = pool->num_regions;
@@ -347,6 +336,17 @@ bool reshard_cast_items(const tc_reshard_view& v, uint64_t scale_off, int32_t ds
 
 namespace tc {
 tc_status hip_status(hipError_t e) { return check(e); }
+
+bool pool_valid(const tc_block_pool* p) {
+  if (!p || !p->region_base) return false;
+  if (p->num_regions < 1 || p->num_regions > TC_MAX_REGIONS) return false;
+  if (p->num_blocks < 1 || p->block_bytes < 1 || p->block_stride < p->block_bytes) return false;
+  if (p->num_blocks > INT64_MAX / p->block_stride) return false;
+  if (p->block_bytes > INT64_MAX / p->num_regions) return false;
+  for (int r = 0; r < p->num_regions; ++r)
+    if (p->region_base[r] == 0) return false;
+  return true;
+}
 }  // namespace tc
 
 namespace tc {

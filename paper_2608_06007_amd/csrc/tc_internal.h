@@ -79,6 +79,11 @@ size_t frag_workspace_min_bytes(int64_t n);
 // and returns TC_ERR_HIP.
 tc_status hip_status(hipError_t e);
 
+// A block pool the movers accept: 1..TC_MAX_REGIONS non-null regions, at
+// least one block, stride >= block bytes, and byte extents (a region's
+// blocks x stride, one id's regions x block bytes) within 63 bits.
+bool pool_valid(const tc_block_pool* p);
+
 // Launch geometry of the current device.
 struct DeviceInfo {
   int device;

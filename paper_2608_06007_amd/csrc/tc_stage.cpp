@@ -220,11 +220,6 @@ tc_status stream_after_copy(tc_stager* st, hipStream_t stream) {
   return fail(e);
 }
 
-bool pool_shape_ok(const tc_block_pool* pool) {
-  return pool && pool->region_base && pool->num_regions >= 1 &&
-         pool->num_regions <= TC_MAX_REGIONS && pool->block_bytes >= 1;
-}
-
 // Validation mode: every id in range and, for a scatter, no id twice (the
 // per-chunk calls cannot see repeats across chunks).
 tc_status check_ids(const tc_block_pool* pool, const int32_t* ids, int64_t n, bool scatter,
@@ -378,7 +373,7 @@ tc_status tc_hydrate_from_host(tc_stager* st, const tc_block_pool* pool, const i
                                int64_t n, const void* host_src, int32_t flags, void* dev_stage,
                                size_t dev_stage_bytes, hipStream_t stream) {
   try {
-    if (!st || n < 0 || !pool_shape_ok(pool) || (flags & ~TC_HOST_PINNED))
+    if (!st || n < 0 || !tc::pool_valid(pool) || (flags & ~TC_HOST_PINNED))
       return TC_ERR_INVALID_ARGUMENT;
     if (n == 0) return TC_OK;
     if (!ids || !host_src || !dev_stage) return TC_ERR_INVALID_ARGUMENT;
@@ -431,7 +426,7 @@ tc_status tc_publish_to_host(tc_stager* st, const tc_block_pool* pool, const int
                              int64_t n, void* host_dst, int32_t flags, void* dev_stage,
                              size_t dev_stage_bytes, hipStream_t stream) {
   try {
-    if (!st || n < 0 || !pool_shape_ok(pool) || (flags & ~TC_HOST_PINNED))
+    if (!st || n < 0 || !tc::pool_valid(pool) || (flags & ~TC_HOST_PINNED))
       return TC_ERR_INVALID_ARGUMENT;
     if (n == 0) return TC_OK;
     if (!ids || !host_dst || !dev_stage) return TC_ERR_INVALID_ARGUMENT;

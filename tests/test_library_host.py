@@ -82,6 +82,15 @@ def test_argument_errors_need_no_gpu(lib):
     assert lib.tc_gather_blocks(ctypes.byref(pool_wide), P(16), 1, P(16), None) == 1
     pool_huge = tc._BlockPool(ctypes.cast(big, ctypes.POINTER(ctypes.c_uint64)), 64, 4, 1 << 30, 1 << 30)
     assert lib.tc_scatter_blocks(ctypes.byref(pool_huge), P(16), 1 << 27, P(16), None) == 1
+    # the staging calls check the pool the same way before any copy (the
+    # stager handle is not dereferenced on these paths)
+    for bad in (pool_bad, pool_wide):
+        assert lib.tc_hydrate_from_host(P(16), ctypes.byref(bad), P(16), 1, P(16), 0, P(16), 1 << 20, None) == 1
+        assert lib.tc_publish_to_host(P(16), ctypes.byref(bad), P(16), 1, P(16), 0, P(16), 1 << 20, None) == 1
+    nul = (ctypes.c_uint64 * 2)(4096, 0)                 # a null region
+    pool_nul = tc._BlockPool(ctypes.cast(nul, ctypes.POINTER(ctypes.c_uint64)), 2, 4, 64, 64)
+    assert lib.tc_hydrate_from_host(P(16), ctypes.byref(pool_nul), P(16), 1, P(16), 0, P(16), 1 << 20, None) == 1
+    assert lib.tc_gather_blocks(ctypes.byref(pool_nul), P(16), 1, P(16), None) == 1
     # fragments: workspace too small, negative count
     assert lib.tc_copy_fragments(P(16), P(16), P(16), 10, P(4096), 8, None) == 5
     assert lib.tc_copy_fragments(P(16), P(16), P(16), 10, P(4100), 1 << 20, None) == 1  # misaligned
