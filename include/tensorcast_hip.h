@@ -88,6 +88,10 @@ typedef struct {
   int64_t block_bytes;         /* bytes per block and region, > 0 */
   int64_t block_stride;        /* bytes between consecutive blocks, >= block_bytes */
 } tc_block_pool;
+/* Every call that takes a pool returns TC_ERR_INVALID_ARGUMENT, before any
+ * work is enqueued, for a pool outside these bounds, a null region address,
+ * or byte extents beyond 2^63 - 1 (num_blocks * block_stride, num_regions *
+ * block_bytes, or a batch's n * num_regions * block_bytes). */
 
 /* publish: out[i][r][0:B] = region_r[ids[i]*stride : +B] for i < n, r < R.
  * ids: device int32[n]; repeated ids are allowed.  out: device buffer of
