@@ -192,6 +192,13 @@ def _nbytes(t) -> int:
 # publish / hydrate
 # ---------------------------------------------------------------------------
 
+def _ids(ids) -> int:
+    """Element count of an id tensor: the library reads int32 ids."""
+    if ids.dtype != _torch().int32:
+        raise ValueError(f"ids must be an int32 tensor, not {ids.dtype}")
+    return ids.numel()
+
+
 def _pool(regions, num_blocks: int, block_bytes: int, block_stride: int):
     bases = [_dev_ptr(r) for r in regions]
     arr = (ctypes.c_uint64 * len(bases))(*bases)
@@ -207,8 +214,8 @@ def tc_gather_blocks(regions, num_blocks: int, block_bytes: int, block_stride: i
     ``regions``: list of device tensors or device addresses (one per layer and
     K|V); ``ids``: device int32 tensor; ``out``: device tensor of
     len(ids) * len(regions) * block_bytes bytes."""
+    n = _ids(ids)
     pool, keep = _pool(regions, num_blocks, block_bytes, block_stride)
-    n = ids.numel()
     if n and _nbytes(out) < n * len(keep) * block_bytes:
         raise ValueError("output buffer too small")
     _ok(load().tc_gather_blocks(ctypes.byref(pool), _dev_ptr(ids) if n else None, n,
@@ -218,8 +225,8 @@ def tc_gather_blocks(regions, num_blocks: int, block_bytes: int, block_stride: i
 def tc_scatter_blocks(regions, num_blocks: int, block_bytes: int, block_stride: int, ids, inp,
                       stream=None) -> None:
     """regions[r][ids[i]*stride : +block_bytes] = inp[i, r, :] on the device (ids distinct)."""
+    n = _ids(ids)
     pool, keep = _pool(regions, num_blocks, block_bytes, block_stride)
-    n = ids.numel()
     if n and _nbytes(inp) < n * len(keep) * block_bytes:
         raise ValueError("input buffer too small")
     _ok(load().tc_scatter_blocks(ctypes.byref(pool), _dev_ptr(ids) if n else None, n,
@@ -239,6 +246,8 @@ def tc_copy_fragments_workspace_min(n: int) -> int:
 
 
 def _frag_count(frags) -> int:
+    if frags.dtype not in (_torch().uint64, _torch().int64):
+        raise ValueError(f"fragments must be a uint64/int64 tensor, not {frags.dtype}")
     nb = _nbytes(frags)
     if nb % 24:
         raise ValueError("fragment tensor is not a whole number of (src_off, dst_off, len) rows")
@@ -362,8 +371,8 @@ def tc_hydrate_from_host(stager: int, regions, num_blocks: int, block_bytes: int
                          ids, host_src, dev_stage, pinned=None, stream=None) -> None:
     """Scatter a host-resident transfer buffer (layout of tc_gather_blocks)
     into the device block pool, staged through ``dev_stage``."""
+    n = _ids(ids)
     pool, keep = _pool(regions, num_blocks, block_bytes, block_stride)
-    n = ids.numel()
     a, hb, det = _host(host_src)
     if n and hb < n * len(keep) * block_bytes:
         raise ValueError("host buffer too small")
@@ -375,8 +384,8 @@ def tc_hydrate_from_host(stager: int, regions, num_blocks: int, block_bytes: int
 def tc_publish_to_host(stager: int, regions, num_blocks: int, block_bytes: int, block_stride: int,
                        ids, host_dst, dev_stage, pinned=None, stream=None) -> None:
     """Gather the pool's blocks of ``ids`` into host memory (blocks until done)."""
+    n = _ids(ids)
     pool, keep = _pool(regions, num_blocks, block_bytes, block_stride)
-    n = ids.numel()
     a, hb, det = _host(host_dst)
     if n and hb < n * len(keep) * block_bytes:
         raise ValueError("host buffer too small")
@@ -532,7 +541,11 @@ def tc_cast_fp8_blockscaled(src, dst, scales, items, workspace, stream=None, til
 
 def tc_cast_fp8_scaled(src, scale: float, dst, stream=None) -> None:
     """dst[i] = E4M3(RN_f32(src[i] / scale)) for a bf16 device tensor ``src``."""
+    if src.element_size() != 2:
+        raise ValueError("src must hold bf16 (2-byte) elements")
     n = src.numel()
+    if _nbytes(dst) < n:
+        raise ValueError("dst too small: one byte per element")
     _ok(load().tc_cast_fp8_scaled(_dev_ptr(src) if n else None, n, float(scale),
                                   _dev_ptr(dst) if n else None, _stream(stream)),
         "tc_cast_fp8_scaled")

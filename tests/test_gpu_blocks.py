@@ -116,6 +116,8 @@ def test_binding_refuses_host_and_strided_tensors():
     with pytest.raises(ValueError):
         tc.tc_gather_blocks(regions, nb, B, B, torch.tensor([1, 0, 3, 0], dtype=torch.int32,
                                                             device=DEV)[::2], out)
+    with pytest.raises(ValueError):                          # the library reads int32 ids
+        tc.tc_gather_blocks(regions, nb, B, B, ids.to(torch.int64), out)
     tc.tc_gather_blocks(regions, nb, B, B, ids, out)         # the same call, contiguous
     torch.cuda.synchronize()
 

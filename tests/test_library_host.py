@@ -142,6 +142,30 @@ def test_argument_errors_need_no_gpu(lib):
                                           16, None) == 5
 
 
+def test_binding_refuses_wrong_dtypes_before_any_call(lib):
+    """Dtype checks in the binding run before a device address is taken, so
+    they need no GPU: ids must be int32 (the library reads 4-byte ids),
+    fragment rows 64-bit integers, and the scaled cast's source 2-byte
+    elements with a byte of output each."""
+    import torch
+    regions = [4096, 8192]                                # raw addresses: never dereferenced
+    with pytest.raises(ValueError, match="int32"):
+        tc.tc_gather_blocks(regions, 4, 64, 64, torch.zeros(2, dtype=torch.int64), 12288)
+    with pytest.raises(ValueError, match="int32"):
+        tc.tc_scatter_blocks(regions, 4, 64, 64, torch.zeros(2, dtype=torch.int16), 12288)
+    with pytest.raises(ValueError, match="int32"):
+        tc.tc_hydrate_from_host(16, regions, 4, 64, 64, torch.zeros(2, dtype=torch.float32),
+                                np.zeros(256, np.uint8), 4096)
+    with pytest.raises(ValueError, match="uint64/int64"):
+        tc.tc_copy_fragments(4096, 8192, torch.zeros((2, 3), dtype=torch.float64), 16384)
+    with pytest.raises(ValueError, match="uint64/int64"):
+        tc.tc_plan_fragments(torch.zeros(48, dtype=torch.uint8), 16384)
+    with pytest.raises(ValueError, match="2-byte"):
+        tc.tc_cast_fp8_scaled(torch.zeros(8, dtype=torch.uint8), 1.0, torch.zeros(8, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="dst too small"):
+        tc.tc_cast_fp8_scaled(torch.zeros(8, dtype=torch.bfloat16), 1.0, torch.zeros(4, dtype=torch.uint8))
+
+
 def test_validate_flag_roundtrip(lib):
     tc.tc_set_validate(True)
     assert tc.tc_get_validate()
