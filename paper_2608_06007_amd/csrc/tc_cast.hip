@@ -18,17 +18,14 @@
 // quotients of a finite tile stay below 449 (|x| <= amax and s is amax/448
 // rounded to nearest, worst case a subnormal s with 8 significant bits), and
 // lo/hi stay below 450, so no clamp is needed on this path.
-#include "tc_internal.h"
+#include "tc_device.h"
 
 namespace tc {
 namespace {
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kThreads = 256;
-constexpr int kWaveLanes = 64;
 constexpr int kTile = 128;
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
@@ -93,23 +90,11 @@ constexpr int kCastThreads = 512;
 constexpr int kCastWaves = kCastThreads / kWaveLanes;
 constexpr int kRowsPerPass = kCastThreads / 16;
 constexpr int kPasses = kTile / kRowsPerPass;
-constexpr int kXcds = 8;
 constexpr uint64_t kCastXcdGroup = 4;  // consecutive tiles per XCD run
 
-// Work item of block b when the 8 XCDs each take runs of G consecutive tiles
-// (a bijection on [0, N); the last partial round keeps the identity order).
-__device__ __forceinline__ uint64_t xcd_grouped(uint64_t b, uint64_t N, uint64_t G) {
-  const uint64_t round = uint64_t(kXcds) * G;
-  const uint64_t full = (N / round) * round;
-  if (b >= full) return b;
-  const uint64_t x = b % kXcds, l = b / kXcds;
-  return (l / G) * round + x * G + (l % G);
-}
-
-__device__ __forceinline__ u32x4 ld_nt(const u32x4* p) { return __builtin_nontemporal_load(p); }
 // Code stores carry the SC1 scope bit with NT, as the copies' stores do
 // (measured on the 70B shard: 5867 against 5841 GB/s with plain NT).
-__device__ __forceinline__ void st_nt(u32x2* p, u32x2 v) {
+__device__ __forceinline__ void st_codes(u32x2* p, u32x2 v) {
   asm volatile("global_store_dwordx2 %0, %1, off sc1 nt" ::"v"(p), "v"(v) : "memory");
 }
 
@@ -124,20 +109,6 @@ __device__ __forceinline__ uint32_t block_amax(uint32_t m, uint32_t* red) {
 #pragma unroll
   for (int k = 0; k < kCastWaves; ++k) r = max(r, red[k]);
   return r;
-}
-
-// Item whose tile range contains tile t: last i in [0, n) with
-// prefix[i] <= t, given prefix[0] <= t < prefix[n].  64-way search per wave.
-__device__ int64_t find_item(const uint64_t* __restrict__ prefix, int64_t n, uint64_t t, int lane) {
-  int64_t lo = 0, hi = n;
-  while (hi - lo > 1) {
-    const int64_t step = (hi - lo + kWaveLanes - 1) / kWaveLanes;
-    const int64_t p = lo + (int64_t(lane) + 1) * step;
-    const bool pred = lane < kWaveLanes - 1 && p < hi && prefix[p] <= t;
-    lo += int64_t(__popcll(__ballot(pred))) * step;
-    hi = min(hi, lo + step);
-  }
-  return lo;
 }
 
 // Full tiles of items whose rows are 16-byte aligned (source) and 8-byte
@@ -201,7 +172,7 @@ __global__ __launch_bounds__(kCastThreads) void k_cast_full(const uint16_t* __re
   }
 #pragma unroll
   for (int p = 0; p < kPasses; ++p)
-    st_nt(reinterpret_cast<u32x2*>(qs + int64_t(p * kRowsPerPass + prow) * item.dst_ld + seg * 8), o[p]);
+    st_codes(reinterpret_cast<u32x2*>(qs + int64_t(p * kRowsPerPass + prow) * item.dst_ld + seg * 8), o[p]);
   if (threadIdx.x == 0) scales[item.scale_off + ti * item.scale_ld + tj] = s;
 }
 
@@ -308,9 +279,6 @@ __global__ __launch_bounds__(kThreads) void k_cast_scaled(const uint16_t* __rest
     }
   }
 }
-
-// Largest grid of one launch (gridDim.x * blockDim.x stays below 2^32).
-constexpr uint64_t kMaxGrid = uint64_t(1) << 22;
 
 }  // namespace
 

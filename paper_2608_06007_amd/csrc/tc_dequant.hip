@@ -8,51 +8,22 @@
 // element-wise kernel.  Decoding uses v_cvt_pk_f32_fp8, which is exact for
 // every finite E4M3 code and gives NaN for S.1111.111; the bf16 rounding is
 // done on the integer bits (nearest, ties to even; NaN -> 0x7FC0).
-#include "tc_internal.h"
+#include "tc_device.h"
 
 namespace tc {
 namespace {
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-// bf16 stores with the SC1 scope bit and NT (measured on the 70B shard:
-// 5809 against 5709 GB/s with plain NT stores).  The store reads its 16 data
-// bytes after issue, and a VALU write to those registers needs 2 wait states;
-// the compiler cannot see into inline asm, so s_nop 1 provides them.
-__device__ __forceinline__ void st_sc1_nt(u32x4* p, u32x4 v) {
-  asm volatile("global_store_dwordx4 %0, %1, off sc1 nt\n\ts_nop 1" ::"v"(p), "v"(v) : "memory");
-}
+// bf16 stores are st_sc1_nt: SC1 NT measured 5809 against 5709 GB/s with
+// plain NT stores on the 70B shard.
 
-constexpr int kWaveLanes = 64;
 constexpr int kTile = 128;
-constexpr int kThreads = 512;
-constexpr int kRowsPerPass = kThreads / 16;
+constexpr int kDequantThreads = 512;
+constexpr int kRowsPerPass = kDequantThreads / 16;
 constexpr int kPasses = kTile / kRowsPerPass;
-constexpr int kXcds = 8;
-constexpr uint64_t kXcdGroup = 4;
-constexpr uint64_t kMaxGrid = uint64_t(1) << 22;
-
-__device__ __forceinline__ uint64_t xcd_grouped(uint64_t b, uint64_t N, uint64_t G) {
-  const uint64_t round = uint64_t(kXcds) * G;
-  const uint64_t full = (N / round) * round;
-  if (b >= full) return b;
-  const uint64_t x = b % kXcds, l = b / kXcds;
-  return (l / G) * round + x * G + (l % G);
-}
-
-__device__ int64_t find_item(const uint64_t* __restrict__ prefix, int64_t n, uint64_t t, int lane) {
-  int64_t lo = 0, hi = n;
-  while (hi - lo > 1) {
-    const int64_t step = (hi - lo + kWaveLanes - 1) / kWaveLanes;
-    const int64_t p = lo + (int64_t(lane) + 1) * step;
-    const bool pred = lane < kWaveLanes - 1 && p < hi && prefix[p] <= t;
-    lo += int64_t(__popcll(__ballot(pred))) * step;
-    hi = min(hi, lo + step);
-  }
-  return lo;
-}
+constexpr uint64_t kDequantXcdGroup = 4;  // consecutive tiles per XCD run
 
 // bf16 bits of a binary32 value: nearest, ties to even; NaN -> 0x7FC0.
 __device__ __forceinline__ uint32_t bf16_bits(float v) {
@@ -69,7 +40,7 @@ __device__ __forceinline__ u32x2 dequant4(uint32_t w, float s) {
                bf16_bits(b.x * s) | (bf16_bits(b.y * s) << 16)};
 }
 
-__global__ __launch_bounds__(kThreads) void k_dequant_full(const uint8_t* __restrict__ codes,
+__global__ __launch_bounds__(kDequantThreads) void k_dequant_full(const uint8_t* __restrict__ codes,
                                                           const float* __restrict__ scales,
                                                           uint16_t* __restrict__ dst,
                                                           const tc_dequant_item* __restrict__ items,
@@ -79,7 +50,7 @@ __global__ __launch_bounds__(kThreads) void k_dequant_full(const uint8_t* __rest
   const int lane = threadIdx.x & (kWaveLanes - 1);
   const int seg = threadIdx.x & 15;  // 8 codes per lane, 16 lanes per 128-byte row
   const int prow = threadIdx.x >> 4;
-  const uint64_t t = t0 + xcd_grouped(blockIdx.x, count, kXcdGroup);
+  const uint64_t t = t0 + xcd_grouped(blockIdx.x, count, kDequantXcdGroup);
   const int64_t it = find_item(prefix, n_items, t, lane);
   const tc_dequant_item item = items[it];
   const int64_t full_c = item.cols / kTile;
@@ -103,7 +74,7 @@ __global__ __launch_bounds__(kThreads) void k_dequant_full(const uint8_t* __rest
 
 // Partial tiles and unaligned items, element by element; numbered within an
 // item like the cast's edge tiles.
-__global__ __launch_bounds__(kThreads) void k_dequant_edge(const uint8_t* __restrict__ codes,
+__global__ __launch_bounds__(kDequantThreads) void k_dequant_edge(const uint8_t* __restrict__ codes,
                                                           const float* __restrict__ scales,
                                                           uint16_t* __restrict__ dst,
                                                           const tc_dequant_item* __restrict__ items,
@@ -133,7 +104,7 @@ __global__ __launch_bounds__(kThreads) void k_dequant_edge(const uint8_t* __rest
   const uint8_t* qs = codes + item.src_off + r0 * item.src_ld + c0;
   uint16_t* ys = dst + item.dst_off + r0 * item.dst_ld + c0;
   const float s = scales[item.scale_off + ti * item.scale_ld + tj];
-  for (int64_t k = threadIdx.x; k < h * wd; k += kThreads) {
+  for (int64_t k = threadIdx.x; k < h * wd; k += kDequantThreads) {
     const int64_t rr = k / wd, cc = k - rr * wd;
     const f32x2 v = __builtin_amdgcn_cvt_pk_f32_fp8((int)qs[rr * item.src_ld + cc], false);
     ys[rr * item.dst_ld + cc] = (uint16_t)bf16_bits(v.x * s);
@@ -153,12 +124,12 @@ hipError_t launch_dequant_blockscaled(const uint8_t* codes, const float* scales,
   const uint8_t* al = base + L.aligned;
   for (uint64_t t0 = 0; t0 < full_tiles; t0 += kMaxGrid) {
     const uint64_t cnt = full_tiles - t0 < kMaxGrid ? full_tiles - t0 : kMaxGrid;
-    hipLaunchKernelGGL(k_dequant_full, dim3((unsigned)cnt), dim3(kThreads), 0, s, codes, scales, dst,
+    hipLaunchKernelGGL(k_dequant_full, dim3((unsigned)cnt), dim3(kDequantThreads), 0, s, codes, scales, dst,
                        items, fp, n_items, t0, cnt);
   }
   for (uint64_t t0 = 0; t0 < edge_tiles; t0 += kMaxGrid) {
     const uint64_t cnt = edge_tiles - t0 < kMaxGrid ? edge_tiles - t0 : kMaxGrid;
-    hipLaunchKernelGGL(k_dequant_edge, dim3((unsigned)cnt), dim3(kThreads), 0, s, codes, scales, dst,
+    hipLaunchKernelGGL(k_dequant_edge, dim3((unsigned)cnt), dim3(kDequantThreads), 0, s, codes, scales, dst,
                        items, ep, al, n_items, t0);
   }
   return hipGetLastError();

@@ -1,6 +1,7 @@
-// Device helpers shared by the byte movers on gfx950: the paged-KV block
-// moves (tc_blocks.hip), fragment plans (tc_plan.hip) and planned copies
-// with their digests (tc_copy.hip).
+// Device helpers shared by the kernels for gfx950: the paged-KV block moves
+// (tc_blocks.hip), fragment plans (tc_plan.hip), planned copies with their
+// digests (tc_copy.hip), and the block-scaled cast and its inverse
+// (tc_cast.hip, tc_dequant.hip).
 //
 // Design (measured on MI355X): the copies are HBM-bound, and the launch
 // shape that streams best is a one-shot grid of small workgroups -- 256
@@ -33,6 +34,24 @@ __device__ __forceinline__ uint64_t xcd_grouped(uint64_t b, uint64_t N, uint64_t
   if (b >= full) return b;
   const uint64_t x = b % kXcds, l = b / kXcds;
   return (l / G) * round + x * G + (l % G);
+}
+
+// Item whose tile range contains tile t: the last i in [0, n) with
+// prefix[i] <= t, given prefix[0] <= t < prefix[n] (the cast and its inverse
+// number their tiles by item).  Each round cuts the range into 64 steps and
+// counts by ballot the step starts at or below t, so a wave needs
+// ceil(log64 n) rounds.
+__device__ inline int64_t find_item(const uint64_t* __restrict__ prefix, int64_t n, uint64_t t,
+                                    int lane) {
+  int64_t lo = 0, hi = n;
+  while (hi - lo > 1) {
+    const int64_t step = (hi - lo + kWaveLanes - 1) / kWaveLanes;
+    const int64_t p = lo + (int64_t(lane) + 1) * step;
+    const bool pred = lane < kWaveLanes - 1 && p < hi && prefix[p] <= t;
+    lo += int64_t(__popcll(__ballot(pred))) * step;
+    hi = min(hi, lo + step);
+  }
+  return lo;
 }
 
 __device__ __forceinline__ u32x4 ld_nt(const u32x4* p) { return __builtin_nontemporal_load(p); }
@@ -84,8 +103,11 @@ namespace {
 // Tasks that one workgroup expands, and reduces: one window of the plan.
 constexpr int kExpandPerBlock = int(kWindowTasks);
 
-// Largest grid used for one launch; bigger jobs loop (grid-stride).
-constexpr uint64_t kMaxGrid = uint64_t(1) << 24;
+// Largest grid used for one launch; bigger jobs loop (grid-stride).  A
+// dispatch counts its work-items in 32 bits, so the cap times the largest
+// workgroup here (512 threads) must stay below 2^32.
+constexpr uint64_t kMaxGrid = uint64_t(1) << 22;
+static_assert(kMaxGrid * 512 < (uint64_t(1) << 32), "grid work-items must fit 32 bits");
 
 inline unsigned grid_for(uint64_t items) { return (unsigned)(items < kMaxGrid ? items : kMaxGrid); }
 

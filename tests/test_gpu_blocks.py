@@ -243,3 +243,29 @@ def test_region_larger_than_4gib():
     assert torch.equal(back, buf)
     del region
     torch.cuda.empty_cache()
+
+
+def test_more_tiles_than_one_grid_holds():
+    """2^24 + 5 one-tile chunks (16-byte blocks, one region): more workgroup
+    tiles than one launch's grid takes, so the grid strides, and enough that a
+    grid of one workgroup per tile would not fit a dispatch's 32-bit count of
+    work-items.  Byte for byte against the oracle, gather and scatter."""
+    n = (1 << 24) + 5
+    B = 16
+    nb = n + 11
+    region = synth.random_bytes(nb * B, 131, device=DEV)
+    ids_np = np.random.default_rng(131).permutation(nb)[:n].astype(np.int32)
+    ids = torch.from_numpy(ids_np).to(DEV)
+    buf = torch.empty(n * B, dtype=torch.uint8, device=DEV)
+    tc.tc_gather_blocks([region], nb, B, B, ids, buf)
+    dst = torch.full_like(region, 0x5A)
+    tc.tc_scatter_blocks([dst], nb, B, B, ids, buf)
+    torch.cuda.synchronize()
+    host = _host(region)
+    want = oracle.gather_blocks([host], B, B, ids_np)
+    assert np.array_equal(_host(buf).reshape(want.shape), want)
+    back = np.full_like(host, 0x5A)
+    oracle.scatter_blocks([back], B, B, ids_np, want)
+    assert np.array_equal(_host(dst), back)
+    del region, dst, buf
+    torch.cuda.empty_cache()
