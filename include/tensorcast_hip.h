@@ -26,8 +26,9 @@
  *   host, enqueue kernels on `stream` and return.  n == 0 enqueues nothing.
  * - Calls are pure functions of their inputs, so re-running one after a
  *   failure is safe (the paper's idempotent retry, Sec. 3.2 "Plan").
- * - Errors: TC_ERR_INVALID_ARGUMENT for null pointers, negative sizes and
- *   geometry that cannot be valid; TC_ERR_WORKSPACE for a workspace that is
+ * - Errors: TC_ERR_INVALID_ARGUMENT for null pointers, negative sizes,
+ *   geometry that cannot be valid, and fragment, item or task counts above
+ *   2^33 (the plan kernels' grids grow with them); TC_ERR_WORKSPACE for a workspace that is
  *   too small; TC_ERR_HOST_RESOURCES when host memory (for validation or
  *   host tables) or host threads cannot be had; no C++ exception leaves the
  *   library; TC_ERR_HIP when the HIP runtime rejects a launch (the HIP
@@ -134,7 +135,7 @@ typedef struct {
  * size has room for 4n + 2^23 tasks, which keeps 1 KiB pieces for payloads
  * up to ~2 KiB per fragment plus 8 GiB.  Offsets plus lengths must stay below
  * 2^48. */
-size_t tc_copy_fragments_workspace(int64_t n); /* 0 for n < 0 or n > 2^40 */
+size_t tc_copy_fragments_workspace(int64_t n); /* 0 for n < 0 or n > 2^33 */
 /* Smallest workspace a plan of n descriptors accepts (room for n + 1 tasks;
  * the task size then grows to fit, so payloads up to 2^30 bytes always fit).
  * Fewer, longer tasks use fewer waves: a copy needs tens of thousands of

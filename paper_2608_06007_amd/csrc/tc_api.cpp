@@ -388,8 +388,11 @@ tc_status tc_scatter_blocks(const tc_block_pool* pool, const int32_t* ids, int64
   }
 }
 
-// Counts above this are refused: the workspace sizes would not fit size_t.
-constexpr int64_t kMaxCount = int64_t(1) << 40;
+// Fragment, item and task counts above this are refused.  The plan and
+// reduce kernels launch one 256-thread workgroup per 1024 fragments or tasks
+// without striding, and a dispatch counts its work-items in 32 bits; 2^33
+// descriptors (206 GB) already exceed what one GPU holds.
+constexpr int64_t kMaxCount = int64_t(1) << 33;
 
 size_t tc_copy_fragments_workspace(int64_t n) {
   if (n < 0 || n > kMaxCount) return 0;
@@ -466,6 +469,7 @@ tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace
       cut = 0;
     }
     if (hdr.total_tasks > L.capacity) return TC_ERR_WORKSPACE;
+    if (hdr.total_tasks > uint64_t(kMaxCount)) return TC_ERR_INVALID_ARGUMENT;
     // Long lists with scattered destinations are planned in destination order
     // (same tasks, so the same count): the copy then writes in address order.
     const tc_fragment* planned = frags;
@@ -491,7 +495,8 @@ tc_status tc_copy_planned(const void* src_base, void* dst_base, const void* work
                           size_t workspace_bytes, uint64_t total_tasks, hipStream_t stream) {
   try {
     if (total_tasks == 0) return TC_OK;
-    if (!src_base || !dst_base || !workspace || (uintptr_t)workspace % 256)
+    if (!src_base || !dst_base || !workspace || (uintptr_t)workspace % 256 ||
+        total_tasks > uint64_t(kMaxCount))
       return TC_ERR_INVALID_ARGUMENT;
     // Whatever the plan's fragment count, its task table lies inside the
     // workspace: a larger count cannot come from a plan made in it.
@@ -539,7 +544,7 @@ static tc_status digest_common(const void* read_base, void* workspace, size_t wo
   if (n == 0) return total_tasks == 0 ? TC_OK : TC_ERR_INVALID_ARGUMENT;
   if (!digests || !workspace || (uintptr_t)workspace % 256 || (uintptr_t)digests % 8)
     return TC_ERR_INVALID_ARGUMENT;
-  if (total_tasks && !read_base) return TC_ERR_INVALID_ARGUMENT;
+  if ((total_tasks && !read_base) || total_tasks > uint64_t(kMaxCount)) return TC_ERR_INVALID_ARGUMENT;
   *L = tc::plan_layout(n, workspace_bytes);
   if (total_tasks > L->capacity) return TC_ERR_WORKSPACE;
   if (validating()) {

@@ -60,6 +60,12 @@ def test_absurd_counts_are_refused_not_wrapped(lib):
     assert lib.tc_dequant_fp8_blockscaled(P(16), P(16), P(16), P(16), huge, 128, P(4096), 1 << 20, None) == 1
     assert lib.tc_plan_fragments(P(16), huge, P(4096), 1 << 20, None, None) == 1
     assert lib.tc_copy_fragments(P(16), P(16), P(16), huge, P(4096), 1 << 20, None) == 1
+    # counts just past the limit (2^33), and task counts past it
+    over = (1 << 33) + 1
+    assert tc.tc_copy_fragments_workspace(over) == 0 and tc.tc_copy_fragments_workspace(1 << 33) > 0
+    assert lib.tc_plan_fragments(P(16), over, P(4096), 1 << 20, None, None) == 1
+    assert lib.tc_copy_planned(P(16), P(16), P(4096), 1 << 62, ctypes.c_uint64(over), None) == 1
+    assert lib.tc_digest_planned(P(16), 0, P(4096), 1 << 62, ctypes.c_uint64(over), 1, P(16), None) == 1
 
 
 def test_argument_errors_need_no_gpu(lib):
