@@ -147,7 +147,9 @@ size_t tc_copy_fragments_workspace_min(int64_t n);
  * BLOCKS the host once, until the plan's task count has been computed on the
  * stream (the copy's launch size depends on it); the copy itself is
  * asynchronous.  The workspace may be reused once the stream has passed the
- * copy. */
+ * copy.  A non-empty fragment whose source or destination range ends past
+ * 2^48 is TC_ERR_OUT_OF_RANGE in every mode: the plan's count pass flags it
+ * on the device and nothing is copied. */
 tc_status tc_copy_fragments(const void* src_base, void* dst_base, const tc_fragment* frags,
                             int64_t n, void* workspace, size_t workspace_bytes,
                             hipStream_t stream);
@@ -158,7 +160,8 @@ tc_status tc_copy_fragments(const void* src_base, void* dst_base, const tc_fragm
  * once.  tc_copy_planned then copies with that plan -- asynchronously, as
  * often as wanted -- for any src/dst bases, while the workspace is kept
  * unchanged.  total_tasks == 0 means there is nothing to copy; a count
- * larger than the workspace's task table can hold is TC_ERR_WORKSPACE. */
+ * larger than the workspace's task table can hold is TC_ERR_WORKSPACE; a
+ * fragment ending past 2^48 is TC_ERR_OUT_OF_RANGE, with no plan written. */
 tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace,
                             size_t workspace_bytes, uint64_t* total_tasks /* host, out */,
                             hipStream_t stream);

@@ -459,6 +459,8 @@ tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace
       e = hipMemcpyAsync(&hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, stream);
       if (e == hipSuccess) e = hipStreamSynchronize(stream);
       if (e != hipSuccess) return hip_fail(e);
+      // a task holds 48-bit offsets: refuse the list before anything is expanded
+      if (hdr.out_of_range) return TC_ERR_OUT_OF_RANGE;
       if (hdr.total_tasks <= L.capacity) break;
       // Too many 1 KiB pieces for the workspace: larger pieces bound the count
       // by n + payload / piece <= capacity.

@@ -49,6 +49,8 @@ struct PlanHeader {
   uint64_t permuted;       // the tasks follow the reordered list; perm maps back
   uint64_t cut;            // 127: tasks after a fragment's first start on a 128-byte
                            // destination line; 0: tasks start at multiples of the piece
+  uint64_t out_of_range;   // some non-empty fragment ends past 2^48 (source or destination):
+                           // its tasks could not hold the offsets, so nothing is planned
 };
 
 // Workspace layout: header | tasks[capacity] | digest slots[capacity] |

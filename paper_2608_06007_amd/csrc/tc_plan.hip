@@ -70,8 +70,9 @@ __device__ uint64_t block_max_u64(uint64_t v) {
 }
 
 // Per block: task and byte sums, whether some destination starts below its
-// predecessor's (checked across the block's last boundary too), and the
-// largest destination end.
+// predecessor's (checked across the block's last boundary too), the largest
+// destination end, and whether some fragment ends past the 48-bit offsets of
+// a task (flag bit 0: unordered, bit 1: out of range).
 __global__ __launch_bounds__(kThreads) void k_plan_count(const tc_fragment* __restrict__ frags,
                                                         const int64_t n, const uint64_t piece,
                                                         const uint64_t cut,
@@ -81,7 +82,7 @@ __global__ __launch_bounds__(kThreads) void k_plan_count(const tc_fragment* __re
                                                         uint64_t* __restrict__ block_dend) {
   const int64_t f0 = int64_t(blockIdx.x) * kPlanPerBlock + int64_t(threadIdx.x) * kPlanPerThread;
   uint64_t c = 0, l = 0, dend = 0;
-  int unord = 0;
+  int unord = 0, bad = 0;
 #pragma unroll
   for (int j = 0; j < kPlanPerThread; ++j)
     if (f0 + j < n) {
@@ -89,17 +90,21 @@ __global__ __launch_bounds__(kThreads) void k_plan_count(const tc_fragment* __re
       c += pieces_of(f, piece, cut);
       l += f.len;
       if (f.len && f.dst_off + f.len > dend) dend = f.dst_off + f.len;
+      if (f.len && (f.len > kOffsetLimit || f.src_off > kOffsetLimit - f.len ||
+                    f.dst_off > kOffsetLimit - f.len))
+        bad = 1;
       if (f0 + j + 1 < n && frags[f0 + j + 1].dst_off < f.dst_off) unord = 1;
     }
   uint64_t tc_, tl;
   block_exclusive_scan(c, &tc_);
   block_exclusive_scan(l, &tl);
   const int any_unord = __syncthreads_or(unord);
+  const int any_bad = __syncthreads_or(bad);
   const uint64_t bdend = block_max_u64(dend);
   if (threadIdx.x == 0) {
     block_cnt[blockIdx.x] = tc_;
     block_len[blockIdx.x] = tl;
-    block_unord[blockIdx.x] = any_unord ? 1 : 0;
+    block_unord[blockIdx.x] = (any_unord ? 1u : 0u) | (any_bad ? 2u : 0u);
     block_dend[blockIdx.x] = bdend;
   }
 }
@@ -117,13 +122,14 @@ __global__ __launch_bounds__(kThreads) void k_plan_scan(uint64_t* __restrict__ b
                                                        PlanHeader* __restrict__ hdr,
                                                        uint64_t* __restrict__ tstart_end) {
   uint64_t carry = 0, bytes = 0, dend = 0;
-  int unord = 0;
+  int unord = 0, bad = 0;
   for (int64_t base = 0; base < nblocks; base += kThreads) {
     const int64_t i = base + threadIdx.x;
     const uint64_t v = i < nblocks ? block_cnt[i] : 0;
     const uint64_t l = i < nblocks ? block_len[i] : 0;
     if (i < nblocks) {
-      unord |= block_unord[i] ? 1 : 0;
+      unord |= (block_unord[i] & 1u) ? 1 : 0;
+      bad |= (block_unord[i] & 2u) ? 1 : 0;
       dend = dend > block_dend[i] ? dend : block_dend[i];
     }
     uint64_t total, ltot;
@@ -134,6 +140,7 @@ __global__ __launch_bounds__(kThreads) void k_plan_scan(uint64_t* __restrict__ b
     bytes += ltot;
   }
   const int any_unord = __syncthreads_or(unord);
+  const int any_bad = __syncthreads_or(bad);
   dend = block_max_u64(dend);
   if (threadIdx.x == 0) {
     hdr->total_tasks = carry;
@@ -145,6 +152,7 @@ __global__ __launch_bounds__(kThreads) void k_plan_scan(uint64_t* __restrict__ b
     hdr->dst_end = dend;
     hdr->permuted = permuted;
     hdr->cut = cut;
+    hdr->out_of_range = any_bad ? 1 : 0;
     *tstart_end = carry;
   }
 }

@@ -129,3 +129,42 @@ def test_cast_and_dequant_guards():
         assert np.array_equal(hs[s0:s0 + wsc.size].view(np.uint32), wsc.reshape(-1).view(np.uint32))
         assert np.array_equal(hy[o:o + rows * cols].reshape(rows, cols), oracle.dequant_fp8_blockscaled(wq, wsc))
     assert np.array_equal(qs.cpu().numpy(), oracle.cast_fp8_scaled(hx[:1001], 0.01))
+
+
+@pytest.mark.parametrize("side", ["src", "dst"])
+def test_plan_refuses_offsets_past_48_bits(side):
+    """A task holds 48-bit offsets, so a non-empty fragment ending past 2^48
+    is refused by the plan's count pass on the device, with validation off,
+    and nothing is copied.  A fragment ending exactly at 2^48 is planned (the
+    plan only reads descriptors; it is not copied here)."""
+    assert not tc.tc_get_validate()
+    lim = 1 << 48
+    ok = np.array([[0, 0, 4096], [8192, 4096, 100]], dtype=np.uint64)
+    bad = ok.copy()
+    col = 0 if side == "src" else 1
+    bad[1, col] = lim - 50                     # ends 50 bytes past 2^48
+    edge = ok.copy()
+    edge[1, col] = lim - 100                   # ends exactly at 2^48
+    src = synth.random_bytes(1 << 16, 95, device=DEV)
+    whole, dst = _guarded(1 << 16, fill=0x33)
+    whole[:GUARD] = CANARY
+    whole[GUARD + (1 << 16):] = CANARY
+    ws = torch.empty(tc.tc_copy_fragments_workspace(2), dtype=torch.uint8, device=DEV)
+    fr = torch.from_numpy(bad.view(np.int64)).to(DEV)
+    with pytest.raises(tc.TcError) as e:
+        tc.tc_plan_fragments(fr, ws)
+    assert e.value.status == 2
+    with pytest.raises(tc.TcError) as e:
+        tc.tc_copy_fragments(src, dst, fr, ws)
+    assert e.value.status == 2
+    torch.cuda.synchronize()
+    assert bool((dst == 0x33).all())
+    _guards_intact(whole, 1 << 16)
+    # a fragment longer than 2^48 on its own is refused the same way
+    huge = ok.copy()
+    huge[1] = (0, 8192, lim + 16)
+    with pytest.raises(tc.TcError) as e:
+        tc.tc_plan_fragments(torch.from_numpy(huge.view(np.int64)).to(DEV), ws)
+    assert e.value.status == 2
+    assert tc.tc_plan_fragments(torch.from_numpy(edge.view(np.int64)).to(DEV), ws) > 0
+    torch.cuda.synchronize()
