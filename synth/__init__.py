@@ -185,6 +185,30 @@ def fragment_storm(n: int, pool_bytes: int, seed: int, lo: int = 64, hi: int = 6
     return np.stack([src, dst, lens], axis=1).astype(np.uint64)
 
 
+def fragment_mix(n: int, seed: int, align: int = 16, slack: float = 0.5, big_max: int = 4 * MiB):
+    """``n`` fragments with mixed lengths -- about 10% empty, 20% tiny
+    (below 64 bytes), 60% log-uniform in [64 B, 64 KiB], 10% large (up to
+    ``big_max``) -- rounded down to multiples of ``align``, laid out at random in a
+    source pool and a destination pool whose sizes exceed the payload by the
+    fraction ``slack``.  Returns (rows, src_pool_bytes, dst_pool_bytes)."""
+    rng = np.random.default_rng(seed)
+    kind = rng.choice(4, size=n, p=[0.1, 0.2, 0.6, 0.1])
+    lens = np.zeros(n, dtype=np.int64)
+    tiny, mid, big = kind == 1, kind == 2, kind == 3
+    lens[tiny] = rng.integers(1, 64, size=int(tiny.sum()))
+    lens[mid] = np.floor(np.exp(rng.uniform(np.log(64), np.log(64 * KiB), size=int(mid.sum()))))
+    lens[big] = rng.integers(64 * KiB, big_max, size=int(big.sum()))
+    lens = (lens // align) * align
+    total = int(lens.sum())
+    pools = []
+    for _ in range(2):
+        pool = ((int(total * (1 + slack)) + 4096) // align + 1) * align
+        pools.append(pool)
+    src = _layout(lens, pools[0], align, rng)
+    dst = _layout(lens, pools[1], align, rng)
+    return np.stack([src, dst, lens], axis=1).astype(np.uint64), pools[0], pools[1]
+
+
 def moe_permutation(n_experts: int, expert_bytes: int, seed: int):
     """Destination expert slot j receives source expert perm[j]."""
     rng = np.random.default_rng(seed)
