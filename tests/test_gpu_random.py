@@ -8,6 +8,9 @@
 * Ragged cast items (random shapes, row strides, element offsets, code and
   scale padding) over values of random magnitude with zeros, subnormals and
   now and then an Inf or NaN; the codes are then decoded by the inverse.
+* Random block pools (region count, block size, stride, unaligned region
+  bases, repeated ids) through gather and scatter, and random staging rings
+  through publish and hydrate.
 """
 import numpy as np
 import pytest
@@ -110,3 +113,95 @@ def test_random_cast_items_and_inverse(seed):
     codes = np.concatenate(qs).astype(np.uint8)
     scales = np.concatenate(ss).astype(np.float32)
     _dequant_matrices(codes, scales, dmats, dst_pad=int(rng.choice([0, 3])))
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_block_pools(seed):
+    """Random pools: 1-8 regions, block sizes from 1 byte to 70,000 (16-byte
+    multiples half the time), stride pads, region bases at random byte
+    offsets inside one allocation, ids with repeats for the gather and
+    distinct for the scatter."""
+    rng = np.random.default_rng(4100 + seed)
+    R = int(rng.integers(1, 9))
+    B = int(rng.integers(1, 70000))
+    if rng.random() < 0.5:
+        B = max(16, (B // 16) * 16)
+    stride = B + int(rng.choice([0, 16, int(rng.integers(1, 64))]))
+    nb = int(rng.integers(1, 200))
+    n = int(rng.integers(1, 3 * nb + 1))
+    span = (nb - 1) * stride + B
+    lead = [int(rng.choice([0, 16, int(rng.integers(0, 64))])) for _ in range(R)]
+    print(f"case seed={seed} R={R} B={B} stride={stride} nb={nb} n={n} lead={lead}", flush=True)
+    whole = synth.random_bytes(sum(lead) + R * span, 5100 + seed, device=DEV)
+    regions, pos = [], 0
+    for r in range(R):
+        pos += lead[r]
+        regions.append(whole[pos:pos + span])
+        pos += span
+    ids_np = rng.integers(0, nb, size=n).astype(np.int32)           # repeats allowed
+    ids = torch.from_numpy(ids_np).to(DEV)
+    out = torch.empty(n * R * B, dtype=torch.uint8, device=DEV)
+    tc.tc_gather_blocks(regions, nb, B, stride, ids, out)
+    uniq_np = rng.permutation(nb)[:int(rng.integers(1, nb + 1))].astype(np.int32)
+    uniq = torch.from_numpy(uniq_np).to(DEV)
+    inp = synth.random_bytes(len(uniq_np) * R * B, 6100 + seed, device=DEV)
+    dst_whole = torch.full_like(whole, 0x3C)
+    dst = []
+    pos = 0
+    for r in range(R):
+        pos += lead[r]
+        dst.append(dst_whole[pos:pos + span])
+        pos += span
+    tc.tc_scatter_blocks(dst, nb, B, stride, uniq, inp)
+    torch.cuda.synchronize()
+    hosts = [_host(x) for x in regions]
+    want = oracle.gather_blocks(hosts, B, stride, ids_np)
+    assert np.array_equal(_host(out).reshape(want.shape), want)
+    back = [np.full(span, 0x3C, np.uint8) for _ in range(R)]
+    oracle.scatter_blocks(back, B, stride, uniq_np, _host(inp).reshape(len(uniq_np), R, B))
+    hd = _host(dst_whole)
+    pos = 0
+    for r in range(R):
+        assert np.all(hd[pos:pos + lead[r]] == 0x3C)            # the gaps between regions
+        pos += lead[r]
+        assert np.array_equal(hd[pos:pos + span], back[r]), f"region {r}"
+        pos += span
+    assert np.all(hd[pos:] == 0x3C)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_staging(seed):
+    """Random rings (2-6 slots of 4 KiB to 1 MiB, 1-4 host threads) moving a
+    random number of ids through publish and hydrate, pageable or pinned."""
+    rng = np.random.default_rng(7100 + seed)
+    R, B = int(rng.integers(1, 5)), int(rng.choice([4096, 4096 + 16, 512, 100]))
+    nb = int(rng.integers(20, 300))
+    per_id = R * B
+    slot = int(max(per_id, rng.integers(4096, 1 << 20)))
+    slots, threads = int(rng.integers(2, 7)), int(rng.integers(1, 5))
+    pinned = bool(rng.random() < 0.5)
+    n = int(rng.integers(1, nb + 1))
+    print(f"case seed={seed} R={R} B={B} nb={nb} n={n} slot={slot} slots={slots} threads={threads} "
+          f"pinned={pinned}", flush=True)
+    span = nb * B
+    regions = [synth.random_bytes(span, 8100 + seed * 8 + r, device=DEV) for r in range(R)]
+    ids_np = rng.permutation(nb)[:n].astype(np.int32)
+    ids = torch.from_numpy(ids_np).to(DEV)
+    stage = torch.empty(int(rng.integers(1, 4)) * slot, dtype=torch.uint8, device=DEV)
+    if pinned:
+        host = torch.zeros(n * per_id, dtype=torch.uint8).pin_memory()
+    else:
+        host = np.zeros(n * per_id, dtype=np.uint8)
+    with tc.Stager(slot_bytes=slot, slots=slots, host_threads=threads) as st:
+        tc.tc_publish_to_host(st.handle, regions, nb, B, B, ids, host, stage)
+        hb = host.numpy() if pinned else host
+        hosts = [_host(r) for r in regions]
+        want = oracle.gather_blocks(hosts, B, B, ids_np)
+        assert np.array_equal(hb.reshape(want.shape), want)
+        dst = [torch.full_like(r, 0x77) for r in regions]
+        tc.tc_hydrate_from_host(st.handle, dst, nb, B, B, ids, host, stage)
+        torch.cuda.synchronize()
+    back = [np.full(span, 0x77, np.uint8) for _ in range(R)]
+    oracle.scatter_blocks(back, B, B, ids_np, want)
+    for r in range(R):
+        assert np.array_equal(_host(dst[r]), back[r]), f"region {r}"
