@@ -349,25 +349,6 @@ bool pool_valid(const tc_block_pool* p) {
 }
 }  // namespace tc
 
-namespace tc {
-hipError_t device_info(DeviceInfo* out) {
-  static int cus[64] = {0};
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-  if (cus[dev] == 0) {
-    int c = 0;
-    e = hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e != hipSuccess) return e;
-    cus[dev] = c > 0 ? c : 1;
-  }
-  out->device = dev;
-  out->cus = cus[dev];
-  return hipSuccess;
-}
-}  // namespace tc
-
 extern "C" {
 
 tc_status tc_gather_blocks(const tc_block_pool* pool, const int32_t* ids, int64_t n, void* out,

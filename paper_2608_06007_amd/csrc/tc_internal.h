@@ -86,13 +86,6 @@ tc_status hip_status(hipError_t e);
 // blocks x stride, one id's regions x block bytes) within 63 bits.
 bool pool_valid(const tc_block_pool* p);
 
-// Launch geometry of the current device.
-struct DeviceInfo {
-  int device;
-  int cus;
-};
-hipError_t device_info(DeviceInfo* out);
-
 // --- block gather / scatter --------------------------------------------
 hipError_t launch_blocks(const RegionTable& tab, int32_t num_regions, int64_t block_bytes,
                          int64_t block_stride, const int32_t* ids, int64_t n, uint8_t* buf,
