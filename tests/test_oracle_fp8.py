@@ -306,3 +306,28 @@ def test_dequant_inverts_the_cast_within_the_rounding_bound():
     bound = np.where(normal, (2.0 ** -4) * np.abs(x), 2.0 ** -10 * scale_el) * (1 + 2.0 ** -8) + \
         2.0 ** -9 * np.abs(back)
     assert np.all(np.abs(back - x) <= bound)
+
+
+def test_bf16_rounding_matches_torch():
+    """The oracle's binary32 -> bf16 step of the inverse against torch's
+    float32 -> bfloat16 conversion (nearest, ties to even): random patterns,
+    exact ties and their neighbours at many exponents, subnormals, the
+    largest finite values, the overflow boundary and infinities; NaN gives
+    the canonical 0x7FC0."""
+    rng = np.random.default_rng(63)
+    pats = [rng.integers(0, 1 << 32, size=20000, dtype=np.uint64)]
+    mant = rng.integers(0, 1 << 7, size=400, dtype=np.uint64) << np.uint64(16)
+    for e in list(range(0, 6)) + list(range(100, 140)) + list(range(248, 256)):
+        base = (np.uint64(e) << np.uint64(23)) | mant
+        for d in (0x7FFF, 0x8000, 0x8001, 0x18000, 0xFFFF):      # below, at, above a tie; odd-LSB tie
+            pats.append(base | np.uint64(d & 0xFFFF) | (np.uint64(d >> 16) << np.uint64(16)))
+    pats.append(np.array([0x7F7F7FFF, 0x7F7F8000, 0x7F7FFFFF, 0x7F800000, 0x00000001, 0x007FFFFF,
+                          0x00008000, 0x00018000], dtype=np.uint64))
+    bits = np.concatenate(pats) & np.uint64(0xFFFFFFFF)
+    bits = np.concatenate([bits, bits | np.uint64(0x80000000)]).astype(np.uint32)
+    vals = bits.view(np.float32)
+    finite_or_inf = ~np.isnan(vals)
+    ref = torch.from_numpy(vals.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    got = np.array([oracle.bf16_round(float(v)) for v in vals], dtype=np.uint16)
+    assert np.array_equal(got[finite_or_inf], ref[finite_or_inf])
+    assert np.all(got[~finite_or_inf] == 0x7FC0)
