@@ -31,7 +31,9 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# TC_ORACLE_LIB loads another build of oracle.c instead (the mutation test
+# runs the pins against deliberately broken copies that way).
+_LIB_PATH = os.environ.get("TC_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 TILE = 128
@@ -43,6 +45,8 @@ def _load():
     if _lib is not None:
         return _lib
     if not os.path.exists(_LIB_PATH):
+        if os.environ.get("TC_ORACLE_LIB"):
+            raise RuntimeError(f"TC_ORACLE_LIB names a missing library: {_LIB_PATH}")
         from . import build as _build
         _build.build()
     lib = ctypes.CDLL(_LIB_PATH)

@@ -11,17 +11,21 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB = os.path.join(HERE, "liboracle.so")
 
 
-def build(verbose: bool = False) -> str:
+def compile_source(c_path: str, out_path: str, verbose: bool = False) -> str:
+    """Compile one C source with the oracle's flags into a shared library."""
     cmd = [
         "gcc", "-O2", "-fno-fast-math", "-std=c11", "-fopenmp", "-shared",
-        "-fPIC", "-Wall", "-Wextra", "-o", LIB + ".tmp",
-        os.path.join(HERE, "oracle.c"), "-lm",
+        "-fPIC", "-Wall", "-Wextra", "-I", HERE, "-o", out_path + ".tmp", c_path, "-lm",
     ]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
-    return LIB
+    os.replace(out_path + ".tmp", out_path)
+    return out_path
+
+
+def build(verbose: bool = False) -> str:
+    return compile_source(os.path.join(HERE, "oracle.c"), LIB, verbose)
 
 
 if __name__ == "__main__":
