@@ -162,3 +162,56 @@ def test_concurrent_streams_independent_plans():
     assert np.array_equal(buf.cpu().numpy(), want.reshape(-1))
     assert int(plans[0][1][56:64].cpu().numpy().view(np.uint64)[0]) == 1   # reordered
     assert int(plans[1][1][56:64].cpu().numpy().view(np.uint64)[0]) == 0
+
+
+def test_two_host_threads_cast_at_once():
+    """Two host threads, each on its own stream, cast different item sets
+    at the same time, over and over: the item tables of both pass through the
+    library's one pinned staging buffer per device, so a call must not
+    overwrite it while the other's copy out of it is still in flight.  Every
+    result against the oracle."""
+    import threading
+    rng = np.random.default_rng(131)
+    jobs = []
+    for k in range(2):
+        rows, cols = 256 + 128 * k, 384 - 128 * k
+        x = rng.normal(0, 0.02 * (k + 1), size=rows * cols).astype(np.float32)
+        bits = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+        # many small items: row bands of one tile row each, so the staged table is long
+        items = np.zeros(rows // 128, dtype=tc.CAST_ITEM_DTYPE)
+        for i in range(rows // 128):
+            items[i] = (i * 128 * cols, 128, cols, cols, i * 128 * cols, cols,
+                        i * ((cols + 127) // 128), (cols + 127) // 128)
+        q_want, s_want = oracle.cast_fp8_blockscaled(bits.reshape(rows, cols))
+        src = torch.from_numpy(bits.view(np.int16)).to(DEV)
+        jobs.append(dict(src=src, items=items, rows=rows, cols=cols, q_want=q_want, s_want=s_want,
+                         stream=torch.cuda.Stream(), errors=[]))
+
+    def run(job):
+        try:
+            with torch.cuda.stream(job["stream"]):
+                for _ in range(25):
+                    q = torch.full((job["rows"] * job["cols"],), 0xEE, dtype=torch.uint8, device=DEV)
+                    s = torch.full((s_len(job),), -1.0, dtype=torch.float32, device=DEV)
+                    ws = torch.empty(tc.tc_cast_fp8_workspace(len(job["items"])), dtype=torch.uint8,
+                                     device=DEV)
+                    tc.tc_cast_fp8_blockscaled(job["src"], q, s, job["items"], ws, stream=job["stream"])
+                    job["stream"].synchronize()
+                    if not (np.array_equal(q.cpu().numpy().reshape(job["q_want"].shape), job["q_want"])
+                            and np.array_equal(s.cpu().numpy().view(np.uint32),
+                                               job["s_want"].reshape(-1).view(np.uint32))):
+                        job["errors"].append("mismatch")
+                        return
+        except Exception as e:  # reported after the join
+            job["errors"].append(repr(e))
+
+    def s_len(job):
+        return (job["rows"] // 128) * ((job["cols"] + 127) // 128)
+
+    threads = [threading.Thread(target=run, args=(j,)) for j in jobs]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert [j["errors"] for j in jobs] == [[], []]
