@@ -391,3 +391,23 @@ def test_reshard_cast_items_refuse_tiles_across_sources(lib):
     f32 = [((0,), 128, 128, 4, tc.SPLIT_NONE, 0)]
     with pytest.raises(tc.TcError):
         tc.tc_reshard_cast_item_count(f32, 1, 0)
+
+
+def test_missing_library_fails_loudly():
+    """Without the HIP library every entry point raises: there is no CPU
+    fallback.  Run in a fresh interpreter with the library path pointed at a
+    file that does not exist."""
+    import subprocess
+    import sys
+    code = ("import paper_2608_06007_amd as tc\n"
+            "tc.lib_path = '/nonexistent/libtchip.so'\n"
+            "try:\n"
+            "    tc.tc_copy_fragments_workspace(10)\n"
+            "except RuntimeError as e:\n"
+            "    print('raised:', e)\n"
+            "else:\n"
+            "    print('no error')\n")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.startswith("raised:") and "missing" in r.stdout
