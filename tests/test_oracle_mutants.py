@@ -3,11 +3,15 @@
 Each mutant is oracle.c with one deliberate, plausible error: a wrong tie
 rule, wrong saturation, wrong subnormal magnitudes, a dropped zero sign, a
 signed amax, a wrong scale constant, the wrong code for a non-finite tile,
-a transposed scale grid in the cast or in its inverse, a ties-away bf16
+a transposed (column-major) scale grid in the cast or in its inverse, a
+ties-away bf16
 rounding, a short copy, a gather that strides by the block size, or a
 digest weight off by one.  Each is compiled with the oracle's own flags and
 the pin suites run against it in a subprocess; a mutant that no pin fails
-would mean the pins do not pin that part of the oracle.
+would mean the pins do not pin that part of the oracle.  Every mutant stays
+inside its buffers (a transposed grid is stored densely column-major, not
+with the row pitch), so a caught mutant fails a test rather than corrupting
+the heap of the pytest process that runs the pins.
 """
 import concurrent.futures as cf
 import os
@@ -38,10 +42,10 @@ MUTANTS = {
     "gather_stride": ("regions[r] + (int64_t)ids[i] * block_stride;\n      uint8_t* to = out",
                       "regions[r] + (int64_t)ids[i] * block_bytes;\n      uint8_t* to = out", MOVES),
     "digest_weight": ("s2 += (i + 1) * (uint64_t)p[i];", "s2 += i * (uint64_t)p[i];", MOVES),
-    "scale_grid_transposed": ("scales[ti * scale_ld + tj] = s;", "scales[tj * scale_ld + ti] = s;", FP8),
+    "scale_grid_transposed": ("scales[ti * scale_ld + tj] = s;", "scales[tj * tile_rows + ti] = s;", FP8),
     "nonfinite_code": ("q[r * q_ld + c] = 0x7F;", "q[r * q_ld + c] = 0x7E;", FP8),
     "inverse_scale_transposed": ("float s = scales[(r / 128) * scale_ld + c / 128];",
-                                 "float s = scales[(c / 128) * scale_ld + r / 128];", FP8),
+                                 "float s = scales[(c / 128) * ((rows + 127) / 128) + r / 128];", FP8),
 }
 
 
