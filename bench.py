@@ -383,9 +383,16 @@ def run_cast(torch, tc, synth, args, stream):
     ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device="cuda")
     it = items
     nbytes = 2 * shard_n + shard_n + 4 * n_scales
-    ms = _time_calls(torch, stream, lambda: tc.tc_cast_fp8_blockscaled(src, q, sc, it, ws, stream=stream),
+    # a rank's item list is the same at every weight synchronization: the
+    # tile table is written once, and each cast launches the kernels alone
+    plan = tc.tc_cast_fp8_prepare(src, q, it, ws, stream=stream)
+    ms = _time_calls(torch, stream, lambda: tc.tc_cast_fp8_planned(src, q, sc, ws, plan, stream=stream),
                      args.warmup, args.cast_steps)
-    out = {"items": int(len(items)), "tiles": int(n_scales), "cast": _stats(ms, nbytes)}
+    # the one-call form, which writes the table (14 small launches) each time
+    ms1 = _time_calls(torch, stream, lambda: tc.tc_cast_fp8_blockscaled(src, q, sc, it, ws, stream=stream),
+                      args.warmup, args.cast_steps)
+    out = {"items": int(len(items)), "tiles": int(n_scales), "cast": _stats(ms, nbytes),
+           "cast_one_call": _stats(ms1, nbytes)}
     if not args.skip_cpu:
         out["cpu_oracle"] = oracle_cast_sample(torch, src, items, 7, "layer 0 of the shard cast")
     del src
@@ -394,9 +401,13 @@ def run_cast(torch, tc, synth, args, stream):
     ditems = tcv.dequant_items(spec, tp)
     y = torch.empty(shard_n, dtype=torch.bfloat16, device="cuda")
     dws = torch.empty(tc.tc_dequant_fp8_workspace(len(ditems)), dtype=torch.uint8, device="cuda")
-    dms = _time_calls(torch, stream, lambda: tc.tc_dequant_fp8_blockscaled(q, sc, y, ditems, dws, stream=stream),
+    dplan = tc.tc_dequant_fp8_prepare(q, y, ditems, dws, stream=stream)
+    dms = _time_calls(torch, stream, lambda: tc.tc_dequant_fp8_planned(q, sc, y, dws, dplan, stream=stream),
                       args.warmup, args.cast_steps)
+    dms1 = _time_calls(torch, stream, lambda: tc.tc_dequant_fp8_blockscaled(q, sc, y, ditems, dws, stream=stream),
+                       args.warmup, args.cast_steps)
     out["dequant"] = _stats(dms, shard_n + 4 * n_scales + 2 * shard_n)
+    out["dequant_one_call"] = _stats(dms1, shard_n + 4 * n_scales + 2 * shard_n)
     del q, sc, ws, it, y, dws
     torch.cuda.empty_cache()
     return out
@@ -420,7 +431,8 @@ def run_reshard_cast(torch, tc, synth, args, stream):
     sc = torch.empty(n_scales, dtype=torch.float32, device="cuda")
     ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device="cuda")
     nbytes = 2 * shard_n + shard_n + 4 * n_scales
-    ms = _time_calls(torch, stream, lambda: tc.tc_cast_fp8_blockscaled(src, q, sc, items, ws, stream=stream),
+    plan = tc.tc_cast_fp8_prepare(src, q, items, ws, stream=stream)
+    ms = _time_calls(torch, stream, lambda: tc.tc_cast_fp8_planned(src, q, sc, ws, plan, stream=stream),
                      args.warmup, args.cast_steps)
     out = {"items": int(len(items)), "tiles": int(n_scales), "reshard_cast": _stats(ms, nbytes)}
     del src, q, sc, ws
@@ -470,10 +482,89 @@ def run_moe(torch, tc, synth, args, stream):
     nbytes = 2 * n_exp * e_bytes
     ms = _time_calls(torch, stream, lambda: tc.tc_copy_fragments(src, dst, frags, ws, stream=stream),
                      args.warmup, args.cast_steps)
-    out = {"plan_and_copy": _stats(ms, nbytes)}
+    total = tc.tc_plan_fragments(frags, ws, stream=stream)
+    planned = _time_calls(torch, stream, lambda: tc.tc_copy_planned(src, dst, ws, total, stream=stream),
+                          args.warmup, args.cast_steps)
+    out = {"plan_and_copy": _stats(ms, nbytes), "copy_planned": _stats(planned, nbytes)}
     del src, dst, frags, ws
     torch.cuda.empty_cache()
     return out
+
+
+# Zero-copy sharing between two processes on this GPU (HIP IPC): a paged KV
+# pool of 64 regions x 512 blocks x 32 KiB (1 GiB, one allocation), exported
+# by one process; another opens it and gathers 256 ids of every region
+# straight out of it.  The importer's gather is timed against the same gather
+# from a local copy of the pool.
+IPC_SHAPE = (64, 512, 32768, 256)
+
+
+def run_ipc(torch, tc, synth, args, stream):
+    import subprocess
+    _log("[ipc] exporter and importer processes, 1 GiB KV pool")
+    env = dict(os.environ)
+    env["PYTORCH_NO_CUDA_MEMORY_CACHING"] = "1"   # the pool is an allocation of its own
+    env["PYTORCH_NO_HIP_MEMORY_CACHING"] = "1"
+    env.setdefault("HSA_ENABLE_IPC_MODE_LEGACY", "0")
+    me = os.path.abspath(__file__)
+    exporter = subprocess.Popen([sys.executable, "-u", me, "--ipc-role", "export"], stdin=subprocess.PIPE,
+                                stdout=subprocess.PIPE, text=True, env=env)
+    try:
+        line = exporter.stdout.readline()
+        if not line:
+            raise RuntimeError("the exporting process ended early")
+        handle = json.loads(line)["handle"]
+        imp = subprocess.run([sys.executable, "-u", me, "--ipc-role", "import", "--ipc-handle", handle,
+                              "--steps", str(args.cast_steps), "--warmup", str(args.warmup)],
+                             capture_output=True, text=True, env=env, timeout=120)
+        if imp.returncode != 0:
+            raise RuntimeError(f"the importing process failed: {imp.stderr[-1000:]}")
+        out = json.loads(imp.stdout.strip().splitlines()[-1])
+        exporter.stdin.write("done\n")
+        exporter.stdin.flush()
+        exporter.wait(timeout=60)
+    finally:
+        if exporter.poll() is None:
+            exporter.kill()
+            exporter.wait()
+    return out
+
+
+def ipc_role(args):
+    """The child processes of run_ipc."""
+    import torch
+    import synth
+    import paper_2608_06007_amd as tc
+    tc.load()
+    torch.cuda.set_device(0)
+    R, NB, B, N = IPC_SHAPE
+    if args.ipc_role == "export":
+        pool = synth.bf16_normal(R * NB * B // 2, 1.0, synth.SEED_KV_8B, device="cuda").view(torch.uint8)
+        torch.cuda.synchronize()
+        print(json.dumps({"handle": tc.tc_ipc_export(pool).hex()}), flush=True)
+        sys.stdin.readline()   # keep the pool until the importer is done
+        return
+    handle = bytes.fromhex(args.ipc_handle)
+    base = tc.tc_ipc_open(handle)
+    stream = torch.cuda.current_stream()
+    regions = [base + r * NB * B for r in range(R)]
+    ids = torch.from_numpy(synth.ids_without_replacement(NB, N, synth.SEED_KV_8B)).cuda()
+    out = torch.empty(N * R * B, dtype=torch.uint8, device="cuda")
+    local = torch.empty(R * NB * B, dtype=torch.uint8, device="cuda")
+    all_ids = torch.arange(NB, dtype=torch.int32, device="cuda")
+    whole = torch.empty(NB * R * B, dtype=torch.uint8, device="cuda")
+    tc.tc_gather_blocks(regions, NB, B, B, all_ids, whole)       # the pool, through the import
+    local.view(R, NB, B).copy_(whole.view(NB, R, B).transpose(0, 1))
+    del whole
+    local_regions = [local[r * NB * B:(r + 1) * NB * B] for r in range(R)]
+    nbytes = 2 * N * R * B
+    imp = _time_calls(torch, stream, lambda: tc.tc_gather_blocks(regions, NB, B, B, ids, out, stream=stream),
+                      args.warmup, args.steps)
+    loc = _time_calls(torch, stream, lambda: tc.tc_gather_blocks(local_regions, NB, B, B, ids, out, stream=stream),
+                      args.warmup, args.steps)
+    tc.tc_ipc_close(handle, base)
+    print(json.dumps({"pool_bytes": R * NB * B, "gather_from_imported_pool": _stats(imp, nbytes),
+                      "gather_from_local_copy": _stats(loc, nbytes)}), flush=True)
 
 
 PEAK_PCIE_GBS = 64.0  # PCIe 5.0 x16, one direction (32 GT/s x 16 lanes, 128b/130b)
@@ -597,7 +688,7 @@ def run_calib(torch, tc, synth, args, stream):
 
 RUNNERS = {"reshard": run_reshard, "reshard_tp8_tp4": run_reshard44, "cast": run_cast,
            "reshard_cast": run_reshard_cast,
-           "storm": run_storm, "moe": run_moe, "stage": run_stage, "calib": run_calib}
+           "storm": run_storm, "moe": run_moe, "stage": run_stage, "calib": run_calib, "ipc": run_ipc}
 
 
 def main():
@@ -608,9 +699,14 @@ def main():
     ap.add_argument("--cast-steps", type=int, default=20, help="timed launches per extra workload")
     # the host staging workload ("stage") runs only when named: it launches the
     # block kernels once per chunk, which would mix into their profiles
-    ap.add_argument("--workloads", default="kv,reshard,reshard_tp8_tp4,cast,reshard_cast,storm,moe,calib")
+    ap.add_argument("--workloads", default="kv,reshard,reshard_tp8_tp4,cast,reshard_cast,storm,moe,ipc,calib")
     ap.add_argument("--skip-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--ipc-role", choices=["export", "import"], help=argparse.SUPPRESS)
+    ap.add_argument("--ipc-handle", help=argparse.SUPPRESS)
     args = ap.parse_args()
+    if args.ipc_role:
+        ipc_role(args)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this library has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)

@@ -23,7 +23,12 @@
  *   Sec. 3.2 "Artifact") and must stay valid until the work enqueued on
  *   `stream` has completed.  The library keeps no pointer after returning.
  * - Calls are asynchronous and stream-ordered: they validate arguments on the
- *   host, enqueue kernels on `stream` and return.  n == 0 enqueues nothing.
+ *   host, enqueue kernels on `stream` and return, without waiting for the
+ *   device.  n == 0 enqueues nothing.  The exceptions say so: the calls that
+ *   hand a device-computed number back to the host (tc_plan_fragments,
+ *   tc_plan_status) and the host staging calls.  The library allocates
+ *   nothing that outlives a call, on the device or the host, apart from a
+ *   stager's own ring (created and destroyed by the caller).
  * - Calls are pure functions of their inputs, so re-running one after a
  *   failure is safe (the paper's idempotent retry, Sec. 3.2 "Plan").
  * - Errors: TC_ERR_INVALID_ARGUMENT for null pointers, negative sizes,
@@ -37,13 +42,16 @@
  *   also copy the descriptors to the host, synchronize the stream, and
  *   report ids out of range (TC_ERR_OUT_OF_RANGE) and aliasing writes
  *   (TC_ERR_ALIAS) before launching; without it those are preconditions.
- * - HIP graph capture: with validation off, tc_gather_blocks,
- *   tc_scatter_blocks, tc_copy_planned, tc_copy_planned_digest,
- *   tc_digest_planned and tc_cast_fp8_scaled only launch kernels on `stream`
- *   (no memset, no host synchronization), so they may be captured and the
- *   graph replayed.  tc_plan_fragments / tc_copy_fragments (they read the
- *   task count back), the block-scaled cast and inverse cast (they stage their
- *   host item table at call time) and the staging calls must not be captured.
+ * - HIP graph capture: with validation off, every call that only enqueues
+ *   kernels may be captured and the graph replayed: tc_gather_blocks,
+ *   tc_scatter_blocks, tc_plan_fragments_async, tc_copy_fragments,
+ *   tc_copy_planned, tc_copy_planned_digest, tc_digest_planned, the
+ *   block-scaled cast and its inverse (one-call, prepare and planned forms)
+ *   and tc_cast_fp8_scaled.  They issue no memset and no host
+ *   synchronization; host-side tables travel by value in the kernel launches,
+ *   so a graph keeps the values it captured.  tc_plan_fragments and
+ *   tc_plan_status (they read the device back) and the staging calls must not
+ *   be captured.
  */
 #ifndef TENSORCAST_HIP_H
 #define TENSORCAST_HIP_H
@@ -142,31 +150,48 @@ size_t tc_copy_fragments_workspace(int64_t n); /* 0 for n < 0 or n > 2^33 */
  * tasks to fill the GPU, which the recommended size provides. */
 size_t tc_copy_fragments_workspace_min(int64_t n);
 
-/* Copy every fragment: tc_plan_fragments + tc_copy_planned.  frags: device
- * tc_fragment[n].  workspace: device buffer, 256-byte aligned.  The call
- * BLOCKS the host once, until the plan's task count has been computed on the
- * stream (the copy's launch size depends on it); the copy itself is
- * asynchronous.  The workspace may be reused once the stream has passed the
- * copy.  A non-empty fragment whose source or destination range ends past
- * 2^48 is TC_ERR_OUT_OF_RANGE in every mode: the plan's count pass flags it
- * on the device and nothing is copied. */
+/* Copy every fragment: a plan (tc_plan_fragments_async) and a copy that
+ * takes the plan's task count on the device (tc_copy_planned with
+ * TC_TASKS_FROM_PLAN).  frags: device tc_fragment[n].  workspace: device
+ * buffer, 256-byte aligned.  Fully asynchronous: the piece size, the
+ * destination reordering and the task count are decided by the planning
+ * kernels, and the copy's grid is bounded by the workspace's capacity.  The
+ * workspace may be reused once the stream has passed the copy.
+ * Failures the plan finds on the device -- a non-empty fragment whose source
+ * or destination range ends past 2^48 (TC_ERR_OUT_OF_RANGE), a payload the
+ * workspace cannot hold even with pieces of 2^30 bytes (TC_ERR_WORKSPACE) --
+ * copy nothing and are reported by tc_plan_status on this workspace;
+ * argument errors are returned at once. */
 tc_status tc_copy_fragments(const void* src_base, void* dst_base, const tc_fragment* frags,
                             int64_t n, void* workspace, size_t workspace_bytes,
                             hipStream_t stream);
 
 /* Plan once, copy many times (a rank's weight-slice list is fixed for a
- * model).  tc_plan_fragments writes the plan for frags into workspace and
- * returns its task count in *total_tasks (host); it synchronizes the stream
- * once.  tc_copy_planned then copies with that plan -- asynchronously, as
- * often as wanted -- for any src/dst bases, while the workspace is kept
- * unchanged.  total_tasks == 0 means there is nothing to copy; a count
- * larger than the workspace's task table can hold is TC_ERR_WORKSPACE; a
- * fragment ending past 2^48 is TC_ERR_OUT_OF_RANGE, with no plan written. */
+ * model).  tc_plan_fragments_async enqueues the plan for frags into
+ * workspace and returns.  tc_plan_fragments does the same and then waits for
+ * it: it returns the plan's status (the device-found failures above) and its
+ * task count in *total_tasks (host).  tc_copy_planned then copies with the
+ * plan -- asynchronously, as often as wanted -- for any src/dst bases, while
+ * the workspace is kept unchanged.  total_tasks is the plan's count (the
+ * copy's grid is then sized exactly), or TC_TASKS_FROM_PLAN (the kernel reads
+ * it from the plan, no host round trip; a failed plan copies nothing).
+ * total_tasks == 0 means there is nothing to copy; a count larger than the
+ * workspace's task table can hold is TC_ERR_WORKSPACE. */
+#define TC_TASKS_FROM_PLAN UINT64_MAX
+tc_status tc_plan_fragments_async(const tc_fragment* frags, int64_t n, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream);
 tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace,
                             size_t workspace_bytes, uint64_t* total_tasks /* host, out */,
                             hipStream_t stream);
 tc_status tc_copy_planned(const void* src_base, void* dst_base, const void* workspace,
                           size_t workspace_bytes, uint64_t total_tasks, hipStream_t stream);
+/* The status of the plan last written into workspace (TC_OK,
+ * TC_ERR_OUT_OF_RANGE, TC_ERR_WORKSPACE, or TC_ERR_INVALID_ARGUMENT for more
+ * than 2^33 tasks), and its task count in *total_tasks (host; 0 unless
+ * TC_OK).  Waits for `stream` to reach that point.  workspace must hold a
+ * plan. */
+tc_status tc_plan_status(const void* workspace, size_t workspace_bytes,
+                         uint64_t* total_tasks /* host, out, may be NULL */, hipStream_t stream);
 
 /* Integrity digests (the "verify integrity" stage of the materialization
  * pipeline, Sec. 5).  The paper names the stage but no checksum; this
@@ -339,17 +364,47 @@ tc_status tc_reshard_cast_items(const tc_reshard_view* views /* host */,
 /* Bytes of device workspace tc_cast_fp8_blockscaled needs for n items. */
 size_t tc_cast_fp8_workspace(int64_t n_items);
 
+/* A tile table made by tc_cast_fp8_prepare or tc_dequant_fp8_prepare (host
+ * struct, filled by the library): the item count, the tiles of the
+ * streaming path and of the element-wise path, and the residues mod 16 of
+ * the input and output bases the table was made for (a tile's path depends
+ * on its rows' alignment). */
+typedef struct {
+  int64_t n_items;
+  uint64_t full_tiles;
+  uint64_t edge_tiles;
+  uint32_t in_align;
+  uint32_t out_align;
+} tc_tile_plan;
+
 /* Cast every item.  items: HOST array tc_cast_item[n_items] (a model has a
- * few hundred); the library copies it, with its tile offsets, into the
- * device workspace (256-byte aligned) through pinned staging memory, so the
- * host array may be reused as soon as the call returns.  Destination codes
- * and scale grids of different items must not overlap one another or the
+ * few hundred); the library writes it, with its tile offsets, into the
+ * device workspace (256-byte aligned) by small kernels that carry the table
+ * in their launch arguments, so the host array may be reused as soon as the
+ * call returns and nothing is staged or allocated.  Destination codes and
+ * scale grids of different items must not overlap one another or the
  * source.  tile must be 128.  Source rows are read through src_ld, so a
  * strided slice of a full weight is cast in place without a gather.  The
- * workspace may be reused once the stream has passed the call. */
+ * workspace may be reused once the stream has passed the call.
+ * This is tc_cast_fp8_prepare followed by tc_cast_fp8_planned. */
 tc_status tc_cast_fp8_blockscaled(const void* src_base, void* dst_base, float* scale_base,
                                   const tc_cast_item* items, int64_t n_items, int32_t tile,
                                   void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* The two halves, for casts repeated with one item list (a rank's weights
+ * at every synchronization, Sec. 6.2): tc_cast_fp8_prepare checks the items
+ * (same errors as tc_cast_fp8_blockscaled), enqueues the table's writes into
+ * the workspace and fills *plan (host).  tc_cast_fp8_planned then launches
+ * only the cast kernels, as often as wanted while the workspace is kept, for
+ * any bases with the residues mod 16 recorded in the plan
+ * (TC_ERR_INVALID_ARGUMENT otherwise). */
+tc_status tc_cast_fp8_prepare(const void* src_base, const void* dst_base, const tc_cast_item* items,
+                              int64_t n_items, int32_t tile, void* workspace,
+                              size_t workspace_bytes, tc_tile_plan* plan /* host, out */,
+                              hipStream_t stream);
+tc_status tc_cast_fp8_planned(const void* src_base, void* dst_base, float* scale_base,
+                              const void* workspace, size_t workspace_bytes,
+                              const tc_tile_plan* plan /* host */, hipStream_t stream);
 
 /* q[i] = E4M3(RN_f32(bf16(src[i]) / scale)) for i < n, one given scale (no
  * amax).  Quotients that overflow saturate; NaN gives 0x7F. */
@@ -376,13 +431,22 @@ typedef struct {
 /* Bytes of device workspace tc_dequant_fp8_blockscaled needs for n items. */
 size_t tc_dequant_fp8_workspace(int64_t n_items);
 
-/* Dequantize every item.  items: HOST array, staged like the cast's.  The
- * bf16 destinations must not overlap one another or the sources.  tile must
- * be 128. */
+/* Dequantize every item.  items: HOST array, written into the workspace
+ * like the cast's.  The bf16 destinations must not overlap one another or the
+ * sources.  tile must be 128.  This is tc_dequant_fp8_prepare followed by
+ * tc_dequant_fp8_planned, the same split as the cast's (the plan's input
+ * base is the codes', its output base the bf16 destination's). */
 tc_status tc_dequant_fp8_blockscaled(const void* codes_base, const float* scale_base,
                                      void* dst_base, const tc_dequant_item* items /* host */,
                                      int64_t n_items, int32_t tile, void* workspace,
                                      size_t workspace_bytes, hipStream_t stream);
+tc_status tc_dequant_fp8_prepare(const void* codes_base, const void* dst_base,
+                                 const tc_dequant_item* items /* host */, int64_t n_items,
+                                 int32_t tile, void* workspace, size_t workspace_bytes,
+                                 tc_tile_plan* plan /* host, out */, hipStream_t stream);
+tc_status tc_dequant_fp8_planned(const void* codes_base, const float* scale_base, void* dst_base,
+                                 const void* workspace, size_t workspace_bytes,
+                                 const tc_tile_plan* plan /* host */, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Host <-> device staging: the materialization pipeline's pinned streaming
@@ -444,6 +508,41 @@ tc_status tc_hydrate_from_host(tc_stager* stager, const tc_block_pool* pool, con
 tc_status tc_publish_to_host(tc_stager* stager, const tc_block_pool* pool, const int32_t* ids,
                              int64_t n, void* host_dst, int32_t flags, void* dev_stage,
                              size_t dev_stage_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Same-host zero-copy sharing between processes (HIP IPC): the Unified
+ * Tensor Pool exposes device tensors of co-hosted instances to one another
+ * without copies (Sec. 4.2, Sec. 5), and a warm start consumes
+ * pre-materialized weights that way (Sec. 6.1).  Every call above accepts
+ * an imported address like any other device pointer, so an engine can, for
+ * example, gather KV blocks straight out of another process's pool.
+ *
+ * tc_ipc_export: a handle for the device range [dev_ptr, dev_ptr + bytes),
+ *   which must lie inside one allocation of this process (IPC shares whole
+ *   allocations; the handle records the range's offset in it).  The handle
+ *   is plain bytes: send it to another process on this host by any channel.
+ *   The exporter must keep the allocation alive while importers use it.
+ *   TC_ERR_INVALID_ARGUMENT for null arguments, memory that is not a device
+ *   allocation of this process, and allocations of 2 GiB or more (opening a
+ *   handle to such an allocation has been seen not to return on some ROCm
+ *   drivers); TC_ERR_OUT_OF_RANGE for a range that leaves its allocation.
+ * tc_ipc_open: maps the exporter's allocation on the current device and
+ *   returns the range's address in this process in *dev_ptr.  A process may
+ *   open a given handle once at a time.
+ * tc_ipc_close: unmaps it (dev_ptr as returned by tc_ipc_open).  The
+ *   exporter's memory is unaffected.
+ * Runtime failures are TC_ERR_HIP (tc_last_hip_error() gives the code).
+ * These calls are synchronous host calls; they enqueue nothing.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  uint8_t handle[64];   /* the runtime's IPC handle of the allocation */
+  uint64_t offset;      /* bytes from the allocation's base to the range */
+  uint64_t bytes;       /* length of the range */
+  uint64_t alloc_bytes; /* size of the allocation */
+} tc_ipc_handle;
+tc_status tc_ipc_export(const void* dev_ptr, size_t bytes, tc_ipc_handle* out /* host */);
+tc_status tc_ipc_open(const tc_ipc_handle* handle /* host */, void** dev_ptr /* host, out */);
+tc_status tc_ipc_close(const tc_ipc_handle* handle /* host */, void* dev_ptr);
 
 /* ------------------------------------------------------------------------ */
 const char* tc_status_string(tc_status status);

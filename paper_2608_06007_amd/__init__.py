@@ -19,8 +19,12 @@ Entry points (see include/tensorcast_hip.h for the contracts):
   pinned-ring staging between host memory and the device (Sec. 5).
 * ``tc_tp_fragments`` / ``tc_tp_cast_item`` -- host builders that describe a
   tensor-parallel rank's view(slice) of each weight (Table 2, Sec. 6.1-6.2).
-* ``tc_cast_fp8_blockscaled`` / ``tc_cast_fp8_scaled`` -- a transform_into
-  rule: bf16 -> fp8 E4M3 with an fp32 scale per 128x128 tile.
+* ``tc_cast_fp8_blockscaled`` (+ ``tc_cast_fp8_prepare`` /
+  ``tc_cast_fp8_planned``) / ``tc_cast_fp8_scaled`` -- a transform_into rule:
+  bf16 -> fp8 E4M3 with an fp32 scale per 128x128 tile; and its inverse,
+  ``tc_dequant_fp8_blockscaled`` (+ prepare / planned).
+* ``tc_ipc_export`` / ``tc_ipc_open`` / ``tc_ipc_close`` -- zero-copy sharing
+  of device ranges between processes on one host (Sec. 4.2, Sec. 5).
 """
 from __future__ import annotations
 
@@ -33,13 +37,17 @@ import numpy as np
 __all__ = [
     "TcError", "lib_path", "load",
     "tc_gather_blocks", "tc_scatter_blocks",
-    "tc_copy_fragments_workspace", "tc_copy_fragments_workspace_min", "tc_copy_fragments", "tc_plan_fragments", "tc_copy_planned",
+    "tc_copy_fragments_workspace", "tc_copy_fragments_workspace_min", "tc_copy_fragments", "tc_plan_fragments",
+    "tc_plan_fragments_async", "tc_plan_status", "tc_copy_planned", "TASKS_FROM_PLAN",
     "tc_copy_planned_digest", "tc_digest_planned", "DIGEST_SRC", "DIGEST_DST",
     "tc_tp_fragment_count", "tc_tp_fragments", "tc_tp_cast_item",
     "tc_reshard_fragment_count", "tc_reshard_fragments",
     "tc_reshard_cast_item_count", "tc_reshard_cast_items",
     "tc_cast_fp8_workspace", "tc_cast_fp8_blockscaled", "tc_cast_fp8_scaled",
+    "tc_cast_fp8_prepare", "tc_cast_fp8_planned", "TilePlan",
     "tc_dequant_fp8_workspace", "tc_dequant_fp8_blockscaled", "DEQUANT_ITEM_DTYPE",
+    "tc_dequant_fp8_prepare", "tc_dequant_fp8_planned",
+    "tc_ipc_export", "tc_ipc_open", "tc_ipc_close", "IPC_HANDLE_BYTES",
     "tc_stager_create", "tc_stager_destroy", "tc_stage_h2d", "tc_stage_d2h",
     "tc_hydrate_from_host", "tc_publish_to_host", "Stager", "HOST_PINNED",
     "tc_status_string", "tc_last_hip_error", "tc_set_validate", "tc_get_validate",
@@ -48,12 +56,15 @@ __all__ = [
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-lib_path = os.path.join(_HERE, "libtchip.so")
+# TC_LIB_PATH loads another build of the same library (the CPU test tier runs
+# the host code under sanitizers that way).
+lib_path = os.environ.get("TC_LIB_PATH") or os.path.join(_HERE, "libtchip.so")
 
 MAX_REGIONS = 256
 SPLIT_NONE, SPLIT_ROWS, SPLIT_COLS = 0, 1, 2
 DIGEST_SRC, DIGEST_DST = 0, 1
 HOST_PINNED = 1
+TASKS_FROM_PLAN = (1 << 64) - 1   # tc_copy_planned: the count is read from the plan on the device
 TC_OK = 0
 _STATUS = {0: "TC_OK", 1: "TC_ERR_INVALID_ARGUMENT", 2: "TC_ERR_OUT_OF_RANGE", 3: "TC_ERR_ALIAS",
            4: "TC_ERR_HIP", 5: "TC_ERR_WORKSPACE", 6: "TC_ERR_HOST_RESOURCES"}
@@ -87,6 +98,21 @@ class _ReshardView(ctypes.Structure):
                 ("src_tp", ctypes.c_int32), ("reserved", ctypes.c_int32), ("dst_off", ctypes.c_uint64)]
 
 
+class TilePlan(ctypes.Structure):
+    """tc_tile_plan: a cast (or inverse-cast) tile table prepared in a workspace."""
+    _fields_ = [("n_items", ctypes.c_int64), ("full_tiles", ctypes.c_uint64),
+                ("edge_tiles", ctypes.c_uint64), ("in_align", ctypes.c_uint32),
+                ("out_align", ctypes.c_uint32)]
+
+
+class _IpcHandle(ctypes.Structure):
+    _fields_ = [("handle", ctypes.c_uint8 * 64), ("offset", ctypes.c_uint64), ("bytes", ctypes.c_uint64),
+                ("alloc_bytes", ctypes.c_uint64)]
+
+
+IPC_HANDLE_BYTES = ctypes.sizeof(_IpcHandle)
+
+
 class _BlockPool(ctypes.Structure):
     _fields_ = [("region_base", ctypes.POINTER(ctypes.c_uint64)), ("num_regions", ctypes.c_int32),
                 ("num_blocks", ctypes.c_int64), ("block_bytes", ctypes.c_int64),
@@ -115,6 +141,8 @@ def load():
     L.tc_copy_fragments.argtypes = [P, P, P, c.c_int64, P, c.c_size_t, P]
     L.tc_plan_fragments.argtypes = [P, c.c_int64, P, c.c_size_t, c.POINTER(c.c_uint64), P]
     L.tc_copy_planned.argtypes = [P, P, P, c.c_size_t, c.c_uint64, P]
+    L.tc_plan_fragments_async.argtypes = [P, c.c_int64, P, c.c_size_t, P]
+    L.tc_plan_status.argtypes = [P, c.c_size_t, c.POINTER(c.c_uint64), P]
     L.tc_copy_planned_digest.argtypes = [P, P, P, c.c_size_t, c.c_uint64, c.c_int64, P, P]
     L.tc_digest_planned.argtypes = [P, c.c_int32, P, c.c_size_t, c.c_uint64, c.c_int64, P, P]
     L.tc_tp_fragment_count.argtypes = [P, c.c_int64, c.c_int32, c.c_int32]
@@ -134,6 +162,13 @@ def load():
     L.tc_cast_fp8_workspace.restype = c.c_size_t
     L.tc_cast_fp8_blockscaled.argtypes = [P, P, P, P, c.c_int64, c.c_int32, P, c.c_size_t, P]
     L.tc_cast_fp8_scaled.argtypes = [P, c.c_int64, c.c_float, P, P]
+    L.tc_cast_fp8_prepare.argtypes = [P, P, P, c.c_int64, c.c_int32, P, c.c_size_t, c.POINTER(TilePlan), P]
+    L.tc_cast_fp8_planned.argtypes = [P, P, P, P, c.c_size_t, c.POINTER(TilePlan), P]
+    L.tc_dequant_fp8_prepare.argtypes = [P, P, P, c.c_int64, c.c_int32, P, c.c_size_t, c.POINTER(TilePlan), P]
+    L.tc_dequant_fp8_planned.argtypes = [P, P, P, P, c.c_size_t, c.POINTER(TilePlan), P]
+    L.tc_ipc_export.argtypes = [P, c.c_size_t, c.POINTER(_IpcHandle)]
+    L.tc_ipc_open.argtypes = [c.POINTER(_IpcHandle), c.POINTER(c.c_void_p)]
+    L.tc_ipc_close.argtypes = [c.POINTER(_IpcHandle), P]
     L.tc_dequant_fp8_workspace.argtypes = [c.c_int64]
     L.tc_dequant_fp8_workspace.restype = c.c_size_t
     L.tc_dequant_fp8_blockscaled.argtypes = [P, P, P, P, c.c_int64, c.c_int32, P, c.c_size_t, P]
@@ -151,8 +186,11 @@ def load():
     L.tc_set_validate.argtypes = [c.c_int]
     L.tc_get_validate.restype = c.c_int
     for name in ("tc_gather_blocks", "tc_scatter_blocks", "tc_copy_fragments", "tc_plan_fragments",
+                 "tc_plan_fragments_async", "tc_plan_status",
                  "tc_copy_planned", "tc_copy_planned_digest", "tc_digest_planned", "tc_tp_fragments", "tc_tp_cast_item", "tc_reshard_fragments", "tc_reshard_cast_items",
                  "tc_cast_fp8_blockscaled", "tc_dequant_fp8_blockscaled",
+                 "tc_cast_fp8_prepare", "tc_cast_fp8_planned", "tc_dequant_fp8_prepare",
+                 "tc_dequant_fp8_planned", "tc_ipc_export", "tc_ipc_open", "tc_ipc_close",
                  "tc_cast_fp8_scaled", "tc_stager_create", "tc_stager_destroy", "tc_stage_h2d",
                  "tc_stage_d2h", "tc_hydrate_from_host", "tc_publish_to_host"):
         getattr(L, name).restype = c.c_int
@@ -256,8 +294,9 @@ def _frag_count(frags) -> int:
 
 def tc_copy_fragments(src, dst, frags, workspace, stream=None) -> None:
     """Copy every (src_off, dst_off, len) row of the device tensor ``frags``
-    (uint64/int64, shape [n, 3]) from ``src`` to ``dst``.  Blocks once until
-    the plan's task count is known."""
+    (uint64/int64, shape [n, 3]) from ``src`` to ``dst``.  Asynchronous: the
+    plan and the copy are enqueued on ``stream``; failures the plan finds on
+    the device are reported by ``tc_plan_status(workspace)``."""
     n = _frag_count(frags)
     _ok(load().tc_copy_fragments(_dev_ptr(src), _dev_ptr(dst), _dev_ptr(frags) if n else None, n,
                                  _dev_ptr(workspace), _nbytes(workspace), _stream(stream)),
@@ -274,10 +313,29 @@ def tc_plan_fragments(frags, workspace, stream=None) -> int:
     return int(total.value)
 
 
-def tc_copy_planned(src, dst, workspace, total_tasks: int, stream=None) -> None:
-    """Copy with a plan made by tc_plan_fragments (same workspace, unchanged)."""
+def tc_plan_fragments_async(frags, workspace, stream=None) -> None:
+    """Enqueue the plan of ``frags`` into ``workspace`` without waiting for it."""
+    n = _frag_count(frags)
+    _ok(load().tc_plan_fragments_async(_dev_ptr(frags) if n else None, n, _dev_ptr(workspace),
+                                       _nbytes(workspace), _stream(stream)),
+        "tc_plan_fragments_async")
+
+
+def tc_plan_status(workspace, stream=None) -> int:
+    """Wait for the plan in ``workspace`` and return its task count; raises
+    TcError with the plan's status if the plan failed on the device."""
+    total = ctypes.c_uint64(0)
+    _ok(load().tc_plan_status(_dev_ptr(workspace), _nbytes(workspace), ctypes.byref(total),
+                              _stream(stream)), "tc_plan_status")
+    return int(total.value)
+
+
+def tc_copy_planned(src, dst, workspace, total_tasks=None, stream=None) -> None:
+    """Copy with a plan made by tc_plan_fragments (same workspace, unchanged).
+    ``total_tasks=None`` lets the kernel read the plan's count on the device."""
+    total = TASKS_FROM_PLAN if total_tasks is None else int(total_tasks)
     _ok(load().tc_copy_planned(_dev_ptr(src), _dev_ptr(dst), _dev_ptr(workspace),
-                               _nbytes(workspace), int(total_tasks), _stream(stream)),
+                               _nbytes(workspace), total, _stream(stream)),
         "tc_copy_planned")
 
 
@@ -539,6 +597,25 @@ def tc_cast_fp8_blockscaled(src, dst, scales, items, workspace, stream=None, til
         "tc_cast_fp8_blockscaled")
 
 
+def tc_cast_fp8_prepare(src, dst, items, workspace, stream=None, tile: int = 128) -> TilePlan:
+    """Write the cast's tile table for ``items`` into ``workspace``; returns
+    the plan for tc_cast_fp8_planned (bases with the same alignment)."""
+    it = np.ascontiguousarray(items, dtype=CAST_ITEM_DTYPE).reshape(-1)
+    n = it.size
+    plan = TilePlan()
+    _ok(load().tc_cast_fp8_prepare(_dev_ptr(src), _dev_ptr(dst), it.ctypes.data if n else None, n, tile,
+                                   _dev_ptr(workspace), _nbytes(workspace), ctypes.byref(plan),
+                                   _stream(stream)), "tc_cast_fp8_prepare")
+    return plan
+
+
+def tc_cast_fp8_planned(src, dst, scales, workspace, plan: TilePlan, stream=None) -> None:
+    """Launch only the cast kernels, with a table prepared in ``workspace``."""
+    _ok(load().tc_cast_fp8_planned(_dev_ptr(src), _dev_ptr(dst), _dev_ptr(scales), _dev_ptr(workspace),
+                                   _nbytes(workspace), ctypes.byref(plan), _stream(stream)),
+        "tc_cast_fp8_planned")
+
+
 def tc_cast_fp8_scaled(src, scale: float, dst, stream=None) -> None:
     """dst[i] = E4M3(RN_f32(src[i] / scale)) for a bf16 device tensor ``src``."""
     if src.element_size() != 2:
@@ -564,6 +641,56 @@ def tc_dequant_fp8_blockscaled(codes, scales, dst, items, workspace, stream=None
                                           it.ctypes.data if n else None, n, tile,
                                           _dev_ptr(workspace), _nbytes(workspace), _stream(stream)),
         "tc_dequant_fp8_blockscaled")
+
+
+def tc_dequant_fp8_prepare(codes, dst, items, workspace, stream=None, tile: int = 128) -> TilePlan:
+    """Write the inverse cast's tile table into ``workspace``; returns its plan."""
+    it = np.ascontiguousarray(items, dtype=DEQUANT_ITEM_DTYPE).reshape(-1)
+    n = it.size
+    plan = TilePlan()
+    _ok(load().tc_dequant_fp8_prepare(_dev_ptr(codes), _dev_ptr(dst), it.ctypes.data if n else None, n,
+                                      tile, _dev_ptr(workspace), _nbytes(workspace), ctypes.byref(plan),
+                                      _stream(stream)), "tc_dequant_fp8_prepare")
+    return plan
+
+
+def tc_dequant_fp8_planned(codes, scales, dst, workspace, plan: TilePlan, stream=None) -> None:
+    """Launch only the inverse-cast kernels, with a prepared table."""
+    _ok(load().tc_dequant_fp8_planned(_dev_ptr(codes), _dev_ptr(scales), _dev_ptr(dst),
+                                      _dev_ptr(workspace), _nbytes(workspace), ctypes.byref(plan),
+                                      _stream(stream)), "tc_dequant_fp8_planned")
+
+
+# ---------------------------------------------------------------------------
+# zero-copy sharing between processes (HIP IPC)
+# ---------------------------------------------------------------------------
+
+def tc_ipc_export(dev, nbytes=None) -> bytes:
+    """Handle (plain bytes) for a device tensor's bytes, or ``nbytes`` bytes at
+    a device address; send it to another process on this host."""
+    n = _nbytes(dev) if nbytes is None else int(nbytes)
+    h = _IpcHandle()
+    _ok(load().tc_ipc_export(_dev_ptr(dev), n, ctypes.byref(h)), "tc_ipc_export")
+    return bytes(h)
+
+
+def _ipc_handle(handle: bytes) -> _IpcHandle:
+    if len(handle) != IPC_HANDLE_BYTES:
+        raise ValueError(f"an IPC handle has {IPC_HANDLE_BYTES} bytes")
+    return _IpcHandle.from_buffer_copy(handle)
+
+
+def tc_ipc_open(handle: bytes) -> int:
+    """Map an exported range into this process; returns its device address."""
+    h = _ipc_handle(handle)
+    p = ctypes.c_void_p(0)
+    _ok(load().tc_ipc_open(ctypes.byref(h), ctypes.byref(p)), "tc_ipc_open")
+    return int(p.value)
+
+
+def tc_ipc_close(handle: bytes, dev_ptr: int) -> None:
+    h = _ipc_handle(handle)
+    _ok(load().tc_ipc_close(ctypes.byref(h), ctypes.c_void_p(dev_ptr)), "tc_ipc_close")
 
 
 # ---------------------------------------------------------------------------

@@ -12,7 +12,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libtchip.so")
-SOURCES = ["tc_blocks.hip", "tc_plan.hip", "tc_copy.hip", "tc_cast.hip", "tc_dequant.hip", "tc_api.cpp", "tc_stage.cpp"]
+SOURCES = ["tc_blocks.hip", "tc_plan.hip", "tc_copy.hip", "tc_cast.hip", "tc_dequant.hip", "tc_api.cpp",
+           "tc_stage.cpp", "tc_ipc.cpp"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -35,23 +36,34 @@ def _run(cmd, verbose):
         sys.stderr.write(err + "\n")
 
 
-def build(verbose: bool = False) -> str:
-    objdir = os.path.join(HERE, "_build")
+# Host-side AddressSanitizer + UndefinedBehaviorSanitizer build (for the CPU
+# test tier: host code only; each option applies to the host pass alone, the
+# device code is compiled as usual).
+SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def build(verbose: bool = False, sanitize: bool = False, out: str = None) -> str:
+    """Compile every source and link the library (``out``, default
+    libtchip.so beside this file).  ``sanitize`` adds the host sanitizers."""
+    objdir = os.path.join(HERE, "_build_san" if sanitize else "_build")
     os.makedirs(objdir, exist_ok=True)
+    extra = SANITIZE if sanitize else []
+    lib = out or LIB
     objs = []
     for src in SOURCES:
         obj = os.path.join(objdir, src + ".o")
-        cmd = [HIPCC, f"--offload-arch={ARCH}", *COMMON, *DEVICE_FLAGS, "-c",
+        cmd = [HIPCC, f"--offload-arch={ARCH}", *COMMON, *DEVICE_FLAGS, *extra, "-c",
                os.path.join(CSRC, src), "-o", obj]
         if src.endswith(".cpp"):
             cmd.insert(1, "-x")
             cmd.insert(2, "hip")
         _run(cmd, verbose)
         objs.append(obj)
-    tmp = LIB + ".tmp"
-    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
-    os.replace(tmp, LIB)
-    return LIB
+    tmp = lib + ".tmp"
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *extra, "-o", tmp, *objs], verbose)
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":

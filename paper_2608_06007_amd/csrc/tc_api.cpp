@@ -8,8 +8,6 @@
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
-#include <initializer_list>
-#include <mutex>
 #include <vector>
 
 #include "tc_internal.h"
@@ -196,55 +194,6 @@ void view_fragments(const tc_tp_view& v, int32_t tp, int32_t rank, Emit emit) {
 }
 
 
-// Pinned host staging for small host-side tables copied to a device
-// workspace: one buffer per device, reused once the previous copy out of it
-// has completed.
-struct Piece {
-  const void* data;
-  size_t bytes;
-  size_t offset;  // in the device destination
-};
-
-struct Staging {
-  void* host = nullptr;
-  size_t cap = 0;
-  hipEvent_t done = nullptr;
-};
-
-std::mutex g_staging_mu;
-Staging g_staging[64];
-
-tc_status stage_to_device(void* dev_dst, hipStream_t s, std::initializer_list<Piece> pieces) {
-  size_t need = 0;
-  for (const Piece& p : pieces) need = std::max(need, p.offset + p.bytes);
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return hip_fail(e);
-  if (dev < 0 || dev >= 64) return hip_fail(hipErrorInvalidDevice);
-  std::lock_guard<std::mutex> lock(g_staging_mu);
-  Staging& st = g_staging[dev];
-  if (st.done) {
-    e = hipEventSynchronize(st.done);  // the previous copy has left the buffer
-    if (e != hipSuccess) return hip_fail(e);
-  } else {
-    e = hipEventCreateWithFlags(&st.done, hipEventDisableTiming);
-    if (e != hipSuccess) return hip_fail(e);
-  }
-  if (st.cap < need) {
-    if (st.host) (void)hipHostFree(st.host);
-    st.host = nullptr;
-    st.cap = 0;
-    size_t cap = std::max<size_t>(need, 1 << 16);
-    e = hipHostMalloc(&st.host, cap, hipHostMallocDefault);
-    if (e != hipSuccess) return hip_fail(e);
-    st.cap = cap;
-  }
-  for (const Piece& p : pieces) std::memcpy(static_cast<uint8_t*>(st.host) + p.offset, p.data, p.bytes);
-  e = hipMemcpyAsync(dev_dst, st.host, need, hipMemcpyHostToDevice, s);
-  if (e == hipSuccess) e = hipEventRecord(st.done, s);
-  return check(e);
-}
-
 bool elem_ok(int32_t eb) { return eb == 1 || eb == 2 || eb == 4 || eb == 8; }
 
 bool reshard_ok(const tc_reshard_view& v, int32_t dst_tp, int32_t dst_rank) {
@@ -332,6 +281,182 @@ bool reshard_cast_items(const tc_reshard_view& v, uint64_t scale_off, int32_t ds
   return true;
 }
 
+// Item counts above this are refused (the cast grids grow with them).
+constexpr int64_t kMaxItems = int64_t(1) << 33;
+
+static_assert(sizeof(tc_dequant_item) == sizeof(tc_cast_item), "shared workspace layout");
+static_assert(sizeof(tc_cast_item) == 8 * tc::kItemWords, "items are copied as 8 words");
+static_assert(sizeof(tc_dequant_item) == 8 * tc::kItemWords, "items are copied as 8 words");
+
+// Tile ranges of an item list, on the host: full tiles of vector-aligned
+// items go to the streaming kernel, every other tile to the element-wise one.
+// Cast items read 16-byte-aligned bf16 rows and write 8-byte-aligned code
+// rows; inverse items read 8-byte-aligned code rows and write 16-byte-aligned
+// bf16 rows.  False for an invalid item.
+template <typename Item>
+bool item_tiles(const Item& it, uint64_t in_base, uint64_t out_base, bool cast, uint8_t* aligned,
+                uint64_t* full, uint64_t* all) {
+  if (it.rows < 0 || it.cols < 0 || it.src_ld < it.cols || it.dst_ld < it.cols) return false;
+  const uint64_t tr = uint64_t((it.rows + 127) / 128), tcn = uint64_t((it.cols + 127) / 128);
+  if (it.rows > 0 && it.cols > 0 && it.scale_ld < int64_t(tcn)) return false;
+  bool al;
+  if (cast) {  // bf16 in (elements), codes out (bytes)
+    const uint64_t x = in_base + 2 * it.src_off, q = out_base + it.dst_off;
+    al = x % 16 == 0 && (2 * uint64_t(it.src_ld)) % 16 == 0 && q % 8 == 0 && uint64_t(it.dst_ld) % 8 == 0;
+  } else {     // codes in (bytes), bf16 out (elements)
+    const uint64_t q = in_base + it.src_off, y = out_base + 2 * it.dst_off;
+    al = q % 8 == 0 && uint64_t(it.src_ld) % 8 == 0 && y % 16 == 0 && (2 * uint64_t(it.dst_ld)) % 16 == 0;
+  }
+  *aligned = al ? 1 : 0;
+  *all = (it.rows > 0 && it.cols > 0) ? tr * tcn : 0;
+  *full = al ? uint64_t(it.rows / 128) * uint64_t(it.cols / 128) : 0;
+  return true;
+}
+
+// Validate every item and total its tiles (no table is kept).
+template <typename Item>
+tc_status tile_totals(const Item* items, int64_t n_items, uint64_t in_base, uint64_t out_base,
+                      bool cast, uint64_t* full, uint64_t* edge) {
+  *full = *edge = 0;
+  for (int64_t i = 0; i < n_items; ++i) {
+    uint8_t al;
+    uint64_t f, all;
+    if (!item_tiles(items[i], in_base, out_base, cast, &al, &f, &all)) return TC_ERR_INVALID_ARGUMENT;
+    *full += f;
+    *edge += all - f;
+  }
+  return TC_OK;
+}
+
+// Enqueue the table's writes chunk by chunk, each chunk built on the stack
+// and carried in its launch's arguments: no host or device memory is taken.
+template <typename Item>
+hipError_t upload_tile_table(const Item* items, int64_t n_items, uint64_t in_base, uint64_t out_base,
+                             bool cast, uint64_t full, uint64_t edge, void* ws, hipStream_t s) {
+  tc::TableChunk c;
+  uint64_t fsum = 0, esum = 0;
+  for (int64_t i0 = 0; i0 < n_items; i0 += tc::kTableChunkItems) {
+    const int64_t cnt = std::min<int64_t>(n_items - i0, tc::kTableChunkItems);
+    c.first = uint64_t(i0);
+    c.count = uint32_t(cnt);
+    c.last = i0 + cnt == n_items ? 1u : 0u;
+    c.ftotal = full;
+    c.etotal = edge;
+    for (int64_t k = 0; k < cnt; ++k) {
+      const Item& it = items[i0 + k];
+      std::memcpy(&c.words[k * tc::kItemWords], &it, sizeof(Item));
+      uint64_t f, all;
+      item_tiles(it, in_base, out_base, cast, &c.aligned[k], &f, &all);
+      c.fprefix[k] = fsum;
+      c.eprefix[k] = esum;
+      fsum += f;
+      esum += all - f;
+    }
+    hipError_t e = tc::launch_tile_chunk(c, n_items, ws, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// Debug checks of a cast's item list: codes and scale grids of different
+// items must not overlap one another or the bf16 source.
+static tc_status check_cast_ranges(const void* src_base, const void* dst_base, const void* scale_base,
+                                   const tc_cast_item* items, int64_t n_items) {
+  std::vector<Range> q, sc, srcr;
+  const uint64_t db = (uint64_t)(uintptr_t)dst_base, sb = (uint64_t)(uintptr_t)scale_base;
+  const uint64_t xb = (uint64_t)(uintptr_t)src_base;
+  for (int64_t i = 0; i < n_items; ++i) {
+    const tc_cast_item& it = items[i];
+    if (it.rows == 0 || it.cols == 0) continue;
+    const int64_t tcn = (it.cols + 127) / 128, tr = (it.rows + 127) / 128;
+    for (int64_t r = 0; r < it.rows; ++r) {
+      const uint64_t a = db + it.dst_off + uint64_t(r) * uint64_t(it.dst_ld);
+      q.push_back({a, a + uint64_t(it.cols)});
+      const uint64_t x = xb + 2 * (it.src_off + uint64_t(r) * uint64_t(it.src_ld));
+      srcr.push_back({x, x + 2 * uint64_t(it.cols)});
+    }
+    for (int64_t r = 0; r < tr; ++r) {
+      const uint64_t a = sb + 4 * (it.scale_off + uint64_t(r) * uint64_t(it.scale_ld));
+      sc.push_back({a, a + 4 * uint64_t(tcn)});
+    }
+  }
+  std::vector<Range> outs = q;
+  outs.insert(outs.end(), sc.begin(), sc.end());
+  if (any_overlap(outs)) return TC_ERR_ALIAS;
+  if (cross_overlap(outs, srcr)) return TC_ERR_ALIAS;
+  return TC_OK;
+}
+
+// The same for the inverse: bf16 outputs disjoint, and apart from the codes
+// and scales they read.
+static tc_status check_dequant_ranges(const void* codes_base, const void* scale_base,
+                                      const void* dst_base, const tc_dequant_item* items,
+                                      int64_t n_items) {
+  std::vector<Range> outs, srcs;
+  const uint64_t db = (uint64_t)(uintptr_t)dst_base, qb = (uint64_t)(uintptr_t)codes_base;
+  const uint64_t sb = (uint64_t)(uintptr_t)scale_base;
+  for (int64_t i = 0; i < n_items; ++i) {
+    const tc_dequant_item& it = items[i];
+    if (it.rows == 0 || it.cols == 0) continue;
+    const int64_t tcn = (it.cols + 127) / 128, tr = (it.rows + 127) / 128;
+    for (int64_t r = 0; r < it.rows; ++r) {
+      const uint64_t a = db + 2 * (it.dst_off + uint64_t(r) * uint64_t(it.dst_ld));
+      outs.push_back({a, a + 2 * uint64_t(it.cols)});
+      const uint64_t x = qb + it.src_off + uint64_t(r) * uint64_t(it.src_ld);
+      srcs.push_back({x, x + uint64_t(it.cols)});
+    }
+    for (int64_t r = 0; r < tr; ++r) {
+      const uint64_t a = sb + 4 * (it.scale_off + uint64_t(r) * uint64_t(it.scale_ld));
+      srcs.push_back({a, a + 4 * uint64_t(tcn)});
+    }
+  }
+  if (any_overlap(outs)) return TC_ERR_ALIAS;
+  if (cross_overlap(outs, srcs)) return TC_ERR_ALIAS;
+  return TC_OK;
+}
+
+// prepare: checks, the host tile table, and its enqueued upload into the
+// workspace (by value, in the launches' arguments).  cast selects the item
+// kind; in_base/out_base are the bases whose alignment the table assumes.
+template <typename Item>
+static tc_status prepare_tiles(const void* in_base, const void* out_base, const Item* items,
+                               int64_t n_items, int32_t tile, void* workspace, size_t workspace_bytes,
+                               bool cast, tc_tile_plan* plan, hipStream_t stream) {
+  if (!plan) return TC_ERR_INVALID_ARGUMENT;
+  *plan = tc_tile_plan{0, 0, 0, 0, 0};
+  if (n_items < 0 || n_items > kMaxItems || tile != 128) return TC_ERR_INVALID_ARGUMENT;
+  if (n_items == 0) return TC_OK;
+  if (!in_base || !out_base || !items || !workspace) return TC_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < tc::cast_workspace_bytes(n_items)) return TC_ERR_WORKSPACE;
+  if ((uintptr_t)workspace % 256) return TC_ERR_INVALID_ARGUMENT;
+  // bf16 bases hold 2-byte elements
+  if ((cast ? (uintptr_t)in_base : (uintptr_t)out_base) % 2) return TC_ERR_INVALID_ARGUMENT;
+  const uint64_t ib = (uint64_t)(uintptr_t)in_base, ob = (uint64_t)(uintptr_t)out_base;
+  uint64_t full, edge;
+  tc_status st = tile_totals(items, n_items, ib, ob, cast, &full, &edge);
+  if (st != TC_OK) return st;
+  st = check(upload_tile_table(items, n_items, ib, ob, cast, full, edge, workspace, stream));
+  if (st != TC_OK) return st;
+  *plan = tc_tile_plan{n_items, full, edge, uint32_t(ib % 16), uint32_t(ob % 16)};
+  return TC_OK;
+}
+
+// Checks of a planned launch: the table's size, and bases with the
+// alignment the table was made for.
+static tc_status planned_args(const void* in_base, const void* out_base, const float* scale_base,
+                              const void* workspace, size_t workspace_bytes,
+                              const tc_tile_plan* plan) {
+  if (!plan || plan->n_items < 0 || plan->n_items > kMaxItems) return TC_ERR_INVALID_ARGUMENT;
+  if (plan->full_tiles + plan->edge_tiles == 0) return TC_OK;
+  if (!in_base || !out_base || !scale_base || !workspace || (uintptr_t)workspace % 256 ||
+      (uintptr_t)scale_base % 4)
+    return TC_ERR_INVALID_ARGUMENT;
+  if (workspace_bytes < tc::cast_workspace_bytes(plan->n_items)) return TC_ERR_WORKSPACE;
+  if ((uintptr_t)in_base % 16 != plan->in_align || (uintptr_t)out_base % 16 != plan->out_align)
+    return TC_ERR_INVALID_ARGUMENT;
+  return TC_OK;
+}
+
 }  // namespace
 
 namespace tc {
@@ -407,68 +532,71 @@ static tc_status check_ranges(const void* src_base, const void* dst_base,
   return TC_OK;
 }
 
-static uint64_t pow2_at_least(uint64_t x) {
-  uint64_t p = 1;
-  while (p < x) p <<= 1;
-  return p;
+// Checks shared by the planning entry points; *L receives the plan's layout.
+static tc_status plan_args(const tc_fragment* frags, int64_t n, void* workspace,
+                           size_t workspace_bytes, tc::PlanLayout* L, hipStream_t stream) {
+  if (n < 0 || n > kMaxCount) return TC_ERR_INVALID_ARGUMENT;
+  if (n == 0) return TC_OK;
+  if (!frags || !workspace || (uintptr_t)workspace % 256) return TC_ERR_INVALID_ARGUMENT;
+  *L = tc::plan_layout(n, workspace_bytes);
+  if (L->capacity < uint64_t(n) + 1) return TC_ERR_WORKSPACE;
+  if (validating()) {
+    std::vector<tc_fragment> h;
+    tc_status st = fetch(frags, n, &h, stream);
+    if (st != TC_OK) return st;
+    st = check_ranges(nullptr, nullptr, h);
+    if (st != TC_OK) return st;
+  }
+  return TC_OK;
+}
+
+// The plan's header, read back after the stream has produced it.
+static tc_status read_header(const void* workspace, tc::PlanHeader* hdr, hipStream_t stream) {
+  hipError_t e = hipMemcpyAsync(hdr, workspace, sizeof(*hdr), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  return check(e);
+}
+
+tc_status tc_plan_fragments_async(const tc_fragment* frags, int64_t n, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+  try {
+    tc::PlanLayout L;
+    tc_status st = plan_args(frags, n, workspace, workspace_bytes, &L, stream);
+    if (st != TC_OK || n == 0) return st;
+    return check(tc::launch_plan(frags, n, workspace, L, stream));
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
+  }
+}
+
+tc_status tc_plan_status(const void* workspace, size_t workspace_bytes, uint64_t* total_tasks,
+                         hipStream_t stream) {
+  try {
+    if (total_tasks) *total_tasks = 0;
+    if (!workspace || (uintptr_t)workspace % 256 || workspace_bytes < tc::kTasksOffset)
+      return TC_ERR_INVALID_ARGUMENT;
+    tc::PlanHeader hdr;
+    tc_status st = read_header(workspace, &hdr, stream);
+    if (st != TC_OK) return st;
+    if (hdr.status != TC_OK) return (tc_status)hdr.status;
+    if (total_tasks) *total_tasks = hdr.total_tasks;
+    return TC_OK;
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
+  }
 }
 
 tc_status tc_plan_fragments(const tc_fragment* frags, int64_t n, void* workspace,
                             size_t workspace_bytes, uint64_t* total_tasks, hipStream_t stream) {
   try {
-    if (n < 0 || n > kMaxCount) return TC_ERR_INVALID_ARGUMENT;
     if (total_tasks) *total_tasks = 0;
-    if (n == 0) return TC_OK;
-    if (!frags || !workspace || (uintptr_t)workspace % 256) return TC_ERR_INVALID_ARGUMENT;
-    const tc::PlanLayout L = tc::plan_layout(n, workspace_bytes);
-    if (L.capacity < uint64_t(n) + 1) return TC_ERR_WORKSPACE;
-    if (validating()) {
-      std::vector<tc_fragment> h;
-      tc_status st = fetch(frags, n, &h, stream);
-      if (st != TC_OK) return st;
-      st = check_ranges(nullptr, nullptr, h);
-      if (st != TC_OK) return st;
-    }
-    // 1 KiB pieces cut on 128-byte destination lines; if that overflows the
-    // workspace, larger pieces at plain multiples (which fit by construction)
-    uint64_t piece = tc::kMinPiece, cut = 127;
-    tc::PlanHeader hdr;
-    for (int attempt = 0; attempt < 2; ++attempt) {
-      hipError_t e = tc::launch_plan_count(frags, n, piece, cut, workspace, L, false, stream);
-      if (e != hipSuccess) return hip_fail(e);
-      // The launch size of the copy depends on the task count: read it back.
-      e = hipMemcpyAsync(&hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, stream);
-      if (e == hipSuccess) e = hipStreamSynchronize(stream);
-      if (e != hipSuccess) return hip_fail(e);
-      // a task holds 48-bit offsets: refuse the list before anything is expanded
-      if (hdr.out_of_range) return TC_ERR_OUT_OF_RANGE;
-      if (hdr.total_tasks <= L.capacity) break;
-      // Too many 1 KiB pieces for the workspace: larger pieces bound the count
-      // by n + payload / piece <= capacity.
-      const uint64_t room = L.capacity - uint64_t(n);
-      piece = pow2_at_least(std::max<uint64_t>(tc::kMinPiece, (hdr.payload + room - 1) / room));
-      // a task's length is stored in 31 bits
-      piece = std::min<uint64_t>(piece, tc::kMaxPiece);
-      cut = 0;
-    }
-    if (hdr.total_tasks > L.capacity) return TC_ERR_WORKSPACE;
-    if (hdr.total_tasks > uint64_t(kMaxCount)) return TC_ERR_INVALID_ARGUMENT;
-    // Long lists with scattered destinations are planned in destination order
-    // (same tasks, so the same count): the copy then writes in address order.
-    const tc_fragment* planned = frags;
-    hipError_t e = hipSuccess;
-    if (hdr.dst_unordered && L.nbuckets) {
-      int shift = 12;
-      while (shift < 62 && (hdr.dst_end >> shift) >= L.nbuckets) ++shift;
-      e = tc::launch_plan_reorder(frags, n, shift, workspace, L, stream);
-      planned = reinterpret_cast<const tc_fragment*>(static_cast<uint8_t*>(workspace) + L.sorted);
-      if (e == hipSuccess) e = tc::launch_plan_count(planned, n, piece, cut, workspace, L, true, stream);
-      if (e != hipSuccess) return hip_fail(e);
-    }
-    e = tc::launch_plan_expand(planned, hdr.total_tasks, piece, cut, workspace, L, stream);
-    if (e != hipSuccess) return hip_fail(e);
-    if (total_tasks) *total_tasks = hdr.total_tasks;
-    return TC_OK;
+    tc::PlanLayout L;
+    tc_status st = plan_args(frags, n, workspace, workspace_bytes, &L, stream);
+    if (st != TC_OK || n == 0) return st;
+    st = check(tc::launch_plan(frags, n, workspace, L, stream));
+    if (st != TC_OK) return st;
+    // the caller asked for the task count: read it back
+    return tc_plan_status(workspace, workspace_bytes, total_tasks, stream);
   } catch (...) {
     return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }
@@ -478,21 +606,25 @@ tc_status tc_copy_planned(const void* src_base, void* dst_base, const void* work
                           size_t workspace_bytes, uint64_t total_tasks, hipStream_t stream) {
   try {
     if (total_tasks == 0) return TC_OK;
+    const bool from_plan = total_tasks == TC_TASKS_FROM_PLAN;
     if (!src_base || !dst_base || !workspace || (uintptr_t)workspace % 256 ||
-        total_tasks > uint64_t(kMaxCount))
+        (!from_plan && total_tasks > uint64_t(kMaxCount)))
       return TC_ERR_INVALID_ARGUMENT;
     // Whatever the plan's fragment count, its task table lies inside the
     // workspace: a larger count cannot come from a plan made in it.
-    if (workspace_bytes < tc::kTasksOffset ||
-        total_tasks > (workspace_bytes - tc::kTasksOffset) / tc::kTaskBytes)
-      return TC_ERR_WORKSPACE;
+    if (workspace_bytes < tc::kTasksOffset) return TC_ERR_WORKSPACE;
+    const uint64_t cap_tasks = (workspace_bytes - tc::kTasksOffset) / tc::kTaskBytes;
+    if (!from_plan && total_tasks > cap_tasks) return TC_ERR_WORKSPACE;
     // The plan's own fragment count sizes its layout.
     tc::PlanHeader hdr;
-    hipError_t e = hipSuccess;
     if (validating()) {
-      e = hipMemcpyAsync(&hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, stream);
-      if (e == hipSuccess) e = hipStreamSynchronize(stream);
-      if (e != hipSuccess) return hip_fail(e);
+      tc_status hst = read_header(workspace, &hdr, stream);
+      if (hst != TC_OK) return hst;
+      if (from_plan) {
+        if (hdr.status != TC_OK) return (tc_status)hdr.status;
+        total_tasks = hdr.total_tasks;
+        if (total_tasks == 0) return TC_OK;
+      }
       if (hdr.total_tasks != total_tasks) return TC_ERR_INVALID_ARGUMENT;
       const tc::PlanLayout L = tc::plan_layout((int64_t)hdr.n, workspace_bytes);
       if (total_tasks > L.capacity) return TC_ERR_WORKSPACE;
@@ -511,7 +643,7 @@ tc_status tc_copy_planned(const void* src_base, void* dst_base, const void* work
     }
     return check(tc::launch_copy_tasks(static_cast<const uint8_t*>(src_base),
                                        static_cast<uint8_t*>(dst_base), workspace, total_tasks,
-                                       stream));
+                                       cap_tasks, stream));
   } catch (...) {
     return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }
@@ -602,10 +734,15 @@ tc_status tc_copy_fragments(const void* src_base, void* dst_base, const tc_fragm
       st = check_ranges(src_base, dst_base, h);
       if (st != TC_OK) return st;
     }
-    uint64_t total = 0;
-    tc_status st = tc_plan_fragments(frags, n, workspace, workspace_bytes, &total, stream);
+    tc::PlanLayout L;
+    tc_status st = plan_args(frags, n, workspace, workspace_bytes, &L, stream);
     if (st != TC_OK) return st;
-    return tc_copy_planned(src_base, dst_base, workspace, workspace_bytes, total, stream);
+    st = check(tc::launch_plan(frags, n, workspace, L, stream));
+    if (st != TC_OK) return st;
+    // the copy takes its task count from the plan, on the device
+    return check(tc::launch_copy_tasks(static_cast<const uint8_t*>(src_base),
+                                       static_cast<uint8_t*>(dst_base), workspace,
+                                       tc::kTasksFromPlan, L.capacity, stream));
   } catch (...) {
     return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }
@@ -724,89 +861,76 @@ size_t tc_cast_fp8_workspace(int64_t n_items) {
   return tc::cast_workspace_bytes(n_items);
 }
 
+size_t tc_dequant_fp8_workspace(int64_t n_items) {
+  if (n_items < 0 || n_items > kMaxCount) return 0;
+  return tc::cast_workspace_bytes(n_items);
+}
+
+tc_status tc_cast_fp8_prepare(const void* src_base, const void* dst_base, const tc_cast_item* items,
+                              int64_t n_items, int32_t tile, void* workspace, size_t workspace_bytes,
+                              tc_tile_plan* plan, hipStream_t stream) {
+  try {
+    return prepare_tiles(src_base, dst_base, items, n_items, tile, workspace, workspace_bytes, true,
+                         plan, stream);
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
+  }
+}
+
+tc_status tc_cast_fp8_planned(const void* src_base, void* dst_base, float* scale_base,
+                              const void* workspace, size_t workspace_bytes,
+                              const tc_tile_plan* plan, hipStream_t stream) {
+  tc_status st = planned_args(src_base, dst_base, scale_base, workspace, workspace_bytes, plan);
+  if (st != TC_OK || plan->full_tiles + plan->edge_tiles == 0) return st;
+  return check(tc::launch_cast_blockscaled(static_cast<const uint16_t*>(src_base),
+                                           static_cast<uint8_t*>(dst_base), scale_base, workspace,
+                                           plan->n_items, plan->full_tiles, plan->edge_tiles, stream));
+}
+
 tc_status tc_cast_fp8_blockscaled(const void* src_base, void* dst_base, float* scale_base,
                                   const tc_cast_item* items, int64_t n_items, int32_t tile,
                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
   try {
     if (n_items < 0 || n_items > kMaxCount || tile != 128) return TC_ERR_INVALID_ARGUMENT;
     if (n_items == 0) return TC_OK;
-    if (!src_base || !dst_base || !scale_base || !items || !workspace) return TC_ERR_INVALID_ARGUMENT;
-    if (workspace_bytes < tc::cast_workspace_bytes(n_items)) return TC_ERR_WORKSPACE;
-    if ((uintptr_t)workspace % 256 || (uintptr_t)src_base % 2 || (uintptr_t)scale_base % 4)
-      return TC_ERR_INVALID_ARGUMENT;
-    // Geometry and the tile ranges, on the host: full tiles of vector-aligned
-    // items go to the streaming kernel, every other tile to the edge kernel.
-    const size_t N = (size_t)n_items;
-    std::vector<uint64_t> fprefix(N + 1), eprefix(N + 1);
-    std::vector<uint8_t> aligned(N);
-    uint64_t full = 0, edge = 0;
-    for (size_t i = 0; i < N; ++i) {
-      const tc_cast_item& it = items[i];
-      if (it.rows < 0 || it.cols < 0 || it.src_ld < it.cols || it.dst_ld < it.cols)
-        return TC_ERR_INVALID_ARGUMENT;
-      const uint64_t tr = uint64_t((it.rows + 127) / 128), tcn = uint64_t((it.cols + 127) / 128);
-      if (it.rows > 0 && it.cols > 0 && it.scale_ld < int64_t(tcn)) return TC_ERR_INVALID_ARGUMENT;
-      const uint64_t x = (uint64_t)(uintptr_t)src_base + 2 * it.src_off;
-      const uint64_t q = (uint64_t)(uintptr_t)dst_base + it.dst_off;
-      aligned[i] = (x % 16 == 0 && (2 * uint64_t(it.src_ld)) % 16 == 0 && q % 8 == 0 &&
-                    uint64_t(it.dst_ld) % 8 == 0) ? 1 : 0;
-      const uint64_t all = (it.rows > 0 && it.cols > 0) ? tr * tcn : 0;
-      const uint64_t f = aligned[i] ? uint64_t(it.rows / 128) * uint64_t(it.cols / 128) : 0;
-      fprefix[i] = full;
-      eprefix[i] = edge;
-      full += f;
-      edge += all - f;
+    if (!scale_base || (uintptr_t)scale_base % 4) return TC_ERR_INVALID_ARGUMENT;
+    if (validating() && src_base && dst_base && items) {
+      tc_status st = check_cast_ranges(src_base, dst_base, scale_base, items, n_items);
+      if (st != TC_OK) return st;
     }
-    fprefix[N] = full;
-    eprefix[N] = edge;
-    if (full + edge == 0) return TC_OK;
-    if (validating()) {
-      std::vector<Range> q, sc, srcr;
-      const uint64_t db = (uint64_t)(uintptr_t)dst_base, sb = (uint64_t)(uintptr_t)scale_base;
-      const uint64_t xb = (uint64_t)(uintptr_t)src_base;
-      for (int64_t i = 0; i < n_items; ++i) {
-        const tc_cast_item& it = items[i];
-        if (it.rows == 0 || it.cols == 0) continue;
-        const int64_t tcn = (it.cols + 127) / 128, tr = (it.rows + 127) / 128;
-        for (int64_t r = 0; r < it.rows; ++r) {
-          const uint64_t a = db + it.dst_off + uint64_t(r) * uint64_t(it.dst_ld);
-          q.push_back({a, a + uint64_t(it.cols)});
-          const uint64_t x = xb + 2 * (it.src_off + uint64_t(r) * uint64_t(it.src_ld));
-          srcr.push_back({x, x + 2 * uint64_t(it.cols)});
-        }
-        for (int64_t r = 0; r < tr; ++r) {
-          const uint64_t a = sb + 4 * (it.scale_off + uint64_t(r) * uint64_t(it.scale_ld));
-          sc.push_back({a, a + 4 * uint64_t(tcn)});
-        }
-      }
-      std::vector<Range> outs = q;
-      outs.insert(outs.end(), sc.begin(), sc.end());
-      if (any_overlap(outs)) return TC_ERR_ALIAS;
-      if (cross_overlap(outs, srcr)) return TC_ERR_ALIAS;
-    }
-    // Items and tile tables go to the workspace through pinned staging memory,
-    // so the caller's host array is free as soon as this call returns.
-    const tc::CastLayout L = tc::cast_layout(n_items);
-    tc_status st = stage_to_device(workspace, stream,
-                                   {{items, sizeof(tc_cast_item) * N, L.items},
-                                    {fprefix.data(), 8 * (N + 1), L.full_prefix},
-                                    {eprefix.data(), 8 * (N + 1), L.edge_prefix},
-                                    {aligned.data(), N, L.aligned}});
+    tc_tile_plan plan;
+    tc_status st = tc_cast_fp8_prepare(src_base, dst_base, items, n_items, tile, workspace,
+                                       workspace_bytes, &plan, stream);
     if (st != TC_OK) return st;
-    return check(tc::launch_cast_blockscaled(static_cast<const uint16_t*>(src_base),
-                                             static_cast<uint8_t*>(dst_base), scale_base, workspace,
-                                             n_items, full, edge, stream));
+    return tc_cast_fp8_planned(src_base, dst_base, scale_base, workspace, workspace_bytes, &plan,
+                               stream);
   } catch (...) {
     return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }
 }
 
-size_t tc_dequant_fp8_workspace(int64_t n_items) {
-  if (n_items < 0 || n_items > kMaxCount) return 0;
-  return tc::cast_workspace_bytes(n_items);
+tc_status tc_dequant_fp8_prepare(const void* codes_base, const void* dst_base,
+                                 const tc_dequant_item* items, int64_t n_items, int32_t tile,
+                                 void* workspace, size_t workspace_bytes, tc_tile_plan* plan,
+                                 hipStream_t stream) {
+  try {
+    return prepare_tiles(codes_base, dst_base, items, n_items, tile, workspace, workspace_bytes,
+                         false, plan, stream);
+  } catch (...) {
+    return TC_ERR_HOST_RESOURCES;  // host memory or threads
+  }
 }
 
-static_assert(sizeof(tc_dequant_item) == sizeof(tc_cast_item), "shared workspace layout");
+tc_status tc_dequant_fp8_planned(const void* codes_base, const float* scale_base, void* dst_base,
+                                 const void* workspace, size_t workspace_bytes,
+                                 const tc_tile_plan* plan, hipStream_t stream) {
+  tc_status st = planned_args(codes_base, dst_base, scale_base, workspace, workspace_bytes, plan);
+  if (st != TC_OK || plan->full_tiles + plan->edge_tiles == 0) return st;
+  return check(tc::launch_dequant_blockscaled(static_cast<const uint8_t*>(codes_base), scale_base,
+                                              static_cast<uint16_t*>(dst_base), workspace,
+                                              plan->n_items, plan->full_tiles, plan->edge_tiles,
+                                              stream));
+}
 
 tc_status tc_dequant_fp8_blockscaled(const void* codes_base, const float* scale_base,
                                      void* dst_base, const tc_dequant_item* items, int64_t n_items,
@@ -815,66 +939,17 @@ tc_status tc_dequant_fp8_blockscaled(const void* codes_base, const float* scale_
   try {
     if (n_items < 0 || n_items > kMaxCount || tile != 128) return TC_ERR_INVALID_ARGUMENT;
     if (n_items == 0) return TC_OK;
-    if (!codes_base || !scale_base || !dst_base || !items || !workspace) return TC_ERR_INVALID_ARGUMENT;
-    if (workspace_bytes < tc::cast_workspace_bytes(n_items)) return TC_ERR_WORKSPACE;
-    if ((uintptr_t)workspace % 256 || (uintptr_t)dst_base % 2 || (uintptr_t)scale_base % 4)
-      return TC_ERR_INVALID_ARGUMENT;
-    const size_t N = (size_t)n_items;
-    std::vector<uint64_t> fprefix(N + 1), eprefix(N + 1);
-    std::vector<uint8_t> aligned(N);
-    uint64_t full = 0, edge = 0;
-    for (size_t i = 0; i < N; ++i) {
-      const tc_dequant_item& it = items[i];
-      if (it.rows < 0 || it.cols < 0 || it.src_ld < it.cols || it.dst_ld < it.cols)
-        return TC_ERR_INVALID_ARGUMENT;
-      const uint64_t tr = uint64_t((it.rows + 127) / 128), tcn = uint64_t((it.cols + 127) / 128);
-      if (it.rows > 0 && it.cols > 0 && it.scale_ld < int64_t(tcn)) return TC_ERR_INVALID_ARGUMENT;
-      const uint64_t q = (uint64_t)(uintptr_t)codes_base + it.src_off;
-      const uint64_t y = (uint64_t)(uintptr_t)dst_base + 2 * it.dst_off;
-      aligned[i] = (q % 8 == 0 && uint64_t(it.src_ld) % 8 == 0 && y % 16 == 0 &&
-                    (2 * uint64_t(it.dst_ld)) % 16 == 0) ? 1 : 0;
-      const uint64_t all = (it.rows > 0 && it.cols > 0) ? tr * tcn : 0;
-      const uint64_t f = aligned[i] ? uint64_t(it.rows / 128) * uint64_t(it.cols / 128) : 0;
-      fprefix[i] = full;
-      eprefix[i] = edge;
-      full += f;
-      edge += all - f;
+    if (!scale_base || (uintptr_t)scale_base % 4) return TC_ERR_INVALID_ARGUMENT;
+    if (validating() && codes_base && dst_base && items) {
+      tc_status st = check_dequant_ranges(codes_base, scale_base, dst_base, items, n_items);
+      if (st != TC_OK) return st;
     }
-    fprefix[N] = full;
-    eprefix[N] = edge;
-    if (full + edge == 0) return TC_OK;
-    if (validating()) {
-      std::vector<Range> outs, srcs;
-      const uint64_t db = (uint64_t)(uintptr_t)dst_base, qb = (uint64_t)(uintptr_t)codes_base;
-      const uint64_t sb = (uint64_t)(uintptr_t)scale_base;
-      for (size_t i = 0; i < N; ++i) {
-        const tc_dequant_item& it = items[i];
-        if (it.rows == 0 || it.cols == 0) continue;
-        const int64_t tcn = (it.cols + 127) / 128, tr = (it.rows + 127) / 128;
-        for (int64_t r = 0; r < it.rows; ++r) {
-          const uint64_t a = db + 2 * (it.dst_off + uint64_t(r) * uint64_t(it.dst_ld));
-          outs.push_back({a, a + 2 * uint64_t(it.cols)});
-          const uint64_t x = qb + it.src_off + uint64_t(r) * uint64_t(it.src_ld);
-          srcs.push_back({x, x + uint64_t(it.cols)});
-        }
-        for (int64_t r = 0; r < tr; ++r) {
-          const uint64_t a = sb + 4 * (it.scale_off + uint64_t(r) * uint64_t(it.scale_ld));
-          srcs.push_back({a, a + 4 * uint64_t(tcn)});
-        }
-      }
-      if (any_overlap(outs)) return TC_ERR_ALIAS;
-      if (cross_overlap(outs, srcs)) return TC_ERR_ALIAS;
-    }
-    const tc::CastLayout L = tc::cast_layout(n_items);
-    tc_status st = stage_to_device(workspace, stream,
-                                   {{items, sizeof(tc_dequant_item) * N, L.items},
-                                    {fprefix.data(), 8 * (N + 1), L.full_prefix},
-                                    {eprefix.data(), 8 * (N + 1), L.edge_prefix},
-                                    {aligned.data(), N, L.aligned}});
+    tc_tile_plan plan;
+    tc_status st = tc_dequant_fp8_prepare(codes_base, dst_base, items, n_items, tile, workspace,
+                                          workspace_bytes, &plan, stream);
     if (st != TC_OK) return st;
-    return check(tc::launch_dequant_blockscaled(static_cast<const uint8_t*>(codes_base), scale_base,
-                                                static_cast<uint16_t*>(dst_base), workspace, n_items,
-                                                full, edge, stream));
+    return tc_dequant_fp8_planned(codes_base, scale_base, dst_base, workspace, workspace_bytes,
+                                  &plan, stream);
   } catch (...) {
     return TC_ERR_HOST_RESOURCES;  // host memory or threads
   }

@@ -280,9 +280,44 @@ __global__ __launch_bounds__(kThreads) void k_cast_scaled(const uint16_t* __rest
   }
 }
 
+// Writes one chunk of the tile table into the workspace: the items (64-byte
+// records, cast or inverse-cast items alike), their tile prefixes and their
+// vector-path flags, and after the last chunk the two totals.  The chunk
+// travels in the kernel arguments, so the host table needs no staging buffer
+// and may be reused once the launch call returns; a graph that captures the
+// launch keeps its own copy of the chunk.
+__global__ __launch_bounds__(kThreads) void k_tile_table(const TableChunk c, uint8_t* __restrict__ ws,
+                                                        const uint64_t items_off,
+                                                        const uint64_t full_off,
+                                                        const uint64_t edge_off,
+                                                        const uint64_t aligned_off) {
+  static_assert(sizeof(tc_cast_item) == 8 * kItemWords, "items are 8 words");
+  uint64_t* items = reinterpret_cast<uint64_t*>(ws + items_off) + c.first * kItemWords;
+  for (uint32_t k = threadIdx.x; k < c.count * kItemWords; k += kThreads) items[k] = c.words[k];
+  uint64_t* fp = reinterpret_cast<uint64_t*>(ws + full_off);
+  uint64_t* ep = reinterpret_cast<uint64_t*>(ws + edge_off);
+  for (uint32_t k = threadIdx.x; k < c.count; k += kThreads) {
+    fp[c.first + k] = c.fprefix[k];
+    ep[c.first + k] = c.eprefix[k];
+    ws[aligned_off + c.first + k] = c.aligned[k];
+  }
+  if (c.last && threadIdx.x == 0) {
+    fp[c.first + c.count] = c.ftotal;
+    ep[c.first + c.count] = c.etotal;
+  }
+}
+
 }  // namespace
 
 static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+hipError_t launch_tile_chunk(const TableChunk& c, int64_t n_items, void* ws, hipStream_t s) {
+  const CastLayout L = cast_layout(n_items);
+  hipLaunchKernelGGL(k_tile_table, dim3(1), dim3(kThreads), 0, s, c, static_cast<uint8_t*>(ws),
+                     uint64_t(L.items), uint64_t(L.full_prefix), uint64_t(L.edge_prefix),
+                     uint64_t(L.aligned));
+  return hipGetLastError();
+}
 
 CastLayout cast_layout(int64_t n_items) {
   CastLayout L;

@@ -51,7 +51,17 @@ struct PlanHeader {
                            // destination line; 0: tasks start at multiples of the piece
   uint64_t out_of_range;   // some non-empty fragment ends past 2^48 (source or destination):
                            // its tasks could not hold the offsets, so nothing is planned
+  uint64_t status;         // tc_status of the plan: TC_OK, TC_ERR_OUT_OF_RANGE (offsets past
+                           // 2^48), TC_ERR_WORKSPACE (the tasks do not fit), or
+                           // TC_ERR_INVALID_ARGUMENT (more than 2^33 tasks); total_tasks is 0
+                           // unless TC_OK
+  uint64_t recount;        // 1 KiB pieces overflowed the workspace: counted again with `piece`
+  uint64_t shift;          // bucket size (log2 bytes) of a destination-ordered plan
 };
+// The planning kernels decide everything on the device (piece, reordering,
+// status), so planning never waits for the host.  A copy launched with this
+// task count reads the count from the plan's header on the device.
+constexpr uint64_t kTasksFromPlan = ~uint64_t(0);
 
 // Workspace layout: header | tasks[capacity] | digest slots[capacity] |
 // windows[ceil(capacity / 1024)] | ... | tstart[n + 1] | block sums |
@@ -92,20 +102,17 @@ hipError_t launch_blocks(const RegionTable& tab, int32_t num_regions, int64_t bl
                          bool gather, bool aligned, hipStream_t s);
 
 // --- fragments ---------------------------------------------------------
-// Count pieces of `piece` bytes per fragment and write tstart; the header
-// receives the totals, whether the destinations are unordered, their end, and
-// `permuted` (the list counted is the reordered one).  Enqueued only.
-hipError_t launch_plan_count(const tc_fragment* frags, int64_t n, uint64_t piece, uint64_t cut,
-                             void* ws, const PlanLayout& L, bool permuted, hipStream_t s);
-// Write the fragments in destination order (buckets of 2^shift bytes) to
-// L.sorted and their original indices to L.perm.
-hipError_t launch_plan_reorder(const tc_fragment* frags, int64_t n, int shift, void* ws,
-                               const PlanLayout& L, hipStream_t s);
-// Expand the counted plan into its task table (total_tasks known on the host).
-hipError_t launch_plan_expand(const tc_fragment* frags, uint64_t total_tasks, uint64_t piece,
-                              uint64_t cut, void* ws, const PlanLayout& L, hipStream_t s);
+// Enqueue the whole plan of n fragments into the workspace (header, task
+// table, windows, tstart; for long unordered lists the destination-ordered
+// copy of the list and its permutation).  Every decision -- piece size,
+// reordering, status -- is taken on the device; nothing waits for the host.
+hipError_t launch_plan(const tc_fragment* frags, int64_t n, void* ws, const PlanLayout& L,
+                       hipStream_t s);
+// Copy with a plan.  total_tasks is the plan's count, or kTasksFromPlan: the
+// kernel then reads it from the header and a bounded grid strides over the
+// tasks (cap_tasks bounds the count, from the workspace size).
 hipError_t launch_copy_tasks(const uint8_t* src, uint8_t* dst, const void* ws,
-                             uint64_t total_tasks, hipStream_t s);
+                             uint64_t total_tasks, uint64_t cap_tasks, hipStream_t s);
 // Copy (mode 0) or only read (1: at the tasks' source offsets, 2: at their
 // destination offsets) with a plan, and write each fragment's digest pair
 // into digests[2n]: zero fill, per-task sums into the digest slots, then a
@@ -122,6 +129,24 @@ struct CastLayout {
 };
 CastLayout cast_layout(int64_t n_items);
 size_t cast_workspace_bytes(int64_t n_items);
+// A chunk of the tile table, passed by value as a kernel argument (3.3 KB,
+// below the 4 KiB of kernel arguments a launch may carry).
+constexpr int kTableChunkItems = 40;
+constexpr int kItemWords = 8;  // a cast or inverse-cast item is eight 64-bit words
+struct TableChunk {
+  uint64_t words[kTableChunkItems * kItemWords];
+  uint64_t fprefix[kTableChunkItems];
+  uint64_t eprefix[kTableChunkItems];
+  uint64_t first;            // index of the chunk's first item
+  uint64_t ftotal, etotal;   // the table's totals, written after the last chunk
+  uint32_t count;            // items in the chunk
+  uint32_t last;             // 1 for the last chunk
+  uint8_t aligned[kTableChunkItems];
+};
+static_assert(sizeof(TableChunk) <= 3584, "a chunk fits the kernel arguments");
+// Enqueue the writes of one chunk of a table of n_items items into the
+// workspace (the table's layout is cast_layout(n_items)).
+hipError_t launch_tile_chunk(const TableChunk& c, int64_t n_items, void* ws, hipStream_t s);
 hipError_t launch_cast_blockscaled(const uint16_t* src, uint8_t* dst, float* scales,
                                    const void* ws, int64_t n_items, uint64_t full_tiles,
                                    uint64_t edge_tiles, hipStream_t s);

@@ -11,9 +11,19 @@ namespace {
 // h = dst_off & cut: with cut = 127 every task after a fragment's first starts
 // on a 128-byte destination line (no line is split between two waves inside
 // a fragment); cut = 0 gives plain multiples of the piece.  tstart[f] is its
-// first task, tstart[n] the total.  Passes: per-block task and byte sums,
-// an exclusive scan of the block sums (one workgroup), the per-fragment
-// prefix, then (after the host has read the total) the task table.
+// first task, tstart[n] the total.
+//
+// Every pass runs on the device and takes its decisions from the plan header,
+// so a plan is enqueued without waiting for the host:
+//   count (1 KiB pieces, line cut; clears the reordering's counters)
+//   -> decide: totals, status, piece, reordering (one workgroup)
+//   [reorder: bucket histogram, bucket scan, scatter -- lists of >= 4096]
+//   count again -- only for a reordered list or a larger piece
+//   tstart + windows (each workgroup sums the block counts before it)
+//   -> expansion into the task table.
+// A pass the header does not ask for returns at once.  Every launch costs a
+// few microseconds even then, so the passes are as few as the decisions
+// allow: 5 launches for short lists, 7 for long ones.
 // ------------------------------------------------------------------------
 __device__ __forceinline__ uint64_t shfl_up_u64(uint64_t v, int delta) {
   const uint32_t lo = __shfl_up((uint32_t)v, delta, kWaveLanes);
@@ -72,14 +82,34 @@ __device__ uint64_t block_max_u64(uint64_t v) {
 // Per block: task and byte sums, whether some destination starts below its
 // predecessor's (checked across the block's last boundary too), the largest
 // destination end, and whether some fragment ends past the 48-bit offsets of
-// a task (flag bit 0: unordered, bit 1: out of range).
-__global__ __launch_bounds__(kThreads) void k_plan_count(const tc_fragment* __restrict__ frags,
-                                                        const int64_t n, const uint64_t piece,
-                                                        const uint64_t cut,
+// a task (flag bit 0: unordered, bit 1: out of range).  First pass: the given
+// list with 1 KiB pieces and the line cut.  Second pass (again != 0): only if
+// the header asks for it, over the list the header names (the reordered one
+// or the given one) with the header's piece and cut; only the task sums.
+// The first pass also clears the reordering's bucket counters (clear[0 ..
+// nclear)), which the histogram adds into if the list is reordered.
+__global__ __launch_bounds__(kThreads) void k_plan_count(const tc_fragment* __restrict__ given,
+                                                        const tc_fragment* __restrict__ sorted,
+                                                        const int64_t n, const int again,
+                                                        const PlanHeader* __restrict__ hdr,
                                                         uint64_t* __restrict__ block_cnt,
                                                         uint64_t* __restrict__ block_len,
                                                         uint64_t* __restrict__ block_unord,
-                                                        uint64_t* __restrict__ block_dend) {
+                                                        uint64_t* __restrict__ block_dend,
+                                                        uint64_t* __restrict__ clear,
+                                                        const uint64_t nclear) {
+  const tc_fragment* frags = given;
+  uint64_t piece = kMinPiece, cut = 127;
+  if (!again) {
+    for (uint64_t i = uint64_t(blockIdx.x) * kThreads + threadIdx.x; i < nclear;
+         i += uint64_t(gridDim.x) * kThreads)
+      clear[i] = 0;
+  } else {
+    if (hdr->status != TC_OK || !(hdr->recount || hdr->permuted)) return;
+    if (hdr->permuted) frags = sorted;
+    piece = hdr->piece;
+    cut = hdr->cut;
+  }
   const int64_t f0 = int64_t(blockIdx.x) * kPlanPerBlock + int64_t(threadIdx.x) * kPlanPerThread;
   uint64_t c = 0, l = 0, dend = 0;
   int unord = 0, bad = 0;
@@ -103,47 +133,68 @@ __global__ __launch_bounds__(kThreads) void k_plan_count(const tc_fragment* __re
   const uint64_t bdend = block_max_u64(dend);
   if (threadIdx.x == 0) {
     block_cnt[blockIdx.x] = tc_;
-    block_len[blockIdx.x] = tl;
-    block_unord[blockIdx.x] = (any_unord ? 1u : 0u) | (any_bad ? 2u : 0u);
-    block_dend[blockIdx.x] = bdend;
+    if (!again) {
+      block_len[blockIdx.x] = tl;
+      block_unord[blockIdx.x] = (any_unord ? 1u : 0u) | (any_bad ? 2u : 0u);
+      block_dend[blockIdx.x] = bdend;
+    }
   }
 }
 
-// One workgroup: block_cnt becomes its exclusive prefix; the header gets
-// the totals.
-__global__ __launch_bounds__(kThreads) void k_plan_scan(uint64_t* __restrict__ block_cnt,
+__device__ __forceinline__ uint64_t pow2_at_least(uint64_t x) {
+  uint64_t p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+// One workgroup: the totals of the first count and the plan's decisions.
+//   status: TC_ERR_OUT_OF_RANGE if a fragment ends past 2^48, else TC_OK;
+//   piece: 1 KiB with the line cut while the tasks fit the workspace;
+//     otherwise the smallest power of two >= payload / (capacity - n) (at most
+//     2^30), without the cut, and the list is counted again (recount);
+//   permuted: a list of >= 4096 fragments (nbuckets > 0) whose destinations
+//     are not in ascending order is reordered by destination, with buckets of
+//     2^shift bytes covering the largest destination end.
+// The task count is final here unless the list is counted again; tstart
+// then sets it, with TC_ERR_WORKSPACE if it still does not fit.
+__global__ __launch_bounds__(kThreads) void k_plan_scan(const uint64_t* __restrict__ block_cnt,
                                                        const uint64_t* __restrict__ block_len,
                                                        const uint64_t* __restrict__ block_unord,
                                                        const uint64_t* __restrict__ block_dend,
-                                                       const int64_t nblocks, const uint64_t piece,
-                                                       const uint64_t cut,
-                                                       const int64_t n, const uint64_t capacity,
-                                                       const uint64_t permuted,
-                                                       PlanHeader* __restrict__ hdr,
-                                                       uint64_t* __restrict__ tstart_end) {
+                                                       const int64_t nblocks, const int64_t n,
+                                                       const uint64_t capacity,
+                                                       const uint64_t nbuckets,
+                                                       PlanHeader* __restrict__ hdr) {
   uint64_t carry = 0, bytes = 0, dend = 0;
   int unord = 0, bad = 0;
-  for (int64_t base = 0; base < nblocks; base += kThreads) {
-    const int64_t i = base + threadIdx.x;
-    const uint64_t v = i < nblocks ? block_cnt[i] : 0;
-    const uint64_t l = i < nblocks ? block_len[i] : 0;
-    if (i < nblocks) {
-      unord |= (block_unord[i] & 1u) ? 1 : 0;
-      bad |= (block_unord[i] & 2u) ? 1 : 0;
-      dend = dend > block_dend[i] ? dend : block_dend[i];
-    }
-    uint64_t total, ltot;
-    const uint64_t ex = block_exclusive_scan(v, &total);
-    block_exclusive_scan(l, &ltot);
-    if (i < nblocks) block_cnt[i] = carry + ex;
-    carry += total;
-    bytes += ltot;
+  for (int64_t i = threadIdx.x; i < nblocks; i += kThreads) {
+    carry += block_cnt[i];
+    bytes += block_len[i];
+    unord |= (block_unord[i] & 1u) ? 1 : 0;
+    bad |= (block_unord[i] & 2u) ? 1 : 0;
+    dend = dend > block_dend[i] ? dend : block_dend[i];
   }
+  block_exclusive_scan(carry, &carry);
+  block_exclusive_scan(bytes, &bytes);
   const int any_unord = __syncthreads_or(unord);
   const int any_bad = __syncthreads_or(bad);
   dend = block_max_u64(dend);
   if (threadIdx.x == 0) {
-    hdr->total_tasks = carry;
+    uint64_t st = any_bad ? TC_ERR_OUT_OF_RANGE : TC_OK;
+    uint64_t piece = kMinPiece, cut = 127, recount = 0;
+    if (st == TC_OK && carry > capacity) {
+      // Too many 1 KiB pieces for the workspace: larger pieces bound the
+      // count by n + payload / piece <= capacity (a task's length has 31 bits).
+      const uint64_t room = capacity - uint64_t(n);
+      piece = pow2_at_least(max(kMinPiece, (bytes + room - 1) / room));
+      piece = min(piece, kMaxPiece);
+      cut = 0;
+      recount = 1;
+    }
+    if (st == TC_OK && !recount && carry > (uint64_t(1) << 33)) st = TC_ERR_INVALID_ARGUMENT;
+    const uint64_t permuted = (st == TC_OK && any_unord && nbuckets) ? 1 : 0;
+    uint64_t shift = 12;
+    while (shift < 62 && (dend >> shift) >= nbuckets) ++shift;
     hdr->piece = piece;
     hdr->payload = bytes;
     hdr->n = uint64_t(n);
@@ -153,17 +204,89 @@ __global__ __launch_bounds__(kThreads) void k_plan_scan(uint64_t* __restrict__ b
     hdr->permuted = permuted;
     hdr->cut = cut;
     hdr->out_of_range = any_bad ? 1 : 0;
-    *tstart_end = carry;
+    hdr->recount = recount;
+    hdr->shift = shift;
+    hdr->status = st;
+    // final unless counted again
+    hdr->total_tasks = (st == TC_OK && !recount) ? carry : 0;
   }
 }
 
-__global__ __launch_bounds__(kThreads) void k_plan_tstart(const tc_fragment* __restrict__ frags,
-                                                         const int64_t n, const uint64_t piece,
-                                                         const uint64_t cut,
+// Long lists only (more than kPrefixBlocks count blocks): the block counts'
+// exclusive prefix into block_off in one workgroup, and, for a list counted
+// again, its task count and status.
+constexpr int64_t kPrefixBlocks = 16384;
+
+__global__ __launch_bounds__(kThreads) void k_plan_offsets(const uint64_t* __restrict__ block_cnt,
+                                                          uint64_t* __restrict__ block_off,
+                                                          const int64_t nblocks,
+                                                          const uint64_t capacity,
+                                                          PlanHeader* __restrict__ hdr) {
+  if (hdr->status != TC_OK) return;
+  uint64_t carry = 0;
+  for (int64_t base = 0; base < nblocks; base += kThreads) {
+    const int64_t i = base + threadIdx.x;
+    uint64_t total;
+    const uint64_t ex = block_exclusive_scan(i < nblocks ? block_cnt[i] : 0, &total);
+    if (i < nblocks) block_off[i] = carry + ex;
+    carry += total;
+  }
+  if (threadIdx.x == 0 && (hdr->recount || hdr->permuted)) {
+    uint64_t st = TC_OK;
+    if (carry > capacity) st = TC_ERR_WORKSPACE;
+    else if (carry > (uint64_t(1) << 33)) st = TC_ERR_INVALID_ARGUMENT;
+    hdr->status = st;
+    hdr->total_tasks = st == TC_OK ? carry : 0;
+  }
+}
+
+// Per-fragment first task and the window table, for the list the header
+// names, with its piece and cut.  Each workgroup takes its offset from the
+// block counts: it sums those before it itself (block_off == nullptr), or
+// reads k_plan_offsets' prefix for long lists.  A list counted again gets its
+// task count and status here (every workgroup finds the same total; the
+// first writes it).  Nothing for a failed plan.
+__global__ __launch_bounds__(kThreads) void k_plan_tstart(const tc_fragment* __restrict__ given,
+                                                         const tc_fragment* __restrict__ sorted,
+                                                         const int64_t n, const int64_t nblocks,
+                                                         PlanHeader* __restrict__ hdr,
+                                                         const uint64_t* __restrict__ block_cnt,
                                                          const uint64_t* __restrict__ block_off,
+                                                         const uint64_t capacity,
                                                          uint64_t* __restrict__ tstart,
-                                                         int64_t* __restrict__ windows,
-                                                         const uint64_t capacity) {
+                                                         int64_t* __restrict__ windows) {
+  if (hdr->status != TC_OK) return;
+  const bool counted_again = hdr->recount || hdr->permuted;
+  uint64_t before, total;
+  if (block_off) {
+    before = block_off[blockIdx.x];
+    total = hdr->total_tasks;
+  } else {
+    uint64_t b = 0, a = 0;
+    for (int64_t j = threadIdx.x; j < nblocks; j += kThreads) {
+      const uint64_t c = block_cnt[j];
+      a += c;
+      if (j < int64_t(blockIdx.x)) b += c;
+    }
+    block_exclusive_scan(b, &before);
+    block_exclusive_scan(a, &total);
+    if (counted_again) {
+      uint64_t st = TC_OK;
+      if (total > capacity) st = TC_ERR_WORKSPACE;
+      else if (total > (uint64_t(1) << 33)) st = TC_ERR_INVALID_ARGUMENT;
+      if (st != TC_OK) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) {
+          hdr->status = st;
+          hdr->total_tasks = 0;
+        }
+        return;
+      }
+      if (blockIdx.x == 0 && threadIdx.x == 0) hdr->total_tasks = total;
+    }
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) tstart[n] = total;
+  const tc_fragment* frags = hdr->permuted ? sorted : given;
+  const uint64_t piece = hdr->piece, cut = hdr->cut;
   const int64_t f0 = int64_t(blockIdx.x) * kPlanPerBlock + int64_t(threadIdx.x) * kPlanPerThread;
   uint64_t c[kPlanPerThread];
   uint64_t s = 0;
@@ -173,11 +296,7 @@ __global__ __launch_bounds__(kThreads) void k_plan_tstart(const tc_fragment* __r
     s += c[j];
   }
   uint64_t block_total;
-  uint64_t run = block_off[blockIdx.x] + block_exclusive_scan(s, &block_total);
-  // the plan's total (written by k_plan_scan); the window table only has
-  // room for a plan that fits the workspace
-  const uint64_t total = tstart[n];
-  const bool fits = total <= capacity;
+  uint64_t run = before + block_exclusive_scan(s, &block_total);
   const uint64_t nwin = (total + kWindowTasks - 1) / kWindowTasks;
 #pragma unroll
   for (int j = 0; j < kPlanPerThread; ++j) {
@@ -186,7 +305,7 @@ __global__ __launch_bounds__(kThreads) void k_plan_tstart(const tc_fragment* __r
       // Every task lies in exactly one non-empty fragment, which is therefore
       // the first fragment of each window whose first task it holds and the
       // last fragment of each window whose last task it holds.
-      if (fits && c[j]) {
+      if (c[j]) {
         const uint64_t te = run + c[j];  // tasks [run, te)
         for (uint64_t w = (run + kWindowTasks - 1) / kWindowTasks; w * kWindowTasks < te; ++w)
           windows[2 * w] = f0 + j;
@@ -206,80 +325,89 @@ __device__ __forceinline__ Task pack_task(uint64_t src, uint64_t dst, uint64_t l
 }
 
 
-// Block j writes tasks [j * 1024, (j + 1) * 1024), whose first and last
-// fragment k_plan_tstart recorded in windows[j].  If they span at most 1024
-// fragments their tstart entries go to LDS and every task finds its fragment
-// there, otherwise (long runs of empty fragments) each task searches
+// Window j's workgroup writes tasks [j * 1024, (j + 1) * 1024), whose first
+// and last fragment k_plan_tstart recorded in windows[j].  If they span at
+// most 1024 fragments their tstart entries go to LDS and every task finds its
+// fragment there, otherwise (long runs of empty fragments) each task searches
 // globally.  A thread's four tasks are found first and their descriptors
-// loaded together, so the loads overlap.
+// loaded together, so the loads overlap.  The grid is bounded by the
+// workspace's capacity (the task count is only known on the device) and
+// strides over the windows; workgroups past the plan's last window return.
 constexpr int kExpandPerThread = kExpandPerBlock / kThreads;
 static_assert(kExpandPerThread * kThreads == kExpandPerBlock, "whole tasks per thread");
 
-__global__ __launch_bounds__(kThreads) void k_plan_expand(const tc_fragment* __restrict__ frags,
+__global__ __launch_bounds__(kThreads) void k_plan_expand(const tc_fragment* __restrict__ given,
+                                                         const tc_fragment* __restrict__ sorted,
                                                          const uint64_t* __restrict__ tstart,
                                                          const int64_t* __restrict__ windows,
-                                                         const uint64_t total, const uint64_t piece,
-                                                         const uint64_t cut,
+                                                         const PlanHeader* __restrict__ hdr,
                                                          Task* __restrict__ tasks) {
   __shared__ uint64_t win[kExpandPerBlock + 1];
-  const uint64_t t0 = uint64_t(blockIdx.x) * kExpandPerBlock;
-  const uint64_t t1 = min(total, t0 + kExpandPerBlock);
-  const int64_t f0 = windows[2 * uint64_t(blockIdx.x)];
-  const int64_t f1 = windows[2 * uint64_t(blockIdx.x) + 1];
-  const int64_t span = f1 - f0 + 1;
-  const bool local = span <= kExpandPerBlock;
-  if (local)
-    for (int64_t k = threadIdx.x; k <= span; k += kThreads) win[k] = tstart[f0 + k];
-  __syncthreads();
-  int64_t frag[kExpandPerThread];
-  uint64_t start[kExpandPerThread];
+  if (hdr->status != TC_OK) return;
+  const uint64_t total = hdr->total_tasks, piece = hdr->piece, cut = hdr->cut;
+  const tc_fragment* frags = hdr->permuted ? sorted : given;
+  const uint64_t nwin = (total + kExpandPerBlock - 1) / kExpandPerBlock;
+  for (uint64_t wj = blockIdx.x; wj < nwin; wj += gridDim.x) {
+    const uint64_t t0 = wj * kExpandPerBlock;
+    const uint64_t t1 = min(total, t0 + kExpandPerBlock);
+    const int64_t f0 = windows[2 * wj];
+    const int64_t f1 = windows[2 * wj + 1];
+    const int64_t span = f1 - f0 + 1;
+    const bool local = span <= kExpandPerBlock;
+    if (local)
+      for (int64_t k = threadIdx.x; k <= span; k += kThreads) win[k] = tstart[f0 + k];
+    __syncthreads();
+    int64_t frag[kExpandPerThread];
+    uint64_t start[kExpandPerThread];
 #pragma unroll
-  for (int j = 0; j < kExpandPerThread; ++j) {
-    const uint64_t t = t0 + threadIdx.x + uint64_t(j) * kThreads;
-    frag[j] = -1;
-    start[j] = 0;
-    if (t >= t1) continue;
-    int64_t lo, hi;
-    if (local) {  // win[lo] <= t < win[hi], indices relative to f0
-      lo = 0;
-      hi = span;
-      while (hi - lo > 1) {
-        const int64_t mid = (lo + hi) >> 1;
-        if (win[mid] <= t)
-          lo = mid;
-        else
-          hi = mid;
+    for (int j = 0; j < kExpandPerThread; ++j) {
+      const uint64_t t = t0 + threadIdx.x + uint64_t(j) * kThreads;
+      frag[j] = -1;
+      start[j] = 0;
+      if (t >= t1) continue;
+      int64_t lo, hi;
+      if (local) {  // win[lo] <= t < win[hi], indices relative to f0
+        lo = 0;
+        hi = span;
+        while (hi - lo > 1) {
+          const int64_t mid = (lo + hi) >> 1;
+          if (win[mid] <= t)
+            lo = mid;
+          else
+            hi = mid;
+        }
+        start[j] = win[lo];
+        frag[j] = f0 + lo;
+      } else {
+        lo = f0;
+        hi = f1 + 1;
+        while (hi - lo > 1) {
+          const int64_t mid = (lo + hi) >> 1;
+          if (tstart[mid] <= t)
+            lo = mid;
+          else
+            hi = mid;
+        }
+        start[j] = tstart[lo];
+        frag[j] = lo;
       }
-      start[j] = win[lo];
-      frag[j] = f0 + lo;
-    } else {
-      lo = f0;
-      hi = f1 + 1;
-      while (hi - lo > 1) {
-        const int64_t mid = (lo + hi) >> 1;
-        if (tstart[mid] <= t)
-          lo = mid;
-        else
-          hi = mid;
-      }
-      start[j] = tstart[lo];
-      frag[j] = lo;
     }
-  }
-  tc_fragment f[kExpandPerThread];
+    tc_fragment f[kExpandPerThread];
 #pragma unroll
-  for (int j = 0; j < kExpandPerThread; ++j)
-    if (frag[j] >= 0) f[j] = frags[frag[j]];
+    for (int j = 0; j < kExpandPerThread; ++j)
+      if (frag[j] >= 0) f[j] = frags[frag[j]];
 #pragma unroll
-  for (int j = 0; j < kExpandPerThread; ++j) {
-    if (frag[j] < 0) continue;
-    const uint64_t t = t0 + threadIdx.x + uint64_t(j) * kThreads;
-    // task k covers [k * piece - h, (k + 1) * piece - h) of the fragment,
-    // clipped to [0, len)
-    const uint64_t k = t - start[j], h = f[j].dst_off & cut;
-    const uint64_t off = k ? k * piece - h : 0;
-    const uint64_t end = min(f[j].len, (k + 1) * piece - h);
-    tasks[t] = pack_task(f[j].src_off + off, f[j].dst_off + off, end - off, k == 0);
+    for (int j = 0; j < kExpandPerThread; ++j) {
+      if (frag[j] < 0) continue;
+      const uint64_t t = t0 + threadIdx.x + uint64_t(j) * kThreads;
+      // task k covers [k * piece - h, (k + 1) * piece - h) of the fragment,
+      // clipped to [0, len)
+      const uint64_t k = t - start[j], h = f[j].dst_off & cut;
+      const uint64_t off = k ? k * piece - h : 0;
+      const uint64_t end = min(f[j].len, (k + 1) * piece - h);
+      tasks[t] = pack_task(f[j].src_off + off, f[j].dst_off + off, end - off, k == 0);
+    }
+    __syncthreads();  // win is refilled by the next window
   }
 }
 
@@ -296,47 +424,32 @@ __device__ __forceinline__ uint64_t bucket_of(uint64_t dst_off, int shift, uint6
   return b < nbk ? b : nbk - 1;
 }
 
+// The reordering passes run only when the header asks for it (permuted);
+// the bucket size comes from the header too.  The counters are cleared by
+// the first count.
 // Bucket sizes; each fragment keeps the count it found as its rank inside
 // its bucket (in no particular order), so the scatter needs no atomics.
 __global__ __launch_bounds__(kThreads) void k_bucket_hist(const tc_fragment* __restrict__ frags,
-                                                         const int64_t n, const int shift,
+                                                         const int64_t n,
+                                                         const PlanHeader* __restrict__ hdr,
                                                          const uint64_t nbk,
                                                          uint64_t* __restrict__ cnt,
                                                          uint64_t* __restrict__ rank) {
+  if (!hdr->permuted) return;
+  const int shift = int(hdr->shift);
   for (int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x; i < n;
        i += int64_t(gridDim.x) * kThreads)
     rank[i] = atomicAdd(
         reinterpret_cast<unsigned long long*>(&cnt[bucket_of(frags[i].dst_off, shift, nbk)]), 1ull);
 }
 
-// Exclusive scan of v[0 .. m) in place, in three passes: sums of 1024
-// entries, a scan of those sums (one workgroup), then each 1024-entry block.
-__global__ __launch_bounds__(kThreads) void k_scan_sums(const uint64_t* __restrict__ v,
-                                                       const uint64_t m,
-                                                       uint64_t* __restrict__ sums) {
-  const uint64_t i0 = uint64_t(blockIdx.x) * kPlanPerBlock + uint64_t(threadIdx.x) * kPlanPerThread;
-  uint64_t t = 0;
-#pragma unroll
-  for (int j = 0; j < kPlanPerThread; ++j)
-    if (i0 + j < m) t += v[i0 + j];
-  uint64_t total;
-  block_exclusive_scan(t, &total);
-  if (threadIdx.x == 0) sums[blockIdx.x] = total;
-}
-
-__global__ __launch_bounds__(kThreads) void k_scan_one(uint64_t* __restrict__ v, const uint64_t m) {
-  uint64_t carry = 0;
-  for (uint64_t base = 0; base < m; base += kThreads) {
-    const uint64_t i = base + threadIdx.x;
-    uint64_t total;
-    const uint64_t ex = block_exclusive_scan(i < m ? v[i] : 0, &total);
-    if (i < m) v[i] = carry + ex;
-    carry += total;
-  }
-}
-
-__global__ __launch_bounds__(kThreads) void k_scan_apply(uint64_t* __restrict__ v, const uint64_t m,
-                                                        const uint64_t* __restrict__ sums) {
+// Bucket offsets in two levels: each workgroup scans 1024 bucket counts in
+// place (exclusive, within its block) and records the block's total; the
+// scatter adds the totals of the blocks before (at most 256 of them).
+__global__ __launch_bounds__(kThreads) void k_bucket_scan(const PlanHeader* __restrict__ hdr,
+                                                         uint64_t* __restrict__ v, const uint64_t m,
+                                                         uint64_t* __restrict__ sums) {
+  if (!hdr->permuted) return;
   const uint64_t i0 = uint64_t(blockIdx.x) * kPlanPerBlock + uint64_t(threadIdx.x) * kPlanPerThread;
   uint64_t c[kPlanPerThread];
   uint64_t t = 0;
@@ -346,26 +459,42 @@ __global__ __launch_bounds__(kThreads) void k_scan_apply(uint64_t* __restrict__ 
     t += c[j];
   }
   uint64_t total;
-  uint64_t run = sums[blockIdx.x] + block_exclusive_scan(t, &total);
+  uint64_t run = block_exclusive_scan(t, &total);
 #pragma unroll
   for (int j = 0; j < kPlanPerThread; ++j) {
     if (i0 + j < m) v[i0 + j] = run;
     run += c[j];
   }
+  if (threadIdx.x == 0) sums[blockIdx.x] = total;
 }
 
-// Fragment i goes to its bucket's start plus its rank.
+// Fragment i goes to its bucket's start plus its rank: the bucket's offset
+// inside its block of 1024 buckets, plus the totals of the blocks before it
+// (scanned here into LDS; nbk <= 2^18, so at most 256 blocks).
+constexpr uint64_t kMaxBucketBlocks = kThreads;
+
 __global__ __launch_bounds__(kThreads) void k_bucket_scatter(const tc_fragment* __restrict__ frags,
-                                                            const int64_t n, const int shift,
+                                                            const int64_t n,
+                                                            const PlanHeader* __restrict__ hdr,
                                                             const uint64_t nbk,
                                                             const uint64_t* __restrict__ off,
+                                                            const uint64_t* __restrict__ sums,
                                                             const uint64_t* __restrict__ rank,
                                                             tc_fragment* __restrict__ sorted,
                                                             uint64_t* __restrict__ perm) {
+  __shared__ uint64_t base[kMaxBucketBlocks];
+  if (!hdr->permuted) return;
+  const int shift = int(hdr->shift);
+  const uint64_t nsb = (nbk + kPlanPerBlock - 1) / kPlanPerBlock;
+  uint64_t total;
+  const uint64_t ex = block_exclusive_scan(threadIdx.x < nsb ? sums[threadIdx.x] : 0, &total);
+  if (threadIdx.x < nsb) base[threadIdx.x] = ex;
+  __syncthreads();
   for (int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x; i < n;
        i += int64_t(gridDim.x) * kThreads) {
     const tc_fragment f = frags[i];
-    const uint64_t pos = off[bucket_of(f.dst_off, shift, nbk)] + rank[i];
+    const uint64_t b = bucket_of(f.dst_off, shift, nbk);
+    const uint64_t pos = base[b / kPlanPerBlock] + off[b] + rank[i];
     sorted[pos] = f;
     perm[pos] = uint64_t(i);
   }
@@ -434,8 +563,13 @@ size_t frag_workspace_min_bytes(int64_t n) {
   return kTasksOffset + task_area_bytes(size_t(n) + 1) + plan_tail_bytes(n) + 256;
 }
 
-hipError_t launch_plan_count(const tc_fragment* frags, int64_t n, uint64_t piece, uint64_t cut, void* ws,
-                             const PlanLayout& L, bool permuted, hipStream_t s) {
+// Workgroups of the expansion: one per window of a plan that fills the
+// workspace, at most this many (the rest stride).  Surplus workgroups read
+// the header and return.
+constexpr uint64_t kExpandGridCap = 16384;
+
+hipError_t launch_plan(const tc_fragment* frags, int64_t n, void* ws, const PlanLayout& L,
+                       hipStream_t s) {
   uint8_t* base = static_cast<uint8_t*>(ws);
   PlanHeader* hdr = reinterpret_cast<PlanHeader*>(base);
   uint64_t* tstart = reinterpret_cast<uint64_t*>(base + L.tstart);
@@ -444,54 +578,53 @@ hipError_t launch_plan_count(const tc_fragment* frags, int64_t n, uint64_t piece
   uint64_t* blen = bcnt + nb;
   uint64_t* bunord = blen + nb;
   uint64_t* bdend = bunord + nb;
-  hipLaunchKernelGGL(k_plan_count, dim3((unsigned)nb), dim3(kThreads), 0, s, frags, n, piece, cut, bcnt,
-                     blen, bunord, bdend);
-  hipLaunchKernelGGL(k_plan_scan, dim3(1), dim3(kThreads), 0, s, bcnt, (const uint64_t*)blen,
-                     (const uint64_t*)bunord, (const uint64_t*)bdend, nb, piece, cut, n,
-                     uint64_t(L.capacity), uint64_t(permuted ? 1 : 0), hdr, tstart + n);
-  hipLaunchKernelGGL(k_plan_tstart, dim3((unsigned)nb), dim3(kThreads), 0, s, frags, n, piece, cut,
-                     (const uint64_t*)bcnt, tstart, reinterpret_cast<int64_t*>(base + L.windows),
-                     uint64_t(L.capacity));
-  return hipGetLastError();
-}
-
-hipError_t launch_plan_reorder(const tc_fragment* frags, int64_t n, int shift, void* ws,
-                               const PlanLayout& L, hipStream_t s) {
-  if (n == 0 || L.nbuckets == 0) return hipSuccess;
-  uint8_t* base = static_cast<uint8_t*>(ws);
-  uint64_t* cnt = reinterpret_cast<uint64_t*>(base + L.buckets);
-  uint64_t* sums = reinterpret_cast<uint64_t*>(base + L.bucket_sums);
-  tc_fragment* sorted = reinterpret_cast<tc_fragment*>(base + L.sorted);
-  uint64_t* perm = reinterpret_cast<uint64_t*>(base + L.perm);
-  // ranks live in tstart's room, which the recount after the reorder rewrites
-  uint64_t* rank = reinterpret_cast<uint64_t*>(base + L.tstart);
+  int64_t* windows = reinterpret_cast<int64_t*>(base + L.windows);
+  // the reordered list (only in layouts with buckets)
+  const tc_fragment* sorted = L.nbuckets ? reinterpret_cast<const tc_fragment*>(base + L.sorted) : frags;
+  uint64_t* cnt = L.nbuckets ? reinterpret_cast<uint64_t*>(base + L.buckets) : nullptr;
   const uint64_t nbk = L.nbuckets;
-  const uint64_t sblocks = (nbk + kPlanPerBlock - 1) / kPlanPerBlock;
-  const unsigned fgrid = grid_for((uint64_t(n) + kThreads - 1) / kThreads);
-  hipLaunchKernelGGL(k_fill_zero, dim3(grid_for((nbk + kThreads - 1) / kThreads)), dim3(kThreads),
-                     0, s, cnt, nbk);
-  hipLaunchKernelGGL(k_bucket_hist, dim3(fgrid), dim3(kThreads), 0, s, frags, n, shift, nbk, cnt,
-                     rank);
-  hipLaunchKernelGGL(k_scan_sums, dim3((unsigned)sblocks), dim3(kThreads), 0, s,
-                     (const uint64_t*)cnt, nbk, sums);
-  hipLaunchKernelGGL(k_scan_one, dim3(1), dim3(kThreads), 0, s, sums, sblocks);
-  hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)sblocks), dim3(kThreads), 0, s, cnt, nbk,
-                     (const uint64_t*)sums);
-  hipLaunchKernelGGL(k_bucket_scatter, dim3(fgrid), dim3(kThreads), 0, s, frags, n, shift, nbk,
-                     (const uint64_t*)cnt, (const uint64_t*)rank, sorted, perm);
-  return hipGetLastError();
-}
-
-hipError_t launch_plan_expand(const tc_fragment* frags, uint64_t total, uint64_t piece, uint64_t cut,
-                              void* ws, const PlanLayout& L, hipStream_t s) {
-  if (total == 0) return hipSuccess;
-  uint8_t* base = static_cast<uint8_t*>(ws);
-  const uint64_t* tstart = reinterpret_cast<const uint64_t*>(base + L.tstart);
-  Task* tasks = reinterpret_cast<Task*>(base + kTasksOffset);
-  const uint64_t grid = (total + kExpandPerBlock - 1) / kExpandPerBlock;
-  const int64_t* windows = reinterpret_cast<const int64_t*>(base + L.windows);
-  hipLaunchKernelGGL(k_plan_expand, dim3((unsigned)grid), dim3(kThreads), 0, s, frags, tstart,
-                     windows, total, piece, cut, tasks);
+  const uint64_t cap = uint64_t(L.capacity);
+  const PlanHeader* ch = hdr;
+  // 1. count with 1 KiB pieces and the line cut (and clear the bucket
+  //    counters); totals and decisions
+  hipLaunchKernelGGL(k_plan_count, dim3((unsigned)nb), dim3(kThreads), 0, s, frags, sorted, n, 0, ch,
+                     bcnt, blen, bunord, bdend, cnt, nbk);
+  hipLaunchKernelGGL(k_plan_scan, dim3(1), dim3(kThreads), 0, s, (const uint64_t*)bcnt,
+                     (const uint64_t*)blen, (const uint64_t*)bunord, (const uint64_t*)bdend, nb, n, cap,
+                     nbk, hdr);
+  // 2. destination order for long unordered lists (each pass checks the header)
+  if (nbk) {
+    static_assert((uint64_t(1) << 18) <= kMaxBucketBlocks * kPlanPerBlock, "bucket blocks fit the scatter's LDS");
+    uint64_t* sums = reinterpret_cast<uint64_t*>(base + L.bucket_sums);
+    tc_fragment* sorted_w = reinterpret_cast<tc_fragment*>(base + L.sorted);
+    uint64_t* perm = reinterpret_cast<uint64_t*>(base + L.perm);
+    // ranks live in tstart's room, which tstart rewrites after the reorder
+    uint64_t* rank = tstart;
+    const uint64_t sblocks = (nbk + kPlanPerBlock - 1) / kPlanPerBlock;
+    const unsigned fgrid = grid_for((uint64_t(n) + kThreads - 1) / kThreads);
+    hipLaunchKernelGGL(k_bucket_hist, dim3(fgrid), dim3(kThreads), 0, s, frags, n, ch, nbk, cnt, rank);
+    hipLaunchKernelGGL(k_bucket_scan, dim3((unsigned)sblocks), dim3(kThreads), 0, s, ch, cnt, nbk, sums);
+    hipLaunchKernelGGL(k_bucket_scatter, dim3(fgrid), dim3(kThreads), 0, s, frags, n, ch, nbk,
+                       (const uint64_t*)cnt, (const uint64_t*)sums, (const uint64_t*)rank, sorted_w, perm);
+  }
+  // 3. count again (a reordered list, or a larger piece), only if the header asks
+  hipLaunchKernelGGL(k_plan_count, dim3((unsigned)nb), dim3(kThreads), 0, s, frags, sorted, n, 1, ch,
+                     bcnt, blen, bunord, bdend, (uint64_t*)nullptr, uint64_t(0));
+  // 4. per-fragment first tasks and windows (long lists read a prefix of the
+  //    block counts; blen is free by then), then the task table
+  uint64_t* boff = nullptr;
+  if (nb > kPrefixBlocks) {
+    boff = blen;
+    hipLaunchKernelGGL(k_plan_offsets, dim3(1), dim3(kThreads), 0, s, (const uint64_t*)bcnt, boff, nb,
+                       cap, hdr);
+  }
+  hipLaunchKernelGGL(k_plan_tstart, dim3((unsigned)nb), dim3(kThreads), 0, s, frags, sorted, n, nb, hdr,
+                     (const uint64_t*)bcnt, (const uint64_t*)boff, cap, tstart, windows);
+  const uint64_t wins = (cap + kExpandPerBlock - 1) / kExpandPerBlock;
+  const uint64_t egrid = wins < kExpandGridCap ? wins : kExpandGridCap;
+  hipLaunchKernelGGL(k_plan_expand, dim3((unsigned)(egrid ? egrid : 1)), dim3(kThreads), 0, s, frags,
+                     sorted, (const uint64_t*)tstart, (const int64_t*)windows, ch,
+                     reinterpret_cast<Task*>(base + kTasksOffset));
   return hipGetLastError();
 }
 

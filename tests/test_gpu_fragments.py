@@ -424,3 +424,29 @@ def test_fragment_longer_than_4gib_beyond_4gib():
     assert np.array_equal(_host(dd).view(np.uint64).reshape(3, 2), want)
     del src, dst
     torch.cuda.empty_cache()
+
+
+def test_plan_of_more_than_16m_fragments():
+    """A list longer than 16,384 count blocks (17M fragments of 64 bytes,
+    destinations unordered): the plan takes the block prefix from its own
+    offsets pass and reorders the list; the asynchronous one-call copy, a
+    planned copy and the plan's task count against the oracle."""
+    n = 17_000_000
+    pool = 2 << 30
+    print(f"case: {n} fragments of 64 B in 2 GiB pools", flush=True)
+    frags = synth.fragment_storm(n, pool, seed=77, lo=64, hi=64)
+    src = _rand_bytes(pool, 78)
+    fr = torch.from_numpy(frags.view(np.int64)).to(DEV)
+    ws = torch.empty(tc.tc_copy_fragments_workspace(n), dtype=torch.uint8, device=DEV)
+    dst = torch.full((pool,), 0x5A, dtype=torch.uint8, device=DEV)
+    tc.tc_copy_fragments(src, dst, fr, ws)
+    total = tc.tc_plan_status(ws)
+    assert total == n                                  # 64 B plus a line offset fit one piece
+    assert _header_word(ws, 7) == 1                    # reordered
+    dst2 = torch.full_like(dst, 0x5A)
+    tc.tc_copy_planned(src, dst2, ws, total)
+    torch.cuda.synchronize()
+    want = np.full(pool, 0x5A, dtype=np.uint8)
+    oracle.copy_fragments(_host(src), want, frags)
+    assert np.array_equal(_host(dst), want)
+    assert np.array_equal(_host(dst2), want)

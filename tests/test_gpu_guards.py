@@ -135,8 +135,10 @@ def test_cast_and_dequant_guards():
 def test_plan_refuses_offsets_past_48_bits(side):
     """A task holds 48-bit offsets, so a non-empty fragment ending past 2^48
     is refused by the plan's count pass on the device, with validation off,
-    and nothing is copied.  A fragment ending exactly at 2^48 is planned (the
-    plan only reads descriptors; it is not copied here)."""
+    and nothing is copied: tc_plan_fragments returns the error, and the
+    asynchronous tc_copy_fragments copies nothing and leaves the error in the
+    plan, where tc_plan_status reads it.  A fragment ending exactly at 2^48
+    is planned (the plan only reads descriptors; it is not copied here)."""
     assert not tc.tc_get_validate()
     lim = 1 << 48
     ok = np.array([[0, 0, 4096], [8192, 4096, 100]], dtype=np.uint64)
@@ -154,9 +156,11 @@ def test_plan_refuses_offsets_past_48_bits(side):
     with pytest.raises(tc.TcError) as e:
         tc.tc_plan_fragments(fr, ws)
     assert e.value.status == 2
+    tc.tc_copy_fragments(src, dst, fr, ws)       # enqueued; the plan fails on the device
     with pytest.raises(tc.TcError) as e:
-        tc.tc_copy_fragments(src, dst, fr, ws)
+        tc.tc_plan_status(ws)
     assert e.value.status == 2
+    tc.tc_copy_planned(src, dst, ws, None)        # a failed plan copies nothing
     torch.cuda.synchronize()
     assert bool((dst == 0x33).all())
     _guards_intact(whole, 1 << 16)

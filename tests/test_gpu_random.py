@@ -53,6 +53,12 @@ def test_random_fragment_lists(seed, n, align, small_ws):
     tc.tc_digest_planned(dst, tc.DIGEST_DST, ws, total, n, dg_dst)
     again = torch.full_like(dst, 0x5A)
     tc.tc_copy_planned(src, again, ws, total)
+    # the asynchronous one-call copy on a workspace of the same size: its plan
+    # (piece, reordering) is decided on the device and the copy reads the count
+    ws2 = torch.empty(ws_bytes, dtype=torch.uint8, device=DEV)
+    third = torch.full_like(dst, 0x5A)
+    tc.tc_copy_fragments(src, third, fr, ws2)
+    assert tc.tc_plan_status(ws2) == total
     torch.cuda.synchronize()
     hsrc = _host(src)
     want = np.full(dp, 0x5A, dtype=np.uint8)
@@ -60,6 +66,7 @@ def test_random_fragment_lists(seed, n, align, small_ws):
     got = _host(dst)
     assert np.array_equal(got, want), f"{int((got != want).sum())} bytes differ"
     assert np.array_equal(_host(again), want)
+    assert np.array_equal(_host(third), want)
     wd = oracle.fragment_digests(hsrc, frags, use_src=True)
     assert np.array_equal(_host(dg).view(np.uint64).reshape(n, 2), wd)
     assert np.array_equal(_host(dg_dst).view(np.uint64).reshape(n, 2),

@@ -2,11 +2,13 @@
 
 Each call runs on a side stream right behind a device fill that produces its
 input on that same stream, so a call that ignored its stream argument would
-read stale bytes.  The calls that do no host-side staging or synchronization
-(block gather/scatter, planned copies with and without digests, the scaled
-cast) are also captured into a HIP graph and replayed several times, with the
-input changed eagerly between replays; every replay is checked against the
-oracle.
+read stale bytes.  Every call that only enqueues kernels (block
+gather/scatter, the asynchronous plan, the one-call fragment copy, planned
+copies with and without digests, the block-scaled cast and its inverse in
+their one-call and planned forms, the scaled cast) is also captured into a
+HIP graph and replayed several times, with the input changed eagerly between
+replays and the host item tables overwritten after the capture; every replay
+is checked against the oracle.
 """
 import numpy as np
 import pytest
@@ -64,6 +66,16 @@ def test_side_stream_ordering():
                           oracle.fragment_digests(hf, frags_np))
 
 
+def _cast_items(rows, cols):
+    """Two items over one ragged matrix: the top 256 rows (full tiles plus a
+    partial right edge) and the rest (partial bottom tiles)."""
+    tcn = (cols + 127) // 128
+    items = np.zeros(2, dtype=tc.CAST_ITEM_DTYPE)
+    items[0] = (0, 256, cols, cols, 0, cols, 0, tcn)
+    items[1] = (256 * cols, rows - 256, cols, cols, 256 * cols, cols, 2 * tcn, tcn)
+    return items
+
+
 def test_graph_capture_and_replay():
     R, nb, B = 4, 256, 8192
     ids_np = synth.ids_without_replacement(nb, 100, seed=65)
@@ -71,16 +83,37 @@ def test_graph_capture_and_replay():
     src_flat, src = _pool(R, nb, B)
     dst_flat, dst = _pool(R, nb, B)
     buf = torch.empty(100 * R * B, dtype=torch.uint8, device=DEV)
-    frags_np = synth.fragment_storm(1000, 16 << 20, seed=66)
+    pool = 64 << 20
+    frags_np = synth.fragment_storm(5000, pool, seed=66)      # unordered: a reordered plan
     frags = torch.from_numpy(frags_np.view(np.int64)).to(DEV)
-    fsrc = torch.empty(16 << 20, dtype=torch.uint8, device=DEV)
-    fdst = torch.zeros(16 << 20, dtype=torch.uint8, device=DEV)
-    ws = torch.empty(tc.tc_copy_fragments_workspace(len(frags_np)), dtype=torch.uint8, device=DEV)
-    dg = torch.empty(2 * len(frags_np), dtype=torch.int64, device=DEV)
+    fsrc = torch.empty(pool, dtype=torch.uint8, device=DEV)
+    fdst = torch.zeros(pool, dtype=torch.uint8, device=DEV)
+    fdst2 = torch.zeros_like(fdst)
+    fdst3 = torch.zeros_like(fdst)
+    n = len(frags_np)
+    wsb = tc.tc_copy_fragments_workspace(n)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=DEV)
+    ws2 = torch.empty(wsb, dtype=torch.uint8, device=DEV)
+    ws3 = torch.empty(tc.tc_copy_fragments_workspace_min(n), dtype=torch.uint8, device=DEV)
+    dg = torch.empty(2 * n, dtype=torch.int64, device=DEV)
     x = torch.empty(65536 + 77, dtype=torch.bfloat16, device=DEV)
     q = torch.empty(x.numel(), dtype=torch.uint8, device=DEV)
+    # block-scaled cast of a ragged matrix (one-call and planned) and its inverse
+    rows, cols = 300, 520
+    tcn = (cols + 127) // 128
+    items = _cast_items(rows, cols)
+    xc = torch.empty(rows * cols, dtype=torch.bfloat16, device=DEV)
+    qc = torch.empty(rows * cols, dtype=torch.uint8, device=DEV)
+    sc = torch.empty(3 * tcn, dtype=torch.float32, device=DEV)
+    qp = torch.empty_like(qc)
+    sp = torch.empty_like(sc)
+    yc = torch.empty(rows * cols, dtype=torch.bfloat16, device=DEV)
+    cws = torch.empty(tc.tc_cast_fp8_workspace(2), dtype=torch.uint8, device=DEV)
+    pws = torch.empty_like(cws)
+    dws = torch.empty(tc.tc_dequant_fp8_workspace(2), dtype=torch.uint8, device=DEV)
+    ditems = items.astype(tc.DEQUANT_ITEM_DTYPE)       # same geometry, codes -> bf16
     total = tc.tc_plan_fragments(frags, ws)
-    n = len(frags_np)
+    plan = tc.tc_cast_fp8_prepare(xc, qp, items, pws)    # prepared eagerly, launched in the graph
     torch.cuda.synchronize()
 
     g = torch.cuda.CUDAGraph()
@@ -92,17 +125,35 @@ def test_graph_capture_and_replay():
             tc.tc_scatter_blocks(dst, nb, B, B, ids, buf, stream=s)
             tc.tc_copy_planned_digest(fsrc, fdst, ws, total, n, dg, stream=s)
             tc.tc_copy_planned(fsrc, fdst, ws, total, stream=s)
+            tc.tc_copy_fragments(fsrc, fdst2, frags, ws2, stream=s)
+            tc.tc_plan_fragments_async(frags, ws3, stream=s)     # the smallest workspace: larger pieces
+            tc.tc_copy_planned(fsrc, fdst3, ws3, None, stream=s)
             tc.tc_cast_fp8_scaled(x, 0.25, q, stream=s)
+            tc.tc_cast_fp8_blockscaled(xc, qc, sc, items, cws, stream=s)
+            tc.tc_cast_fp8_planned(xc, qp, sp, pws, plan, stream=s)
+            tc.tc_dequant_fp8_blockscaled(qc, sc, yc, ditems, dws, stream=s)
     torch.cuda.synchronize()
+    # the graph holds its own copy of the item tables
+    items[:] = np.zeros(1, dtype=tc.CAST_ITEM_DTYPE)
+    ditems[:] = np.zeros(1, dtype=tc.DEQUANT_ITEM_DTYPE)
+    want_items = _cast_items(rows, cols)
 
     for rep in range(4):
         # new inputs, written eagerly between replays
         src_flat.copy_(synth.random_bytes(src_flat.numel(), 70 + rep, device=DEV))
         fsrc.copy_(synth.random_bytes(fsrc.numel(), 80 + rep, device=DEV))
         x.copy_(synth.bf16_normal(x.numel(), 1.0, 90 + rep, device=DEV))
+        xc.copy_(synth.bf16_normal(xc.numel(), 0.02 * (rep + 1), 95 + rep, device=DEV))
         dst_flat.zero_()
         fdst.zero_()
+        fdst2.zero_()
+        fdst3.zero_()
         dg.fill_(-1)
+        for t in (qc, qp):
+            t.fill_(0xEE)
+        for t in (sc, sp):
+            t.fill_(-1.0)
+        yc.zero_()
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
@@ -113,13 +164,27 @@ def test_graph_capture_and_replay():
         oracle.scatter_blocks(hd, B, B, ids_np, want.reshape(-1))
         assert np.array_equal(dst_flat.cpu().numpy(), np.concatenate(hd)), rep
         hf = fsrc.cpu().numpy()
-        wf = np.zeros(16 << 20, np.uint8)
+        wf = np.zeros(pool, np.uint8)
         oracle.copy_fragments(hf, wf, frags_np)
         assert np.array_equal(fdst.cpu().numpy(), wf), rep
+        assert np.array_equal(fdst2.cpu().numpy(), wf), rep
+        assert np.array_equal(fdst3.cpu().numpy(), wf), rep
         assert np.array_equal(dg.cpu().numpy().view(np.uint64).reshape(-1, 2),
                               oracle.fragment_digests(hf, frags_np)), rep
         xb = x.view(torch.int16).cpu().numpy().view(np.uint16)
         assert np.array_equal(q.cpu().numpy(), oracle.cast_fp8_scaled(xb, 0.25)), rep
+        xcb = xc.view(torch.int16).cpu().numpy().view(np.uint16).reshape(rows, cols)
+        wq_top, ws_top = oracle.cast_fp8_blockscaled(xcb[:256])
+        wq_bot, ws_bot = oracle.cast_fp8_blockscaled(xcb[256:])
+        wq = np.concatenate([wq_top, wq_bot])
+        wsc = np.concatenate([ws_top.reshape(-1), ws_bot.reshape(-1)])
+        for qq, ss in ((qc, sc), (qp, sp)):
+            assert np.array_equal(qq.cpu().numpy().reshape(rows, cols), wq), rep
+            assert np.array_equal(ss.cpu().numpy().view(np.uint32), wsc.view(np.uint32)), rep
+        wy = np.concatenate([oracle.dequant_fp8_blockscaled(wq_top, ws_top),
+                             oracle.dequant_fp8_blockscaled(wq_bot, ws_bot)])
+        assert np.array_equal(yc.view(torch.int16).cpu().numpy().view(np.uint16).reshape(rows, cols), wy), rep
+    assert want_items.tobytes() != items.tobytes()
 
 
 def test_concurrent_streams_independent_plans():
@@ -166,9 +231,9 @@ def test_concurrent_streams_independent_plans():
 
 def test_two_host_threads_cast_at_once():
     """Two host threads, each on its own stream, cast different item sets
-    at the same time, over and over: the item tables of both pass through the
-    library's one pinned staging buffer per device, so a call must not
-    overwrite it while the other's copy out of it is still in flight.  Every
+    at the same time, over and over, each with its own workspace: nothing of
+    one call's item table may leak into the other's (the tables travel in
+    the launches' arguments; the library holds no shared buffer).  Every
     result against the oracle."""
     import threading
     rng = np.random.default_rng(131)

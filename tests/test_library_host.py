@@ -148,6 +148,58 @@ def test_argument_errors_need_no_gpu(lib):
                                           16, None) == 5
 
 
+def test_new_entry_points_check_arguments_without_a_gpu(lib):
+    """The asynchronous planning, prepared casts and IPC calls refuse bad
+    arguments on the host, before anything is enqueued."""
+    P = ctypes.c_void_p
+    U64 = ctypes.c_uint64
+    # planning without waiting: the same argument checks as tc_plan_fragments
+    assert lib.tc_plan_fragments_async(P(16), -1, P(4096), 1 << 20, None) == 1
+    assert lib.tc_plan_fragments_async(P(16), 10, P(4100), 1 << 20, None) == 1   # misaligned
+    assert lib.tc_plan_fragments_async(P(16), 10, P(4096), 8, None) == 5        # too small
+    assert lib.tc_plan_fragments_async(None, 0, None, 0, None) == 0
+    assert lib.tc_plan_status(None, 1 << 20, None, None) == 1
+    assert lib.tc_plan_status(P(4100), 1 << 20, None, None) == 1
+    # a copy that takes its count from the plan still needs a task table
+    assert lib.tc_copy_planned(P(16), P(16), P(4096), 100, U64((1 << 64) - 1), None) == 5
+    assert lib.tc_copy_planned(None, P(16), P(4096), 1 << 20, U64((1 << 64) - 1), None) == 1
+    # prepared casts
+    plan = tc.TilePlan()
+    item = np.zeros(1, dtype=tc.CAST_ITEM_DTYPE)
+    item[0] = (0, 128, 128, 128, 0, 128, 0, 1)
+    it = item.ctypes.data
+    assert lib.tc_cast_fp8_prepare(P(16), P(16), it, 1, 128, P(4096), 1 << 20, None, None) == 1
+    assert lib.tc_cast_fp8_prepare(P(16), P(16), it, 1, 64, P(4096), 1 << 20, ctypes.byref(plan), None) == 1
+    assert lib.tc_cast_fp8_prepare(P(16), P(16), it, 1, 128, P(4096), 64, ctypes.byref(plan), None) == 5
+    assert lib.tc_cast_fp8_prepare(P(17), P(16), it, 1, 128, P(4096), 1 << 20, ctypes.byref(plan), None) == 1
+    bad = item.copy()
+    bad[0]["src_ld"] = 100                                   # row stride below the width
+    assert lib.tc_cast_fp8_prepare(P(16), P(16), bad.ctypes.data, 1, 128, P(4096), 1 << 20,
+                                   ctypes.byref(plan), None) == 1
+    assert lib.tc_dequant_fp8_prepare(P(16), P(17), it, 1, 128, P(4096), 1 << 20, ctypes.byref(plan), None) == 1
+    # a plan made for 16-byte-aligned bases refuses bases of another alignment
+    plan = tc.TilePlan(1, 1, 0, 0, 0)
+    assert lib.tc_cast_fp8_planned(P(34), P(64), P(128), P(4096), 1 << 20, ctypes.byref(plan), None) == 1
+    assert lib.tc_cast_fp8_planned(P(32), P(64), P(130), P(4096), 1 << 20, ctypes.byref(plan), None) == 1
+    assert lib.tc_cast_fp8_planned(P(32), P(64), P(128), P(4096), 64, ctypes.byref(plan), None) == 5
+    assert lib.tc_cast_fp8_planned(P(32), P(64), P(128), P(4096), 1 << 20, None, None) == 1
+    empty = tc.TilePlan(0, 0, 0, 0, 0)
+    assert lib.tc_cast_fp8_planned(None, None, None, None, 0, ctypes.byref(empty), None) == 0
+    assert lib.tc_dequant_fp8_planned(P(34), P(128), P(64), P(4096), 1 << 20, ctypes.byref(plan), None) == 1
+    # IPC: null arguments, and handles that describe impossible ranges
+    h = tc._IpcHandle()
+    out = ctypes.c_void_p(0)
+    assert lib.tc_ipc_export(None, 16, ctypes.byref(h)) == 1
+    assert lib.tc_ipc_export(P(4096), 16, None) == 1
+    assert lib.tc_ipc_open(None, ctypes.byref(out)) == 1
+    h.alloc_bytes = 1 << 31                                  # allocations of 2 GiB or more are refused
+    assert lib.tc_ipc_open(ctypes.byref(h), ctypes.byref(out)) == 1
+    h.alloc_bytes, h.offset, h.bytes = 4096, 4000, 200       # a range past its allocation
+    assert lib.tc_ipc_open(ctypes.byref(h), ctypes.byref(out)) == 1
+    assert lib.tc_ipc_close(None, P(4096)) == 1
+    assert tc.IPC_HANDLE_BYTES == 88
+
+
 def test_binding_refuses_wrong_dtypes_before_any_call(lib):
     """Dtype checks in the binding run before a device address is taken, so
     they need no GPU: ids must be int32 (the library reads 4-byte ids),
