@@ -406,6 +406,22 @@ tc_status tc_cast_fp8_planned(const void* src_base, void* dst_base, float* scale
                               const void* workspace, size_t workspace_bytes,
                               const tc_tile_plan* plan /* host */, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * tc_cast_fp8_blockscaled without a workspace.  The tile table lives in a
+ * fixed array of device memory that the library holds on each device it
+ * runs on, 332,288 bytes, until the process ends; nothing is allocated, on
+ * the device or the host.  At most TC_NOALLOC_MAX_ITEMS items: more is
+ * TC_ERR_WORKSPACE, before anything is enqueued.  Validation mode does not
+ * apply (its checks need host memory).  Every call on one device rewrites
+ * that device's array, so two calls that overlap in time on one device race:
+ * serialize them (for example, issue them on one stream).  Other arguments
+ * and errors as for tc_cast_fp8_blockscaled. */
+#define TC_NOALLOC_MAX_ITEMS 4096
+tc_status tc_cast_fp8_blockscaled_noalloc(const void* src_base, void* dst_base, float* scale_base,
+                                          const tc_cast_item* items /* host */, int64_t n_items,
+                                          int32_t tile, hipStream_t stream);
+
 /* q[i] = E4M3(RN_f32(bf16(src[i]) / scale)) for i < n, one given scale (no
  * amax).  Quotients that overflow saturate; NaN gives 0x7F. */
 tc_status tc_cast_fp8_scaled(const void* src_bf16, int64_t n, float scale, void* dst_e4m3,

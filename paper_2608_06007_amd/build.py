@@ -13,7 +13,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libtchip.so")
 SOURCES = ["tc_blocks.hip", "tc_plan.hip", "tc_copy.hip", "tc_cast.hip", "tc_dequant.hip", "tc_api.cpp",
-           "tc_stage.cpp", "tc_ipc.cpp"]
+           "tc_stage.cpp", "tc_ipc.cpp", "tc_noalloc.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
