@@ -471,6 +471,32 @@ def run_storm(torch, tc, synth, args, stream):
     return out
 
 
+def run_storm_bytes(torch, tc, synth, args, stream):
+    """The storm's byte-granular variant: lengths and offsets at byte
+    granularity, so source and destination differ mod 16 for 15 fragments in
+    16 (copied with realigned 16-byte vectors).  Reported, no bar."""
+    pool = 16 << 30
+    frags_np = synth.fragment_storm(1_000_000, pool, seed=synth.SEED_STORM, align=1)
+    _log(f"[storm_bytes] 1,000,000 byte-granular fragments, {frags_np[:, 2].sum() / 1e9:.2f} GB payload")
+    src = synth.random_bytes(pool, synth.SEED_STORM, device="cuda")
+    dst = torch.empty(pool, dtype=torch.uint8, device="cuda")
+    frags = torch.from_numpy(frags_np.view(np.int64)).cuda()
+    ws = torch.empty(tc.tc_copy_fragments_workspace(len(frags_np)), dtype=torch.uint8, device="cuda")
+    nbytes = 2 * int(frags_np[:, 2].sum())
+    total = tc.tc_plan_fragments(frags, ws, stream=stream)
+    planned = _time_calls(torch, stream, lambda: tc.tc_copy_planned(src, dst, ws, total, stream=stream),
+                          args.warmup, args.cast_steps)
+    ms = _time_calls(torch, stream, lambda: tc.tc_copy_fragments(src, dst, frags, ws, stream=stream),
+                     args.warmup, args.cast_steps)
+    congruent = int(((frags_np[:, 0] - frags_np[:, 1]) % 16 == 0).sum())
+    out = {"fragments": 1_000_000, "payload_bytes": int(frags_np[:, 2].sum()), "tasks": int(total),
+           "congruent_mod16": congruent, "copy_planned": _stats(planned, nbytes),
+           "plan_and_copy": _stats(ms, nbytes), "descriptors_sha256": synth.sha256(frags_np)}
+    del src, dst, frags, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def run_moe(torch, tc, synth, args, stream):
     n_exp, e_bytes = 256, 7168 * 2048
     frags_np, _ = synth.moe_permutation(n_exp, e_bytes, seed=synth.SEED_STORM)
@@ -688,7 +714,7 @@ def run_calib(torch, tc, synth, args, stream):
 
 RUNNERS = {"reshard": run_reshard, "reshard_tp8_tp4": run_reshard44, "cast": run_cast,
            "reshard_cast": run_reshard_cast,
-           "storm": run_storm, "moe": run_moe, "stage": run_stage, "calib": run_calib, "ipc": run_ipc}
+           "storm": run_storm, "storm_bytes": run_storm_bytes, "moe": run_moe, "stage": run_stage, "calib": run_calib, "ipc": run_ipc}
 
 
 def main():
@@ -699,7 +725,8 @@ def main():
     ap.add_argument("--cast-steps", type=int, default=20, help="timed launches per extra workload")
     # the host staging workload ("stage") runs only when named: it launches the
     # block kernels once per chunk, which would mix into their profiles
-    ap.add_argument("--workloads", default="kv,reshard,reshard_tp8_tp4,cast,reshard_cast,storm,moe,ipc,calib")
+    ap.add_argument("--workloads",
+                    default="kv,reshard,reshard_tp8_tp4,cast,reshard_cast,storm,storm_bytes,moe,ipc,calib")
     ap.add_argument("--skip-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--ipc-role", choices=["export", "import"], help=argparse.SUPPRESS)
     ap.add_argument("--ipc-handle", help=argparse.SUPPRESS)

@@ -36,14 +36,18 @@ __global__ __launch_bounds__(kThreads) void k_blocks_vec(const RegionTable tab, 
   }
 }
 
-// Byte-granular variant for pools whose bases, stride or block size are not
-// 16-byte multiples.
+// Pools whose bases, stride or block size are not 16-byte multiples: one
+// workgroup per (id, region) chunk, its waves taking 1 KiB runs in turn, each
+// copied at vector width whatever the alignment of its two ends.
 template <bool kGather>
 __global__ __launch_bounds__(kThreads) void k_blocks_bytes(const RegionTable tab, const int32_t R,
                                                           const int64_t B, const int64_t stride,
                                                           const int32_t* __restrict__ ids,
                                                           const uint64_t n_chunks,
                                                           uint8_t* __restrict__ buf) {
+  const int lane = threadIdx.x & (kWaveLanes - 1);
+  const int64_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  constexpr int64_t kRun = int64_t(kWaveLanes) * 16;
   for (uint64_t c = blockIdx.x; c < n_chunks; c += gridDim.x) {
     const uint64_t i = c / uint64_t(R);
     const int32_t r = (int32_t)(c - i * uint64_t(R));
@@ -51,7 +55,13 @@ __global__ __launch_bounds__(kThreads) void k_blocks_bytes(const RegionTable tab
     uint8_t* xfer = buf + c * uint64_t(B);
     const uint8_t* from = kGather ? pool : xfer;
     uint8_t* to = kGather ? xfer : pool;
-    for (int64_t x = threadIdx.x; x < B; x += kThreads) to[x] = from[x];
+    for (int64_t o = w * kRun; o < B; o += (kThreads / kWaveLanes) * kRun) {
+      const uint64_t n = uint64_t(B - o < kRun ? B - o : kRun);
+      if (kGather)
+        wave_copy_any(from + o, to + o, n, lane, [](u32x4* p, u32x4 v) { st_sc1(p, v); });
+      else
+        wave_copy_any(from + o, to + o, n, lane, [](u32x4* p, u32x4 v) { st_sc1_nt(p, v); });
+    }
   }
 }
 

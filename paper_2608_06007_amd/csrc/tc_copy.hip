@@ -54,7 +54,8 @@ __global__ __launch_bounds__(kThreads) void k_copy_tasks(const uint8_t* __restri
       const uint64_t tail = len & 15;
       if (uint64_t(lane) < tail) d[(n16 << 4) + lane] = s[(n16 << 4) + lane];
     } else {
-      for (uint64_t i = lane; i < len; i += kWaveLanes) d[i] = s[i];
+      // source and destination differ mod 16: realigned 16-byte vectors
+      wave_copy_any(s, d, len, lane, [reordered](u32x4* p, u32x4 v) { st_task(p, v, reordered); });
     }
   }
 }
@@ -162,13 +163,18 @@ __device__ __forceinline__ void task_sums(const uint8_t* s, uint8_t* d, const ui
     const uint32_t ta = wave_sum32_lane63(a), tw = wave_sum32_lane63(ws);
     if (lane == kWaveLanes - 1) *slot = u64x2{ta, uint64_t(tw) + (dof + 1) * ta};
     return;
-  } else if (mis == 0) {
-    uint64_t head = (16 - (sa & 15)) & 15;
+  } else {
+    // Vectors aligned on the destination when copying (on the source when
+    // only reading); a copy whose source and destination differ mod 16
+    // assembles each vector from the two source vectors it straddles.
+    const uintptr_t anchor = kMode == kCopyDigest ? reinterpret_cast<uintptr_t>(d) : sa;
+    uint64_t head = (16 - (anchor & 15)) & 15;
     if (head > len) head = len;
     const uint64_t n16 = (len - head) >> 4;
     const uint64_t body_end = head + (n16 << 4);
     const uint64_t nchunks = n16 == 0 ? 1 : (n16 + kChunkVecs - 1) / kChunkVecs;
-    const u32x4* sv = reinterpret_cast<const u32x4*>(s + head);
+    const uint32_t r = mis ? uint32_t((sa + head) & 15) : 0;
+    const u32x4* sv = reinterpret_cast<const u32x4*>(s + head - r);
     u32x4* dv = kMode == kCopyDigest ? reinterpret_cast<u32x4*>(d + head) : nullptr;
     for (uint64_t c = 0; c < nchunks; ++c) {
       const uint64_t base = c == 0 ? 0 : head + (c << 12);
@@ -181,7 +187,7 @@ __device__ __forceinline__ void task_sums(const uint8_t* s, uint8_t* d, const ui
       }
       const uint64_t i_end = min(n16, (c + 1) * kChunkVecs);
       for (uint64_t i = c * kChunkVecs + lane; i < i_end; i += kWaveLanes) {
-        const u32x4 v = ld_nt(sv + i);
+        const u32x4 v = r ? realign(sv[i], sv[i + 1], r) : ld_nt(sv + i);
         if (kMode == kCopyDigest) st_task(dv + i, v, plain);
         uint32_t vs, vw;
         vec_sums(v, &vs, &vw);
@@ -193,22 +199,6 @@ __device__ __forceinline__ void task_sums(const uint8_t* s, uint8_t* d, const ui
         if (kMode == kCopyDigest) d[body_end + lane] = x;
         a += x;
         ws += uint32_t(body_end + lane - base) * x;
-      }
-      const uint64_t ca = wave_sum32(a), cw = wave_sum32(ws);
-      A += ca;
-      W += cw + base * ca;
-    }
-  } else {
-    const uint64_t nchunks = len == 0 ? 0 : (len + 4095) >> 12;
-    for (uint64_t c = 0; c < nchunks; ++c) {
-      const uint64_t base = c << 12;
-      const uint64_t i_end = min(len, base + 4096);
-      uint32_t a = 0, ws = 0;
-      for (uint64_t i = base + lane; i < i_end; i += kWaveLanes) {
-        const uint8_t x = s[i];
-        if (kMode == kCopyDigest) d[i] = x;
-        a += x;
-        ws += uint32_t(i - base) * x;
       }
       const uint64_t ca = wave_sum32(a), cw = wave_sum32(ws);
       A += ca;

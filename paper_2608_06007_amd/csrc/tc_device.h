@@ -88,6 +88,53 @@ __device__ __forceinline__ void st_task(u32x4* p, u32x4 v, bool plain) {
     st_sc1_nt(p, v);
 }
 
+// The 16 bytes that start r bytes (1..15) into the aligned vector a and run
+// on into the next aligned vector b: bytes r .. r + 15 of a || b.  r is
+// wave-uniform (one fragment per wave), so the word selection is a uniform
+// branch, and each output word is one v_alignbyte_b32 of two neighbours.
+__device__ __forceinline__ u32x4 realign(const u32x4 a, const u32x4 b, const uint32_t r) {
+  const uint32_t sh = r & 3;
+  uint32_t x0, x1, x2, x3, x4;
+  switch (r >> 2) {
+    case 0: x0 = a.x; x1 = a.y; x2 = a.z; x3 = a.w; x4 = b.x; break;
+    case 1: x0 = a.y; x1 = a.z; x2 = a.w; x3 = b.x; x4 = b.y; break;
+    case 2: x0 = a.z; x1 = a.w; x2 = b.x; x3 = b.y; x4 = b.z; break;
+    default: x0 = a.w; x1 = b.x; x2 = b.y; x3 = b.z; x4 = b.w; break;
+  }
+  return u32x4{__builtin_amdgcn_alignbyte(x1, x0, sh), __builtin_amdgcn_alignbyte(x2, x1, sh),
+               __builtin_amdgcn_alignbyte(x3, x2, sh), __builtin_amdgcn_alignbyte(x4, x3, sh)};
+}
+
+// One wave copies len bytes from s to d whatever their alignment: bytes up
+// to d's 16-byte alignment, then 16-byte vectors, then a byte tail.  When s
+// and d are congruent mod 16 each vector is one non-temporal load; otherwise
+// it is assembled from the two aligned source vectors it straddles (lane i's
+// second vector is lane i + 1's first, served by the cache).  Every aligned
+// source vector read holds at least one byte of the range, so no read leaves
+// the 16-byte granules the range touches.  store(p, v) writes one vector.
+template <typename Store>
+__device__ __forceinline__ void wave_copy_any(const uint8_t* s, uint8_t* d, uint64_t len, const int lane,
+                                              Store store) {
+  uint64_t head = (16 - (reinterpret_cast<uintptr_t>(d) & 15)) & 15;
+  if (head > len) head = len;
+  if (uint64_t(lane) < head) d[lane] = s[lane];
+  s += head;
+  d += head;
+  len -= head;
+  const uint64_t n16 = len >> 4;
+  u32x4* dv = reinterpret_cast<u32x4*>(d);
+  const uint32_t r = uint32_t(reinterpret_cast<uintptr_t>(s) & 15);
+  if (r == 0) {
+    const u32x4* sv = reinterpret_cast<const u32x4*>(s);
+    for (uint64_t i = lane; i < n16; i += kWaveLanes) store(dv + i, ld_nt(sv + i));
+  } else {
+    const u32x4* sv = reinterpret_cast<const u32x4*>(s - r);
+    for (uint64_t i = lane; i < n16; i += kWaveLanes) store(dv + i, realign(sv[i], sv[i + 1], r));
+  }
+  const uint64_t tail = len & 15;
+  if (uint64_t(lane) < tail) d[(n16 << 4) + lane] = s[(n16 << 4) + lane];
+}
+
 namespace {
 // p[0 .. n) = 0: a fill kernel rather than hipMemsetAsync, so the calls that
 // clear memory can be captured into a graph (digests with no task to run,
