@@ -225,10 +225,11 @@ def test_blockscaled_exhaustive_amax_and_value(part):
     print(f"A in [{a0:#x}, {a1:#x}): {checked / 1e6:.0f} M elements checked")
 
 
-@pytest.mark.parametrize("layers,ranks", [(2, [0, 3, 7])])
+@pytest.mark.parametrize("layers,ranks", [(2, [0, 7]), (10, [3])])
 def test_tp_shard_cast_70b_layers(layers, ranks):
     """70B-shaped layers (hidden 8192, 64 q / 8 kv heads, MLP 28672), N(0, 0.02),
-    cast into TP=8 shards, compared in full with the oracle."""
+    cast into TP=8 shards, compared in full with the oracle.  Ten layers make
+    70 items, so the kernel's item search takes its second round."""
     spec = synth.spec_70b(layers)
     n = synth.spec_elems(spec)
     stream = synth.bf16_normal(n, 0.02, synth.SEED_CAST_70B, device=DEV)
@@ -279,6 +280,23 @@ def _sampled_tiles_match_oracle(src, q, s, items, rng, count):
         assert got_s.view(np.uint32) == want_s.view(np.uint32)[0, 0]
 
 
+def _item_matches_oracle(src, q, hs, it):
+    """One cast item in full: the oracle's cast of a host copy of the item's
+    (strided) source rows against the GPU's codes and scale grid."""
+    rows, cols, ld = int(it["rows"]), int(it["cols"]), int(it["src_ld"])
+    so = int(it["src_off"])
+    x = src[so:so + (rows - 1) * ld + cols].as_strided((rows, cols), (ld, 1)).contiguous()
+    hx = _host(x.view(torch.int16)).view(np.uint16)
+    want_q, want_s = oracle.cast_fp8_blockscaled(hx)
+    dld, do = int(it["dst_ld"]), int(it["dst_off"])
+    got_q = q[do:do + (rows - 1) * dld + cols].as_strided((rows, cols), (dld, 1)).contiguous()
+    assert np.array_equal(_host(got_q), want_q), it
+    tr, tcn = want_s.shape
+    sld, sof = int(it["scale_ld"]), int(it["scale_off"])
+    got_s = np.lib.stride_tricks.as_strided(hs[sof:], shape=(tr, tcn), strides=(4 * sld, 4))
+    assert np.array_equal(got_s.view(np.uint32), want_s.view(np.uint32)), it
+
+
 def _every_tile_reaches_448(q, items):
     """The element with |x| = amax encodes to +-448 (0x7E / 0xFE): the
     largest code magnitude of every tile is 0x7E.  Item sizes here are
@@ -296,11 +314,12 @@ def test_tp_shard_cast_70b_full_size():
     """All 80 layers (136.9 GB of bf16 in HBM), rank 3 of TP=8: the shard
     slices hold N(0, 0.02) values and everything outside them is poisoned with
     a huge value, so a read outside the slice would change the scales.
-    Sampled tiles against the oracle; every scale is checked to be a normal
-    N(0, 0.02) tile scale (no poison), and every tile's largest code is +-448.
-    Then the inverse rule over the whole shard: sampled tiles against the
-    oracle, and every element within the E4M3 + bf16 rounding bound of its
-    source value."""
+    Every item against the oracle, codes and scale bits; every scale is
+    checked to be a normal N(0, 0.02) tile scale (no poison), and every tile's
+    largest code is +-448.
+    Then the inverse rule over the whole shard: every item against the
+    oracle's inverse of the GPU codes, and every element within the E4M3 +
+    bf16 rounding bound of its source value."""
     tp, rank = 8, 3
     spec = synth.spec_70b(80)
     n = synth.spec_elems(spec)
@@ -327,8 +346,13 @@ def test_tp_shard_cast_70b_full_size():
     # no poisoned tile: every scale is what an N(0, 0.02) tile gives
     assert bool(((s > 1e-5) & (s < 1e-3)).all())
     _every_tile_reaches_448(q, items)
-    rng = np.random.default_rng(55)
-    _sampled_tiles_match_oracle(stream, q, s, items, rng, 40)
+    # every item against the oracle, layer by layer (80 passes over host
+    # copies of the items' strided source rows)
+    hs = _host(s)
+    for k, it in enumerate(items):
+        if k % 70 == 0:
+            print(f"cast item {k} of {len(items)}", flush=True)
+        _item_matches_oracle(stream, q, hs, it)
 
     # the inverse rule over the whole shard
     ditems = tcv.dequant_items(spec, tp)
@@ -346,19 +370,20 @@ def test_tp_shard_cast_70b_full_size():
         # 2^-8; below the normal range the step is s * 2^-9 (half: s * 2^-10)
         bound = (2.0 ** -4 + 2.0 ** -8 + 2.0 ** -12) * x.abs() + smax * 2.0 ** -10
         assert bool(((yy - x).abs() <= bound).all()), it
-    for k in rng.choice(len(ditems), size=20, replace=False):
-        dit = ditems[k]
+    # every item of the inverse against the oracle's inverse of the GPU codes
+    for k, dit in enumerate(ditems):
+        if k % 70 == 0:
+            print(f"inverse item {k} of {len(ditems)}", flush=True)
         rows, cols = int(dit["rows"]), int(dit["cols"])
-        ti, tj = int(rng.integers(0, rows // 128)), int(rng.integers(0, cols // 128))
-        qo = int(dit["src_off"]) + ti * 128 * int(dit["src_ld"]) + tj * 128
-        qt = _host(q[qo:qo + 127 * int(dit["src_ld"]) + 128])
-        qt = np.lib.stride_tricks.as_strided(qt, shape=(128, 128), strides=(int(dit["src_ld"]), 1))
-        st = _host(s[int(dit["scale_off"]) + ti * int(dit["scale_ld"]) + tj]).reshape(1, 1)
-        want = oracle.dequant_fp8_blockscaled(np.ascontiguousarray(qt), st)
-        yo = int(dit["dst_off"]) + ti * 128 * int(dit["dst_ld"]) + tj * 128
-        got = _host(y[yo:yo + 127 * int(dit["dst_ld"]) + 128].view(torch.int16)).view(np.uint16)
-        got = np.lib.stride_tricks.as_strided(got, shape=(128, 128), strides=(2 * int(dit["dst_ld"]), 2))
-        assert np.array_equal(got, want), (k, ti, tj)
+        assert int(dit["src_ld"]) == cols and int(dit["dst_ld"]) == cols
+        qo, yo = int(dit["src_off"]), int(dit["dst_off"])
+        qt = _host(q[qo:qo + rows * cols]).reshape(rows, cols)
+        tr, tcn = (rows + 127) // 128, (cols + 127) // 128
+        so = int(dit["scale_off"])
+        st = hs[so:so + tr * tcn].reshape(tr, tcn)
+        want = oracle.dequant_fp8_blockscaled(qt, st)
+        got = _host(y[yo:yo + rows * cols].view(torch.int16)).view(np.uint16).reshape(rows, cols)
+        assert np.array_equal(got, want), k
     del stream, q, s, y
     torch.cuda.empty_cache()
 
@@ -366,7 +391,7 @@ def test_tp_shard_cast_70b_full_size():
 def test_reshard_cast_70b_full_size():
     """The timed reshard into fp8 at full size: 70B-shaped weights held as the
     eight bf16 shards of a TP=8 split (136.9 GB, N(0, 0.02)) cast into rank 1
-    of a TP=4 split.  Sampled tiles against the oracle; every scale in the
+    of a TP=4 split.  Every item against the oracle; every scale in the
     N(0, 0.02) range; every tile's largest code is +-448."""
     src_tp, dst_tp, rank = 8, 4, 1
     spec = synth.spec_70b(80)
@@ -380,7 +405,11 @@ def test_reshard_cast_70b_full_size():
     torch.cuda.synchronize()
     assert bool(((s > 1e-5) & (s < 1e-3)).all())      # every scale written, none poisoned
     _every_tile_reaches_448(q, items)
-    _sampled_tiles_match_oracle(src, q, s, items, np.random.default_rng(56), 40)
+    hs = _host(s)
+    for k, it in enumerate(items):
+        if k % 140 == 0:
+            print(f"reshard-cast item {k} of {len(items)}", flush=True)
+        _item_matches_oracle(src, q, hs, it)
     del src, q, s
     torch.cuda.empty_cache()
 
@@ -465,9 +494,10 @@ def test_dequant_ragged_strided_unaligned():
 
 
 def test_cast_then_dequant_70b_layers():
-    """Two 70B-shaped layers: cast rank 5 of TP=8 to fp8, dequantize the
-    shard back to bf16, and compare both results with the oracle."""
-    spec = synth.spec_70b(2)
+    """Ten 70B-shaped layers (70 items: the item search's second round): cast
+    rank 5 of TP=8 to fp8, dequantize the shard back to bf16, and compare both
+    results with the oracle in full."""
+    spec = synth.spec_70b(10)
     n = synth.spec_elems(spec)
     stream = synth.bf16_normal(n, 0.02, synth.SEED_CAST_70B, device=DEV)
     tp, rank = 8, 5
