@@ -19,7 +19,7 @@ __global__ __launch_bounds__(kThreads) void k_blocks_vec(const RegionTable tab, 
                                                         const uint64_t tiles_per_chunk,
                                                         uint8_t* __restrict__ buf) {
   for (uint64_t b = blockIdx.x; b < total_tiles; b += gridDim.x) {
-    const uint64_t w = xcd_grouped(b, total_tiles, kGather ? kXcdGroup : kXcdGroupScatter);
+    const uint64_t w = xcd_grouped(b, total_tiles, kGather ? kXcdGroupGather : kXcdGroupScatter);
     const uint64_t c = w / tiles_per_chunk;
     const uint64_t k = w - c * tiles_per_chunk;
     const uint64_t i = c / uint64_t(R);

@@ -22,7 +22,11 @@ constexpr int kThreads = 256;  // 4 waves of 64 lanes
 constexpr int kWaveLanes = 64;
 constexpr int64_t kTileBytes = int64_t(kThreads) * 16;  // 4 KiB per workgroup
 constexpr int kXcds = 8;
-constexpr uint64_t kXcdGroup = 64;           // consecutive tiles per XCD run
+constexpr uint64_t kXcdGroup = 64;           // consecutive tiles per XCD run (task copies)
+// publish (block gather): runs of 32 tiles.  Measured on one request's pages
+// (512 tokens, 64 MiB) 6273 against 5575 GB/s with runs of 64, and equal at
+// the 8 GiB batch (6599 / 6563); runs of 16 lost at the batch (6024).
+constexpr uint64_t kXcdGroupGather = 32;
 constexpr uint64_t kXcdGroupScatter = 512;   // hydrate: longer runs stream its reads better
 constexpr uint64_t kXcdGroupReordered = 256;  // task copies of destination-ordered plans
 

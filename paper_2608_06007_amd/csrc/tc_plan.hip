@@ -25,6 +25,12 @@ namespace {
 // few microseconds even then, so the passes are as few as the decisions
 // allow: 5 launches for short lists, 7 for long ones.
 // ------------------------------------------------------------------------
+// v of lane l (l the same in every lane).
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int l) {
+  return (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v >> 32)), l))) << 32) |
+         uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v)), l));
+}
+
 __device__ __forceinline__ uint64_t shfl_up_u64(uint64_t v, int delta) {
   const uint32_t lo = __shfl_up((uint32_t)v, delta, kWaveLanes);
   const uint32_t hi = __shfl_up((uint32_t)(v >> 32), delta, kWaveLanes);
@@ -56,6 +62,11 @@ __device__ uint64_t block_exclusive_scan(uint64_t v, uint64_t* block_total) {
 }
 
 constexpr int kPlanPerThread = kPlanPerBlock / kThreads;  // 4
+// Window entries a lane writes for its fragment by itself; a fragment with
+// more goes to its whole wave.  With 8, the 256 experts of a MoE permutation
+// (28 entries each, all in the first wave of one workgroup) took 40 us in 256
+// wave rounds; alone, one 4 GiB fragment (8192 entries) took 437 us.
+constexpr uint64_t kWideFragmentWindows = 64;
 
 __device__ __forceinline__ uint64_t pieces_of(const tc_fragment& f, uint64_t piece, uint64_t cut) {
   return f.len ? (f.len + (f.dst_off & cut) + piece - 1) / piece : 0;
@@ -298,23 +309,37 @@ __global__ __launch_bounds__(kThreads) void k_plan_tstart(const tc_fragment* __r
   uint64_t block_total;
   uint64_t run = before + block_exclusive_scan(s, &block_total);
   const uint64_t nwin = (total + kWindowTasks - 1) / kWindowTasks;
+  const int lane = threadIdx.x & (kWaveLanes - 1);
 #pragma unroll
   for (int j = 0; j < kPlanPerThread; ++j) {
-    if (f0 + j < n) {
-      tstart[f0 + j] = run;
-      // Every task lies in exactly one non-empty fragment, which is therefore
-      // the first fragment of each window whose first task it holds and the
-      // last fragment of each window whose last task it holds.
-      if (c[j]) {
-        const uint64_t te = run + c[j];  // tasks [run, te)
-        for (uint64_t w = (run + kWindowTasks - 1) / kWindowTasks; w * kWindowTasks < te; ++w)
-          windows[2 * w] = f0 + j;
-        for (uint64_t w = run / kWindowTasks; w < nwin; ++w) {
-          const uint64_t last = min(w * kWindowTasks + kWindowTasks - 1, total - 1);
-          if (last >= te) break;
-          windows[2 * w + 1] = f0 + j;
-        }
-      }
+    const int64_t f = f0 + j;
+    if (f < n) tstart[f] = run;
+    // Every task lies in exactly one non-empty fragment.  The one holding
+    // tasks [run, te) is therefore the first fragment of the windows whose
+    // first task it holds, [ceil(run/W), ceil(te/W)), and the last fragment of
+    // those whose last task (w*W + W-1, total-1 for the last window) it holds,
+    // [run/W, te/W), or up to the last window when te is the total.
+    uint64_t a0 = 0, a1 = 0, b0 = 0, b1 = 0;
+    if (f < n && c[j]) {
+      const uint64_t te = run + c[j];
+      a0 = (run + kWindowTasks - 1) / kWindowTasks;
+      a1 = (te + kWindowTasks - 1) / kWindowTasks;
+      b0 = run / kWindowTasks;
+      b1 = te == total ? nwin : te / kWindowTasks;
+    }
+    // A fragment spanning many windows (a large tensor) is written by its
+    // whole wave, one such fragment after another.
+    const bool wide = (a1 - a0) + (b1 - b0) > kWideFragmentWindows;
+    if (!wide) {
+      for (uint64_t w = a0; w < a1; ++w) windows[2 * w] = f;
+      for (uint64_t w = b0; w < b1; ++w) windows[2 * w + 1] = f;
+    }
+    for (uint64_t m = __ballot(wide); m; m &= m - 1) {
+      const int l = __ffsll((unsigned long long)m) - 1;
+      const int64_t fl = int64_t(readlane_u64(uint64_t(f), l));
+      const uint64_t la1 = readlane_u64(a1, l), lb1 = readlane_u64(b1, l);
+      for (uint64_t w = readlane_u64(a0, l) + lane; w < la1; w += kWaveLanes) windows[2 * w] = fl;
+      for (uint64_t w = readlane_u64(b0, l) + lane; w < lb1; w += kWaveLanes) windows[2 * w + 1] = fl;
     }
     run += c[j];
   }
