@@ -28,7 +28,8 @@
  *   hand a device-computed number back to the host (tc_plan_fragments,
  *   tc_plan_status) and the host staging calls.  The library allocates
  *   nothing that outlives a call, on the device or the host, apart from a
- *   stager's own ring (created and destroyed by the caller).
+ *   stager's own ring (created and destroyed by the caller) and the fixed
+ *   device array behind tc_cast_fp8_blockscaled_noalloc.
  * - Calls are pure functions of their inputs, so re-running one after a
  *   failure is safe (the paper's idempotent retry, Sec. 3.2 "Plan").
  * - Errors: TC_ERR_INVALID_ARGUMENT for null pointers, negative sizes,
