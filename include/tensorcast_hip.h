@@ -412,7 +412,8 @@ tc_status tc_cast_fp8_planned(const void* src_base, void* dst_base, float* scale
  * tc_cast_fp8_blockscaled without a workspace.  The tile table lives in a
  * fixed array of device memory that the library holds on each device it
  * runs on, 332,288 bytes, until the process ends; nothing is allocated, on
- * the device or the host.  At most TC_NOALLOC_MAX_ITEMS items: more is
+ * the device or the host.  The array used is that of the device that runs
+ * `stream` (the current device for the null stream).  At most TC_NOALLOC_MAX_ITEMS items: more is
  * TC_ERR_WORKSPACE, before anything is enqueued.  Validation mode does not
  * apply (its checks need host memory).  Every call on one device rewrites
  * that device's array, so two calls that overlap in time on one device race:

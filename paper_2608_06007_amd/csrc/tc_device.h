@@ -23,9 +23,10 @@ constexpr int kWaveLanes = 64;
 constexpr int64_t kTileBytes = int64_t(kThreads) * 16;  // 4 KiB per workgroup
 constexpr int kXcds = 8;
 constexpr uint64_t kXcdGroup = 64;           // consecutive tiles per XCD run (task copies)
-// publish (block gather): runs of 32 tiles.  Measured on one request's pages
-// (512 tokens, 64 MiB) 6273 against 5575 GB/s with runs of 64, and equal at
-// the 8 GiB batch (6599 / 6563); runs of 16 lost at the batch (6024).
+// publish (block gather): runs of 32 tiles.  Measured on distinct requests
+// of 512 to 16,384 tokens (64 MiB to 2 GiB each way) 1-2% faster than runs
+// of 64, and equal at the 8 GiB batch (6557-6582 / 6593-6595 GB/s); runs of
+// 16 lost 8% at the batch.
 constexpr uint64_t kXcdGroupGather = 32;
 constexpr uint64_t kXcdGroupScatter = 512;   // hydrate: longer runs stream its reads better
 constexpr uint64_t kXcdGroupReordered = 256;  // task copies of destination-ordered plans

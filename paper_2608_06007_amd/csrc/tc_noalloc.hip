@@ -5,9 +5,10 @@
 // `scratch` is a file-scope device array.  In host code its name is only a
 // host-side stand-in, so the device address is looked up once per device
 // with hipGetSymbolAddress (with that device current) and kept; every launch
-// takes that address.  Each device holds its own copy until the process
-// ends.  Calls on one device share it: the table is rewritten by every call,
-// so two calls that overlap in time on one device race.
+// takes the address on the device of its stream.  Each device holds its own
+// copy until the process ends.  Calls on one device share it: the table is
+// rewritten by every call, so two calls that overlap in time on one device
+// race.
 #include <mutex>
 
 #include "tc_device.h"
@@ -27,16 +28,26 @@ constexpr int kMaxDevices = 64;
 std::mutex g_scratch_mu;
 void* g_scratch_ptr[kMaxDevices];  // device address of `scratch` on each device (null: not yet)
 
-// The current device's address of `scratch`, looked up on its first use.
-hipError_t scratch_for_current_device(void** out) {
+// The address of `scratch` on the device that runs `stream` (the current
+// device for the null stream), looked up with that device current on its
+// first use there.
+hipError_t scratch_for_stream(hipStream_t stream, void** out) {
   int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
+  hipError_t e = stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
   std::lock_guard<std::mutex> lock(g_scratch_mu);
   if (!g_scratch_ptr[dev]) {
+    int cur = 0;
+    e = hipGetDevice(&cur);
+    if (e != hipSuccess) return e;
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
     void* p = nullptr;
     e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) {
+      const hipError_t back = hipSetDevice(cur);
+      if (e == hipSuccess) e = back;
+    }
     if (e != hipSuccess) return e;
     g_scratch_ptr[dev] = p;
   }
@@ -56,7 +67,7 @@ extern "C" tc_status tc_cast_fp8_blockscaled_noalloc(const void* src_base, void*
   if (n_items > TC_NOALLOC_MAX_ITEMS) return TC_ERR_WORKSPACE;
   if (tc::cast_workspace_bytes(TC_NOALLOC_MAX_ITEMS) > tc::kScratchBytes) return TC_ERR_WORKSPACE;
   void* ws = nullptr;
-  hipError_t e = tc::scratch_for_current_device(&ws);
+  hipError_t e = tc::scratch_for_stream(stream, &ws);
   if (e != hipSuccess) return tc::hip_status(e);
   tc_tile_plan plan;
   tc_status st = tc_cast_fp8_prepare(src_base, dst_base, items, n_items, tile, ws, tc::kScratchBytes,

@@ -23,7 +23,7 @@ namespace {
 //   -> expansion into the task table.
 // A pass the header does not ask for returns at once.  Every launch costs a
 // few microseconds even then, so the passes are as few as the decisions
-// allow: 5 launches for short lists, 7 for long ones.
+// allow: 5 launches for short lists, 8 for long ones (9 past 16M fragments).
 // ------------------------------------------------------------------------
 // v of lane l (l the same in every lane).
 __device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int l) {
