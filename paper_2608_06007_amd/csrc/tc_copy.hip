@@ -55,7 +55,12 @@ __global__ __launch_bounds__(kThreads) void k_copy_tasks(const uint8_t* __restri
       if (uint64_t(lane) < tail) d[(n16 << 4) + lane] = s[(n16 << 4) + lane];
     } else {
       // source and destination differ mod 16: realigned 16-byte vectors
-      wave_copy_any(s, d, len, lane, [reordered](u32x4* p, u32x4 v) { st_task(p, v, reordered); });
+      // (two stateless store functors: a lambda capturing the flag was kept
+      // per lane in LDS by the compiler)
+      if (reordered)
+        wave_copy_any(s, d, len, lane, [](u32x4* p, u32x4 v) { st_nt(p, v); });
+      else
+        wave_copy_any(s, d, len, lane, [](u32x4* p, u32x4 v) { st_sc1_nt(p, v); });
     }
   }
 }
