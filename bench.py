@@ -797,10 +797,23 @@ def main():
     if kv is not None:
         extra = {"kv_requests": kv["requests"], **extra}
     result["workloads"] = extra
-    if "roofline" in result and "calib" in extra:
+    if "calib" in extra:
+        # every device rate also as a fraction of the same run's copy ceiling
+        # (this library's copy of one 4 GiB fragment), which separates the
+        # box's spread from the kernel's
         ceiling = extra["calib"]["library_copy"]["GBps"]
-        result["roofline"]["copy_ceiling_GBps"] = ceiling
-        result["roofline"]["frac_of_copy_ceiling"] = round(result["roofline"]["achieved"] / ceiling, 4)
+        if "roofline" in result:
+            result["roofline"]["copy_ceiling_GBps"] = ceiling
+            result["roofline"]["frac_of_copy_ceiling"] = round(result["roofline"]["achieved"] / ceiling, 4)
+
+        def add_ceiling(node):
+            if isinstance(node, dict):
+                if "GBps" in node and "frac_of_peak" in node:
+                    node["frac_of_copy_ceiling"] = round(node["GBps"] / ceiling, 4)
+                for v in node.values():
+                    add_ceiling(v)
+        add_ceiling(result.get("kernels"))
+        add_ceiling(extra)
     # The paper's own results, with the hardware it states: context only.  It
     # reports no device-side rate for these operations, so vs_baseline is null.
     result["paper_context"] = {
