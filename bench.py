@@ -800,7 +800,7 @@ def main():
     if "calib" in extra:
         # every device rate also as a fraction of the same run's copy ceiling
         # (this library's copy of one 4 GiB fragment), which separates the
-        # box's spread from the kernel's
+        # spread between GPUs from the kernel's
         ceiling = extra["calib"]["library_copy"]["GBps"]
         if "roofline" in result:
             result["roofline"]["copy_ceiling_GBps"] = ceiling

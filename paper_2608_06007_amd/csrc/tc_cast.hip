@@ -102,7 +102,7 @@ __device__ __forceinline__ void st_codes(u32x2* p, u32x2 v) {
 // within each row of 16 lanes (swap neighbours, swap pairs, mirror halves,
 // mirror the row), then the four row maxima read into scalars.  A butterfly
 // of __shfl_xor compiled to six dependent ds_bpermute round trips; this
-// measured +1.3% on the C4 shard cast (one box, interleaved).
+// measured +1.3% on the C4 shard cast (one GPU, the two builds interleaved).
 __device__ __forceinline__ uint32_t wave_max32(uint32_t v) {
   v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
   v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1

@@ -26,12 +26,12 @@ constexpr uint64_t kXcdGroup = 64;           // consecutive tiles per XCD run (t
 // publish (block gather): runs of 256 tiles.  In publish + hydrate steps
 // (each gather after a hydrate, as a serving engine and the benchmark run
 // them) the 8 GiB batch gathers at 6672-6687 GB/s with runs of 256 against
-// 6293-6406 with runs of 32 (two boxes; 128: 6619-6662, 512: 6637-6645).
+// 6293-6406 with runs of 32 (two GPUs; 128: 6619-6662, 512: 6637-6645).
 // Gathers back to back barely tell them apart (32: 6731-6749, 256:
 // 6759-6768), and on distinct single requests runs of 256 are 1% slower.
 constexpr uint64_t kXcdGroupGather = 256;
 // hydrate: longer runs stream its contiguous reads better.  Runs of 128 /
-// 512 / 2048 / 8192 tiles on the 8 GiB batch, one box: 6307 / 6372 / 6413 /
+// 512 / 2048 / 8192 tiles on the 8 GiB batch, one GPU: 6307 / 6372 / 6413 /
 // 6399 GB/s; on distinct single requests 2048 is within 1% of 512.
 constexpr uint64_t kXcdGroupScatter = 2048;
 constexpr uint64_t kXcdGroupReordered = 256;  // task copies of destination-ordered plans
