@@ -36,7 +36,18 @@ __global__ __launch_bounds__(kThreads) void k_copy_tasks(const uint8_t* __restri
     uint8_t* d = dst + task_dst(tk);
     uint64_t len = task_len(tk);
     const uintptr_t sa = reinterpret_cast<uintptr_t>(s), da = reinterpret_cast<uintptr_t>(d);
-    if (((sa ^ da) & 15) == 0) {
+    if (((sa | da | len) & 15) == 0 && len <= uint64_t(kWaveLanes) * 16) {
+      // The common task: both ends 16-byte aligned, at most one vector per
+      // lane, no head or tail bytes (C3 planned copy -0.4%, the storm -0.8%,
+      // its one-call copy -1.6% against the general path alone).
+      if (uint64_t(lane) * 16 < len) {
+        const u32x4 v = ld_nt(reinterpret_cast<const u32x4*>(s) + lane);
+        if (reordered)
+          st_nt(reinterpret_cast<u32x4*>(d) + lane, v);
+        else
+          st_sc1_nt(reinterpret_cast<u32x4*>(d) + lane, v);
+      }
+    } else if (((sa ^ da) & 15) == 0) {
       // byte head up to 16-byte alignment, 16-byte body, byte tail
       uint64_t head = (16 - (sa & 15)) & 15;
       if (head > len) head = len;
