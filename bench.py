@@ -398,15 +398,17 @@ def run_cast(torch, tc, synth, args, stream):
     n_scales = tcv.scale_elems(spec, tp)
     q = torch.empty(shard_n, dtype=torch.uint8, device="cuda")
     sc = torch.empty(n_scales, dtype=torch.float32, device="cuda")
-    ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device="cuda")
+    # room for the per-tile table: each tile's offsets are one 32-byte load
+    ws = torch.empty(tc.tc_cast_fp8_workspace_tiles(items), dtype=torch.uint8, device="cuda")
     it = items
     nbytes = 2 * shard_n + shard_n + 4 * n_scales
     # a rank's item list is the same at every weight synchronization: the
     # tile table is written once, and each cast launches the kernels alone
     plan = tc.tc_cast_fp8_prepare(src, q, it, ws, stream=stream)
+    assert plan.tiled == 1
     ms = _time_calls(torch, stream, lambda: tc.tc_cast_fp8_planned(src, q, sc, ws, plan, stream=stream),
                      args.warmup, args.cast_steps)
-    # the one-call form, which writes the table (14 small launches) each time
+    # the one-call form, which writes the tables (small launches before the cast) each time
     ms1 = _time_calls(torch, stream, lambda: tc.tc_cast_fp8_blockscaled(src, q, sc, it, ws, stream=stream),
                       args.warmup, args.cast_steps)
     out = {"items": int(len(items)), "tiles": int(n_scales), "cast": _stats(ms, nbytes),
@@ -418,8 +420,9 @@ def run_cast(torch, tc, synth, args, stream):
     # the inverse rule on the shard just produced: e4m3 + scales -> bf16
     ditems = tcv.dequant_items(spec, tp)
     y = torch.empty(shard_n, dtype=torch.bfloat16, device="cuda")
-    dws = torch.empty(tc.tc_dequant_fp8_workspace(len(ditems)), dtype=torch.uint8, device="cuda")
+    dws = torch.empty(tc.tc_dequant_fp8_workspace_tiles(ditems), dtype=torch.uint8, device="cuda")
     dplan = tc.tc_dequant_fp8_prepare(q, y, ditems, dws, stream=stream)
+    assert dplan.tiled == 1
     dms = _time_calls(torch, stream, lambda: tc.tc_dequant_fp8_planned(q, sc, y, dws, dplan, stream=stream),
                       args.warmup, args.cast_steps)
     dms1 = _time_calls(torch, stream, lambda: tc.tc_dequant_fp8_blockscaled(q, sc, y, ditems, dws, stream=stream),
@@ -447,9 +450,10 @@ def run_reshard_cast(torch, tc, synth, args, stream):
     n_scales = tcv.scale_elems(spec, dst_tp)
     q = torch.empty(shard_n, dtype=torch.uint8, device="cuda")
     sc = torch.empty(n_scales, dtype=torch.float32, device="cuda")
-    ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(tc.tc_cast_fp8_workspace_tiles(items), dtype=torch.uint8, device="cuda")
     nbytes = 2 * shard_n + shard_n + 4 * n_scales
     plan = tc.tc_cast_fp8_prepare(src, q, items, ws, stream=stream)
+    assert plan.tiled == 1
     ms = _time_calls(torch, stream, lambda: tc.tc_cast_fp8_planned(src, q, sc, ws, plan, stream=stream),
                      args.warmup, args.cast_steps)
     out = {"items": int(len(items)), "tiles": int(n_scales), "reshard_cast": _stats(ms, nbytes)}

@@ -43,9 +43,10 @@ __all__ = [
     "tc_tp_fragment_count", "tc_tp_fragments", "tc_tp_cast_item",
     "tc_reshard_fragment_count", "tc_reshard_fragments",
     "tc_reshard_cast_item_count", "tc_reshard_cast_items",
-    "tc_cast_fp8_workspace", "tc_cast_fp8_blockscaled", "tc_cast_fp8_scaled",
+    "tc_cast_fp8_workspace", "tc_cast_fp8_workspace_tiles", "tc_cast_fp8_blockscaled", "tc_cast_fp8_scaled",
     "tc_cast_fp8_prepare", "tc_cast_fp8_planned", "TilePlan",
-    "tc_dequant_fp8_workspace", "tc_dequant_fp8_blockscaled", "DEQUANT_ITEM_DTYPE",
+    "tc_dequant_fp8_workspace", "tc_dequant_fp8_workspace_tiles", "tc_dequant_fp8_blockscaled",
+    "DEQUANT_ITEM_DTYPE",
     "tc_dequant_fp8_prepare", "tc_dequant_fp8_planned",
     "tc_ipc_export", "tc_ipc_open", "tc_ipc_close", "IPC_HANDLE_BYTES",
     "tc_stager_create", "tc_stager_destroy", "tc_stage_h2d", "tc_stage_d2h",
@@ -102,7 +103,8 @@ class TilePlan(ctypes.Structure):
     """tc_tile_plan: a cast (or inverse-cast) tile table prepared in a workspace."""
     _fields_ = [("n_items", ctypes.c_int64), ("full_tiles", ctypes.c_uint64),
                 ("edge_tiles", ctypes.c_uint64), ("in_align", ctypes.c_uint32),
-                ("out_align", ctypes.c_uint32)]
+                ("out_align", ctypes.c_uint32), ("tiled", ctypes.c_uint32),
+                ("reserved", ctypes.c_uint32)]
 
 
 class _IpcHandle(ctypes.Structure):
@@ -171,6 +173,10 @@ def load():
     L.tc_ipc_close.argtypes = [c.POINTER(_IpcHandle), P]
     L.tc_dequant_fp8_workspace.argtypes = [c.c_int64]
     L.tc_dequant_fp8_workspace.restype = c.c_size_t
+    L.tc_cast_fp8_workspace_tiles.argtypes = [P, c.c_int64]
+    L.tc_cast_fp8_workspace_tiles.restype = c.c_size_t
+    L.tc_dequant_fp8_workspace_tiles.argtypes = [P, c.c_int64]
+    L.tc_dequant_fp8_workspace_tiles.restype = c.c_size_t
     L.tc_dequant_fp8_blockscaled.argtypes = [P, P, P, P, c.c_int64, c.c_int32, P, c.c_size_t, P]
     L.tc_stager_create.argtypes = [c.c_size_t, c.c_int32, c.c_int32, c.POINTER(c.c_void_p)]
     L.tc_stager_destroy.argtypes = [P]
@@ -586,6 +592,13 @@ def tc_cast_fp8_workspace(n_items: int) -> int:
     return int(load().tc_cast_fp8_workspace(int(n_items)))
 
 
+def tc_cast_fp8_workspace_tiles(items) -> int:
+    """Workspace bytes with room for the per-tile table of ``items`` (host
+    CAST_ITEM_DTYPE records); 0 for an invalid item."""
+    it = np.ascontiguousarray(items, dtype=CAST_ITEM_DTYPE).reshape(-1)
+    return int(load().tc_cast_fp8_workspace_tiles(it.ctypes.data if it.size else None, it.size))
+
+
 def tc_cast_fp8_blockscaled(src, dst, scales, items, workspace, stream=None, tile: int = 128) -> None:
     """Cast every item; ``items`` is a host numpy array of CAST_ITEM_DTYPE
     records (the library stages it into ``workspace``)."""
@@ -630,6 +643,13 @@ def tc_cast_fp8_scaled(src, scale: float, dst, stream=None) -> None:
 
 def tc_dequant_fp8_workspace(n_items: int) -> int:
     return int(load().tc_dequant_fp8_workspace(int(n_items)))
+
+
+def tc_dequant_fp8_workspace_tiles(items) -> int:
+    """Workspace bytes with room for the per-tile table of ``items`` (host
+    DEQUANT_ITEM_DTYPE records); 0 for an invalid item."""
+    it = np.ascontiguousarray(items, dtype=DEQUANT_ITEM_DTYPE).reshape(-1)
+    return int(load().tc_dequant_fp8_workspace_tiles(it.ctypes.data if it.size else None, it.size))
 
 
 def tc_dequant_fp8_blockscaled(codes, scales, dst, items, workspace, stream=None, tile: int = 128) -> None:

@@ -423,7 +423,7 @@ static tc_status prepare_tiles(const void* in_base, const void* out_base, const 
                                int64_t n_items, int32_t tile, void* workspace, size_t workspace_bytes,
                                bool cast, tc_tile_plan* plan, hipStream_t stream) {
   if (!plan) return TC_ERR_INVALID_ARGUMENT;
-  *plan = tc_tile_plan{0, 0, 0, 0, 0};
+  *plan = tc_tile_plan{0, 0, 0, 0, 0, 0, 0};
   if (n_items < 0 || n_items > kMaxItems || tile != 128) return TC_ERR_INVALID_ARGUMENT;
   if (n_items == 0) return TC_OK;
   if (!in_base || !out_base || !items || !workspace) return TC_ERR_INVALID_ARGUMENT;
@@ -437,8 +437,33 @@ static tc_status prepare_tiles(const void* in_base, const void* out_base, const 
   if (st != TC_OK) return st;
   st = check(upload_tile_table(items, n_items, ib, ob, cast, full, edge, workspace, stream));
   if (st != TC_OK) return st;
-  *plan = tc_tile_plan{n_items, full, edge, uint32_t(ib % 16), uint32_t(ob % 16)};
+  // The per-tile table, when the workspace has room for it and every row
+  // pitch fits its 32-bit fields.
+  bool tiled = full > 0 && full < (uint64_t(1) << 50) &&
+               workspace_bytes - tc::cast_workspace_bytes(n_items) >= full * tc::kTileEntryBytes;
+  for (int64_t i = 0; tiled && i < n_items; ++i)
+    tiled = uint64_t(items[i].src_ld) >> 32 == 0 && uint64_t(items[i].dst_ld) >> 32 == 0;
+  if (tiled) {
+    st = check(tc::launch_tile_expand(workspace, n_items, full, stream));
+    if (st != TC_OK) return st;
+  }
+  *plan = tc_tile_plan{n_items, full, edge, uint32_t(ib % 16), uint32_t(ob % 16), tiled ? 1u : 0u, 0};
   return TC_OK;
+}
+
+// Workspace for n_items items and the per-tile table of all their full
+// tiles (counted as if every item were aligned; 0 for an invalid item).
+template <typename Item>
+static size_t workspace_with_tiles(const Item* items, int64_t n_items) {
+  if (n_items < 0 || n_items > kMaxItems || (n_items > 0 && !items)) return 0;
+  uint64_t tiles = 0;
+  for (int64_t i = 0; i < n_items; ++i) {
+    const Item& it = items[i];
+    if (it.rows < 0 || it.cols < 0) return 0;
+    tiles += uint64_t(it.rows / 128) * uint64_t(it.cols / 128);
+    if (tiles > (uint64_t(1) << 40)) return 0;
+  }
+  return tc::cast_workspace_bytes(n_items) + ((tiles * tc::kTileEntryBytes + 255) & ~uint64_t(255));
 }
 
 // Checks of a planned launch: the table's size, and bases with the
@@ -452,6 +477,10 @@ static tc_status planned_args(const void* in_base, const void* out_base, const f
       (uintptr_t)scale_base % 4)
     return TC_ERR_INVALID_ARGUMENT;
   if (workspace_bytes < tc::cast_workspace_bytes(plan->n_items)) return TC_ERR_WORKSPACE;
+  if (plan->tiled > 1) return TC_ERR_INVALID_ARGUMENT;
+  if (plan->tiled && (workspace_bytes - tc::cast_workspace_bytes(plan->n_items)) / tc::kTileEntryBytes <
+                         plan->full_tiles)
+    return TC_ERR_WORKSPACE;
   if ((uintptr_t)in_base % 16 != plan->in_align || (uintptr_t)out_base % 16 != plan->out_align)
     return TC_ERR_INVALID_ARGUMENT;
   return TC_OK;
@@ -866,6 +895,14 @@ size_t tc_dequant_fp8_workspace(int64_t n_items) {
   return tc::cast_workspace_bytes(n_items);
 }
 
+size_t tc_cast_fp8_workspace_tiles(const tc_cast_item* items, int64_t n_items) {
+  return workspace_with_tiles(items, n_items);
+}
+
+size_t tc_dequant_fp8_workspace_tiles(const tc_dequant_item* items, int64_t n_items) {
+  return workspace_with_tiles(items, n_items);
+}
+
 tc_status tc_cast_fp8_prepare(const void* src_base, const void* dst_base, const tc_cast_item* items,
                               int64_t n_items, int32_t tile, void* workspace, size_t workspace_bytes,
                               tc_tile_plan* plan, hipStream_t stream) {
@@ -884,7 +921,8 @@ tc_status tc_cast_fp8_planned(const void* src_base, void* dst_base, float* scale
   if (st != TC_OK || plan->full_tiles + plan->edge_tiles == 0) return st;
   return check(tc::launch_cast_blockscaled(static_cast<const uint16_t*>(src_base),
                                            static_cast<uint8_t*>(dst_base), scale_base, workspace,
-                                           plan->n_items, plan->full_tiles, plan->edge_tiles, stream));
+                                           plan->n_items, plan->full_tiles, plan->edge_tiles,
+                                           plan->tiled != 0, stream));
 }
 
 tc_status tc_cast_fp8_blockscaled(const void* src_base, void* dst_base, float* scale_base,
@@ -929,7 +967,7 @@ tc_status tc_dequant_fp8_planned(const void* codes_base, const float* scale_base
   return check(tc::launch_dequant_blockscaled(static_cast<const uint8_t*>(codes_base), scale_base,
                                               static_cast<uint16_t*>(dst_base), workspace,
                                               plan->n_items, plan->full_tiles, plan->edge_tiles,
-                                              stream));
+                                              plan->tiled != 0, stream));
 }
 
 tc_status tc_dequant_fp8_blockscaled(const void* codes_base, const float* scale_base,

@@ -147,15 +147,29 @@ static_assert(sizeof(TableChunk) <= 3584, "a chunk fits the kernel arguments");
 // Enqueue the writes of one chunk of a table of n_items items into the
 // workspace (the table's layout is cast_layout(n_items)).
 hipError_t launch_tile_chunk(const TableChunk& c, int64_t n_items, void* ws, hipStream_t s);
+// Optional per-tile table after the item table (at cast_layout(n).bytes):
+// one entry per full tile, so that a workgroup finds its tile's rows with a
+// single load instead of searching the items and dividing for the tile's
+// row and column.  Offsets are in elements of each side (bf16 elements or
+// code bytes); lds packs src_ld | dst_ld << 32 (both below 2^32).
+struct TileEntry {
+  uint64_t in_off, out_off, scale_idx, lds;
+};
+static_assert(sizeof(TileEntry) == 32, "tile entries are 32 bytes");
+constexpr size_t kTileEntryBytes = sizeof(TileEntry);
+// Fill the per-tile table of the full tiles from the item table already
+// enqueued in the workspace (one thread per tile).
+hipError_t launch_tile_expand(void* ws, int64_t n_items, uint64_t full_tiles, hipStream_t s);
+// tiled: the workspace holds the per-tile table (full tiles read it).
 hipError_t launch_cast_blockscaled(const uint16_t* src, uint8_t* dst, float* scales,
                                    const void* ws, int64_t n_items, uint64_t full_tiles,
-                                   uint64_t edge_tiles, hipStream_t s);
+                                   uint64_t edge_tiles, bool tiled, hipStream_t s);
 hipError_t launch_cast_scaled(const uint16_t* src, int64_t n, float scale, uint8_t* dst,
                               hipStream_t s);
 // The inverse cast uses the same workspace layout (its items are the same
 // size as cast items).
 hipError_t launch_dequant_blockscaled(const uint8_t* codes, const float* scales, uint16_t* dst,
                                       const void* ws, int64_t n_items, uint64_t full_tiles,
-                                      uint64_t edge_tiles, hipStream_t s);
+                                      uint64_t edge_tiles, bool tiled, hipStream_t s);
 
 }  // namespace tc

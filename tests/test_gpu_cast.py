@@ -86,9 +86,17 @@ def _cast_matrices(src_bits_1d: np.ndarray, mats, code_pad=0, scale_pad=0):
         q_off += rows * (cols + code_pad)
         s_off += tr * (tcn + scale_pad)
     src = _to_dev_bits(src_bits_1d)
+    # the item table alone (tiles found by searching the items), then with
+    # the per-tile table as well: both against the oracle
+    for ws_bytes in (tc.tc_cast_fp8_workspace(len(mats)), tc.tc_cast_fp8_workspace_tiles(items)):
+        hq, hs = _cast_and_check(src, src_bits_1d, items, mats, q_off, s_off, ws_bytes)
+    return hq, hs
+
+
+def _cast_and_check(src, src_bits_1d, items, mats, q_off, s_off, ws_bytes):
     dst = torch.full((max(q_off, 1),), 0xCC, dtype=torch.uint8, device=DEV)
     scales = torch.full((max(s_off, 1),), -7.0, dtype=torch.float32, device=DEV)
-    ws = torch.empty(tc.tc_cast_fp8_workspace(len(mats)), dtype=torch.uint8, device=DEV)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=DEV)
     tc.tc_cast_fp8_blockscaled(src, dst, scales, items, ws)
     torch.cuda.synchronize()
     hq, hs = _host(dst), _host(scales)
@@ -189,21 +197,29 @@ def _tiles_under_amax(a_lo, a_hi):
     return np.ascontiguousarray(tiles.reshape(-1, 128, 128).transpose(1, 0, 2).reshape(128, -1))
 
 
+@pytest.mark.parametrize("tiled", [False, True])
 @pytest.mark.parametrize("part", range(4))
-def test_blockscaled_exhaustive_amax_and_value(part):
+def test_blockscaled_exhaustive_amax_and_value(part, tiled):
     """Every finite positive tile maximum A (bf16 0x0001 .. 0x7F7F, in four
     parts) with every bf16 value |x| <= A of both signs: all pairs of element
     and tile scale that a finite, non-zero tile can present to the full-tile
     kernel (its quotient and its choice of fast or dividing path depend on
-    nothing else).  Codes and scales against the oracle, in chunks."""
+    nothing else).  Codes and scales against the oracle, in chunks; through
+    the kernel that searches the items and through the one that reads the
+    per-tile table."""
     bounds = [1, 0x3F80, 0x5A00, 0x6D00, 0x7F80]     # about equal work per part
     a0, a1 = bounds[part], bounds[part + 1]
-    ws = torch.empty(tc.tc_cast_fp8_workspace(1), dtype=torch.uint8, device=DEV)
     step = 512 if part == 0 else 128
+    # room for the largest chunk's per-tile table, or the item table alone
+    big = np.zeros(1, dtype=tc.CAST_ITEM_DTYPE)
+    big[0] = (0, 128, 128 * 4096, 128 * 4096, 0, 128 * 4096, 0, 4096)
+    ws = torch.empty(tc.tc_cast_fp8_workspace_tiles(big) if tiled else tc.tc_cast_fp8_workspace(1),
+                     dtype=torch.uint8, device=DEV)
     checked = 0
     for lo in range(a0, a1, step):
         m = _tiles_under_amax(lo, min(a1, lo + step))
         rows, cols = m.shape
+        assert cols // 128 <= 4096          # the tiled workspace holds this chunk's table
         items = np.zeros(1, dtype=tc.CAST_ITEM_DTYPE)
         items[0] = (0, rows, cols, cols, 0, cols, 0, cols // 128)
         src = _to_dev_bits(m.reshape(-1))
@@ -340,8 +356,11 @@ def test_tp_shard_cast_70b_full_size():
     del fill
     q = torch.empty(tcv.shard_elems(spec, tp), dtype=torch.uint8, device=DEV)
     s = torch.empty(tcv.scale_elems(spec, tp), dtype=torch.float32, device=DEV)
-    ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device=DEV)
-    tc.tc_cast_fp8_blockscaled(stream, q, s, items, ws)
+    # the timed configuration: a workspace with the per-tile table
+    ws = torch.empty(tc.tc_cast_fp8_workspace_tiles(items), dtype=torch.uint8, device=DEV)
+    plan = tc.tc_cast_fp8_prepare(stream, q, items, ws)
+    assert plan.tiled == 1 and plan.full_tiles == tcv.scale_elems(spec, tp)
+    tc.tc_cast_fp8_planned(stream, q, s, ws, plan)
     torch.cuda.synchronize()
     # no poisoned tile: every scale is what an N(0, 0.02) tile gives
     assert bool(((s > 1e-5) & (s < 1e-3)).all())
@@ -357,8 +376,10 @@ def test_tp_shard_cast_70b_full_size():
     # the inverse rule over the whole shard
     ditems = tcv.dequant_items(spec, tp)
     y = torch.empty(tcv.shard_elems(spec, tp), dtype=torch.bfloat16, device=DEV)
-    dws = torch.empty(tc.tc_dequant_fp8_workspace(len(ditems)), dtype=torch.uint8, device=DEV)
-    tc.tc_dequant_fp8_blockscaled(q, s, y, ditems, dws)
+    dws = torch.empty(tc.tc_dequant_fp8_workspace_tiles(ditems), dtype=torch.uint8, device=DEV)
+    dplan = tc.tc_dequant_fp8_prepare(q, y, ditems, dws)
+    assert dplan.tiled == 1
+    tc.tc_dequant_fp8_planned(q, s, y, dws, dplan)
     torch.cuda.synchronize()
     smax = float(s.max())
     for it, dit in zip(items, ditems):
@@ -400,7 +421,7 @@ def test_reshard_cast_70b_full_size():
     items = tcv.reshard_cast_items(spec, src_tp, dst_tp, rank)
     q = torch.empty(tcv.shard_elems(spec, dst_tp), dtype=torch.uint8, device=DEV)
     s = torch.full((tcv.scale_elems(spec, dst_tp),), float("nan"), dtype=torch.float32, device=DEV)
-    ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device=DEV)
+    ws = torch.empty(tc.tc_cast_fp8_workspace_tiles(items), dtype=torch.uint8, device=DEV)
     tc.tc_cast_fp8_blockscaled(src, q, s, items, ws)
     torch.cuda.synchronize()
     assert bool(((s > 1e-5) & (s < 1e-3)).all())      # every scale written, none poisoned
@@ -428,8 +449,14 @@ def _dequant_matrices(codes_1d: np.ndarray, scales_1d: np.ndarray, mats, dst_pad
         y_off += rows * (cols + dst_pad)
     q = torch.from_numpy(codes_1d).to(DEV)
     s = torch.from_numpy(scales_1d.astype(np.float32)).to(DEV)
+    # the item table alone, then with the per-tile table as well
+    for ws_bytes in (tc.tc_dequant_fp8_workspace(len(mats)), tc.tc_dequant_fp8_workspace_tiles(items)):
+        _dequant_and_check(codes_1d, scales_1d, mats, items, q, s, y_off, ws_bytes)
+
+
+def _dequant_and_check(codes_1d, scales_1d, mats, items, q, s, y_off, ws_bytes):
     y = torch.full((max(y_off, 1),), -1, dtype=torch.int16, device=DEV)
-    ws = torch.empty(tc.tc_dequant_fp8_workspace(len(mats)), dtype=torch.uint8, device=DEV)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=DEV)
     tc.tc_dequant_fp8_blockscaled(q, s, y, items, ws)
     torch.cuda.synchronize()
     hy = _host(y).view(np.uint16)
@@ -493,10 +520,12 @@ def test_dequant_ragged_strided_unaligned():
     _dequant_matrices(codes, scales, mats, dst_pad=3)   # unaligned bf16 rows
 
 
-def test_cast_then_dequant_70b_layers():
+@pytest.mark.parametrize("tiled", [False, True])
+def test_cast_then_dequant_70b_layers(tiled):
     """Ten 70B-shaped layers (70 items: the item search's second round): cast
     rank 5 of TP=8 to fp8, dequantize the shard back to bf16, and compare both
-    results with the oracle in full."""
+    results with the oracle in full; with the item table alone and with the
+    per-tile table."""
     spec = synth.spec_70b(10)
     n = synth.spec_elems(spec)
     stream = synth.bf16_normal(n, 0.02, synth.SEED_CAST_70B, device=DEV)
@@ -504,11 +533,13 @@ def test_cast_then_dequant_70b_layers():
     items = tcv.cast_items(spec, tp, rank)
     q = torch.empty(tcv.shard_elems(spec, tp), dtype=torch.uint8, device=DEV)
     s = torch.empty(tcv.scale_elems(spec, tp), dtype=torch.float32, device=DEV)
-    ws = torch.empty(tc.tc_cast_fp8_workspace(len(items)), dtype=torch.uint8, device=DEV)
+    ws = torch.empty(tc.tc_cast_fp8_workspace_tiles(items) if tiled else tc.tc_cast_fp8_workspace(len(items)),
+                     dtype=torch.uint8, device=DEV)
     tc.tc_cast_fp8_blockscaled(stream, q, s, items, ws)
     y = torch.empty(tcv.shard_elems(spec, tp), dtype=torch.bfloat16, device=DEV)
     ditems = tcv.dequant_items(spec, tp)
-    dws = torch.empty(tc.tc_dequant_fp8_workspace(len(ditems)), dtype=torch.uint8, device=DEV)
+    dws = torch.empty(tc.tc_dequant_fp8_workspace_tiles(ditems) if tiled else
+                      tc.tc_dequant_fp8_workspace(len(ditems)), dtype=torch.uint8, device=DEV)
     tc.tc_dequant_fp8_blockscaled(q, s, y, ditems, dws)
     torch.cuda.synchronize()
     hq, hs, hy = _host(q), _host(s), _host(y.view(torch.int16)).view(np.uint16)

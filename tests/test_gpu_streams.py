@@ -112,8 +112,17 @@ def test_graph_capture_and_replay():
     pws = torch.empty_like(cws)
     dws = torch.empty(tc.tc_dequant_fp8_workspace(2), dtype=torch.uint8, device=DEV)
     ditems = items.astype(tc.DEQUANT_ITEM_DTYPE)       # same geometry, codes -> bf16
+    # the planned cast and inverse with a per-tile table (workspace sized by items)
+    qt, st = torch.empty_like(qc), torch.empty_like(sc)
+    yt = torch.empty_like(yc)
+    tws = torch.empty(tc.tc_cast_fp8_workspace_tiles(items), dtype=torch.uint8, device=DEV)
+    tdws = torch.empty(tc.tc_dequant_fp8_workspace_tiles(ditems), dtype=torch.uint8, device=DEV)
     total = tc.tc_plan_fragments(frags, ws)
     plan = tc.tc_cast_fp8_prepare(xc, qp, items, pws)    # prepared eagerly, launched in the graph
+    tplan = tc.tc_cast_fp8_prepare(xc, qt, items, tws)
+    dplan = tc.tc_dequant_fp8_prepare(qt, yt, ditems, tdws)
+    assert plan.tiled == 0 and tplan.tiled == 1 and dplan.tiled == 1
+    assert tplan.full_tiles == dplan.full_tiles == 8    # the top 256 rows: 2 x 4 full tiles
     torch.cuda.synchronize()
 
     g = torch.cuda.CUDAGraph()
@@ -132,6 +141,8 @@ def test_graph_capture_and_replay():
             tc.tc_cast_fp8_blockscaled(xc, qc, sc, items, cws, stream=s)
             tc.tc_cast_fp8_planned(xc, qp, sp, pws, plan, stream=s)
             tc.tc_dequant_fp8_blockscaled(qc, sc, yc, ditems, dws, stream=s)
+            tc.tc_cast_fp8_planned(xc, qt, st, tws, tplan, stream=s)
+            tc.tc_dequant_fp8_planned(qt, st, yt, tdws, dplan, stream=s)
     torch.cuda.synchronize()
     # the graph holds its own copy of the item tables
     items[:] = np.zeros(1, dtype=tc.CAST_ITEM_DTYPE)
@@ -149,11 +160,12 @@ def test_graph_capture_and_replay():
         fdst2.zero_()
         fdst3.zero_()
         dg.fill_(-1)
-        for t in (qc, qp):
+        for t in (qc, qp, qt):
             t.fill_(0xEE)
-        for t in (sc, sp):
+        for t in (sc, sp, st):
             t.fill_(-1.0)
         yc.zero_()
+        yt.zero_()
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
@@ -178,12 +190,13 @@ def test_graph_capture_and_replay():
         wq_bot, ws_bot = oracle.cast_fp8_blockscaled(xcb[256:])
         wq = np.concatenate([wq_top, wq_bot])
         wsc = np.concatenate([ws_top.reshape(-1), ws_bot.reshape(-1)])
-        for qq, ss in ((qc, sc), (qp, sp)):
+        for qq, ss in ((qc, sc), (qp, sp), (qt, st)):
             assert np.array_equal(qq.cpu().numpy().reshape(rows, cols), wq), rep
             assert np.array_equal(ss.cpu().numpy().view(np.uint32), wsc.view(np.uint32)), rep
         wy = np.concatenate([oracle.dequant_fp8_blockscaled(wq_top, ws_top),
                              oracle.dequant_fp8_blockscaled(wq_bot, ws_bot)])
-        assert np.array_equal(yc.view(torch.int16).cpu().numpy().view(np.uint16).reshape(rows, cols), wy), rep
+        for yy in (yc, yt):
+            assert np.array_equal(yy.view(torch.int16).cpu().numpy().view(np.uint16).reshape(rows, cols), wy), rep
     assert want_items.tobytes() != items.tobytes()
 
 

@@ -186,6 +186,17 @@ def test_new_entry_points_check_arguments_without_a_gpu(lib):
     empty = tc.TilePlan(0, 0, 0, 0, 0)
     assert lib.tc_cast_fp8_planned(None, None, None, None, 0, ctypes.byref(empty), None) == 0
     assert lib.tc_dequant_fp8_planned(P(34), P(128), P(64), P(4096), 1 << 20, ctypes.byref(plan), None) == 1
+    # a plan that reads a per-tile table needs room for it; the flag is 0 or 1
+    base = tc.tc_cast_fp8_workspace(1)
+    tiled = tc.TilePlan(1, 10, 0, 0, 0, 1, 0)
+    assert lib.tc_cast_fp8_planned(P(32), P(64), P(128), P(4096), base + 32 * 9, ctypes.byref(tiled), None) == 5
+    assert lib.tc_dequant_fp8_planned(P(32), P(128), P(64), P(4096), base + 32 * 9, ctypes.byref(tiled),
+                                      None) == 5
+    tiled.full_tiles = (1 << 63) + 1                          # no wrap in the size check
+    assert lib.tc_cast_fp8_planned(P(32), P(64), P(128), P(4096), 1 << 30, ctypes.byref(tiled), None) == 5
+    odd = tc.TilePlan(1, 1, 0, 0, 0, 2, 0)
+    assert lib.tc_cast_fp8_planned(P(32), P(64), P(128), P(4096), 1 << 20, ctypes.byref(odd), None) == 1
+    assert lib.tc_dequant_fp8_planned(P(32), P(128), P(64), P(4096), 1 << 20, ctypes.byref(odd), None) == 1
     # IPC: null arguments, and handles that describe impossible ranges
     h = tc._IpcHandle()
     out = ctypes.c_void_p(0)
@@ -198,6 +209,29 @@ def test_new_entry_points_check_arguments_without_a_gpu(lib):
     assert lib.tc_ipc_open(ctypes.byref(h), ctypes.byref(out)) == 1
     assert lib.tc_ipc_close(None, P(4096)) == 1
     assert tc.IPC_HANDLE_BYTES == 88
+
+
+def test_tile_table_workspace_sizes(lib):
+    """The workspace that also holds the per-tile table: the items' own
+    workspace plus 32 bytes for each full 128 x 128 tile, rounded up to 256
+    bytes; 0 for items it cannot size."""
+    items = np.zeros(3, dtype=tc.CAST_ITEM_DTYPE)
+    items[0] = (0, 300, 520, 520, 0, 520, 0, 5)         # 2 x 4 full tiles
+    items[1] = (0, 127, 4096, 4096, 0, 4096, 0, 32)     # no full row of tiles
+    items[2] = (0, 1024, 1024, 1024, 0, 1024, 0, 8)     # 8 x 8
+    for fn, dt, base in ((tc.tc_cast_fp8_workspace_tiles, tc.CAST_ITEM_DTYPE, tc.tc_cast_fp8_workspace),
+                         (tc.tc_dequant_fp8_workspace_tiles, tc.DEQUANT_ITEM_DTYPE,
+                          tc.tc_dequant_fp8_workspace)):
+        it = items.astype(dt)
+        assert fn(it) == base(3) + (72 * 32 + 255) // 256 * 256
+        assert fn(it[1:2]) == base(1)
+        assert fn(it[:0]) == base(0)
+        bad = it.copy()
+        bad[1]["rows"] = -1
+        assert fn(bad) == 0
+    P = ctypes.c_void_p
+    assert lib.tc_cast_fp8_workspace_tiles(None, 2) == 0
+    assert lib.tc_dequant_fp8_workspace_tiles(P(items.ctypes.data), -1) == 0
 
 
 def test_binding_refuses_wrong_dtypes_before_any_call(lib):
