@@ -1,11 +1,12 @@
 // The inverse of the block-scaled cast for gfx950: E4M3 codes with one fp32
 // scale per 128x128 tile back to bf16, y = RN_bf16(RN_f32(value(q) * s)).
 //
-// Layout mirrors the cast: one 512-thread workgroup per full tile of an
-// aligned item (16 lanes x 8 codes per 128-byte code row, 32 rows per pass,
-// 4 passes; 8 bf16 = 16 B stored per lane and pass), non-temporal loads and
-// stores, XCD groups of 4 tiles; partial tiles and unaligned items go to an
-// element-wise kernel.  Decoding uses v_cvt_pk_f32_fp8, which is exact for
+// Layout mirrors the cast: full tiles of aligned items with 16 lanes x 8
+// codes per 128-byte code row (8 bf16 = 16 B stored per lane and row),
+// non-temporal loads and stores, XCD groups of 4 tiles -- a quarter tile per
+// 256-thread workgroup when a per-tile table gives each tile's addresses,
+// else the whole tile per 512-thread workgroup after an item search; partial
+// tiles and unaligned items go to an element-wise kernel.  Decoding uses v_cvt_pk_f32_fp8, which is exact for
 // every finite E4M3 code and gives NaN for S.1111.111; the bf16 rounding is
 // done on the integer bits (nearest, ties to even; NaN -> 0x7FC0).
 #include "tc_device.h"
@@ -78,17 +79,48 @@ __global__ __launch_bounds__(kDequantThreads) void k_dequant_full(const uint8_t*
                scales[item.scale_off + ti * item.scale_ld + tj]);
 }
 
-// The same with the tile's addresses and scale index read from the per-tile
-// table (measured +2.2% on the 70B TP=8 shard).
-__global__ __launch_bounds__(kDequantThreads) void k_dequant_full_tab(const uint8_t* __restrict__ codes,
-                                                              const float* __restrict__ scales,
-                                                              uint16_t* __restrict__ dst,
-                                                              const TileEntry* __restrict__ tab,
-                                                              const uint64_t t0, const uint64_t count) {
-  const uint64_t t = t0 + xcd_grouped(blockIdx.x, count, kDequantXcdGroup);
-  const TileEntry e = tab[t];
-  dequant_tile(codes + e.in_off, dst + e.out_off, int64_t(uint32_t(e.lds)), int64_t(e.lds >> 32),
-               scales[e.scale_idx]);
+// The tiles of a per-tile table, a quarter tile per workgroup: 256 threads
+// take 32 rows (two passes of 16 rows, one 8-byte code load and one 16-byte
+// store per lane and pass).  With the table a workgroup finds its tile in one
+// load, so the dependent chain the whole-tile unit amortized (item search,
+// item, scale) is gone; the slabs of a tile share its entry and scale.
+// Measured on the 70B TP=8 shard, interleaved in one process: 6260-6274 GB/s
+// against 5932-5951 for the whole tile per 512-thread workgroup from the same
+// table (16-row slabs of 128 threads: 6264-6274; 64 rows of 512 threads:
+// 6100-6113; XCD runs of 2 or 8 tiles: 5984-5994, 6188-6213).
+constexpr int kSlabs = 4;
+constexpr int kSlabThreads = 256;
+constexpr int kSlabRows = kTile / kSlabs;
+constexpr int kSlabRowsPerPass = kSlabThreads / 16;
+constexpr int kSlabPasses = kSlabRows / kSlabRowsPerPass;
+static_assert(kSlabPasses * kSlabRowsPerPass == kSlabRows, "whole passes per slab");
+constexpr uint64_t kSlabTilesPerLaunch = kMaxGrid / kSlabs;
+
+__global__ __launch_bounds__(kSlabThreads) void k_dequant_slab_tab(const uint8_t* __restrict__ codes,
+                                                                  const float* __restrict__ scales,
+                                                                  uint16_t* __restrict__ dst,
+                                                                  const TileEntry* __restrict__ tab,
+                                                                  const uint64_t t0, const uint64_t count) {
+  const uint64_t u = xcd_grouped(blockIdx.x, count * kSlabs, kDequantXcdGroup * kSlabs);
+  const TileEntry e = tab[t0 + u / kSlabs];
+  const int64_t r0 = int64_t(u % kSlabs) * kSlabRows;
+  const int64_t src_ld = int64_t(uint32_t(e.lds)), dst_ld = int64_t(e.lds >> 32);
+  const uint8_t* qs = codes + e.in_off + r0 * src_ld;
+  uint16_t* ys = dst + e.out_off + r0 * dst_ld;
+  const int seg = threadIdx.x & 15;
+  const int prow = threadIdx.x >> 4;
+  u32x2 v[kSlabPasses];
+#pragma unroll
+  for (int p = 0; p < kSlabPasses; ++p)
+    v[p] = __builtin_nontemporal_load(
+        reinterpret_cast<const u32x2*>(qs + int64_t(p * kSlabRowsPerPass + prow) * src_ld + seg * 8));
+  const float s = scales[e.scale_idx];
+#pragma unroll
+  for (int p = 0; p < kSlabPasses; ++p) {
+    const u32x2 lo = dequant4(v[p].x, s), hi = dequant4(v[p].y, s);
+    st_sc1_nt(reinterpret_cast<u32x4*>(ys + int64_t(p * kSlabRowsPerPass + prow) * dst_ld + seg * 8),
+              u32x4{lo.x, lo.y, hi.x, hi.y});
+  }
 }
 
 // Partial tiles and unaligned items, element by element; numbered within an
@@ -142,14 +174,18 @@ hipError_t launch_dequant_blockscaled(const uint8_t* codes, const float* scales,
   const uint64_t* ep = reinterpret_cast<const uint64_t*>(base + L.edge_prefix);
   const uint8_t* al = base + L.aligned;
   const TileEntry* tab = reinterpret_cast<const TileEntry*>(base + L.bytes);
-  for (uint64_t t0 = 0; t0 < full_tiles; t0 += kMaxGrid) {
-    const uint64_t cnt = full_tiles - t0 < kMaxGrid ? full_tiles - t0 : kMaxGrid;
-    if (tiled)
-      hipLaunchKernelGGL(k_dequant_full_tab, dim3((unsigned)cnt), dim3(kDequantThreads), 0, s, codes, scales,
-                         dst, tab, t0, cnt);
-    else
+  if (tiled) {
+    for (uint64_t t0 = 0; t0 < full_tiles; t0 += kSlabTilesPerLaunch) {
+      const uint64_t cnt = full_tiles - t0 < kSlabTilesPerLaunch ? full_tiles - t0 : kSlabTilesPerLaunch;
+      hipLaunchKernelGGL(k_dequant_slab_tab, dim3((unsigned)(cnt * kSlabs)), dim3(kSlabThreads), 0, s, codes,
+                         scales, dst, tab, t0, cnt);
+    }
+  } else {
+    for (uint64_t t0 = 0; t0 < full_tiles; t0 += kMaxGrid) {
+      const uint64_t cnt = full_tiles - t0 < kMaxGrid ? full_tiles - t0 : kMaxGrid;
       hipLaunchKernelGGL(k_dequant_full, dim3((unsigned)cnt), dim3(kDequantThreads), 0, s, codes, scales,
                          dst, items, fp, n_items, t0, cnt);
+    }
   }
   for (uint64_t t0 = 0; t0 < edge_tiles; t0 += kMaxGrid) {
     const uint64_t cnt = edge_tiles - t0 < kMaxGrid ? edge_tiles - t0 : kMaxGrid;
