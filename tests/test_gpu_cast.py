@@ -132,6 +132,61 @@ def test_blockscaled_ragged_strided_and_offsets():
     _cast_matrices(bits, mats, code_pad=5, scale_pad=2)     # unaligned code rows
 
 
+def test_workspace_short_of_the_tile_table_takes_the_search():
+    """A workspace with room for the item table but not for every full
+    tile's entry: prepare falls back to the item search (plan.tiled == 0)
+    for the cast and its inverse, and both still match the oracle; one
+    more byte and the table is used."""
+    rng = np.random.default_rng(56)
+    bits = _bits_from_float(rng.normal(0, 0.02, size=520 * 400).astype(np.float32))
+    # 2 x 3 and 1 x 2 full tiles, every row vector-aligned (bf16 pitch a multiple
+    # of 16 B, code pitch of 8 B), so all eight go through the table
+    mats = [(0, 256, 384, 400), (256 * 400, 130, 264, 264)]
+    items = np.zeros(len(mats), dtype=tc.CAST_ITEM_DTYPE)
+    q_off = s_off = 0
+    for k, (so, rows, cols, ld) in enumerate(mats):
+        tr, tcn = (rows + 127) // 128, (cols + 127) // 128
+        items[k] = (so, rows, cols, ld, q_off, cols, s_off, tcn)
+        q_off += rows * cols
+        s_off += tr * tcn
+    base, full = tc.tc_cast_fp8_workspace(len(mats)), tc.tc_cast_fp8_workspace_tiles(items)
+    assert full == base + 256                                  # 8 entries of 32 B, rounded up
+    src = _to_dev_bits(bits)
+    q = torch.empty(q_off, dtype=torch.uint8, device=DEV)
+    ditems = items.astype(tc.DEQUANT_ITEM_DTYPE)
+    ditems["src_off"], ditems["src_ld"] = items["dst_off"], items["dst_ld"]
+    ditems["dst_ld"] = items["dst_ld"]
+    y = torch.empty(q_off, dtype=torch.bfloat16, device=DEV)
+    for ws_bytes, want_tiled in ((full - 1, 0), (full, 1)):
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device=DEV)
+        plan = tc.tc_cast_fp8_prepare(src, q, items, ws)
+        dplan = tc.tc_dequant_fp8_prepare(q, y, ditems, ws)
+        assert plan.tiled == want_tiled and dplan.tiled == want_tiled and plan.full_tiles == 8
+        _cast_and_check(src, bits, items, mats, q_off, s_off, ws_bytes)
+        # the inverse of the oracle's codes, planned in the same workspace
+        hq = np.zeros(q_off, dtype=np.uint8)
+        hs = np.zeros(s_off, dtype=np.float32)
+        for k, (so, rows, cols, ld) in enumerate(mats):
+            view = np.lib.stride_tricks.as_strided(bits[so:], shape=(rows, cols), strides=(2 * ld, 2))
+            cq, cs = oracle.cast_fp8_blockscaled(view)
+            hq[int(items[k]["dst_off"]):int(items[k]["dst_off"]) + rows * cols] = cq.reshape(-1)
+            hs[int(items[k]["scale_off"]):int(items[k]["scale_off"]) + cs.size] = cs.reshape(-1)
+        qd = torch.from_numpy(hq).to(DEV)
+        sd = torch.from_numpy(hs).to(DEV)
+        dplan = tc.tc_dequant_fp8_prepare(qd, y, ditems, ws)
+        assert dplan.tiled == want_tiled
+        y.zero_()
+        tc.tc_dequant_fp8_planned(qd, sd, y, ws, dplan)
+        torch.cuda.synchronize()
+        hy = _host(y.view(torch.int16)).view(np.uint16)
+        for k, (so, rows, cols, ld) in enumerate(mats):
+            o, tr, tcn = int(items[k]["dst_off"]), (rows + 127) // 128, (cols + 127) // 128
+            cq = hq[o:o + rows * cols].reshape(rows, cols)
+            cs = hs[int(items[k]["scale_off"]):int(items[k]["scale_off"]) + tr * tcn].reshape(tr, tcn)
+            assert np.array_equal(hy[o:o + rows * cols].reshape(rows, cols),
+                                  oracle.dequant_fp8_blockscaled(cq, cs)), (ws_bytes, k)
+
+
 def test_blockscaled_special_tiles():
     rng = np.random.default_rng(53)
     a = rng.normal(0, 1, size=(256, 640)).astype(np.float32)
