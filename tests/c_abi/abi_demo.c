@@ -7,9 +7,15 @@
  *   1. publish / hydrate: gather 10 blocks of a 2-region pool into a transfer
  *      buffer, scatter them into a second pool (distinct ids);
  *   2. fragments: plan three byte fragments once, copy them twice;
- *   3. digests of the same plan, against sums computed here.
+ *   3. digests of the same plan, against sums computed here;
+ *   4. the block-scaled fp8 cast of a 256 x 256 bf16 matrix, prepared once
+ *      in a workspace with the per-tile table, and its inverse.  Every tile
+ *      holds the values {1, 2, 1/2, 448, -7/2} times its own power of two,
+ *      so its scale is that power exactly, the E4M3 codes are known
+ *      constants and the inverse gives the source back bit for bit.
  */
 #include <hip/hip_runtime_api.h>
+#include <math.h>
 #include <stdint.h>
 #include <stdio.h>
 #include <stdlib.h>
@@ -122,10 +128,73 @@ int main(void) {
       return 1;
     }
   }
-  printf("C ABI demo: gather, scatter, planned copies and digests correct (%llu tasks)\n",
-         (unsigned long long)total);
+  /* 4. block-scaled cast and its inverse */
+  enum { M = 256, T = 128 };
+  static const float base[5] = {1.0f, 2.0f, 0.5f, 448.0f, -3.5f};
+  static const uint8_t code[5] = {0x38, 0x40, 0x30, 0x7E, 0xC6}; /* E4M3 of base */
+  static const int ex[2][2] = {{-4, -1}, {2, 5}};                  /* tile exponents */
+  uint16_t* xb = (uint16_t*)malloc((size_t)M * M * 2);
+  uint16_t* yb = (uint16_t*)malloc((size_t)M * M * 2);
+  uint8_t* qb = (uint8_t*)malloc((size_t)M * M);
+  if (!xb || !yb || !qb) return 1;
+  for (int r = 0; r < M; ++r)
+    for (int c = 0; c < M; ++c) {
+      const float v = ldexpf(base[(r * M + c) % 5], ex[r / T][c / T]);
+      uint32_t u;
+      memcpy(&u, &v, 4);
+      xb[r * M + c] = (uint16_t)(u >> 16); /* exact: at most 3 significant bits */
+    }
+  void *x_d, *q_d, *s_d, *y_d, *cws, *dws;
+  CHECK_HIP(hipMalloc(&x_d, (size_t)M * M * 2));
+  CHECK_HIP(hipMalloc(&q_d, (size_t)M * M));
+  CHECK_HIP(hipMalloc(&s_d, 4 * sizeof(float)));
+  CHECK_HIP(hipMalloc(&y_d, (size_t)M * M * 2));
+  CHECK_HIP(hipMemcpy(x_d, xb, (size_t)M * M * 2, hipMemcpyHostToDevice));
+  const tc_cast_item item = {0, M, M, M, 0, M, 0, 2};
+  const size_t cws_bytes = tc_cast_fp8_workspace_tiles(&item, 1);
+  if (cws_bytes < tc_cast_fp8_workspace(1) + 4 * 32) {
+    fprintf(stderr, "the tile workspace has no room for the 4 tile entries\n");
+    return 1;
+  }
+  CHECK_HIP(hipMalloc(&cws, cws_bytes));
+  tc_tile_plan plan;
+  CHECK_TC(tc_cast_fp8_prepare(x_d, q_d, &item, 1, 128, cws, cws_bytes, &plan, 0));
+  if (plan.tiled != 1 || plan.full_tiles != 4 || plan.edge_tiles != 0) {
+    fprintf(stderr, "cast plan: tiled %u, %llu full and %llu edge tiles\n", plan.tiled,
+            (unsigned long long)plan.full_tiles, (unsigned long long)plan.edge_tiles);
+    return 1;
+  }
+  CHECK_TC(tc_cast_fp8_planned(x_d, q_d, (float*)s_d, cws, cws_bytes, &plan, 0));
+  float sc[4];
+  CHECK_HIP(hipMemcpy(qb, q_d, (size_t)M * M, hipMemcpyDeviceToHost));
+  CHECK_HIP(hipMemcpy(sc, s_d, sizeof(sc), hipMemcpyDeviceToHost));
+  for (int t = 0; t < 4; ++t)
+    if (sc[t] != ldexpf(1.0f, ex[t / 2][t % 2])) {
+      fprintf(stderr, "scale of tile %d: %g\n", t, (double)sc[t]);
+      return 1;
+    }
+  for (int i = 0; i < M * M; ++i)
+    if (qb[i] != code[i % 5]) {
+      fprintf(stderr, "code %d: 0x%02x, want 0x%02x\n", i, qb[i], code[i % 5]);
+      return 1;
+    }
+  const tc_dequant_item ditem = {0, M, M, M, 0, M, 0, 2};
+  const size_t dws_bytes = tc_dequant_fp8_workspace_tiles(&ditem, 1);
+  CHECK_HIP(hipMalloc(&dws, dws_bytes));
+  tc_tile_plan dplan;
+  CHECK_TC(tc_dequant_fp8_prepare(q_d, y_d, &ditem, 1, 128, dws, dws_bytes, &dplan, 0));
+  CHECK_TC(tc_dequant_fp8_planned(q_d, (const float*)s_d, y_d, dws, dws_bytes, &dplan, 0));
+  CHECK_HIP(hipMemcpy(yb, y_d, (size_t)M * M * 2, hipMemcpyDeviceToHost));
+  if (dplan.tiled != 1 || memcmp(yb, xb, (size_t)M * M * 2)) {
+    fprintf(stderr, "the inverse cast did not give the source back\n");
+    return 1;
+  }
+
+  printf("C ABI demo: gather, scatter, planned copies, digests, fp8 cast and inverse correct "
+         "(%llu tasks)\n", (unsigned long long)total);
   hipFree(pool_a); hipFree(pool_b); hipFree(buf); hipFree(ids_d);
   hipFree(src); hipFree(dst); hipFree(fr_d); hipFree(ws); hipFree(dg);
-  free(host); free(got);
+  hipFree(x_d); hipFree(q_d); hipFree(s_d); hipFree(y_d); hipFree(cws); hipFree(dws);
+  free(host); free(got); free(xb); free(yb); free(qb);
   return 0;
 }

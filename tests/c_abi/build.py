@@ -22,7 +22,7 @@ def build(verbose: bool = False) -> str:
            f"-I{os.path.join(ROOT, 'include')}", f"-I{os.path.join(ROCM, 'include')}",
            os.path.join(HERE, "abi_demo.c"), "-o", EXE + ".tmp",
            f"-L{LIBDIR}", "-ltchip", "-Wl,-rpath,$ORIGIN/../../paper_2608_06007_amd",
-           f"-L{os.path.join(ROCM, 'lib')}", "-lamdhip64", f"-Wl,-rpath,{os.path.join(ROCM, 'lib')}"]
+           f"-L{os.path.join(ROCM, 'lib')}", "-lamdhip64", f"-Wl,-rpath,{os.path.join(ROCM, 'lib')}", "-lm"]
     if verbose:
         print(" ".join(cmd))
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -1,7 +1,8 @@
 """The library driven from plain C: tests/c_abi/abi_demo.c includes only the
 C header and the HIP runtime API, allocates with hipMalloc and checks the
-results of gather, scatter, planned copies and digests itself.  It runs as a
-child process; this test passes when it exits 0."""
+results of gather, scatter, planned copies, digests, and the fp8 cast and
+its inverse itself.  It runs as a child process; this test passes when it
+exits 0."""
 import os
 import subprocess
 
