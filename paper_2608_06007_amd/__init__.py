@@ -601,7 +601,10 @@ def tc_cast_fp8_workspace_tiles(items) -> int:
 
 def tc_cast_fp8_blockscaled(src, dst, scales, items, workspace, stream=None, tile: int = 128) -> None:
     """Cast every item; ``items`` is a host numpy array of CAST_ITEM_DTYPE
-    records (the library stages it into ``workspace``)."""
+    records, written into ``workspace`` on the stream by kernels that carry
+    it in their arguments (the array may be reused once the call returns).
+    A workspace of tc_cast_fp8_workspace_tiles(items) bytes also holds the
+    per-tile table, which the cast then reads."""
     it = np.ascontiguousarray(items, dtype=CAST_ITEM_DTYPE).reshape(-1)
     n = it.size
     _ok(load().tc_cast_fp8_blockscaled(_dev_ptr(src), _dev_ptr(dst), _dev_ptr(scales),
